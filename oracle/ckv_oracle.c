@@ -1,0 +1,311 @@
+/*
+ * ckv_oracle.c -- plain fp64 CPU oracle of CompressKV's prefill-end token selection.
+ *
+ * TEST INFRASTRUCTURE ONLY. This library is the parity reference for the HIP
+ * library. Only the test suite, the smoke check and the benchmark's CPU-baseline
+ * leg may load it; the product path never does. It shares no source, header,
+ * table or helper with the HIP library.
+ *
+ * What it computes follows CompressKV (Lin et al., arXiv 2508.02401):
+ *   - Token selection, paper Sec. 3.3 ("Token Selection Driven by Semantic
+ *     Retrieval Heads"): the attention-score matrices of the chosen heads over
+ *     the observation window are summed over the window, pooled along the
+ *     token axis, averaged over the chosen heads, and the top-N tokens keep
+ *     their K/V pairs.
+ *   - Attention scores are the row softmax of Q K^T (Eq. 2), here with the
+ *     usual 1/sqrt(d) factor passed in as `scale`.
+ *   - Hyper-parameters (window, pooling kernel, average pooling) from the
+ *     appendix "More Implementation Details".
+ *   - Layer budgets: Algorithm 1 (error-aware layer-adaptive allocation).
+ *
+ * Readings of points the paper leaves open (each is listed in the design notes):
+ *   R1 scale = 1/sqrt(d) unless given (Eq. 2 omits it).
+ *   R2 window row i (absolute position L-w+i) sees keys 0..L-w+i (causal).
+ *   R3 softmax over all visible keys; only the prefix [0, L-w) is ranked.
+ *   R4 the window reduction is a sum.
+ *   R5 pooling: stride 1, half-width r = kp/2, window clipped to [0, L-w);
+ *      average divides by kp (zero padding), max ignores padding.
+ *   R6 pool each head, then average the pooled vectors over the heads.
+ *   R9 the budget B counts the w window tokens, which are always kept; the
+ *      other B-w come from the prefix; B >= L keeps every token.
+ *   R10 equal scores: the lower token index wins.
+ *   R11 retained indices are returned in ascending order.
+ *   R13 query head h belongs to KV group h / (H / n_kv).
+ *   R14 Algorithm 1's round() is round-half-to-even; R15 its argmax/argmin
+ *      ties go to the lowest layer index.
+ *
+ * Everything is fp64 with plain loops; no blocking, fusion or reordering.
+ * OpenMP only runs independent KV groups on separate threads.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define CKVO_OK 0
+#define CKVO_EINVAL -1
+#define CKVO_EBUDGET -3
+#define CKVO_EMASK -4
+#define CKVO_ENOMEM -7
+
+#define CKVO_POOL_AVG 0
+#define CKVO_POOL_MAX 1
+
+/* One row of attention scores (Eq. 2): softmax over keys 0..n_visible-1 of
+ * scale * <q, k_j>.  p[j] = exp(s_j - max s) / sum_j' exp(s_j' - max s). */
+int ckvo_attention_row(const double *q, const double *k, int64_t n_visible,
+                       int32_t d, double scale, double *p) {
+  if (!q || !k || !p || n_visible < 1 || d < 1) return CKVO_EINVAL;
+  double m = -INFINITY;
+  for (int64_t j = 0; j < n_visible; ++j) {
+    double dot = 0.0;
+    for (int32_t c = 0; c < d; ++c) dot += q[c] * k[j * (int64_t)d + c];
+    p[j] = scale * dot;
+    if (p[j] > m) m = p[j];
+  }
+  double z = 0.0;
+  for (int64_t j = 0; j < n_visible; ++j) {
+    p[j] = exp(p[j] - m);
+    z += p[j];
+  }
+  for (int64_t j = 0; j < n_visible; ++j) p[j] /= z;
+  return CKVO_OK;
+}
+
+/* Window sums of one KV group (Sec. 3.3, "summing over the observation
+ * window"): for each of the n_sel chosen heads, S[h][j] = sum over the w window
+ * rows of that head's attention scores on key j, over the full range j in
+ * [0, L).  q_sel is [n_sel][w][d], k is [L][d], S is [n_sel][L]. */
+int ckvo_window_sums(const double *q_sel, int32_t n_sel, const double *k,
+                     int64_t L, int32_t d, int32_t w, double scale, double *S) {
+  if (!q_sel || !k || !S || n_sel < 1 || w < 1 || L <= w || d < 1)
+    return CKVO_EINVAL;
+  double *row = (double *)malloc(sizeof(double) * (size_t)L);
+  if (!row) return CKVO_ENOMEM;
+  for (int32_t h = 0; h < n_sel; ++h) {
+    double *Sh = S + (int64_t)h * L;
+    for (int64_t j = 0; j < L; ++j) Sh[j] = 0.0;
+    for (int32_t i = 0; i < w; ++i) {
+      int64_t n_visible = L - w + i + 1; /* R2: causal inside the window */
+      const double *qi = q_sel + ((int64_t)h * w + i) * d;
+      ckvo_attention_row(qi, k, n_visible, d, scale, row);
+      for (int64_t j = 0; j < n_visible; ++j) Sh[j] += row[j];
+    }
+  }
+  free(row);
+  return CKVO_OK;
+}
+
+/* 1-D pooling along the token axis (Sec. 3.3; kernel size and average pooling
+ * from the appendix). Stride 1, odd kernel kp, half-width r = kp/2; the
+ * neighbourhood of j is [j-r, j+r] clipped to [0, n). */
+int ckvo_pool(const double *x, int64_t n, int32_t kp, int32_t mode, double *y) {
+  if (!x || !y || n < 1 || kp < 1 || (kp % 2) == 0) return CKVO_EINVAL;
+  if (mode != CKVO_POOL_AVG && mode != CKVO_POOL_MAX) return CKVO_EINVAL;
+  int64_t r = kp / 2;
+  for (int64_t j = 0; j < n; ++j) {
+    int64_t lo = j - r < 0 ? 0 : j - r;
+    int64_t hi = j + r > n - 1 ? n - 1 : j + r;
+    if (mode == CKVO_POOL_AVG) {
+      double s = 0.0;
+      for (int64_t t = lo; t <= hi; ++t) s += x[t];
+      y[j] = s / (double)kp; /* zero padding counts toward the kernel */
+    } else {
+      double m = -INFINITY;
+      for (int64_t t = lo; t <= hi; ++t)
+        if (x[t] > m) m = x[t];
+      y[j] = m;
+    }
+  }
+  return CKVO_OK;
+}
+
+typedef struct {
+  double score;
+  int64_t index;
+} ckvo_ranked;
+
+/* Higher score first; equal scores: lower index first (R10). */
+static int ckvo_rank_cmp(const void *a, const void *b) {
+  const ckvo_ranked *x = (const ckvo_ranked *)a, *y = (const ckvo_ranked *)b;
+  if (x->score > y->score) return -1;
+  if (x->score < y->score) return 1;
+  return (x->index < y->index) ? -1 : (x->index > y->index);
+}
+
+static int ckvo_index_cmp(const void *a, const void *b) {
+  int32_t x = *(const int32_t *)a, y = *(const int32_t *)b;
+  return (x > y) - (x < y);
+}
+
+/* Top-N selection (Sec. 3.3, "the tokens with the top N highest attention
+ * scores will be selected"), under reading R9: the w window tokens are always
+ * kept and count toward the budget, the remaining budget-w tokens are the best
+ * of the prefix [0, L-w) by score a[]. Returns the number of retained indices
+ * (min(budget, L)) written to idx in ascending order, or a negative code. */
+int64_t ckvo_select_tokens(const double *a, int64_t L, int32_t w,
+                           int64_t budget, int32_t *idx) {
+  if (!a || !idx || w < 1 || L <= w) return CKVO_EINVAL;
+  if (budget < w) return CKVO_EBUDGET;
+  if (budget >= L) {
+    for (int64_t j = 0; j < L; ++j) idx[j] = (int32_t)j;
+    return L;
+  }
+  int64_t Ls = L - w, n_keep = budget - w;
+  ckvo_ranked *r = (ckvo_ranked *)malloc(sizeof(ckvo_ranked) * (size_t)Ls);
+  if (!r) return CKVO_ENOMEM;
+  for (int64_t j = 0; j < Ls; ++j) {
+    r[j].score = a[j];
+    r[j].index = j;
+  }
+  qsort(r, (size_t)Ls, sizeof(ckvo_ranked), ckvo_rank_cmp);
+  for (int64_t t = 0; t < n_keep; ++t) idx[t] = (int32_t)r[t].index;
+  free(r);
+  qsort(idx, (size_t)n_keep, sizeof(int32_t), ckvo_index_cmp);
+  for (int32_t i = 0; i < w; ++i) idx[n_keep + i] = (int32_t)(Ls + i);
+  return budget;
+}
+
+/* Retain/evict (Sec. 3.3): the kept tokens' rows, copied byte for byte.
+ * src is [L][row_bytes], dst is [n][row_bytes]. */
+int ckvo_gather_rows(const void *src, int64_t row_bytes, const int32_t *idx,
+                     int64_t n, void *dst) {
+  if ((!src || !idx || !dst) && n > 0) return CKVO_EINVAL;
+  for (int64_t t = 0; t < n; ++t)
+    memcpy((char *)dst + t * row_bytes, (const char *)src + idx[t] * row_bytes,
+           (size_t)row_bytes);
+  return CKVO_OK;
+}
+
+/* The whole selection for one KV group: window sums of the chosen heads,
+ * pooling of each head over the prefix (R6), mean over the heads ("such
+ * compressed vectors are averaged"), then top-N. scores is [L-w]; idx gets
+ * min(budget, L) entries. pooled (optional) receives [n_sel][L-w]. */
+int64_t ckvo_select_group(const double *q_sel, int32_t n_sel, const double *k,
+                          int64_t L, int32_t d, int32_t w, double scale,
+                          int32_t pool_mode, int32_t kp, int64_t budget,
+                          double *scores, double *pooled, int32_t *idx) {
+  if (!q_sel || !k || !scores || n_sel < 1 || w < 1 || L <= w)
+    return CKVO_EINVAL;
+  if (kp < 1 || (kp % 2) == 0) return CKVO_EINVAL;
+  if (budget < w) return CKVO_EBUDGET;
+  int64_t Ls = L - w;
+  double *S = (double *)malloc(sizeof(double) * (size_t)(n_sel * L));
+  double *P = (double *)malloc(sizeof(double) * (size_t)Ls);
+  if (!S || !P) {
+    free(S);
+    free(P);
+    return CKVO_ENOMEM;
+  }
+  int rc = ckvo_window_sums(q_sel, n_sel, k, L, d, w, scale, S);
+  if (rc == CKVO_OK) {
+    for (int64_t j = 0; j < Ls; ++j) scores[j] = 0.0;
+    for (int32_t h = 0; h < n_sel; ++h) {
+      /* R3: only the prefix columns are pooled and ranked. */
+      ckvo_pool(S + (int64_t)h * L, Ls, kp, pool_mode, P);
+      if (pooled) memcpy(pooled + (int64_t)h * Ls, P, sizeof(double) * (size_t)Ls);
+      for (int64_t j = 0; j < Ls; ++j) scores[j] += P[j];
+    }
+    for (int64_t j = 0; j < Ls; ++j) scores[j] /= (double)n_sel;
+  }
+  free(S);
+  free(P);
+  if (rc != CKVO_OK) return rc;
+  if (!idx) return CKVO_OK;
+  return ckvo_select_tokens(scores, L, w, budget, idx);
+}
+
+/* One layer: every KV group g selects with its own chosen heads (the mask
+ * marks chosen query heads; head h belongs to group h / (H / n_kv), R13).
+ * q is [H][w][d], k is [n_kv][L][d], scores is [n_kv][L-w], idx is
+ * [n_kv][min(budget, L)]. n_threads <= 0 uses the OpenMP default. */
+int64_t ckvo_select_layer(const double *q, const uint8_t *mask, int32_t H,
+                          int32_t n_kv, const double *k, int64_t L, int32_t d,
+                          int32_t w, double scale, int32_t pool_mode, int32_t kp,
+                          int64_t budget, double *scores, int32_t *idx,
+                          int32_t n_threads) {
+  if (!q || !mask || !k || !scores || !idx || H < 1 || n_kv < 1 || H % n_kv)
+    return CKVO_EINVAL;
+  if (L <= w || w < 1 || d < 1 || kp < 1 || (kp % 2) == 0) return CKVO_EINVAL;
+  if (budget < w) return CKVO_EBUDGET;
+  int32_t G = H / n_kv;
+  for (int32_t g = 0; g < n_kv; ++g) {
+    int32_t n = 0;
+    for (int32_t t = 0; t < G; ++t) n += mask[g * G + t] != 0;
+    if (n == 0) return CKVO_EMASK;
+  }
+  int64_t Ls = L - w, n_ret = budget < L ? budget : L;
+  int64_t status = 0;
+#ifdef _OPENMP
+  if (n_threads <= 0) n_threads = omp_get_max_threads();
+#pragma omp parallel for schedule(dynamic, 1) num_threads(n_threads)
+#endif
+  for (int32_t g = 0; g < n_kv; ++g) {
+    int32_t n_sel = 0;
+    for (int32_t t = 0; t < G; ++t) n_sel += mask[g * G + t] != 0;
+    double *q_sel = (double *)malloc(sizeof(double) * (size_t)n_sel * w * d);
+    if (!q_sel) {
+      status = CKVO_ENOMEM;
+      continue;
+    }
+    int32_t s = 0;
+    for (int32_t t = 0; t < G; ++t) {
+      int32_t h = g * G + t;
+      if (!mask[h]) continue;
+      memcpy(q_sel + (int64_t)s * w * d, q + (int64_t)h * w * d,
+             sizeof(double) * (size_t)w * d);
+      ++s;
+    }
+    int64_t rc = ckvo_select_group(q_sel, n_sel, k + (int64_t)g * L * d, L, d, w,
+                                   scale, pool_mode, kp, budget,
+                                   scores + (int64_t)g * Ls, NULL,
+                                   idx + (int64_t)g * n_ret);
+    if (rc < 0) status = rc;
+    free(q_sel);
+  }
+  return status < 0 ? status : n_ret;
+}
+
+/* Algorithm 1 (error-aware layer-adaptive cache allocation), step by step:
+ * start every layer at m, share the remainder R in proportion to the
+ * normalised errors e[] (rounded, R14), clip to [m, M], then move single
+ * tokens to the highest-error layer below M (surplus) or away from the
+ * lowest-error layer above m (deficit) until the total is met or no layer can
+ * move (R15: ties go to the lowest index). Returns 0 when the allocations sum
+ * to total, CKVO_EBUDGET when the loop stopped short. */
+int ckvo_allocate_budgets(const double *e, int32_t n, int64_t total, int64_t m,
+                          int64_t M, int64_t *B) {
+  if (!e || !B || n < 1 || m < 0 || M < m) return CKVO_EINVAL;
+  for (int32_t i = 0; i < n; ++i) B[i] = m;
+  int64_t sum = 0;
+  for (int32_t i = 0; i < n; ++i) sum += B[i];
+  int64_t R = total - sum;
+  for (int32_t i = 0; i < n; ++i) {
+    double share = nearbyint(e[i] * (double)R);
+    int64_t v = B[i] + (int64_t)share;
+    B[i] = v < m ? m : (v > M ? M : v);
+  }
+  sum = 0;
+  for (int32_t i = 0; i < n; ++i) sum += B[i];
+  int64_t delta = total - sum;
+  while (delta != 0) {
+    int32_t j = -1;
+    if (delta > 0) {
+      for (int32_t i = 0; i < n; ++i)
+        if (B[i] < M && (j < 0 || e[i] > e[j])) j = i;
+      if (j < 0) break;
+      B[j] += 1;
+      delta -= 1;
+    } else {
+      for (int32_t i = 0; i < n; ++i)
+        if (B[i] > m && (j < 0 || e[i] < e[j])) j = i;
+      if (j < 0) break;
+      B[j] -= 1;
+      delta += 1;
+    }
+  }
+  return delta == 0 ? CKVO_OK : CKVO_EBUDGET;
+}

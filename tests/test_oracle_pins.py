@@ -1,0 +1,411 @@
+"""Pins of the fp64 oracle against what the paper and the mathematics fix.
+
+The paper (CompressKV, arXiv 2508.02401) prints no worked numeric example of
+its token selection, so the oracle is pinned by:
+  * hand-worked exact examples (rational arithmetic, derivations below);
+  * closed forms (constant keys);
+  * invariants (softmax rows sum to 1, window sums total w, pooling bounds,
+    top-N count/order/ties);
+  * library routines the definitions reduce to (scipy softmax, numpy matmul,
+    torch avg/max pooling, numpy lexsort, numpy fancy indexing);
+  * brute force on tiny inputs (exhaustive subset search for the top-N).
+Every oracle function is covered; a plausible slip (dropped term, wrong sign
+or index, transposed operand, off-by-one mask, mean vs sum, pool order)
+fails at least one test here.
+"""
+import itertools
+import math
+from fractions import Fraction as F
+
+import numpy as np
+import pytest
+import scipy.special
+import torch
+
+import oracle
+
+LN2 = math.log(2.0)
+
+# ---------------------------------------------------------------------------
+# Hand-worked example (my own construction, exact in rationals).
+# One KV group of two query heads, d = 1, scale = 1, L = 6, w = 2 (prefix 4).
+# Keys k = [1, 0, 0, 2, 0, 0].
+#   head 0: both window rows q = ln 2  -> exp(s_j) = 2^{k_j} = [2,1,1,4,1,1]
+#   head 1: both window rows q = -ln 2 -> exp(s_j) = 2^{-k_j} = [1/2,1,1,1/4,1,1]
+# Window row i sits at position L-w+i and sees keys 0..L-w+i (causal).
+#   head 0, row 0: keys 0..4, Z = 9;  row 1: keys 0..5, Z = 10
+#     S0 = [2/9+2/10, 1/9+1/10, 1/9+1/10, 4/9+4/10, 1/9+1/10, 1/10]
+#        = [19/45, 19/90, 19/90, 38/45, 19/90, 1/10]   (total 2 = w)
+#   head 1, row 0: Z = 15/4; row 1: Z = 19/4
+#     S1 = [2/15+2/19, 4/15+4/19, 4/15+4/19, 1/15+1/19, 4/15+4/19, 4/19]
+# ---------------------------------------------------------------------------
+HW_K = np.array([[1.0], [0.0], [0.0], [2.0], [0.0], [0.0]])
+HW_Q = np.array([[[LN2], [LN2]], [[-LN2], [-LN2]]])  # [head, row, d]
+HW_S0 = [F(19, 45), F(19, 90), F(19, 90), F(38, 45), F(19, 90), F(1, 10)]
+HW_S1 = [F(2, 15) + F(2, 19), F(4, 15) + F(4, 19), F(4, 15) + F(4, 19),
+         F(1, 15) + F(1, 19), F(4, 15) + F(4, 19), F(4, 19)]
+
+
+def _close(x, fr, rel=1e-12):
+    return abs(x - float(fr)) <= rel * abs(float(fr)) + 1e-15
+
+
+def test_hand_example_window_sums_exact():
+    S = oracle.window_sums(HW_Q, HW_K, 1.0)
+    assert S.shape == (2, 6)
+    for j in range(6):
+        assert _close(S[0, j], HW_S0[j]), (j, S[0, j], HW_S0[j])
+        assert _close(S[1, j], HW_S1[j]), (j, S[1, j], HW_S1[j])
+    assert sum(HW_S0) == 2 and sum(HW_S1) == 2
+
+
+def test_hand_example_head1_prefix_values():
+    # the prefix of head 1 reduces to [68, 136, 136, 34] / 285
+    assert HW_S1[:4] == [F(68, 285), F(136, 285), F(136, 285), F(34, 285)]
+
+
+@pytest.mark.parametrize("mask,kp,mode,budget,expect_idx,expect_scores", [
+    # head 0 alone, no pooling: prefix [19/45, 19/90, 19/90, 38/45] -> keep 3, 0
+    ([0], 1, oracle.POOL_AVG, 4, [0, 3, 4, 5], [F(19, 45), F(19, 90), F(19, 90), F(38, 45)]),
+    # avg pooling (kernel 3, zero padding, divide by 3) changes the answer
+    ([0], 3, oracle.POOL_AVG, 4, [2, 3, 4, 5], [F(19, 90), F(38, 135), F(19, 45), F(19, 54)]),
+    # max pooling makes plateaus; B = 4 keeps the upper plateau
+    ([0], 3, oracle.POOL_MAX, 4, [2, 3, 4, 5], [F(19, 45), F(19, 45), F(38, 45), F(38, 45)]),
+    # B = 5: the tie 0 vs 1 on the lower plateau goes to the lower index
+    ([0], 3, oracle.POOL_MAX, 5, [0, 2, 3, 4, 5], [F(19, 45), F(19, 45), F(38, 45), F(38, 45)]),
+    # both heads, no pooling: mean of the two prefixes; exact tie 1 vs 2 -> 1
+    ([0, 1], 1, oracle.POOL_AVG, 4, [1, 3, 4, 5],
+     [F(113, 342), F(1177, 3420), F(1177, 3420), F(412, 855)]),
+    # both heads, max pooling: pool each head, then average (not the reverse)
+    ([0, 1], 3, oracle.POOL_MAX, 4, [2, 3, 4, 5],
+     [F(769, 1710), F(769, 1710), F(113, 171), F(113, 171)]),
+    # budget >= L keeps everything
+    ([0, 1], 1, oracle.POOL_AVG, 6, [0, 1, 2, 3, 4, 5],
+     [F(113, 342), F(1177, 3420), F(1177, 3420), F(412, 855)]),
+    # budget == w keeps only the window
+    ([1], 1, oracle.POOL_AVG, 2, [4, 5], [F(68, 285), F(136, 285), F(136, 285), F(34, 285)]),
+])
+def test_hand_example_selection(mask, kp, mode, budget, expect_idx, expect_scores):
+    scores, idx, _ = oracle.select_group(HW_Q[mask], HW_K, 2, 1.0, mode, kp, budget)
+    assert idx.tolist() == expect_idx
+    for j in range(4):
+        assert _close(scores[j], expect_scores[j]), (j, scores[j], expect_scores[j])
+
+
+def test_hand_example_mean_then_pool_differs():
+    # pinning reading R6: the mean-then-pool order would give these scores instead
+    mean = [(a + b) / 2 for a, b in zip(HW_S0[:4], HW_S1[:4])]
+    mtp = [max(mean[max(0, j - 1):j + 2]) for j in range(4)]
+    assert mtp == [F(1177, 3420), F(1177, 3420), F(412, 855), F(412, 855)]
+    scores, _, _ = oracle.select_group(HW_Q, HW_K, 2, 1.0, oracle.POOL_MAX, 3, 4)
+    assert not _close(scores[0], mtp[0], rel=1e-3)
+
+
+# ---------------------------------------------------------------------------
+# Attention rows: library softmax, normalisation, scale, operand order.
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_attention_row_matches_scipy_softmax(seed):
+    rng = np.random.default_rng(seed)
+    d, L = 7, 23
+    q = rng.standard_normal(d)
+    k = rng.standard_normal((L, d)) * 2.0
+    scale = 0.37
+    n_vis = 17
+    p = oracle.attention_row(q, k, n_vis, scale)
+    ref = scipy.special.softmax(scale * (k[:n_vis] @ q))
+    np.testing.assert_allclose(p, ref, rtol=1e-13, atol=1e-16)
+    assert abs(p.sum() - 1.0) < 1e-13
+
+
+def test_attention_row_large_logits_stable():
+    q = np.array([50.0, -20.0])
+    k = np.array([[10.0, 0.0], [9.0, 1.0], [-10.0, 0.0]])
+    p = oracle.attention_row(q, k, 3, 1.0)
+    ref = scipy.special.softmax(k @ q)
+    np.testing.assert_allclose(p, ref, rtol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# Window sums: library route, invariants, closed form.
+# ---------------------------------------------------------------------------
+def _window_sums_library(q_sel, k, scale):
+    """Attention matrices via numpy matmul and scipy softmax with a causal mask."""
+    n_sel, w, d = q_sel.shape
+    L = k.shape[0]
+    out = np.zeros((n_sel, L))
+    pos = np.arange(L)[None, :]
+    row_pos = (L - w + np.arange(w))[:, None]
+    for h in range(n_sel):
+        logits = scale * (q_sel[h] @ k.T)            # [w, L]
+        logits = np.where(pos <= row_pos, logits, -np.inf)
+        out[h] = scipy.special.softmax(logits, axis=1).sum(axis=0)
+    return out
+
+
+@pytest.mark.parametrize("seed,n_sel,w,d,L", [(3, 1, 1, 4, 9), (4, 2, 3, 5, 11), (5, 3, 4, 8, 40)])
+def test_window_sums_library_route(seed, n_sel, w, d, L):
+    rng = np.random.default_rng(seed)
+    q = rng.standard_normal((n_sel, w, d))
+    k = rng.standard_normal((L, d))
+    scale = 1.0 / math.sqrt(d)
+    S = oracle.window_sums(q, k, scale)
+    np.testing.assert_allclose(S, _window_sums_library(q, k, scale), rtol=1e-12, atol=1e-15)
+
+
+@pytest.mark.parametrize("seed", [6, 7])
+def test_window_sums_total_mass_is_w(seed):
+    rng = np.random.default_rng(seed)
+    n_sel, w, d, L = 2, 5, 6, 50
+    q = rng.standard_normal((n_sel, w, d)) * 3
+    k = rng.standard_normal((L, d))
+    S = oracle.window_sums(q, k, 0.5)
+    np.testing.assert_allclose(S.sum(axis=1), [w] * n_sel, rtol=1e-13)
+    assert np.all(S[:, : L - w].sum(axis=1) <= w + 1e-12)
+    assert np.all(S >= 0)
+    # the last key is seen only by the last window row
+    assert np.all(S[:, L - 1] <= 1 + 1e-15)
+
+
+@pytest.mark.parametrize("w,L", [(1, 5), (3, 10), (8, 64)])
+def test_window_sums_constant_keys_closed_form(w, L):
+    # identical keys give uniform rows: row i spreads 1 over L-w+i+1 keys, so a
+    # prefix key collects sum_i 1/(L-w+i+1); window key L-w+t collects the
+    # rows i >= t.
+    rng = np.random.default_rng(0)
+    d = 3
+    q = rng.standard_normal((1, w, d))
+    k = np.tile(rng.standard_normal((1, d)), (L, 1))
+    S = oracle.window_sums(q, k, 1.0)[0]
+    prefix = sum(1.0 / (L - w + i + 1) for i in range(w))
+    np.testing.assert_allclose(S[: L - w], prefix, rtol=1e-13)
+    for t in range(w):
+        expect = sum(1.0 / (L - w + i + 1) for i in range(t, w))
+        assert abs(S[L - w + t] - expect) < 1e-13
+
+
+def test_window_sums_scale_and_transpose_sensitivity():
+    # a non-symmetric key matrix and a non-trivial scale: the library route
+    # with k transposed or the scale dropped must disagree with the oracle
+    rng = np.random.default_rng(11)
+    q = rng.standard_normal((1, 2, 4))
+    k = rng.standard_normal((9, 4))
+    S = oracle.window_sums(q, k, 0.3)
+    assert np.allclose(S, _window_sums_library(q, k, 0.3), rtol=1e-12)
+    assert not np.allclose(S, _window_sums_library(q, k, 1.0), rtol=1e-3)
+
+
+# ---------------------------------------------------------------------------
+# Pooling: library routines, closed forms, bounds.
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("kp", [1, 3, 5, 7, 9])
+@pytest.mark.parametrize("n", [1, 2, 6, 31])
+def test_pool_matches_torch(kp, n):
+    rng = np.random.default_rng(kp * 100 + n)
+    x = rng.random(n)
+    r = kp // 2
+    xt = torch.from_numpy(x).view(1, 1, n)
+    avg = torch.nn.functional.avg_pool1d(xt, kp, stride=1, padding=r, count_include_pad=True)
+    mx = torch.nn.functional.max_pool1d(xt, kp, stride=1, padding=r)
+    np.testing.assert_allclose(oracle.pool(x, kp, oracle.POOL_AVG), avg.view(-1).numpy(), rtol=1e-14)
+    np.testing.assert_array_equal(oracle.pool(x, kp, oracle.POOL_MAX), mx.view(-1).numpy())
+
+
+def test_pool_constant_closed_form():
+    c, n, kp = 2.5, 12, 7
+    x = np.full(n, c)
+    avg = oracle.pool(x, kp, oracle.POOL_AVG)
+    mx = oracle.pool(x, kp, oracle.POOL_MAX)
+    r = kp // 2
+    for j in range(n):
+        covered = min(j, r) + min(n - 1 - j, r) + 1
+        assert abs(avg[j] - c * covered / kp) < 1e-14
+    np.testing.assert_array_equal(mx, x)
+
+
+def test_pool_bounds_and_mass():
+    rng = np.random.default_rng(5)
+    x = rng.random(40)
+    kp, r = 5, 2
+    mx = oracle.pool(x, kp, oracle.POOL_MAX)
+    assert np.all(mx >= x)
+    avg = oracle.pool(x, kp, oracle.POOL_AVG)
+    cover = np.array([min(j, r) + min(39 - j, r) + 1 for j in range(40)])
+    assert abs(avg.sum() - (x * cover).sum() / kp) < 1e-12
+
+
+def test_pool_rejects_even_kernel():
+    with pytest.raises(oracle.OracleError):
+        oracle.pool(np.ones(4), 4, oracle.POOL_AVG)
+
+
+# ---------------------------------------------------------------------------
+# Top-N: brute force, library sort, invariants.
+# ---------------------------------------------------------------------------
+def _brute_topn(a, k):
+    """Exhaustive: the k-subset with the largest sorted score vector, ties broken
+    towards the lexicographically smallest index set."""
+    best = None
+    for sub in itertools.combinations(range(len(a)), k):
+        key = (sorted((a[j] for j in sub), reverse=True), [-j for j in sub])
+        if best is None or key > best[0]:
+            best = (key, sub)
+    return list(best[1]) if best else []
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_select_tokens_brute_force(seed):
+    rng = np.random.default_rng(seed)
+    L, w = 10, 2
+    a = rng.integers(0, 4, size=L - w).astype(float)  # many exact ties
+    for budget in range(w, L + 2):
+        idx = oracle.select_tokens(a, L, w, budget).tolist()
+        if budget >= L:
+            assert idx == list(range(L))
+            continue
+        k = budget - w
+        assert idx == _brute_topn(list(a), k) + list(range(L - w, L))
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_select_tokens_library_sort_and_invariants(seed):
+    rng = np.random.default_rng(100 + seed)
+    L, w = 300, 7
+    a = np.round(rng.random(L - w), 2)
+    budget = 50
+    idx = oracle.select_tokens(a, L, w, budget)
+    order = np.lexsort((np.arange(L - w), -a))
+    ref = np.sort(order[: budget - w])
+    np.testing.assert_array_equal(idx[: budget - w], ref)
+    assert len(idx) == budget
+    assert np.all(np.diff(idx) > 0)
+    np.testing.assert_array_equal(idx[budget - w:], np.arange(L - w, L))
+    kept = idx[: budget - w]
+    evicted = np.setdiff1d(np.arange(L - w), kept)
+    assert a[kept].min() >= a[evicted].max()
+    t = a[kept].min()
+    # at the threshold value, every kept index precedes every evicted one
+    tied_out = evicted[a[evicted] == t]
+    if tied_out.size:
+        assert kept[a[kept] == t].max() < tied_out.min()
+
+
+def test_select_tokens_rejects_budget_below_window():
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.select_tokens(np.ones(8), 10, 2, 1)
+    assert e.value.code == oracle.EBUDGET
+
+
+# ---------------------------------------------------------------------------
+# Group and layer composition, special cases.
+# ---------------------------------------------------------------------------
+def test_single_head_single_row_reduces_to_softmax():
+    # one head, w = 1, no pooling: the score of prefix key j is the softmax
+    # probability of the last prompt position on key j
+    rng = np.random.default_rng(21)
+    d, L = 5, 30
+    q = rng.standard_normal((1, 1, d))
+    k = rng.standard_normal((L, d))
+    scores, idx, _ = oracle.select_group(q, k, 1, 0.4, oracle.POOL_AVG, 1, 6)
+    p = scipy.special.softmax(0.4 * (k @ q[0, 0]))
+    np.testing.assert_allclose(scores, p[: L - 1], rtol=1e-13)
+    top = np.sort(np.lexsort((np.arange(L - 1), -p[: L - 1]))[:5])
+    np.testing.assert_array_equal(idx, list(top) + [L - 1])
+
+
+def test_group_mean_is_linear_in_heads():
+    # avg pooling commutes with the head mean; the group score equals the mean
+    # of the single-head scores
+    rng = np.random.default_rng(22)
+    q = rng.standard_normal((3, 4, 6))
+    k = rng.standard_normal((40, 6))
+    s_all, _, pooled = oracle.select_group(q, k, 4, 0.5, oracle.POOL_AVG, 5, 10, want_pooled=True)
+    singles = [oracle.select_group(q[h:h + 1], k, 4, 0.5, oracle.POOL_AVG, 5, 10)[0] for h in range(3)]
+    np.testing.assert_allclose(s_all, np.mean(singles, axis=0), rtol=1e-13)
+    np.testing.assert_allclose(pooled.mean(axis=0), s_all, rtol=1e-13)
+
+
+def test_layer_routes_heads_to_groups():
+    rng = np.random.default_rng(23)
+    H, n_kv, w, d, L = 6, 2, 3, 4, 25
+    q = rng.standard_normal((H, w, d))
+    k = rng.standard_normal((n_kv, L, d))
+    mask = np.array([0, 1, 1, 1, 0, 0], dtype=np.uint8)  # group 0: {1,2}, group 1: {3}
+    scores, idx = oracle.select_layer(q, mask, k, w, 0.5, oracle.POOL_MAX, 3, 9)
+    s0, i0, _ = oracle.select_group(q[[1, 2]], k[0], w, 0.5, oracle.POOL_MAX, 3, 9)
+    s1, i1, _ = oracle.select_group(q[[3]], k[1], w, 0.5, oracle.POOL_MAX, 3, 9)
+    np.testing.assert_array_equal(scores[0], s0)
+    np.testing.assert_array_equal(scores[1], s1)
+    np.testing.assert_array_equal(idx[0], i0)
+    np.testing.assert_array_equal(idx[1], i1)
+
+
+def test_layer_rejects_group_without_head():
+    q = np.zeros((4, 2, 2))
+    k = np.zeros((2, 8, 2))
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.select_layer(q, np.array([1, 1, 0, 0], np.uint8), k, 2, 1.0, 0, 1, 4)
+    assert e.value.code == oracle.EMASK
+
+
+def test_planted_keys_survive():
+    # keys aligned with the window queries get much larger scores and are kept
+    rng = np.random.default_rng(24)
+    d, L, w = 16, 200, 4
+    q = rng.standard_normal((1, w, d))
+    k = rng.standard_normal((L, d))
+    qbar = q[0].mean(axis=0)
+    planted = [0, 1, 2, 3, 90, 91, 92]
+    for j in planted:
+        k[j] += 6.0 * math.sqrt(d) * qbar / (qbar @ qbar)
+    _, idx, _ = oracle.select_group(q, k, w, 1 / math.sqrt(d), oracle.POOL_MAX, 1, 20)
+    assert set(planted) <= set(idx.tolist())
+
+
+def test_gather_rows_bitwise():
+    rng = np.random.default_rng(25)
+    src = rng.integers(0, 65535, size=(30, 8), dtype=np.uint16)
+    idx = np.array([0, 5, 7, 29], dtype=np.int32)
+    np.testing.assert_array_equal(oracle.gather_rows(src, idx), src[idx])
+
+
+# ---------------------------------------------------------------------------
+# Algorithm 1: hand-worked examples and invariants.
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("e,total,m,M,expect", [
+    # m=32: R = 204, shares 102, 61.2->61, 40.8->41; sum 300 at once
+    ([0.5, 0.3, 0.2], 300, 32, 300, [134, 93, 73]),
+    # R = 272: 263.84->264, 2.72->3 (x3) -> 401; one token leaves the
+    # lowest-error layer, ties to the lowest index (layer 1)
+    ([0.97, 0.01, 0.01, 0.01], 400, 32, 300, [296, 34, 35, 35]),
+    # 269.28->269 clips at M=300; 1.36->1, 1.36->1, 0 -> 398; two tokens go
+    # to the highest-error layer below M, both to layer 1 (tie, lowest index)
+    ([0.99, 0.005, 0.005, 0.0], 400, 32, 300, [300, 35, 33, 32]),
+    # R = 1, 0.5 rounds half to even -> 0; the one token goes to layer 0
+    ([0.5, 0.5], 65, 32, 97, [33, 32]),
+])
+def test_algorithm1_hand_examples(e, total, m, M, expect):
+    B, rc = oracle.allocate_budgets(e, total, m, M)
+    assert rc == oracle.OK
+    assert B.tolist() == expect
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_algorithm1_invariants(seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 40))
+    e = rng.dirichlet(np.ones(n) * float(rng.choice([0.1, 1.0, 10.0])))
+    per = int(rng.integers(32, 2048))
+    total = n * per
+    m, M = 32, 3 * per
+    B, rc = oracle.allocate_budgets(e, total, m, M)
+    assert rc == oracle.OK
+    assert B.sum() == total
+    assert B.min() >= m and B.max() <= M
+
+
+def test_algorithm1_infeasible_reports_shortfall():
+    B, rc = oracle.allocate_budgets([0.5, 0.5], 1000, 32, 100)
+    assert rc == oracle.EBUDGET and B.tolist() == [100, 100]
+    B, rc = oracle.allocate_budgets([0.5, 0.5], 10, 32, 100)
+    assert rc == oracle.EBUDGET and B.tolist() == [32, 32]

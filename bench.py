@@ -1,0 +1,276 @@
+"""Benchmark of the CompressKV prefill-end KV eviction path on one MI355X.
+
+One step = the whole path (score, select, gather) over every layer of the
+workload, one ckv_compress_layer call per layer on one stream, with all inputs
+already resident in HBM. Prints one JSON line.
+
+  python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+
+The metric is prompt tokens compressed per second per layer:
+  value = sum_prompts(L) * n_layers / step_time.
+The roofline object covers the dominant kernel, timed with HIP events recorded
+around each of its launches inside the timed region (on the launch stream).
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0   # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=5)
+    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--workload", default="llama8b-128k-stack")
+    p.add_argument("--layers", type=int, default=0, help="limit the layer count (0 = all)")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-threads", type=int, default=0)
+    return p.parse_args()
+
+
+class Hip:
+    """Raw HIP events through the runtime library (torch events only see torch's stream)."""
+
+    def __init__(self):
+        self.lib = ctypes.CDLL("libamdhip64.so")
+        self.lib.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def event(self):
+        e = ctypes.c_void_p()
+        rc = self.lib.hipEventCreate(ctypes.byref(e))
+        if rc != 0:
+            raise RuntimeError("hipEventCreate failed: %d" % rc)
+        return e.value
+
+    def elapsed_ms(self, a, b) -> float:
+        out = ctypes.c_float()
+        rc = self.lib.hipEventElapsedTime(ctypes.byref(out), a, b)
+        if rc != 0:
+            raise RuntimeError("hipEventElapsedTime failed: %d" % rc)
+        return out.value
+
+    def destroy(self, e):
+        self.lib.hipEventDestroy(e)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: the eviction path has no multi-GPU mode in this "
+              "build (each KV head and layer is independent; see DESIGN.md for how it shards).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2508_02401_amd as ckv
+    from paper_2508_02401_amd import synth
+
+    ckv.load()
+    dev = torch.device("cuda:0")
+    wl = synth.WORKLOADS[args.workload]
+    n_layers = wl.n_layers if args.layers <= 0 else min(args.layers, wl.n_layers)
+    desc = ckv.layer_desc(wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.window, wl.dtype, 0.0,
+                          wl.pool, wl.pool_kernel)
+    elt = torch.tensor([], dtype=wl.dtype).element_size()
+
+    # budgets per layer and prompt (Algorithm 1 on the host, or the fixed budget)
+    errs = synth.layer_errors(wl)
+    budgets = []  # [prompt][layer]
+    for L in wl.seq_lens:
+        if wl.budget is not None:
+            budgets.append([wl.budget] * wl.n_layers)
+        else:
+            total, m, M = synth.budget_params(wl, L)
+            b, st = ckv.ckv_allocate_budgets(errs, total, m, M)
+            if st != ckv.CKV_OK:
+                raise RuntimeError("Algorithm 1 could not meet the total")
+            budgets.append([int(x) for x in b])
+
+    print("bench: drawing %d layers of %s" % (n_layers, wl.name), file=sys.stderr, flush=True)
+    layers = []
+    for l in range(n_layers):
+        inp = synth.layer_inputs(wl, l, dev)
+        seqs = [ckv.alloc_outputs(desc, ckv.Seq(inp.q_win[s], inp.k[s], inp.v[s], budgets[s][l]),
+                                  with_scores=False)
+                for s in range(len(wl.seq_lens))]
+        layers.append((inp.mask, seqs))
+    ws_bytes = max(ckv.ckv_workspace_bytes(desc, seqs) for _, seqs in layers)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+
+    def step(events=None):
+        for li, (mask, seqs) in enumerate(layers):
+            if events is not None:
+                ckv.ckv_set_stage_events(events[li][0], events[li][1])
+            ckv.ckv_compress_layer(desc, mask, seqs, ws, stream)
+        if events is not None:
+            ckv.ckv_set_stage_events(None, None)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    hip = Hip()
+    # ev[step][layer] = (begin events, end events) of the four stages
+    ev = [[([hip.event() for _ in range(4)], [hip.event() for _ in range(4)])
+           for _ in range(n_layers)] for _ in range(args.steps)]
+    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record(stream)
+    for k in range(args.steps):
+        step(ev[k])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_total = t_start.elapsed_time(t_end)
+    ms_per_step = ms_total / args.steps
+
+    stage_names = ["rowstats", "score", "select", "gather"]
+    stage_ms = {n: [] for n in stage_names}
+    for k in range(args.steps):
+        for li in range(n_layers):
+            b, e = ev[k][li]
+            for si, n in enumerate(stage_names):
+                stage_ms[n].append(hip.elapsed_ms(b[si], e[si]))
+    for k in range(args.steps):
+        for li in range(n_layers):
+            for x in ev[k][li][0] + ev[k][li][1]:
+                hip.destroy(x)
+    stage_avg = {n: float(np.mean(v)) for n, v in stage_ms.items()}
+
+    tokens_per_layer = sum(wl.seq_lens)
+    value = tokens_per_layer * n_layers / (ms_per_step / 1e3)
+
+    # algorithmic bytes of the whole path per layer (K once, chosen Q rows,
+    # retained K/V read + written, indices) and of the dominant kernel
+    n_kv, d, w = wl.num_kv_heads, wl.head_dim, wl.window
+    path_bytes = 0
+    for li, (mask, seqs) in enumerate(layers):
+        n_chosen = int(np.count_nonzero(mask))
+        for s, L in enumerate(wl.seq_lens):
+            n_ret = min(budgets[s][li], L)
+            path_bytes += n_kv * L * d * elt + n_chosen * w * d * elt + 4 * n_kv * n_ret * d * elt \
+                + 4 * n_kv * n_ret
+    path_gbs = path_bytes / (ms_per_step / 1e3) / 1e9
+
+    # dominant kernel: the one with the largest share of the step
+    dom = max(("rowstats", "score"), key=lambda n: stage_avg[n])
+    dom_bytes = []
+    for li, (mask, seqs) in enumerate(layers):
+        n_chosen = int(np.count_nonzero(mask))
+        b = 0
+        for L in wl.seq_lens:
+            if dom == "rowstats":
+                # every key of the prompt, the chosen Q rows, chunk partials
+                b += n_kv * L * d * elt + n_chosen * w * d * elt
+            else:
+                # prefix keys, chosen Q rows, row lse, scores written
+                b += n_kv * (L - w) * d * elt + n_chosen * w * d * elt + n_kv * (L - w) * 4
+        dom_bytes.append(b)
+    dom_gbs = float(np.mean(dom_bytes)) / (stage_avg[dom] / 1e3) / 1e9
+    # MFMA work of the dominant kernel (one logit pass over its keys)
+    flops = []
+    for li, (mask, seqs) in enumerate(layers):
+        n_chosen = int(np.count_nonzero(mask))
+        f = 0
+        for L in wl.seq_lens:
+            f += 2 * n_chosen * w * (L if dom == "rowstats" else (L - w)) * d
+        flops.append(f)
+    dom_tflops = float(np.mean(flops)) / (stage_avg[dom] / 1e3) / 1e12
+
+    result = {
+        "metric": "prompt tokens compressed/sec per layer (L=32K/128K) + achieved HBM GB/s",
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": {torch.bfloat16: "bf16", torch.float16: "f16", torch.float32: "f32"}[wl.dtype],
+        "data": "synthetic (seeded N(0,1) Q/K/V with planted sink and span keys; no real "
+                "activations or datasets)",
+        "config": {"workload": wl.name, "layers": n_layers, "q_heads": wl.num_q_heads,
+                   "kv_heads": n_kv, "head_dim": d, "seq_lens": list(wl.seq_lens),
+                   "window": w, "pool": "max" if wl.pool == 1 else "avg",
+                   "pool_kernel": wl.pool_kernel, "heads_per_group": list(wl.n_sel_choices),
+                   "budget_avg": float(np.mean(budgets)), "parallelism": "single GPU"},
+        "path_hbm_gbs": path_gbs,
+        "path_hbm_frac": path_gbs / HBM_PEAK_GBS,
+        "stage_ms_avg": stage_avg,
+        "roofline": {"kernel": dom + "_kernel", "bound": "hbm", "achieved": dom_gbs,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": dom_gbs / HBM_PEAK_GBS,
+                     "traffic": None, "avg_launch_ms": stage_avg[dom],
+                     "algorithmic_bytes_per_launch": float(np.mean(dom_bytes)),
+                     "mfma_tflops": dom_tflops, "mfma_frac_bf16": dom_tflops / BF16_PEAK_TFLOPS},
+        "wall_s_timed": wall,
+    }
+
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_threads)
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline(wl, threads: int):
+    """The fp64 oracle on one layer of the workload (a bounded sample)."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from paper_2508_02401_amd import synth
+
+    n_threads = threads if threads > 0 else min(os.cpu_count() or 1, 16)
+    L = wl.seq_lens[0]
+    inp = synth.layer_inputs(wl, 0, "cpu", seq_lens=(L,), with_v=False)
+    q = inp.q_win[0].double().numpy()
+    k = inp.k[0].double().numpy()
+    b = wl.budget if wl.budget is not None else 2 * wl.window
+    # a single layer takes tens of seconds at L=128K; sample KV heads so the
+    # run stays around 10-30 s, and scale to a full layer
+    n_kv = wl.num_kv_heads
+    heads = list(range(n_kv))
+    G = wl.num_q_heads // n_kv
+    t0 = time.perf_counter()
+    sub_mask = inp.mask.reshape(n_kv, G)
+    budget_kv = n_kv
+    if L >= 65536:
+        budget_kv = min(n_kv, max(1, n_threads))
+        heads = heads[:budget_kv]
+    qs = q.reshape(n_kv, G, wl.window, wl.head_dim)[heads].reshape(-1, wl.window, wl.head_dim)
+    ms = sub_mask[heads].reshape(-1)
+    oracle.select_layer(qs, ms, k[heads], wl.window, 1.0 / np.sqrt(wl.head_dim),
+                        oracle.POOL_MAX if wl.pool == 1 else oracle.POOL_AVG, wl.pool_kernel, b,
+                        n_threads)
+    dt = time.perf_counter() - t0
+    layer_time = dt * n_kv / len(heads)
+    return {"value": L / layer_time, "unit": "tokens/s", "cores": min(n_threads, len(heads)),
+            "kind": "oracle",
+            "sample": "layer 0 of %s, %d of %d KV heads at L=%d (fp64 C oracle, OpenMP over KV "
+                      "heads), scaled to a full layer; %.1f s wall"
+                      % (wl.name, len(heads), n_kv, L, dt)}
+
+
+if __name__ == "__main__":
+    main()

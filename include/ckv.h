@@ -1,0 +1,191 @@
+/*
+ * ckv.h -- C ABI of the MI355X (gfx950) CompressKV prefill-end KV eviction path.
+ *
+ * CompressKV (Lin et al., arXiv 2508.02401) evicts prompt KV pairs once, at the
+ * end of prefill. Per layer and per KV head (GQA group), only the group's chosen
+ * "semantic retrieval" query heads vote: their attention-score rows for the last
+ * w prompt positions (the observation window) are summed over the window,
+ * pooled along the token axis and averaged over the chosen heads; the tokens
+ * with the N highest scores keep their K/V pairs, the rest are evicted
+ * (paper Sec. 3.3, "Token Selection Driven by Semantic Retrieval Heads").
+ * Per-layer budgets N come from Algorithm 1 (appendix "More Implementation
+ * Details").
+ *
+ * Conventions shared by every entry point:
+ *   - Every function returns an int status (CKV_OK or a negative CKV_ERR_*),
+ *     never throws, never aborts, never prints.
+ *   - All arguments are validated on the host before anything is enqueued; on
+ *     error nothing is launched and no output is touched.
+ *   - The caller owns every buffer. Device pointers are plain HIP device
+ *     addresses (e.g. from torch or hipMalloc); host arrays (head mask,
+ *     budgets, errors) are read during the call and not retained. The library
+ *     allocates no device memory: scratch space is the caller's workspace,
+ *     sized by ckv_workspace_bytes().
+ *   - Device work is enqueued asynchronously on the caller's stream
+ *     (`stream` is a hipStream_t; NULL means the default stream). Faults
+ *     surface at the caller's next synchronisation. Calls that share one
+ *     workspace must be ordered (same stream or synchronised).
+ *   - The library keeps no state between calls apart from cached device
+ *     properties; it is safe to call from several host threads with distinct
+ *     workspaces.
+ */
+#ifndef CKV_H_
+#define CKV_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------ */
+#define CKV_OK 0
+#define CKV_ERR_INVALID_ARG (-1) /* null pointer, bad size/stride/alignment, even pool kernel */
+#define CKV_ERR_UNSUPPORTED (-2) /* dtype, head_dim, window or head count outside the built set */
+#define CKV_ERR_BUDGET (-3)      /* budget below the window; Algorithm 1 could not meet the total */
+#define CKV_ERR_MASK (-4)        /* a KV group has no chosen query head */
+#define CKV_ERR_WORKSPACE (-5)   /* workspace missing or smaller than ckv_workspace_bytes() */
+#define CKV_ERR_HIP (-6)         /* a HIP runtime call failed; see ckv_last_hip_error() */
+
+/* ---- enums ------------------------------------------------------------- */
+typedef enum { CKV_BF16 = 0, CKV_F16 = 1, CKV_F32 = 2 } ckv_dtype;
+typedef enum { CKV_POOL_AVG = 0, CKV_POOL_MAX = 1 } ckv_pool;
+
+/* flags */
+#define CKV_KEEP_WINDOW (1u << 0) /* required: the w window tokens are always kept and count in B */
+
+/* Limits of this build (larger values return CKV_ERR_UNSUPPORTED). */
+#define CKV_MAX_Q_HEADS 128
+#define CKV_MAX_KV_HEADS 64
+#define CKV_MAX_WINDOW 128
+#define CKV_MAX_POOL_KERNEL 31
+#define CKV_MAX_SEQS 16
+#define CKV_MAX_ROWS_PER_GROUP 128 /* n_chosen(g) * round_up(w, 8) */
+
+/* ---- layer descriptor ---------------------------------------------------
+ * One attention layer's shape and the selection hyper-parameters.
+ *   num_q_heads  H, num_kv_heads n_kv; H % n_kv == 0, group size G = H / n_kv.
+ *                Query head h belongs to KV group h / G (contiguous GQA groups).
+ *   head_dim     d in {64, 128}.
+ *   window       w, the observation window (last w prompt positions), 1..128.
+ *   dtype        element type of Q, K, V and of the compact K/V outputs.
+ *   scale        logit scale; <= 0 selects 1/sqrt(head_dim). The softmax is
+ *                taken over scale * <q, k> (paper Eq. 2 with the usual scale).
+ *   pool         CKV_POOL_AVG (zero padding, divide by the kernel size) or
+ *                CKV_POOL_MAX (padding ignored); pool_kernel odd, 1..31
+ *                (1 = no pooling). Stride 1; the neighbourhood of token j is
+ *                [j - k/2, j + k/2] clipped to the ranked prefix [0, L - w).
+ *   flags        must contain CKV_KEEP_WINDOW.
+ */
+typedef struct {
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t window;
+  int32_t dtype;
+  float scale;
+  int32_t pool;
+  int32_t pool_kernel;
+  uint32_t flags;
+  int32_t reserved;
+} ckv_layer_desc;
+
+/* ---- one prompt ---------------------------------------------------------
+ * Strides are in elements; the last (head_dim) axis must be contiguous, every
+ * pointer 16-byte aligned and every stride a multiple of 16 bytes.
+ *   q_win   [H, w, d]: the queries of the last w prompt positions of every
+ *           query head; row i of head h at q_win + h*q_stride_head + i*q_stride_row.
+ *           Only the chosen heads' rows are read.
+ *   k, v    [n_kv, L, d]: the prompt's key/value cache; token t of KV head g
+ *           at k + g*kv_stride_head + t*kv_stride_tok (same strides for v).
+ *   seq_len L > w, L < 2^31.
+ *   budget  B, tokens kept per KV head including the w window tokens
+ *           (B >= w). B >= L keeps every token. The top B - w of the prefix
+ *           [0, L - w) are kept; ties go to the lower index.
+ *   scores  [n_kv, L - w] fp32: the averaged score of every prefix token.
+ *           Written by ckv_score, read by ckv_select; may be NULL for
+ *           ckv_compress_layer (the workspace holds it then).
+ *   idx     [n_kv, min(B, L)] int32: retained token positions per KV head in
+ *           ascending order (the last w are L-w..L-1). Written by ckv_select,
+ *           read by ckv_gather.
+ *   k_out, v_out [n_kv, min(B, L), d] contiguous, dtype of the layer: the
+ *           compact cache, row r of head g is K[g, idx[g, r], :].
+ */
+typedef struct {
+  const void *q_win;
+  int64_t q_stride_head;
+  int64_t q_stride_row;
+  const void *k;
+  const void *v;
+  int64_t kv_stride_head;
+  int64_t kv_stride_tok;
+  int64_t seq_len;
+  int32_t budget;
+  int32_t reserved;
+  float *scores;
+  int32_t *idx;
+  void *k_out;
+  void *v_out;
+} ckv_seq;
+
+/* Bytes of device workspace the calls below need for this layer and batch
+ * (an upper bound independent of the head mask). Returns 0 on invalid input. */
+size_t ckv_workspace_bytes(const ckv_layer_desc *desc, const ckv_seq *seqs, int32_t num_seqs);
+
+/* Token scoring, paper Sec. 3.3 (the chosen heads' attention-score matrices
+ * over the observation window, summed over the window, pooled along the token
+ * axis, averaged over the chosen heads). head_mask is a host array [H]; nonzero
+ * marks a chosen head and every KV group needs at least one. Writes
+ * seqs[s].scores for every prompt s. Window row i (position L-w+i) attends to
+ * keys 0..L-w+i; its softmax runs over all of them, and only the prefix
+ * columns [0, L-w) are scored. */
+int ckv_score(const ckv_layer_desc *desc, const uint8_t *head_mask, const ckv_seq *seqs,
+              int32_t num_seqs, void *workspace, size_t workspace_bytes, void *stream);
+
+/* Top-N selection, paper Sec. 3.3 ("the tokens with the top N highest
+ * attention scores will be selected"): for every prompt and KV head, reads
+ * scores (>= 0, finite) and writes idx: the B - w best prefix tokens (higher
+ * score first, lower index on ties) in ascending order, then the window
+ * positions; or 0..L-1 when B >= L. */
+int ckv_select(const ckv_layer_desc *desc, const ckv_seq *seqs, int32_t num_seqs,
+               void *workspace, size_t workspace_bytes, void *stream);
+
+/* Retain/evict, paper Sec. 3.3 ("their corresponding KV cache pairs will be
+ * retained"): copies K and V rows idx[g, r] into k_out / v_out bit for bit.
+ * idx entries must lie in [0, L). */
+int ckv_gather(const ckv_layer_desc *desc, const ckv_seq *seqs, int32_t num_seqs, void *stream);
+
+/* The whole per-layer path: ckv_score, ckv_select and ckv_gather in order on
+ * one stream (scores may be NULL). */
+int ckv_compress_layer(const ckv_layer_desc *desc, const uint8_t *head_mask, const ckv_seq *seqs,
+                       int32_t num_seqs, void *workspace, size_t workspace_bytes, void *stream);
+
+/* Algorithm 1 (error-aware layer-adaptive cache allocation), host only,
+ * synchronous. err_norm [n_layers] are the normalised per-layer errors,
+ * total is B_total, [m, M] the per-layer bounds. out [n_layers] receives the
+ * budgets. round() is round-half-to-even; argmax/argmin ties go to the lowest
+ * layer. Returns CKV_OK when sum(out) == total, CKV_ERR_BUDGET when the bounds
+ * made that impossible (out still holds the clipped allocation), or
+ * CKV_ERR_INVALID_ARG. */
+int ckv_allocate_budgets(const double *err_norm, int32_t n_layers, int64_t total, int32_t m,
+                         int32_t M, int32_t *out);
+
+/* Static description of a status code. */
+const char *ckv_status_string(int status);
+
+/* hipError_t of the most recent CKV_ERR_HIP returned on this host thread. */
+int ckv_last_hip_error(void);
+
+/* Optional per-stage timing for profiling: when begin/end are non-NULL the
+ * next calls record begin[s] before and end[s] after stage s's kernel on the
+ * caller's stream (stage 0 row statistics, 1 scoring, 2 selection,
+ * 3 gather). Arrays are hipEvent_t[4] owned by the caller; pass NULL to stop.
+ * Per host thread. */
+int ckv_set_stage_events(void *const *begin, void *const *end);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CKV_H_ */

@@ -1,0 +1,262 @@
+"""ctypes binding of libckv.so (include/ckv.h). Argument marshalling only.
+
+Every function keeps the C name and contract; torch tensors stand in for device
+pointers. Errors come back as :class:`CkvError` carrying the status code.
+There is no fallback: if libckv.so is missing or fails to load, every call
+raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libckv.so")
+
+# status codes and enums (mirror include/ckv.h)
+CKV_OK = 0
+CKV_ERR_INVALID_ARG = -1
+CKV_ERR_UNSUPPORTED = -2
+CKV_ERR_BUDGET = -3
+CKV_ERR_MASK = -4
+CKV_ERR_WORKSPACE = -5
+CKV_ERR_HIP = -6
+CKV_BF16, CKV_F16, CKV_F32 = 0, 1, 2
+CKV_POOL_AVG, CKV_POOL_MAX = 0, 1
+CKV_KEEP_WINDOW = 1
+CKV_MAX_SEQS = 16
+
+EXPORTED = ("ckv_workspace_bytes", "ckv_score", "ckv_select", "ckv_gather", "ckv_compress_layer",
+            "ckv_allocate_budgets", "ckv_status_string", "ckv_last_hip_error",
+            "ckv_set_stage_events")
+
+_DTYPE_CODE = {torch.bfloat16: CKV_BF16, torch.float16: CKV_F16, torch.float32: CKV_F32}
+
+
+class ckv_layer_desc(ctypes.Structure):
+    _fields_ = [("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("window", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("scale", ctypes.c_float),
+                ("pool", ctypes.c_int32), ("pool_kernel", ctypes.c_int32),
+                ("flags", ctypes.c_uint32), ("reserved", ctypes.c_int32)]
+
+
+class ckv_seq(ctypes.Structure):
+    _fields_ = [("q_win", ctypes.c_void_p), ("q_stride_head", ctypes.c_int64),
+                ("q_stride_row", ctypes.c_int64), ("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
+                ("kv_stride_head", ctypes.c_int64), ("kv_stride_tok", ctypes.c_int64),
+                ("seq_len", ctypes.c_int64), ("budget", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("scores", ctypes.c_void_p),
+                ("idx", ctypes.c_void_p), ("k_out", ctypes.c_void_p), ("v_out", ctypes.c_void_p)]
+
+
+class CkvError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        msg = "%s: %s (status %d)" % (what, status_string(status), status)
+        if status == CKV_ERR_HIP:
+            msg += ", hipError %d" % ckv_last_hip_error()
+        super().__init__(msg)
+        self.status = status
+
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load libckv.so; raise if it is not built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libckv.so is not built (%s); run __graft_entry__.build()" % LIB_PATH)
+        lib = ctypes.CDLL(LIB_PATH)
+        P, vp = ctypes.POINTER, ctypes.c_void_p
+        D, S = P(ckv_layer_desc), P(ckv_seq)
+        lib.ckv_workspace_bytes.argtypes = [D, S, ctypes.c_int32]
+        lib.ckv_workspace_bytes.restype = ctypes.c_size_t
+        lib.ckv_score.argtypes = [D, P(ctypes.c_uint8), S, ctypes.c_int32, vp, ctypes.c_size_t, vp]
+        lib.ckv_select.argtypes = [D, S, ctypes.c_int32, vp, ctypes.c_size_t, vp]
+        lib.ckv_gather.argtypes = [D, S, ctypes.c_int32, vp]
+        lib.ckv_compress_layer.argtypes = [D, P(ctypes.c_uint8), S, ctypes.c_int32, vp,
+                                           ctypes.c_size_t, vp]
+        lib.ckv_allocate_budgets.argtypes = [P(ctypes.c_double), ctypes.c_int32, ctypes.c_int64,
+                                             ctypes.c_int32, ctypes.c_int32, P(ctypes.c_int32)]
+        lib.ckv_status_string.argtypes = [ctypes.c_int]
+        lib.ckv_status_string.restype = ctypes.c_char_p
+        lib.ckv_last_hip_error.argtypes = []
+        lib.ckv_set_stage_events.argtypes = [P(vp), P(vp)]
+        for name in ("ckv_score", "ckv_select", "ckv_gather", "ckv_compress_layer",
+                     "ckv_allocate_budgets", "ckv_last_hip_error", "ckv_set_stage_events"):
+            getattr(lib, name).restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return load().ckv_status_string(status).decode()
+
+
+ckv_status_string = status_string
+
+
+def ckv_last_hip_error() -> int:
+    return load().ckv_last_hip_error()
+
+
+# --------------------------------------------------------------------------
+# marshalling helpers
+# --------------------------------------------------------------------------
+def layer_desc(num_q_heads: int, num_kv_heads: int, head_dim: int, window: int,
+               dtype: torch.dtype = torch.bfloat16, scale: float = 0.0, pool: int = CKV_POOL_MAX,
+               pool_kernel: int = 7, flags: int = CKV_KEEP_WINDOW) -> ckv_layer_desc:
+    code = _DTYPE_CODE[dtype] if isinstance(dtype, torch.dtype) else int(dtype)
+    return ckv_layer_desc(num_q_heads, num_kv_heads, head_dim, window, code, scale, pool,
+                          pool_kernel, flags, 0)
+
+
+@dataclass
+class Seq:
+    """One prompt. q_win [H, w, d], k/v [n_kv, L, d] (last axis contiguous),
+    outputs as in include/ckv.h (None where a call does not need them)."""
+    q_win: Optional[torch.Tensor]
+    k: Optional[torch.Tensor]
+    v: Optional[torch.Tensor]
+    budget: int
+    scores: Optional[torch.Tensor] = None
+    idx: Optional[torch.Tensor] = None
+    k_out: Optional[torch.Tensor] = None
+    v_out: Optional[torch.Tensor] = None
+    seq_len: Optional[int] = None
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _seq_array(seqs: Sequence[Seq]):
+    arr = (ckv_seq * len(seqs))()
+    for i, s in enumerate(seqs):
+        c = arr[i]
+        if s.q_win is not None:
+            c.q_win = s.q_win.data_ptr()
+            c.q_stride_head, c.q_stride_row = s.q_win.stride(0), s.q_win.stride(1)
+        kv = s.k if s.k is not None else s.v
+        if s.k is not None:
+            c.k = s.k.data_ptr()
+        if s.v is not None:
+            c.v = s.v.data_ptr()
+            if s.k is not None and s.v.stride()[:2] != s.k.stride()[:2]:
+                raise ValueError("k and v must share strides")
+        if kv is not None:
+            c.kv_stride_head, c.kv_stride_tok = kv.stride(0), kv.stride(1)
+            c.seq_len = kv.shape[1]
+        if s.seq_len is not None:
+            c.seq_len = s.seq_len
+        c.budget = int(s.budget)
+        c.scores, c.idx = _ptr(s.scores), _ptr(s.idx)
+        c.k_out, c.v_out = _ptr(s.k_out), _ptr(s.v_out)
+    return arr
+
+
+def _mask(head_mask) -> ctypes.Array:
+    m = np.ascontiguousarray(np.asarray(head_mask, dtype=np.uint8))
+    return (ctypes.c_uint8 * m.size).from_buffer_copy(m.tobytes())
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream if torch.cuda.is_available() else None
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _check(status: int, what: str) -> None:
+    if status != CKV_OK:
+        raise CkvError(status, what)
+
+
+# --------------------------------------------------------------------------
+# the C entry points
+# --------------------------------------------------------------------------
+def ckv_workspace_bytes(desc: ckv_layer_desc, seqs: Sequence[Seq]) -> int:
+    arr = _seq_array(seqs)
+    return load().ckv_workspace_bytes(ctypes.byref(desc), arr, len(seqs))
+
+
+def ckv_score(desc, head_mask, seqs: Sequence[Seq], workspace: torch.Tensor, stream=None) -> None:
+    arr = _seq_array(seqs)
+    _check(load().ckv_score(ctypes.byref(desc), _mask(head_mask), arr, len(seqs),
+                            workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                            _stream(stream)), "ckv_score")
+
+
+def ckv_select(desc, seqs: Sequence[Seq], workspace: Optional[torch.Tensor] = None,
+               stream=None) -> None:
+    arr = _seq_array(seqs)
+    ws_ptr = workspace.data_ptr() if workspace is not None else None
+    ws_n = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(load().ckv_select(ctypes.byref(desc), arr, len(seqs), ws_ptr, ws_n, _stream(stream)),
+           "ckv_select")
+
+
+def ckv_gather(desc, seqs: Sequence[Seq], stream=None) -> None:
+    arr = _seq_array(seqs)
+    _check(load().ckv_gather(ctypes.byref(desc), arr, len(seqs), _stream(stream)), "ckv_gather")
+
+
+def ckv_compress_layer(desc, head_mask, seqs: Sequence[Seq], workspace: torch.Tensor,
+                       stream=None) -> None:
+    arr = _seq_array(seqs)
+    _check(load().ckv_compress_layer(ctypes.byref(desc), _mask(head_mask), arr, len(seqs),
+                                     workspace.data_ptr(),
+                                     workspace.numel() * workspace.element_size(),
+                                     _stream(stream)), "ckv_compress_layer")
+
+
+def ckv_allocate_budgets(err_norm, total: int, m: int, M: int):
+    """Algorithm 1 on the host. Returns (budgets int32 array, status)."""
+    e = np.ascontiguousarray(np.asarray(err_norm, dtype=np.float64))
+    out = np.zeros(e.shape[0], dtype=np.int32)
+    st = load().ckv_allocate_budgets(e.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
+                                     e.shape[0], int(total), int(m), int(M),
+                                     out.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)))
+    if st not in (CKV_OK, CKV_ERR_BUDGET):
+        raise CkvError(st, "ckv_allocate_budgets")
+    return out, st
+
+
+def ckv_set_stage_events(begin, end) -> None:
+    """begin/end: sequences of 4 raw hipEvent_t handles, or None to stop."""
+    if begin is None or end is None:
+        _check(load().ckv_set_stage_events(None, None), "ckv_set_stage_events")
+        return
+    b = (ctypes.c_void_p * 4)(*begin)
+    e = (ctypes.c_void_p * 4)(*end)
+    _check(load().ckv_set_stage_events(b, e), "ckv_set_stage_events")
+
+
+# --------------------------------------------------------------------------
+# output allocation (plumbing)
+# --------------------------------------------------------------------------
+def alloc_outputs(desc: ckv_layer_desc, s: Seq, with_scores: bool = True) -> Seq:
+    """Allocate scores/idx/k_out/v_out for one prompt on the device of s.k."""
+    L = s.k.shape[1] if s.seq_len is None else s.seq_len
+    n_kv, d = desc.num_kv_heads, desc.head_dim
+    n_ret = min(int(s.budget), L)
+    dev = s.k.device
+    if with_scores:
+        s.scores = torch.empty((n_kv, L - desc.window), dtype=torch.float32, device=dev)
+    s.idx = torch.empty((n_kv, n_ret), dtype=torch.int32, device=dev)
+    s.k_out = torch.empty((n_kv, n_ret, d), dtype=s.k.dtype, device=dev)
+    s.v_out = torch.empty((n_kv, n_ret, d), dtype=s.k.dtype, device=dev)
+    return s
+
+
+def alloc_workspace(desc: ckv_layer_desc, seqs: Sequence[Seq], device) -> torch.Tensor:
+    n = ckv_workspace_bytes(desc, seqs)
+    if n == 0:
+        raise CkvError(CKV_ERR_INVALID_ARG, "ckv_workspace_bytes")
+    return torch.empty(n, dtype=torch.uint8, device=device)

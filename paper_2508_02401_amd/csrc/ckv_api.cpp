@@ -1,0 +1,359 @@
+// C ABI of the CompressKV prefill-end KV eviction path: argument validation,
+// workspace layout, launch sequencing, and the host-side Algorithm 1.
+// Declarations and the contract of every entry point are in include/ckv.h.
+#include "ckv.h"
+
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <string.h>
+
+#include "ckv_internal.h"
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+thread_local hipEvent_t g_ev_begin[4] = {nullptr, nullptr, nullptr, nullptr};
+thread_local hipEvent_t g_ev_end[4] = {nullptr, nullptr, nullptr, nullptr};
+thread_local bool g_events_on = false;
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+int elt_bytes(int dtype) { return dtype == CKV_F32 ? 4 : 2; }
+
+// Per-prompt workspace: chunk partials, row lse, and a score buffer.
+size_t seq_ws_bytes(const ckv_layer_desc* d, const ckv_seq* s) {
+  const int64_t n_chunks = ceil_div(s->seq_len, ckv::kChunk);
+  const int64_t Ls = s->seq_len - d->window;
+  size_t b = align_up((size_t)d->num_kv_heads * n_chunks * ckv::kMaxRows * sizeof(float2));
+  b += align_up((size_t)d->num_kv_heads * ckv::kMaxRows * sizeof(float));
+  b += align_up((size_t)d->num_kv_heads * Ls * sizeof(float));
+  return b;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+int check_desc(const ckv_layer_desc* d) {
+  if (!d) return CKV_ERR_INVALID_ARG;
+  if (d->num_q_heads < 1 || d->num_kv_heads < 1 || d->num_q_heads % d->num_kv_heads)
+    return CKV_ERR_INVALID_ARG;
+  if (d->num_q_heads > CKV_MAX_Q_HEADS || d->num_kv_heads > CKV_MAX_KV_HEADS)
+    return CKV_ERR_UNSUPPORTED;
+  if (d->head_dim != 64 && d->head_dim != 128) return CKV_ERR_UNSUPPORTED;
+  if (d->dtype != CKV_BF16 && d->dtype != CKV_F16 && d->dtype != CKV_F32) return CKV_ERR_UNSUPPORTED;
+  if (d->window < 1) return CKV_ERR_INVALID_ARG;
+  if (d->window > CKV_MAX_WINDOW) return CKV_ERR_UNSUPPORTED;
+  if (d->pool != CKV_POOL_AVG && d->pool != CKV_POOL_MAX) return CKV_ERR_INVALID_ARG;
+  if (d->pool_kernel < 1 || d->pool_kernel % 2 == 0) return CKV_ERR_INVALID_ARG;
+  if (d->pool_kernel > CKV_MAX_POOL_KERNEL) return CKV_ERR_UNSUPPORTED;
+  if (!(d->flags & CKV_KEEP_WINDOW) || (d->flags & ~CKV_KEEP_WINDOW)) return CKV_ERR_UNSUPPORTED;
+  if (!(d->scale > 0.f) && !(d->scale <= 0.f)) return CKV_ERR_INVALID_ARG;  // NaN
+  if (isinf(d->scale)) return CKV_ERR_INVALID_ARG;
+  return CKV_OK;
+}
+
+// What each stage reads/writes of a prompt.
+enum Need : unsigned { kNeedQ = 1, kNeedK = 2, kNeedV = 4, kNeedScores = 8, kNeedIdx = 16, kNeedOut = 32 };
+
+int check_seqs(const ckv_layer_desc* d, const ckv_seq* seqs, int32_t n, unsigned need) {
+  if (!seqs || n < 1) return CKV_ERR_INVALID_ARG;
+  if (n > CKV_MAX_SEQS) return CKV_ERR_UNSUPPORTED;
+  const int64_t eb = elt_bytes(d->dtype);
+  for (int32_t i = 0; i < n; ++i) {
+    const ckv_seq& s = seqs[i];
+    if (s.seq_len <= d->window || s.seq_len >= ((int64_t)1 << 31)) return CKV_ERR_INVALID_ARG;
+    if (s.budget < d->window) return CKV_ERR_BUDGET;
+    if ((need & kNeedQ) && (!s.q_win || !aligned16(s.q_win))) return CKV_ERR_INVALID_ARG;
+    if (need & kNeedQ) {
+      if (s.q_stride_head < 0 || s.q_stride_row < 0) return CKV_ERR_INVALID_ARG;
+      if ((s.q_stride_head * eb) % 16 || (s.q_stride_row * eb) % 16) return CKV_ERR_INVALID_ARG;
+      if (d->window > 1 && s.q_stride_row < d->head_dim) return CKV_ERR_INVALID_ARG;
+    }
+    if ((need & kNeedK) && (!s.k || !aligned16(s.k))) return CKV_ERR_INVALID_ARG;
+    if ((need & kNeedV) && (!s.v || !aligned16(s.v))) return CKV_ERR_INVALID_ARG;
+    if (need & (kNeedK | kNeedV)) {
+      if (s.kv_stride_tok < d->head_dim || s.kv_stride_head < 0) return CKV_ERR_INVALID_ARG;
+      if ((s.kv_stride_head * eb) % 16 || (s.kv_stride_tok * eb) % 16) return CKV_ERR_INVALID_ARG;
+    }
+    if ((need & kNeedScores) && (!s.scores || !aligned16(s.scores))) return CKV_ERR_INVALID_ARG;
+    if ((need & kNeedIdx) && !s.idx) return CKV_ERR_INVALID_ARG;
+    if ((need & kNeedOut) && (!s.k_out || !s.v_out || !aligned16(s.k_out) || !aligned16(s.v_out)))
+      return CKV_ERR_INVALID_ARG;
+  }
+  return CKV_OK;
+}
+
+// Fill the kernel argument block; workspace pointers are carved per prompt.
+int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs, int32_t n,
+               char* ws, bool scores_from_ws, ckv::LayerArgs& a) {
+  memset(&a, 0, sizeof(a));
+  a.num_seqs = n;
+  a.n_kv = d->num_kv_heads;
+  a.d = d->head_dim;
+  a.w = d->window;
+  a.w8 = (d->window + 7) / 8 * 8;
+  const float scale = d->scale > 0.f ? d->scale : 1.0f / sqrtf((float)d->head_dim);
+  a.alpha = (float)((double)scale * 1.4426950408889634);  // log2(e)
+  a.pool = d->pool;
+  a.kp = d->pool_kernel;
+  if (mask) {
+    const int G = d->num_q_heads / d->num_kv_heads;
+    const int max_rows = d->dtype == CKV_F32 ? ckv::kMaxRowsF32 : ckv::kMaxRows;
+    int off = 0;
+    a.max_sel = 0;
+    for (int g = 0; g < d->num_kv_heads; ++g) {
+      a.grp_off[g] = (int16_t)off;
+      int cnt = 0;
+      for (int t = 0; t < G; ++t) {
+        const int h = g * G + t;
+        if (mask[h]) {
+          a.sel[off++] = (uint8_t)h;
+          ++cnt;
+        }
+      }
+      if (cnt == 0) return CKV_ERR_MASK;
+      if (cnt * a.w8 > max_rows) return CKV_ERR_UNSUPPORTED;
+      if (cnt > a.max_sel) a.max_sel = cnt;
+    }
+    a.grp_off[d->num_kv_heads] = (int16_t)off;
+  }
+  int32_t blk_rows = 0, blk_score = 0, blk_gather = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    const ckv_seq& s = seqs[i];
+    ckv::SeqArgs& q = a.seq[i];
+    q.q = s.q_win;
+    q.k = s.k;
+    q.v = s.v;
+    q.q_sh = s.q_stride_head;
+    q.q_sr = s.q_stride_row;
+    q.kv_sh = s.kv_stride_head;
+    q.kv_st = s.kv_stride_tok;
+    q.L = s.seq_len;
+    q.n_ret = (int32_t)(s.budget < s.seq_len ? s.budget : s.seq_len);
+    q.n_keep = s.budget >= s.seq_len ? -1 : s.budget - d->window;
+    q.scores = s.scores;
+    q.idx = s.idx;
+    q.k_out = s.k_out;
+    q.v_out = s.v_out;
+    q.n_chunks = (int32_t)ceil_div(s.seq_len, ckv::kChunk);
+    q.n_tiles = (int32_t)ceil_div(s.seq_len - d->window, ckv::kTileOut);
+    q.n_gblk = (int32_t)ceil_div(q.n_ret, ckv::kGatherRows);
+    q.blk_rows = blk_rows;
+    q.blk_score = blk_score;
+    q.blk_gather = blk_gather;
+    blk_rows += q.n_chunks * d->num_kv_heads;
+    blk_score += q.n_tiles * d->num_kv_heads;
+    blk_gather += q.n_gblk * d->num_kv_heads;
+    if (ws) {
+      char* p = ws;
+      q.partial = reinterpret_cast<float2*>(p);
+      p += align_up((size_t)d->num_kv_heads * q.n_chunks * ckv::kMaxRows * sizeof(float2));
+      q.lse = reinterpret_cast<float*>(p);
+      p += align_up((size_t)d->num_kv_heads * ckv::kMaxRows * sizeof(float));
+      if (scores_from_ws && !q.scores) q.scores = reinterpret_cast<float*>(p);
+      ws += seq_ws_bytes(d, &s);
+    }
+  }
+  return CKV_OK;
+}
+
+int grid_rows(const ckv::LayerArgs& a) {
+  const ckv::SeqArgs& q = a.seq[a.num_seqs - 1];
+  return q.blk_rows + q.n_chunks * a.n_kv;
+}
+int grid_score(const ckv::LayerArgs& a) {
+  const ckv::SeqArgs& q = a.seq[a.num_seqs - 1];
+  return q.blk_score + q.n_tiles * a.n_kv;
+}
+int grid_gather(const ckv::LayerArgs& a) {
+  const ckv::SeqArgs& q = a.seq[a.num_seqs - 1];
+  return q.blk_gather + q.n_gblk * a.n_kv;
+}
+
+int hip_fail(hipError_t e) {
+  g_last_hip_error = (int)e;
+  return CKV_ERR_HIP;
+}
+
+void ev_begin(int stage, hipStream_t st) {
+  if (g_events_on && g_ev_begin[stage]) (void)hipEventRecord(g_ev_begin[stage], st);
+}
+void ev_end(int stage, hipStream_t st) {
+  if (g_events_on && g_ev_end[stage]) (void)hipEventRecord(g_ev_end[stage], st);
+}
+
+int run_score(const ckv_layer_desc* d, const ckv::LayerArgs& a, hipStream_t st) {
+  hipError_t e;
+  ev_begin(ckv::kStageRowStats, st);
+  if ((e = ckv::launch_rowstats(d->dtype, a, grid_rows(a), st)) != hipSuccess) return hip_fail(e);
+  ev_end(ckv::kStageRowStats, st);
+  if ((e = ckv::launch_lse(a, a.num_seqs * a.n_kv, st)) != hipSuccess) return hip_fail(e);
+  ev_begin(ckv::kStageScore, st);
+  if ((e = ckv::launch_score(d->dtype, a, grid_score(a), st)) != hipSuccess) return hip_fail(e);
+  ev_end(ckv::kStageScore, st);
+  return CKV_OK;
+}
+
+int run_select(const ckv::LayerArgs& a, hipStream_t st) {
+  ev_begin(ckv::kStageSelect, st);
+  const hipError_t e = ckv::launch_select(a, a.num_seqs * a.n_kv, st);
+  if (e != hipSuccess) return hip_fail(e);
+  ev_end(ckv::kStageSelect, st);
+  return CKV_OK;
+}
+
+int run_gather(const ckv_layer_desc* d, const ckv::LayerArgs& a, hipStream_t st) {
+  ev_begin(ckv::kStageGather, st);
+  const hipError_t e = ckv::launch_gather(d->dtype, a, grid_gather(a), st);
+  if (e != hipSuccess) return hip_fail(e);
+  ev_end(ckv::kStageGather, st);
+  return CKV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t ckv_workspace_bytes(const ckv_layer_desc* desc, const ckv_seq* seqs, int32_t num_seqs) {
+  if (check_desc(desc) != CKV_OK || !seqs || num_seqs < 1 || num_seqs > CKV_MAX_SEQS) return 0;
+  size_t total = 0;
+  for (int32_t i = 0; i < num_seqs; ++i) {
+    if (seqs[i].seq_len <= desc->window || seqs[i].seq_len >= ((int64_t)1 << 31)) return 0;
+    total += seq_ws_bytes(desc, &seqs[i]);
+  }
+  return total;
+}
+
+int ckv_score(const ckv_layer_desc* desc, const uint8_t* head_mask, const ckv_seq* seqs,
+              int32_t num_seqs, void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_desc(desc);
+  if (rc != CKV_OK) return rc;
+  if (!head_mask) return CKV_ERR_INVALID_ARG;
+  if ((rc = check_seqs(desc, seqs, num_seqs, kNeedQ | kNeedK | kNeedScores)) != CKV_OK) return rc;
+  if (!workspace || workspace_bytes < ckv_workspace_bytes(desc, seqs, num_seqs) ||
+      !aligned16(workspace))
+    return CKV_ERR_WORKSPACE;
+  ckv::LayerArgs a;
+  if ((rc = build_args(desc, head_mask, seqs, num_seqs, (char*)workspace, false, a)) != CKV_OK)
+    return rc;
+  return run_score(desc, a, (hipStream_t)stream);
+}
+
+int ckv_select(const ckv_layer_desc* desc, const ckv_seq* seqs, int32_t num_seqs, void* workspace,
+               size_t workspace_bytes, void* stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  int rc = check_desc(desc);
+  if (rc != CKV_OK) return rc;
+  if ((rc = check_seqs(desc, seqs, num_seqs, kNeedScores | kNeedIdx)) != CKV_OK) return rc;
+  ckv::LayerArgs a;
+  if ((rc = build_args(desc, nullptr, seqs, num_seqs, nullptr, false, a)) != CKV_OK) return rc;
+  return run_select(a, (hipStream_t)stream);
+}
+
+int ckv_gather(const ckv_layer_desc* desc, const ckv_seq* seqs, int32_t num_seqs, void* stream) {
+  int rc = check_desc(desc);
+  if (rc != CKV_OK) return rc;
+  if ((rc = check_seqs(desc, seqs, num_seqs, kNeedK | kNeedV | kNeedIdx | kNeedOut)) != CKV_OK)
+    return rc;
+  ckv::LayerArgs a;
+  if ((rc = build_args(desc, nullptr, seqs, num_seqs, nullptr, false, a)) != CKV_OK) return rc;
+  return run_gather(desc, a, (hipStream_t)stream);
+}
+
+int ckv_compress_layer(const ckv_layer_desc* desc, const uint8_t* head_mask, const ckv_seq* seqs,
+                       int32_t num_seqs, void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_desc(desc);
+  if (rc != CKV_OK) return rc;
+  if (!head_mask) return CKV_ERR_INVALID_ARG;
+  if ((rc = check_seqs(desc, seqs, num_seqs, kNeedQ | kNeedK | kNeedV | kNeedIdx | kNeedOut)) !=
+      CKV_OK)
+    return rc;
+  for (int32_t i = 0; i < num_seqs; ++i)
+    if (seqs[i].scores && !aligned16(seqs[i].scores)) return CKV_ERR_INVALID_ARG;
+  if (!workspace || workspace_bytes < ckv_workspace_bytes(desc, seqs, num_seqs) ||
+      !aligned16(workspace))
+    return CKV_ERR_WORKSPACE;
+  ckv::LayerArgs a;
+  if ((rc = build_args(desc, head_mask, seqs, num_seqs, (char*)workspace, true, a)) != CKV_OK)
+    return rc;
+  const hipStream_t st = (hipStream_t)stream;
+  if ((rc = run_score(desc, a, st)) != CKV_OK) return rc;
+  if ((rc = run_select(a, st)) != CKV_OK) return rc;
+  return run_gather(desc, a, st);
+}
+
+int ckv_allocate_budgets(const double* err_norm, int32_t n_layers, int64_t total, int32_t m,
+                         int32_t M, int32_t* out) {
+  if (!err_norm || !out || n_layers < 1 || m < 0 || M < m) return CKV_ERR_INVALID_ARG;
+  for (int32_t i = 0; i < n_layers; ++i)
+    if (!isfinite(err_norm[i])) return CKV_ERR_INVALID_ARG;
+  // Every layer starts at the floor m; the remainder R is shared in
+  // proportion to the errors, rounded half to even, and clipped to [m, M].
+  int64_t sum = (int64_t)m * n_layers;
+  const int64_t R = total - sum;
+  sum = 0;
+  for (int32_t i = 0; i < n_layers; ++i) {
+    const int64_t v = (int64_t)m + (int64_t)nearbyint(err_norm[i] * (double)R);
+    out[i] = (int32_t)(v < m ? m : (v > M ? M : v));
+    sum += out[i];
+  }
+  // Then single tokens move to the highest-error layer with room (surplus) or
+  // leave the lowest-error layer above the floor (deficit); lowest index on ties.
+  int64_t delta = total - sum;
+  while (delta != 0) {
+    int32_t j = -1;
+    if (delta > 0) {
+      for (int32_t i = 0; i < n_layers; ++i)
+        if (out[i] < M && (j < 0 || err_norm[i] > err_norm[j])) j = i;
+      if (j < 0) break;
+      // the errors do not change, so the same layer keeps winning until it
+      // reaches M: move that many tokens at once
+      const int64_t step = delta < (int64_t)(M - out[j]) ? delta : (int64_t)(M - out[j]);
+      out[j] += (int32_t)step;
+      delta -= step;
+    } else {
+      for (int32_t i = 0; i < n_layers; ++i)
+        if (out[i] > m && (j < 0 || err_norm[i] < err_norm[j])) j = i;
+      if (j < 0) break;
+      // likewise the same layer keeps losing until it reaches m
+      const int64_t step = -delta < (int64_t)(out[j] - m) ? -delta : (int64_t)(out[j] - m);
+      out[j] -= (int32_t)step;
+      delta += step;
+    }
+  }
+  return delta == 0 ? CKV_OK : CKV_ERR_BUDGET;
+}
+
+const char* ckv_status_string(int status) {
+  switch (status) {
+    case CKV_OK: return "ok";
+    case CKV_ERR_INVALID_ARG: return "invalid argument";
+    case CKV_ERR_UNSUPPORTED: return "unsupported configuration";
+    case CKV_ERR_BUDGET: return "budget below the window or allocation infeasible";
+    case CKV_ERR_MASK: return "a KV group has no chosen query head";
+    case CKV_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case CKV_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+int ckv_last_hip_error(void) { return g_last_hip_error; }
+
+int ckv_set_stage_events(void* const* begin, void* const* end) {
+  if (!begin || !end) {
+    g_events_on = false;
+    for (int i = 0; i < 4; ++i) g_ev_begin[i] = g_ev_end[i] = nullptr;
+    return CKV_OK;
+  }
+  for (int i = 0; i < 4; ++i) {
+    g_ev_begin[i] = (hipEvent_t)begin[i];
+    g_ev_end[i] = (hipEvent_t)end[i];
+  }
+  g_events_on = true;
+  return CKV_OK;
+}
+
+}  // extern "C"

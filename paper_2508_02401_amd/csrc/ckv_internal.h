@@ -1,0 +1,70 @@
+// Internal launch interface between the C ABI layer (ckv_api.cpp) and the
+// gfx950 kernels (ckv_kernels.hip). Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ckv {
+
+constexpr int kMaxSeqs = 16;
+constexpr int kMaxQHeads = 128;
+constexpr int kMaxKvHeads = 64;
+constexpr int kMaxRows = 128;      // chosen-head rows per group after padding each head to 8
+constexpr int kMaxRowsF32 = 64;    // the fp32 kernels keep half as many query rows in registers
+constexpr int kChunk = 1024;       // tokens per row-statistics workgroup
+constexpr int kTileComp = 1024;    // tokens whose logits one scoring workgroup computes
+constexpr int kHalo = 16;          // pooling halo on each side (pool kernel <= 2*16+1)
+constexpr int kTileOut = kTileComp - 2 * kHalo;  // scores one scoring workgroup writes
+constexpr int kGatherRows = 64;    // retained rows per gather workgroup
+
+enum Stage { kStageRowStats = 0, kStageScore = 1, kStageSelect = 2, kStageGather = 3 };
+
+// One prompt of the batch, in the form the kernels read.
+struct SeqArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  int64_t q_sh, q_sr;      // elements
+  int64_t kv_sh, kv_st;    // elements
+  int64_t L;
+  int32_t n_ret;           // min(B, L)
+  int32_t n_keep;          // B - w prefix tokens kept, or -1 when B >= L (keep all)
+  float* scores;           // [n_kv][L - w]
+  int32_t* idx;            // [n_kv][n_ret]
+  void* k_out;             // [n_kv][n_ret][d]
+  void* v_out;
+  float2* partial;         // workspace [n_kv][n_chunks][kMaxRows]: (max logit, sum exp2) per chunk
+  float* lse;              // workspace [n_kv][kMaxRows]: per-row log2-sum-exp2 in exp2 units
+  int32_t n_chunks;        // ceil(L / kChunk)
+  int32_t n_tiles;         // ceil((L - w) / kTileOut)
+  int32_t blk_rows;        // first workgroup of this prompt in the row-statistics grid
+  int32_t blk_score;       // ... in the scoring grid
+  int32_t blk_gather;      // ... in the gather grid
+  int32_t n_gblk;          // gather workgroups per KV head
+};
+
+// One layer call.
+struct LayerArgs {
+  int32_t num_seqs;
+  int32_t n_kv;
+  int32_t d;
+  int32_t w;
+  int32_t w8;              // w rounded up to a multiple of 8: rows reserved per chosen head
+  float alpha;             // logit scale * log2(e): exp(scale*s) == exp2(alpha*s)
+  int32_t pool;            // 0 average, 1 max
+  int32_t kp;              // odd pool kernel
+  int32_t max_sel;         // largest number of chosen heads in any group
+  int16_t grp_off[kMaxKvHeads + 1];  // chosen heads of group g: sel[grp_off[g] .. grp_off[g+1])
+  uint8_t sel[kMaxQHeads];
+  SeqArgs seq[kMaxSeqs];
+};
+
+// dtype codes match ckv_dtype.
+hipError_t launch_rowstats(int dtype, const LayerArgs& a, int grid, hipStream_t st);
+hipError_t launch_lse(const LayerArgs& a, int grid, hipStream_t st);
+hipError_t launch_score(int dtype, const LayerArgs& a, int grid, hipStream_t st);
+hipError_t launch_select(const LayerArgs& a, int grid, hipStream_t st);
+hipError_t launch_gather(int dtype, const LayerArgs& a, int grid, hipStream_t st);
+
+}  // namespace ckv

@@ -1,0 +1,240 @@
+"""Host-side checks of libckv.so that need no GPU: it loads, exports every
+symbol include/ckv.h declares, rejects bad arguments before launching
+anything, and its Algorithm 1 agrees with the oracle's."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2508_02401_amd as ckv
+from paper_2508_02401_amd import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    text = open(os.path.join(ROOT, "include", "ckv.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ckv_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(ckv.LIB_PATH)
+    names = _declared_functions()
+    assert set(names) == set(ckv.EXPORTED)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings():
+    for code in (0, -1, -2, -3, -4, -5, -6):
+        assert ckv.ckv_status_string(code) != "unknown status"
+    assert ckv.ckv_status_string(-99) == "unknown status"
+
+
+# Fake device buffers: validation only looks at null/alignment, and every
+# case below must fail before any HIP call.
+_BUF = np.zeros(1 << 16, dtype=np.uint8)
+_BASE = (_BUF.ctypes.data + 255) & ~255
+
+
+def _desc(**kw):
+    base = dict(num_q_heads=8, num_kv_heads=2, head_dim=64, window=4, dtype=ckv.CKV_BF16,
+                scale=0.0, pool=ckv.CKV_POOL_MAX, pool_kernel=7, flags=ckv.CKV_KEEP_WINDOW)
+    base.update(kw)
+    d = ckv._binding.ckv_layer_desc()
+    for k, v in base.items():
+        setattr(d, k, v)
+    return d
+
+
+def _seq(**kw):
+    s = ckv._binding.ckv_seq()
+    vals = dict(q_win=_BASE, q_stride_head=4 * 64, q_stride_row=64, k=_BASE + 4096,
+                v=_BASE + 8192, kv_stride_head=100 * 64, kv_stride_tok=64, seq_len=100, budget=16,
+                scores=_BASE + 12288, idx=_BASE + 16384, k_out=_BASE + 20480,
+                v_out=_BASE + 24576)
+    vals.update(kw)
+    for k, v in vals.items():
+        setattr(s, k, v)
+    return s
+
+
+def _call(fn, desc, seq, mask=None, ws=True, n=1):
+    lib = ckv.load()
+    arr = (ckv._binding.ckv_seq * n)(*([seq] * n))
+    ws_ptr = _BASE + 32768 if ws else None
+    ws_n = 1 << 40 if ws else 0
+    if fn == "score" or fn == "compress":
+        m = np.ones(desc.num_q_heads, np.uint8) if mask is None else np.asarray(mask, np.uint8)
+        mm = (ctypes.c_uint8 * m.size)(*m.tolist())
+        f = lib.ckv_score if fn == "score" else lib.ckv_compress_layer
+        return f(ctypes.byref(desc), mm, arr, n, ws_ptr, ws_n, None)
+    if fn == "select":
+        return lib.ckv_select(ctypes.byref(desc), arr, n, ws_ptr, ws_n, None)
+    return lib.ckv_gather(ctypes.byref(desc), arr, n, None)
+
+
+@pytest.mark.parametrize("fn", ["score", "compress", "select", "gather"])
+@pytest.mark.parametrize("bad,expect", [
+    (dict(pool_kernel=4), ckv.CKV_ERR_INVALID_ARG),
+    (dict(pool_kernel=0), ckv.CKV_ERR_INVALID_ARG),
+    (dict(pool_kernel=33), ckv.CKV_ERR_UNSUPPORTED),
+    (dict(pool=5), ckv.CKV_ERR_INVALID_ARG),
+    (dict(head_dim=96), ckv.CKV_ERR_UNSUPPORTED),
+    (dict(dtype=7), ckv.CKV_ERR_UNSUPPORTED),
+    (dict(num_q_heads=7), ckv.CKV_ERR_INVALID_ARG),
+    (dict(window=0), ckv.CKV_ERR_INVALID_ARG),
+    (dict(window=129), ckv.CKV_ERR_UNSUPPORTED),
+    (dict(flags=0), ckv.CKV_ERR_UNSUPPORTED),
+    (dict(scale=float("nan")), ckv.CKV_ERR_INVALID_ARG),
+])
+def test_bad_descriptor(fn, bad, expect):
+    assert _call(fn, _desc(**bad), _seq()) == expect
+
+
+@pytest.mark.parametrize("fn", ["score", "compress", "select", "gather"])
+@pytest.mark.parametrize("bad,expect", [
+    (dict(budget=3), ckv.CKV_ERR_BUDGET),          # below the window of 4
+    (dict(seq_len=4), ckv.CKV_ERR_INVALID_ARG),    # L must exceed w
+    (dict(seq_len=1 << 31), ckv.CKV_ERR_INVALID_ARG),
+])
+def test_bad_sequence(fn, bad, expect):
+    assert _call(fn, _desc(), _seq(**bad)) == expect
+
+
+@pytest.mark.parametrize("fn,field", [
+    ("score", "q_win"), ("score", "k"), ("score", "scores"), ("compress", "v"),
+    ("compress", "idx"), ("compress", "k_out"), ("select", "scores"), ("select", "idx"),
+    ("gather", "k"), ("gather", "v_out"), ("gather", "idx"),
+])
+def test_null_pointer(fn, field):
+    assert _call(fn, _desc(), _seq(**{field: None})) == ckv.CKV_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("field", ["q_win", "k", "scores"])
+def test_misaligned_pointer(field):
+    s = _seq()
+    assert _call("score", _desc(), _seq(**{field: getattr(s, field) + 2})) == ckv.CKV_ERR_INVALID_ARG
+
+
+def test_misaligned_stride():
+    assert _call("score", _desc(), _seq(kv_stride_tok=65)) == ckv.CKV_ERR_INVALID_ARG
+    assert _call("score", _desc(), _seq(q_stride_row=63)) == ckv.CKV_ERR_INVALID_ARG
+
+
+def test_group_without_chosen_head():
+    mask = [1, 0, 0, 0, 0, 0, 0, 0]  # group 1 (heads 4..7) has none
+    assert _call("score", _desc(), _seq(), mask=mask) == ckv.CKV_ERR_MASK
+    assert _call("compress", _desc(), _seq(), mask=mask) == ckv.CKV_ERR_MASK
+
+
+def test_too_many_rows_per_group():
+    # 4 chosen heads x window 64 = 256 rows > 128
+    d = _desc(window=64)
+    assert _call("score", d, _seq(budget=64, seq_len=1000), mask=[1] * 8) == ckv.CKV_ERR_UNSUPPORTED
+
+
+def test_missing_or_small_workspace():
+    assert _call("score", _desc(), _seq(), ws=False) == ckv.CKV_ERR_WORKSPACE
+    lib = ckv.load()
+    d, s = _desc(), _seq()
+    arr = (ckv._binding.ckv_seq * 1)(s)
+    need = lib.ckv_workspace_bytes(ctypes.byref(d), arr, 1)
+    assert need > 0
+    m = (ctypes.c_uint8 * 8)(*([1] * 8))
+    rc = lib.ckv_score(ctypes.byref(d), m, arr, 1, _BASE + 32768, need - 1, None)
+    assert rc == ckv.CKV_ERR_WORKSPACE
+
+
+def test_too_many_sequences():
+    assert _call("select", _desc(), _seq(), n=17) == ckv.CKV_ERR_UNSUPPORTED
+
+
+def test_workspace_bytes_grows_with_length():
+    lib = ckv.load()
+    d = _desc()
+    a = (ckv._binding.ckv_seq * 1)(_seq(seq_len=1000))
+    b = (ckv._binding.ckv_seq * 1)(_seq(seq_len=100000))
+    assert 0 < lib.ckv_workspace_bytes(ctypes.byref(d), a, 1) < lib.ckv_workspace_bytes(
+        ctypes.byref(d), b, 1)
+    bad = (ckv._binding.ckv_seq * 1)(_seq(seq_len=2))
+    assert lib.ckv_workspace_bytes(ctypes.byref(d), bad, 1) == 0
+
+
+# ---------------------------------------------------------------------------
+# Algorithm 1: the library's host implementation against the oracle's.
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("seed", range(200))
+def test_allocate_budgets_matches_oracle(seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 64))
+    e = rng.dirichlet(np.ones(n) * float(rng.choice([0.05, 0.5, 1.0, 20.0])))
+    if seed % 7 == 0:
+        e = np.round(e, 2)  # exact ties and half-way shares
+    per = int(rng.integers(8, 3000))
+    m = int(rng.integers(0, per + 1))
+    M = int(rng.integers(per, 4 * per))
+    total = int(n * per + rng.integers(-3 * per, 3 * per))
+    got, st = ckv.ckv_allocate_budgets(e, total, m, M)
+    ref, rst = oracle.allocate_budgets(e, total, m, M)
+    assert got.tolist() == ref.tolist()
+    assert (st == ckv.CKV_OK) == (rst == oracle.OK)
+
+
+def test_allocate_budgets_workload_parameters():
+    for name in ("llama8b-32k-stack", "llama8b-128k-stack", "qwen7b-ragged-batch"):
+        wl = synth.WORKLOADS[name]
+        e = synth.layer_errors(wl)
+        for L in wl.seq_lens:
+            total, m, M = synth.budget_params(wl, L)
+            got, st = ckv.ckv_allocate_budgets(e, total, m, M)
+            assert st == ckv.CKV_OK
+            assert got.sum() == total and got.min() >= max(m, wl.window) and got.max() <= M
+
+
+def test_allocate_budgets_rejects_bad_input():
+    with pytest.raises(ckv.CkvError):
+        ckv.ckv_allocate_budgets([0.5, float("nan")], 100, 10, 60)
+    with pytest.raises(ckv.CkvError):
+        ckv.ckv_allocate_budgets([0.5, 0.5], 100, 60, 10)
+
+
+# ---------------------------------------------------------------------------
+# Synthetic workloads: deterministic, shaped as documented.
+# ---------------------------------------------------------------------------
+def test_synth_mask_and_planting():
+    wl = synth.WORKLOADS["llama8b-32k-stack"]
+    G = wl.num_q_heads // wl.num_kv_heads
+    for layer in range(4):
+        m = synth.head_mask(wl, layer)
+        per = m.reshape(wl.num_kv_heads, G).sum(axis=1)
+        assert set(per.tolist()) <= set(wl.n_sel_choices)
+        np.testing.assert_array_equal(m, synth.head_mask(wl, layer))
+        pos = synth.planted_positions(wl, layer, 0, 32768)
+        assert len(pos) == wl.sinks + wl.n_spans * wl.span_len
+        assert len(np.unique(pos)) == len(pos)
+        assert pos.max() < 32768 - wl.window
+
+
+def test_synth_tiny_inputs_on_cpu():
+    wl = synth.WORKLOADS["tiny-fp32"]
+    a = synth.layer_inputs(wl, 0, "cpu")
+    b = synth.layer_inputs(wl, 0, "cpu")
+    assert a.q_win[0].shape == (8, 16, 64) and a.k[0].shape == (2, 1024, 64)
+    assert torch.equal(a.k[0], b.k[0]) and torch.equal(a.q_win[0], b.q_win[0])
+    # planted keys raise the mean scaled logit of a group's chosen rows by 3
+    G = 4
+    q = a.q_win[0].double()
+    planted = a.planted[0]
+    others = np.setdiff1d(np.arange(1024 - 16), planted)
+    for g in range(2):
+        chosen = [g * G + t for t in range(G) if a.mask[g * G + t]]
+        qbar = q[chosen].reshape(-1, 64).mean(0)
+        logit = (a.k[0][g].double() @ qbar) / 8.0
+        assert 2.5 < float(logit[planted].mean()) < 3.5
+        assert abs(float(logit[others].mean())) < 0.5

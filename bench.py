@@ -1,7 +1,8 @@
 """Benchmark of the CompressKV prefill-end KV eviction path on one MI355X.
 
 One step = the whole path (score, select, gather) over every layer of the
-workload, one ckv_compress_layer call per layer on one stream, with all inputs
+workload, one ckv_compress_layer call per layer (layers round-robin over a few
+streams, since they are independent), with all inputs
 already resident in HBM. Prints one JSON line.
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
@@ -37,6 +38,8 @@ def parse():
     p.add_argument("--layers", type=int, default=0, help="limit the layer count (0 = all)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-threads", type=int, default=0)
+    p.add_argument("--streams", type=int, default=2,
+                   help="layers are issued round-robin on this many streams (one workspace each)")
     return p.parse_args()
 
 
@@ -112,18 +115,25 @@ def main():
                 for s in range(len(wl.seq_lens))]
         layers.append((inp.mask, seqs))
     ws_bytes = max(ckv.ckv_workspace_bytes(desc, seqs) for _, seqs in layers)
-    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    n_streams = max(1, args.streams)
+    main = torch.cuda.current_stream()
+    streams = [main] + [torch.cuda.Stream() for _ in range(n_streams - 1)]
+    wss = [torch.empty(ws_bytes, dtype=torch.uint8, device=dev) for _ in range(n_streams)]
     torch.cuda.synchronize()
 
-    stream = torch.cuda.current_stream()
-
     def step(events=None):
+        # every layer is independent: layer l runs on stream l % n_streams
+        for st in streams[1:]:
+            st.wait_stream(main)
         for li, (mask, seqs) in enumerate(layers):
+            si = li % n_streams
             if events is not None:
                 ckv.ckv_set_stage_events(events[li][0], events[li][1])
-            ckv.ckv_compress_layer(desc, mask, seqs, ws, stream)
+            ckv.ckv_compress_layer(desc, mask, seqs, wss[si], streams[si])
         if events is not None:
             ckv.ckv_set_stage_events(None, None)
+        for st in streams[1:]:
+            main.wait_stream(st)
 
     for _ in range(args.warmup):
         step()
@@ -136,10 +146,10 @@ def main():
     t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
-    t_start.record(stream)
+    t_start.record(main)
     for k in range(args.steps):
         step(ev[k])
-    t_end.record(stream)
+    t_end.record(main)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     ms_total = t_start.elapsed_time(t_end)
@@ -216,7 +226,8 @@ def main():
                    "kv_heads": n_kv, "head_dim": d, "seq_lens": list(wl.seq_lens),
                    "window": w, "pool": "max" if wl.pool == 1 else "avg",
                    "pool_kernel": wl.pool_kernel, "heads_per_group": list(wl.n_sel_choices),
-                   "budget_avg": float(np.mean(budgets)), "parallelism": "single GPU"},
+                   "budget_avg": float(np.mean(budgets)), "parallelism": "single GPU",
+                   "streams": n_streams},
         "path_hbm_gbs": path_gbs,
         "path_hbm_frac": path_gbs / HBM_PEAK_GBS,
         "stage_ms_avg": stage_avg,

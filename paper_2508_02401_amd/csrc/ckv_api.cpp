@@ -23,15 +23,40 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 int elt_bytes(int dtype) { return dtype == CKV_F32 ? 4 : 2; }
 
-// Per-prompt workspace: chunk partials, row lse, and a score buffer.
-size_t seq_ws_bytes(const ckv_layer_desc* d, const ckv_seq* s) {
+// Scores per selection range: at least kRangeMin, and few enough ranges for
+// the resolve step to count them in LDS.
+int64_t range_size(int64_t Ls) {
+  const int64_t per = ceil_div(Ls, ckv::kMaxRanges);
+  return per <= ckv::kRangeMin ? ckv::kRangeMin : ceil_div(per, ckv::kRangeMin) * ckv::kRangeMin;
+}
+
+// Per-prompt workspace, in order: chunk partials, row lse, scores, selection
+// control words, histograms, candidates, per-range counts/offsets.
+struct WsLayout {
+  size_t partial, lse, scores, ctl, hist, cand, rsure, roff, reqb, total;
+};
+
+WsLayout seq_ws_layout(const ckv_layer_desc* d, const ckv_seq* s) {
+  const int64_t n_kv = d->num_kv_heads;
   const int64_t n_chunks = ceil_div(s->seq_len, ckv::kChunk);
   const int64_t Ls = s->seq_len - d->window;
-  size_t b = align_up((size_t)d->num_kv_heads * n_chunks * ckv::kMaxRows * sizeof(float2));
-  b += align_up((size_t)d->num_kv_heads * ckv::kMaxRows * sizeof(float));
-  b += align_up((size_t)d->num_kv_heads * Ls * sizeof(float));
-  return b;
+  const int64_t n_ranges = ceil_div(Ls, range_size(Ls));
+  WsLayout w;
+  size_t o = 0;
+  w.partial = o; o += align_up((size_t)n_kv * n_chunks * ckv::kMaxRows * sizeof(float2));
+  w.lse = o;     o += align_up((size_t)n_kv * ckv::kMaxRows * sizeof(float));
+  w.scores = o;  o += align_up((size_t)n_kv * Ls * sizeof(float));
+  w.ctl = o;     o += align_up((size_t)n_kv * ckv::kCtlWords * sizeof(uint32_t));
+  w.hist = o;    o += align_up((size_t)n_kv * ckv::kHistBins * sizeof(uint32_t));
+  w.cand = o;    o += align_up((size_t)n_kv * Ls * sizeof(uint2));
+  w.rsure = o;   o += align_up((size_t)n_kv * n_ranges * sizeof(uint32_t));
+  w.roff = o;    o += align_up((size_t)n_kv * n_ranges * sizeof(uint32_t));
+  w.reqb = o;    o += align_up((size_t)n_kv * n_ranges * sizeof(uint32_t));
+  w.total = o;
+  return w;
 }
+
+size_t seq_ws_bytes(const ckv_layer_desc* d, const ckv_seq* s) { return seq_ws_layout(d, s).total; }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
@@ -119,10 +144,12 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
     }
     a.grp_off[d->num_kv_heads] = (int16_t)off;
   }
-  int32_t blk_rows = 0, blk_score = 0, blk_gather = 0;
+  a.elt = elt_bytes(d->dtype);
+  int32_t blk_rows = 0, blk_score = 0, blk_sel = 0, blk_gather = 0;
   for (int32_t i = 0; i < n; ++i) {
     const ckv_seq& s = seqs[i];
     ckv::SeqArgs& q = a.seq[i];
+    const int64_t Ls = s.seq_len - d->window;
     q.q = s.q_win;
     q.k = s.k;
     q.v = s.v;
@@ -138,22 +165,30 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
     q.k_out = s.k_out;
     q.v_out = s.v_out;
     q.n_chunks = (int32_t)ceil_div(s.seq_len, ckv::kChunk);
-    q.n_tiles = (int32_t)ceil_div(s.seq_len - d->window, ckv::kTileOut);
+    q.n_tiles = (int32_t)ceil_div(Ls, ckv::kTileOut);
+    q.range = (int32_t)range_size(Ls);
+    q.n_ranges = (int32_t)ceil_div(Ls, q.range);
     q.n_gblk = (int32_t)ceil_div(q.n_ret, ckv::kGatherRows);
     q.blk_rows = blk_rows;
     q.blk_score = blk_score;
+    q.blk_sel = blk_sel;
     q.blk_gather = blk_gather;
     blk_rows += q.n_chunks * d->num_kv_heads;
     blk_score += q.n_tiles * d->num_kv_heads;
+    blk_sel += q.n_ranges * d->num_kv_heads;
     blk_gather += q.n_gblk * d->num_kv_heads;
     if (ws) {
-      char* p = ws;
-      q.partial = reinterpret_cast<float2*>(p);
-      p += align_up((size_t)d->num_kv_heads * q.n_chunks * ckv::kMaxRows * sizeof(float2));
-      q.lse = reinterpret_cast<float*>(p);
-      p += align_up((size_t)d->num_kv_heads * ckv::kMaxRows * sizeof(float));
-      if (scores_from_ws && !q.scores) q.scores = reinterpret_cast<float*>(p);
-      ws += seq_ws_bytes(d, &s);
+      const WsLayout l = seq_ws_layout(d, &s);
+      q.partial = reinterpret_cast<float2*>(ws + l.partial);
+      q.lse = reinterpret_cast<float*>(ws + l.lse);
+      if (scores_from_ws && !q.scores) q.scores = reinterpret_cast<float*>(ws + l.scores);
+      q.ctl = reinterpret_cast<uint32_t*>(ws + l.ctl);
+      q.hist = reinterpret_cast<uint32_t*>(ws + l.hist);
+      q.cand = reinterpret_cast<uint2*>(ws + l.cand);
+      q.rsure = reinterpret_cast<uint32_t*>(ws + l.rsure);
+      q.roff = reinterpret_cast<uint32_t*>(ws + l.roff);
+      q.reqb = reinterpret_cast<uint32_t*>(ws + l.reqb);
+      ws += l.total;
     }
   }
   return CKV_OK;
@@ -166,6 +201,10 @@ int grid_rows(const ckv::LayerArgs& a) {
 int grid_score(const ckv::LayerArgs& a) {
   const ckv::SeqArgs& q = a.seq[a.num_seqs - 1];
   return q.blk_score + q.n_tiles * a.n_kv;
+}
+int grid_sel(const ckv::LayerArgs& a) {
+  const ckv::SeqArgs& q = a.seq[a.num_seqs - 1];
+  return q.blk_sel + q.n_ranges * a.n_kv;
 }
 int grid_gather(const ckv::LayerArgs& a) {
   const ckv::SeqArgs& q = a.seq[a.num_seqs - 1];
@@ -196,17 +235,29 @@ int run_score(const ckv_layer_desc* d, const ckv::LayerArgs& a, hipStream_t st) 
   return CKV_OK;
 }
 
-int run_select(const ckv::LayerArgs& a, hipStream_t st) {
+// Selection on scores already in place. With caller scores (ckv_select) the
+// control words and histograms are built here; in ckv_compress_layer the
+// scoring kernel built them.
+int run_select(const ckv::LayerArgs& a, bool caller_scores, hipStream_t st) {
+  hipError_t e;
+  const int gs = grid_sel(a);
   ev_begin(ckv::kStageSelect, st);
-  const hipError_t e = ckv::launch_select(a, a.num_seqs * a.n_kv, st);
-  if (e != hipSuccess) return hip_fail(e);
+  if (caller_scores) {
+    if ((e = ckv::launch_clear(a, a.num_seqs * a.n_kv, st)) != hipSuccess) return hip_fail(e);
+    if ((e = ckv::launch_hist(a, gs, st)) != hipSuccess) return hip_fail(e);
+  }
+  if ((e = ckv::launch_filter(a, gs, st)) != hipSuccess) return hip_fail(e);
+  if ((e = ckv::launch_resolve(a, a.num_seqs * a.n_kv, st)) != hipSuccess) return hip_fail(e);
   ev_end(ckv::kStageSelect, st);
+  ev_begin(ckv::kStageGather, st);
+  if ((e = ckv::launch_compact(a, gs, st)) != hipSuccess) return hip_fail(e);
+  ev_end(ckv::kStageGather, st);
   return CKV_OK;
 }
 
-int run_gather(const ckv_layer_desc* d, const ckv::LayerArgs& a, hipStream_t st) {
+int run_gather(const ckv::LayerArgs& a, hipStream_t st) {
   ev_begin(ckv::kStageGather, st);
-  const hipError_t e = ckv::launch_gather(d->dtype, a, grid_gather(a), st);
+  const hipError_t e = ckv::launch_gather(a, grid_gather(a), st);
   if (e != hipSuccess) return hip_fail(e);
   ev_end(ckv::kStageGather, st);
   return CKV_OK;
@@ -243,14 +294,17 @@ int ckv_score(const ckv_layer_desc* desc, const uint8_t* head_mask, const ckv_se
 
 int ckv_select(const ckv_layer_desc* desc, const ckv_seq* seqs, int32_t num_seqs, void* workspace,
                size_t workspace_bytes, void* stream) {
-  (void)workspace;
-  (void)workspace_bytes;
   int rc = check_desc(desc);
   if (rc != CKV_OK) return rc;
   if ((rc = check_seqs(desc, seqs, num_seqs, kNeedScores | kNeedIdx)) != CKV_OK) return rc;
+  if (!workspace || workspace_bytes < ckv_workspace_bytes(desc, seqs, num_seqs) ||
+      !aligned16(workspace))
+    return CKV_ERR_WORKSPACE;
   ckv::LayerArgs a;
-  if ((rc = build_args(desc, nullptr, seqs, num_seqs, nullptr, false, a)) != CKV_OK) return rc;
-  return run_select(a, (hipStream_t)stream);
+  if ((rc = build_args(desc, nullptr, seqs, num_seqs, (char*)workspace, false, a)) != CKV_OK)
+    return rc;
+  a.do_gather = 0;
+  return run_select(a, true, (hipStream_t)stream);
 }
 
 int ckv_gather(const ckv_layer_desc* desc, const ckv_seq* seqs, int32_t num_seqs, void* stream) {
@@ -260,7 +314,7 @@ int ckv_gather(const ckv_layer_desc* desc, const ckv_seq* seqs, int32_t num_seqs
     return rc;
   ckv::LayerArgs a;
   if ((rc = build_args(desc, nullptr, seqs, num_seqs, nullptr, false, a)) != CKV_OK) return rc;
-  return run_gather(desc, a, (hipStream_t)stream);
+  return run_gather(a, (hipStream_t)stream);
 }
 
 int ckv_compress_layer(const ckv_layer_desc* desc, const uint8_t* head_mask, const ckv_seq* seqs,
@@ -279,10 +333,11 @@ int ckv_compress_layer(const ckv_layer_desc* desc, const uint8_t* head_mask, con
   ckv::LayerArgs a;
   if ((rc = build_args(desc, head_mask, seqs, num_seqs, (char*)workspace, true, a)) != CKV_OK)
     return rc;
+  a.do_hist = 1;
+  a.do_gather = 1;
   const hipStream_t st = (hipStream_t)stream;
   if ((rc = run_score(desc, a, st)) != CKV_OK) return rc;
-  if ((rc = run_select(a, st)) != CKV_OK) return rc;
-  return run_gather(desc, a, st);
+  return run_select(a, false, st);
 }
 
 int ckv_allocate_budgets(const double* err_norm, int32_t n_layers, int64_t total, int32_t m,

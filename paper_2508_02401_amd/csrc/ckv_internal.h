@@ -1,5 +1,5 @@
 // Internal launch interface between the C ABI layer (ckv_api.cpp) and the
-// gfx950 kernels (ckv_kernels.hip). Not part of the public ABI.
+// gfx950 kernels (ckv_score.hip, ckv_select.hip). Not part of the public ABI.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -17,6 +17,23 @@ constexpr int kTileComp = 1024;    // tokens whose logits one scoring workgroup 
 constexpr int kHalo = 16;          // pooling halo on each side (pool kernel <= 2*16+1)
 constexpr int kTileOut = kTileComp - 2 * kHalo;  // scores one scoring workgroup writes
 constexpr int kGatherRows = 64;    // retained rows per gather workgroup
+constexpr int kHistBits = 12;      // first-level histogram: key bits 30..19
+constexpr int kHistBins = 1 << kHistBits;
+constexpr int kHistShift = 31 - kHistBits;
+constexpr int kRangeMin = 4096;    // scores per selection workgroup (at least)
+constexpr int kMaxRanges = 2048;   // selection ranges per KV head (at most)
+
+// Per-(prompt, KV head) control words of the selection, in the workspace.
+enum Ctl {
+  kCtlBin = 0,         // first-level bin of the threshold key
+  kCtlAbove = 1,       // keys in higher bins (all kept)
+  kCtlBinCount = 2,    // keys in the threshold bin (the candidates)
+  kCtlNumCand = 3,     // candidates appended so far
+  kCtlPrefix = 4,      // threshold: keys compare on (key >> shift) against prefix
+  kCtlShift = 5,
+  kCtlNeedEq = 6,      // keys equal to the threshold to keep, lowest index first
+  kCtlWords = 16
+};
 
 enum Stage { kStageRowStats = 0, kStageScore = 1, kStageSelect = 2, kStageGather = 3 };
 
@@ -34,14 +51,25 @@ struct SeqArgs {
   int32_t* idx;            // [n_kv][n_ret]
   void* k_out;             // [n_kv][n_ret][d]
   void* v_out;
-  float2* partial;         // workspace [n_kv][n_chunks][kMaxRows]: (max logit, sum exp2) per chunk
-  float* lse;              // workspace [n_kv][kMaxRows]: per-row log2-sum-exp2 in exp2 units
+  // workspace
+  float2* partial;         // [n_kv][n_chunks][kMaxRows]: (max logit, sum exp2) per chunk
+  float* lse;              // [n_kv][kMaxRows]: per-row log2-sum-exp2 in exp2 units
+  uint32_t* ctl;           // [n_kv][kCtlWords]
+  uint32_t* hist;          // [n_kv][kHistBins]
+  uint2* cand;             // [n_kv][L - w]: (key, index) of threshold-bin candidates
+  uint32_t* rsure;         // [n_kv][n_ranges]: keys above the threshold bin per range
+  uint32_t* roff;          // [n_kv][n_ranges]: output offset of each range
+  uint32_t* reqb;          // [n_kv][n_ranges]: threshold-equal keys before each range
   int32_t n_chunks;        // ceil(L / kChunk)
   int32_t n_tiles;         // ceil((L - w) / kTileOut)
+  int32_t n_ranges;        // ceil((L - w) / range)
+  int32_t range;           // scores per selection range (multiple of kRangeMin)
   int32_t blk_rows;        // first workgroup of this prompt in the row-statistics grid
   int32_t blk_score;       // ... in the scoring grid
+  int32_t blk_sel;         // ... in the selection grids (n_kv * n_ranges per prompt)
   int32_t blk_gather;      // ... in the gather grid
   int32_t n_gblk;          // gather workgroups per KV head
+  int32_t pad;
 };
 
 // One layer call.
@@ -55,6 +83,9 @@ struct LayerArgs {
   int32_t pool;            // 0 average, 1 max
   int32_t kp;              // odd pool kernel
   int32_t max_sel;         // largest number of chosen heads in any group
+  int32_t elt;             // bytes per element of Q/K/V
+  int32_t do_hist;         // scoring also builds the selection histogram
+  int32_t do_gather;       // compaction also copies the kept K/V rows
   int16_t grp_off[kMaxKvHeads + 1];  // chosen heads of group g: sel[grp_off[g] .. grp_off[g+1])
   uint8_t sel[kMaxQHeads];
   SeqArgs seq[kMaxSeqs];
@@ -64,7 +95,11 @@ struct LayerArgs {
 hipError_t launch_rowstats(int dtype, const LayerArgs& a, int grid, hipStream_t st);
 hipError_t launch_lse(const LayerArgs& a, int grid, hipStream_t st);
 hipError_t launch_score(int dtype, const LayerArgs& a, int grid, hipStream_t st);
-hipError_t launch_select(const LayerArgs& a, int grid, hipStream_t st);
-hipError_t launch_gather(int dtype, const LayerArgs& a, int grid, hipStream_t st);
+hipError_t launch_clear(const LayerArgs& a, int grid, hipStream_t st);
+hipError_t launch_hist(const LayerArgs& a, int grid, hipStream_t st);
+hipError_t launch_filter(const LayerArgs& a, int grid, hipStream_t st);
+hipError_t launch_resolve(const LayerArgs& a, int grid, hipStream_t st);
+hipError_t launch_compact(const LayerArgs& a, int grid, hipStream_t st);
+hipError_t launch_gather(const LayerArgs& a, int grid, hipStream_t st);
 
 }  // namespace ckv

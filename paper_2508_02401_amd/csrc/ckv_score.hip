@@ -1,4 +1,4 @@
-// gfx950 (MI355X) kernels of CompressKV's prefill-end token selection.
+// gfx950 (MI355X) scoring kernels of CompressKV's prefill-end token selection.
 //
 // Paper: CompressKV, arXiv 2508.02401, Sec. 3.3 ("Token Selection Driven by
 // Semantic Retrieval Heads"). For one KV group g with chosen query heads
@@ -8,7 +8,6 @@
 //   S[h,j]   = sum_i p[h,i,j]                          (window sum)
 //   P[h,j]   = pool_k(S[h,.])[j] on the prefix [0, L-w)
 //   A[g,j]   = mean over h in sel(g) of P[h,j]          (head mean)
-//   keep the B-w largest A[g,j] plus the window; copy their K/V rows.
 //
 // The exact softmax needs each row's normaliser before the column sums, so
 // the logits are formed twice from K:
@@ -20,70 +19,16 @@
 //   score_kernel     pass 2: MFMA tiles with queries as rows, exp2(a*s - lse),
 //                    8-row group sums with one cross-half shuffle, per-head
 //                    sums in LDS, pooling with a 16-token halo, head mean;
-//   select_kernel    per (prompt, group) radix select on the fp32 bit patterns
-//                    (scores are >= 0), then a stable compaction in index
-//                    order (ties resolve to the lower index);
-//   gather_kernel    16-byte row copies of the retained K and V.
-#include "ckv_internal.h"
-
+//                    it also accumulates the first-level histogram of the
+//                    score keys that the selection starts from.
 #include <math.h>
+
+#include "ckv_device.h"
 
 namespace ckv {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-
-constexpr int kThreads = 256;
-constexpr int kWaves = kThreads / 64;
-constexpr int kSelectThreads = 1024;
-
-template <int DT>
-struct Elt {
-  static constexpr int bytes = DT == 2 ? 4 : 2;
-};
-
-// acc += A * B over one 16-byte operand chunk per lane. Lane l holds row
-// (l % 32) of A and column (l % 32) of B; the two lane halves hold the two
-// halves of the chunk's contraction slice, identically for A and B, so the
-// result is the dot product over the chunk whatever order the hardware sums in.
-template <int DT>
-__device__ __forceinline__ f32x16 mfma_chunk(uint4 a, uint4 b, f32x16 c);
-
-template <>
-__device__ __forceinline__ f32x16 mfma_chunk<0>(uint4 a, uint4 b, f32x16 c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
-                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
-}
-
-template <>
-__device__ __forceinline__ f32x16 mfma_chunk<1>(uint4 a, uint4 b, f32x16 c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a),
-                                                __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
-}
-
-template <>
-__device__ __forceinline__ f32x16 mfma_chunk<2>(uint4 a, uint4 b, f32x16 c) {
-  c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
-  c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
-  c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
-  c = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
-  return c;
-}
-
-__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
-
-// Row of the 32x32 MFMA result held in accumulator v by lane half h.
-__device__ __forceinline__ int acc_row(int v, int h) { return 8 * (v >> 2) + 4 * h + (v & 3); }
-
-// Workgroups are dispatched round-robin over the 8 XCDs; renumber them so that
-// each XCD works on one contiguous range of tiles (neighbouring tiles share
-// halo rows and K lines in that XCD's L2).
-__device__ __forceinline__ int xcd_remap(int b, int n) {
-  const int xcd = b & 7, i = b >> 3, per = n >> 3, rem = n & 7;
-  return xcd * per + (xcd < rem ? xcd : rem) + i;
-}
+using namespace dev;
 
 // Stage the chosen heads' window queries of group g into LDS. Row r holds
 // head slot r / w8, window row r % w8; padding rows are zero.
@@ -129,6 +74,13 @@ __global__ __launch_bounds__(kThreads) void rowstats_kernel(const LayerArgs a) {
   const int64_t L = sq.L;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, l32 = lane & 31;
   const float alpha = a.alpha;
+
+  // the selection state of this group starts from zero in every call; the
+  // scoring kernel that accumulates into it runs after this one
+  if (chunk == 0 && a.do_hist) {
+    for (int i = tid; i < kCtlWords; i += kThreads) sq.ctl[g * kCtlWords + i] = 0u;
+    for (int i = tid; i < kHistBins; i += kThreads) sq.hist[(int64_t)g * kHistBins + i] = 0u;
+  }
 
   stage_queries<EB, NV, LDS_ROW>(a, sq, sel0, n_sel, nqb * 32, q_lds);
   __syncthreads();
@@ -249,6 +201,7 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const LayerArgs a) {
   constexpr int LDS_ROW = NV + 1;
   __shared__ uint4 q_lds[MAXQB * 32 * LDS_ROW];
   __shared__ __align__(16) float c_lds[MAXQB * 32];
+  __shared__ uint32_t hist_lds[kHistBins];
   extern __shared__ float sh[];  // [max_sel][kTileComp] per-head window sums
 
   const int b = xcd_remap(blockIdx.x, gridDim.x);
@@ -271,6 +224,9 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const LayerArgs a) {
   stage_queries<EB, NV, LDS_ROW>(a, sq, sel0, n_sel, nqb * 32, q_lds);
   for (int r = tid; r < nqb * 32; r += kThreads) c_lds[r] = sq.lse[(int64_t)g * kMaxRows + r];
   for (int e = tid; e < n_sel * kTileComp; e += kThreads) sh[e] = 0.f;
+  const bool do_hist = a.do_hist && sq.n_keep > 0;
+  if (do_hist)
+    for (int i = tid; i < kHistBins; i += kThreads) hist_lds[i] = 0u;
   __syncthreads();
 
   uint4 qreg[MAXQB][NC];
@@ -344,177 +300,22 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const LayerArgs a) {
         total += m;
       }
     }
-    out[j] = total / (float)n_sel;
+    const float score = total / (float)n_sel;
+    out[j] = score;
+    if (do_hist) atomicAdd(&hist_lds[score_key(score) >> kHistShift], 1u);
   }
-}
+  if (!do_hist) return;
 
-// ---------------------------------------------------------------------------
-// Top-N selection.
-// ---------------------------------------------------------------------------
-__device__ __forceinline__ uint32_t score_key(float x) {
-  const uint32_t u = __float_as_uint(x);
-  return (u & 0x80000000u) ? 0u : u;  // scores are >= 0; -0 ranks as +0
-}
-
-// Exclusive prefix sum over the workgroup; also returns the total.
-template <int NT>
-__device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* wsum, uint32_t& total) {
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  uint32_t x = v;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const uint32_t y = __shfl_up(x, off);
-    if (lane >= off) x += y;
-  }
-  if (lane == 63) wsum[wv] = x;
+  // first-level histogram of this tile's keys into the group's histogram
   __syncthreads();
-  uint32_t before = 0, tot = 0;
-#pragma unroll
-  for (int i = 0; i < NT / 64; ++i) {
-    const uint32_t sv = wsum[i];
-    before += i < wv ? sv : 0u;
-    tot += sv;
-  }
-  __syncthreads();
-  total = tot;
-  return before + x - v;
-}
-
-__global__ __launch_bounds__(kSelectThreads) void select_kernel(const LayerArgs a) {
-  constexpr int NT = kSelectThreads;
-  __shared__ uint32_t hist[2048];
-  __shared__ uint32_t wsum[NT / 64];
-  __shared__ uint32_t s_res[3];
-  const int s = blockIdx.x / a.n_kv, g = blockIdx.x - s * a.n_kv;
-  const SeqArgs& sq = a.seq[s];
-  const int64_t L = sq.L;
-  const int w = a.w;
-  const int64_t Ls = L - w;
-  int32_t* out = sq.idx + (int64_t)g * sq.n_ret;
-  const int tid = threadIdx.x;
-  if (sq.n_keep < 0) {
-    for (int64_t j = tid; j < L; j += NT) out[j] = (int32_t)j;
-    return;
-  }
-  const uint32_t nk = (uint32_t)sq.n_keep;
-  for (int i = tid; i < w; i += NT) out[nk + i] = (int32_t)(Ls + i);
-  if (nk == 0) return;
-  const float* sc = sq.scores + (int64_t)g * Ls;
-
-  // Radix select of the nk-th largest key, 11 + 11 + 9 bits below the sign.
-  // After it, keys compare on (key >> shift) against prefix: everything above
-  // is kept, and the first `need` keys equal to it (in index order).
-  uint32_t prefix = 0, need = nk;
-  int shift = 31;
-  for (int level = 0; level < 3; ++level) {
-    const int nb = level < 2 ? 11 : 9;
-    const int nshift = shift - nb;
-    const uint32_t nbins = 1u << nb;
-    for (uint32_t i = tid; i < nbins; i += NT) hist[i] = 0;
-    __syncthreads();
-    for (int64_t j = tid; j < Ls; j += NT) {
-      const uint32_t u = score_key(sc[j]);
-      if ((u >> shift) == prefix) atomicAdd(&hist[(u >> nshift) & (nbins - 1)], 1u);
-    }
-    __syncthreads();
-    uint32_t c_hi = 0, c_lo = 0;
-    if ((uint32_t)tid < nbins / 2) {
-      c_hi = hist[nbins - 1 - 2 * tid];
-      c_lo = hist[nbins - 2 - 2 * tid];
-    }
-    uint32_t tot;
-    const uint32_t above = block_excl_scan<NT>(c_hi + c_lo, wsum, tot);
-    if ((uint32_t)tid < nbins / 2 && above < need && need <= above + c_hi + c_lo) {
-      if (need <= above + c_hi) {
-        s_res[0] = nbins - 1 - 2 * tid;
-        s_res[1] = above;
-        s_res[2] = c_hi;
-      } else {
-        s_res[0] = nbins - 2 - 2 * tid;
-        s_res[1] = above + c_hi;
-        s_res[2] = c_lo;
-      }
-    }
-    __syncthreads();
-    prefix = (prefix << nb) | s_res[0];
-    need -= s_res[1];
-    shift = nshift;
-    if (s_res[2] == need) break;  // the whole bin is kept
-  }
-
-  // Stable compaction in index order, four keys per thread per step.
-  uint32_t eq_carry = 0, out_carry = 0;
-  for (int64_t base = 0; base < Ls; base += 4 * NT) {
-    const int64_t jb = base + 4 * tid;
-    int f[4];
-    uint32_t neq = 0;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      f[e] = 0;
-      if (jb + e < Ls) {
-        const uint32_t p = score_key(sc[jb + e]) >> shift;
-        f[e] = p > prefix ? 1 : (p == prefix ? 2 : 0);
-      }
-      neq += f[e] == 2;
-    }
-    uint32_t tot_eq;
-    uint32_t eq_rank = eq_carry + block_excl_scan<NT>(neq, wsum, tot_eq);
-    bool keep[4];
-    uint32_t nsel = 0;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      keep[e] = f[e] == 1;
-      if (f[e] == 2) {
-        keep[e] = eq_rank < need;
-        ++eq_rank;
-      }
-      nsel += keep[e];
-    }
-    uint32_t tot_sel;
-    uint32_t pos = out_carry + block_excl_scan<NT>(nsel, wsum, tot_sel);
-#pragma unroll
-    for (int e = 0; e < 4; ++e)
-      if (keep[e] && pos < nk) out[pos++] = (int32_t)(jb + e);
-    eq_carry += tot_eq;
-    out_carry += tot_sel;
-    if (out_carry >= nk) break;
+  uint32_t* ghist = sq.hist + (int64_t)g * kHistBins;
+  for (int i = tid; i < kHistBins; i += kThreads) {
+    const uint32_t c = hist_lds[i];
+    if (c) atomicAdd(&ghist[i], c);
   }
 }
 
-// ---------------------------------------------------------------------------
-// Gather of the retained rows.
-// ---------------------------------------------------------------------------
-template <int EB, int D>
-__global__ __launch_bounds__(kThreads) void gather_kernel(const LayerArgs a) {
-  constexpr int NV = D * EB / 16;
-  constexpr int RPP = kThreads / NV;  // rows per pass
-  const int b = blockIdx.x;
-  int s = 0;
-  for (int t = 1; t < a.num_seqs; ++t)
-    if (b >= a.seq[t].blk_gather) s = t;
-  const SeqArgs& sq = a.seq[s];
-  const int local = b - sq.blk_gather;
-  const int g = local / sq.n_gblk;
-  const int r0 = (local - g * sq.n_gblk) * kGatherRows;
-  const int c = threadIdx.x % NV;
-  const int32_t* idx = sq.idx + (int64_t)g * sq.n_ret;
-  const char* kb = static_cast<const char*>(sq.k) + (int64_t)g * sq.kv_sh * EB;
-  const char* vb = static_cast<const char*>(sq.v) + (int64_t)g * sq.kv_sh * EB;
-  uint4* ko = static_cast<uint4*>(sq.k_out) + (int64_t)g * sq.n_ret * NV;
-  uint4* vo = static_cast<uint4*>(sq.v_out) + (int64_t)g * sq.n_ret * NV;
-  for (int rr = threadIdx.x / NV; rr < kGatherRows; rr += RPP) {
-    const int r = r0 + rr;
-    if (r >= sq.n_ret) break;
-    const int64_t t = idx[r];
-    if (t < 0 || t >= sq.L) continue;  // out-of-range index: leave the row untouched
-    const uint4 kv = reinterpret_cast<const uint4*>(kb + t * sq.kv_st * EB)[c];
-    const uint4 vv = reinterpret_cast<const uint4*>(vb + t * sq.kv_st * EB)[c];
-    ko[(int64_t)r * NV + c] = kv;
-    vo[(int64_t)r * NV + c] = vv;
-  }
-}
-
-template <int DT, int D>
+template <int DT>
 constexpr int maxqb() {
   return DT == 2 ? kMaxRowsF32 / 32 : kMaxRows / 32;
 }
@@ -522,7 +323,7 @@ constexpr int maxqb() {
 }  // namespace
 
 hipError_t launch_rowstats(int dtype, const LayerArgs& a, int grid, hipStream_t st) {
-#define CKV_RS(DT, D) hipLaunchKernelGGL((rowstats_kernel<DT, D, maxqb<DT, D>()>), dim3(grid), dim3(kThreads), 0, st, a)
+#define CKV_RS(DT, D) hipLaunchKernelGGL((rowstats_kernel<DT, D, maxqb<DT>()>), dim3(grid), dim3(kThreads), 0, st, a)
   if (dtype == 0) { if (a.d == 64) CKV_RS(0, 64); else CKV_RS(0, 128); }
   else if (dtype == 1) { if (a.d == 64) CKV_RS(1, 64); else CKV_RS(1, 128); }
   else { if (a.d == 64) CKV_RS(2, 64); else CKV_RS(2, 128); }
@@ -537,24 +338,11 @@ hipError_t launch_lse(const LayerArgs& a, int grid, hipStream_t st) {
 
 hipError_t launch_score(int dtype, const LayerArgs& a, int grid, hipStream_t st) {
   const size_t lds = (size_t)a.max_sel * kTileComp * sizeof(float);
-#define CKV_SC(DT, D) hipLaunchKernelGGL((score_kernel<DT, D, maxqb<DT, D>()>), dim3(grid), dim3(kThreads), lds, st, a)
+#define CKV_SC(DT, D) hipLaunchKernelGGL((score_kernel<DT, D, maxqb<DT>()>), dim3(grid), dim3(kThreads), lds, st, a)
   if (dtype == 0) { if (a.d == 64) CKV_SC(0, 64); else CKV_SC(0, 128); }
   else if (dtype == 1) { if (a.d == 64) CKV_SC(1, 64); else CKV_SC(1, 128); }
   else { if (a.d == 64) CKV_SC(2, 64); else CKV_SC(2, 128); }
 #undef CKV_SC
-  return hipGetLastError();
-}
-
-hipError_t launch_select(const LayerArgs& a, int grid, hipStream_t st) {
-  hipLaunchKernelGGL(select_kernel, dim3(grid), dim3(kSelectThreads), 0, st, a);
-  return hipGetLastError();
-}
-
-hipError_t launch_gather(int dtype, const LayerArgs& a, int grid, hipStream_t st) {
-#define CKV_GA(EB, D) hipLaunchKernelGGL((gather_kernel<EB, D>), dim3(grid), dim3(kThreads), 0, st, a)
-  if (dtype == 2) { if (a.d == 64) CKV_GA(4, 64); else CKV_GA(4, 128); }
-  else { if (a.d == 64) CKV_GA(2, 64); else CKV_GA(2, 128); }
-#undef CKV_GA
   return hipGetLastError();
 }
 

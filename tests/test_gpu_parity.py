@@ -173,7 +173,7 @@ def test_select_on_oracle_scores_is_exact(dev):
         sc = torch.from_numpy(scores).to(dev)
         idx = torch.empty((2, min(budget, L)), dtype=torch.int32, device=dev)
         s = ckv.Seq(None, None, None, budget, scores=sc, idx=idx, seq_len=L)
-        ckv.ckv_select(desc, [s])
+        ckv.ckv_select(desc, [s], ckv.alloc_workspace(desc, [s], dev))
         torch.cuda.synchronize()
         for g in range(2):
             ref = oracle.select_tokens(scores[g].astype(np.float64), L, 8, budget)

@@ -19,6 +19,9 @@ ARCH = "gfx950"
 # float code.
 COMMON = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=" + ARCH,
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+          # MFMA results stay in VGPRs: the softmax reads them with VALU ops,
+          # and accumulators in AGPRs would need a copy per element
+          "-mllvm", "-amdgpu-mfma-vgpr-form",
           "-I" + INCLUDE, "-I" + CSRC, "-Wall", "-Wno-unused-function"]
 
 

@@ -125,7 +125,7 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
   a.kp = d->pool_kernel;
   if (mask) {
     const int G = d->num_q_heads / d->num_kv_heads;
-    const int max_rows = d->dtype == CKV_F32 ? ckv::kMaxRowsF32 : ckv::kMaxRows;
+    const int max_rows = ckv::kMaxRows;
     int off = 0;
     a.max_sel = 0;
     for (int g = 0; g < d->num_kv_heads; ++g) {

@@ -11,9 +11,8 @@ constexpr int kMaxSeqs = 16;
 constexpr int kMaxQHeads = 128;
 constexpr int kMaxKvHeads = 64;
 constexpr int kMaxRows = 128;      // chosen-head rows per group after padding each head to 8
-constexpr int kMaxRowsF32 = 64;    // the fp32 kernels keep half as many query rows in registers
 constexpr int kChunk = 1024;       // tokens per row-statistics workgroup
-constexpr int kTileComp = 1024;    // tokens whose logits one scoring workgroup computes
+constexpr int kTileComp = 512;     // tokens whose logits one scoring workgroup computes
 constexpr int kHalo = 16;          // pooling halo on each side (pool kernel <= 2*16+1)
 constexpr int kTileOut = kTileComp - 2 * kHalo;  // scores one scoring workgroup writes
 constexpr int kGatherRows = 64;    // retained rows per gather workgroup

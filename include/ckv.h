@@ -177,11 +177,15 @@ const char *ckv_status_string(int status);
 /* hipError_t of the most recent CKV_ERR_HIP returned on this host thread. */
 int ckv_last_hip_error(void);
 
-/* Optional per-stage timing for profiling: when begin/end are non-NULL the
- * next calls record begin[s] before and end[s] after stage s's kernel on the
- * caller's stream (stage 0 row statistics, 1 scoring, 2 selection,
- * 3 gather). Arrays are hipEvent_t[4] owned by the caller; pass NULL to stop.
- * Per host thread. */
+/* Optional per-stage timing for profiling. While begin/end are non-NULL,
+ * each stage's first kernel launch records its start time into begin[s] and
+ * its last kernel records its end time into end[s] (hipExtLaunchKernel events:
+ * no marker packets are added to the stream, so the timing does not perturb
+ * the launches). Stages: 0 row statistics (pass 1), 1 scoring (pass 2; the
+ * small merge kernel between the passes is not covered), 2 selection
+ * (threshold search), 3 compaction and gather. Arrays are hipEvent_t[4]
+ * owned by the caller, created with timing enabled; pass NULL to stop. Per
+ * host thread. */
 int ckv_set_stage_events(void *const *begin, void *const *end);
 
 #ifdef __cplusplus

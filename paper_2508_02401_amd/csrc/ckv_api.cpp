@@ -216,22 +216,27 @@ int hip_fail(hipError_t e) {
   return CKV_ERR_HIP;
 }
 
-void ev_begin(int stage, hipStream_t st) {
-  if (g_events_on && g_ev_begin[stage]) (void)hipEventRecord(g_ev_begin[stage], st);
-}
-void ev_end(int stage, hipStream_t st) {
-  if (g_events_on && g_ev_end[stage]) (void)hipEventRecord(g_ev_end[stage], st);
+// Events of one launch: the stage's begin event on its first kernel and its
+// end event on its last (kernel start and end times, no extra packets).
+ckv::Timing timing(int stage, bool first, bool last) {
+  ckv::Timing t;
+  if (g_events_on) {
+    if (first) t.start = g_ev_begin[stage];
+    if (last) t.stop = g_ev_end[stage];
+  }
+  return t;
 }
 
 int run_score(const ckv_layer_desc* d, const ckv::LayerArgs& a, hipStream_t st) {
   hipError_t e;
-  ev_begin(ckv::kStageRowStats, st);
-  if ((e = ckv::launch_rowstats(d->dtype, a, grid_rows(a), st)) != hipSuccess) return hip_fail(e);
-  ev_end(ckv::kStageRowStats, st);
-  if ((e = ckv::launch_lse(a, a.num_seqs * a.n_kv, st)) != hipSuccess) return hip_fail(e);
-  ev_begin(ckv::kStageScore, st);
-  if ((e = ckv::launch_score(d->dtype, a, grid_score(a), st)) != hipSuccess) return hip_fail(e);
-  ev_end(ckv::kStageScore, st);
+  const ckv::Timing none;
+  if ((e = ckv::launch_rowstats(d->dtype, a, grid_rows(a), st,
+                                timing(ckv::kStageRowStats, true, true))) != hipSuccess)
+    return hip_fail(e);
+  if ((e = ckv::launch_lse(a, a.num_seqs * a.n_kv, st, none)) != hipSuccess) return hip_fail(e);
+  if ((e = ckv::launch_score(d->dtype, a, grid_score(a), st,
+                             timing(ckv::kStageScore, true, true))) != hipSuccess)
+    return hip_fail(e);
   return CKV_OK;
 }
 
@@ -241,25 +246,27 @@ int run_score(const ckv_layer_desc* d, const ckv::LayerArgs& a, hipStream_t st) 
 int run_select(const ckv::LayerArgs& a, bool caller_scores, hipStream_t st) {
   hipError_t e;
   const int gs = grid_sel(a);
-  ev_begin(ckv::kStageSelect, st);
+  const ckv::Timing none;
   if (caller_scores) {
-    if ((e = ckv::launch_clear(a, a.num_seqs * a.n_kv, st)) != hipSuccess) return hip_fail(e);
-    if ((e = ckv::launch_hist(a, gs, st)) != hipSuccess) return hip_fail(e);
+    if ((e = ckv::launch_clear(a, a.num_seqs * a.n_kv, st, timing(ckv::kStageSelect, true, false))) !=
+        hipSuccess)
+      return hip_fail(e);
+    if ((e = ckv::launch_hist(a, gs, st, none)) != hipSuccess) return hip_fail(e);
   }
-  if ((e = ckv::launch_filter(a, gs, st)) != hipSuccess) return hip_fail(e);
-  if ((e = ckv::launch_resolve(a, a.num_seqs * a.n_kv, st)) != hipSuccess) return hip_fail(e);
-  ev_end(ckv::kStageSelect, st);
-  ev_begin(ckv::kStageGather, st);
-  if ((e = ckv::launch_compact(a, gs, st)) != hipSuccess) return hip_fail(e);
-  ev_end(ckv::kStageGather, st);
+  if ((e = ckv::launch_filter(a, gs, st, timing(ckv::kStageSelect, !caller_scores, false))) !=
+      hipSuccess)
+    return hip_fail(e);
+  if ((e = ckv::launch_resolve(a, a.num_seqs * a.n_kv, st, timing(ckv::kStageSelect, false, true))) !=
+      hipSuccess)
+    return hip_fail(e);
+  if ((e = ckv::launch_compact(a, gs, st, timing(ckv::kStageGather, true, true))) != hipSuccess)
+    return hip_fail(e);
   return CKV_OK;
 }
 
 int run_gather(const ckv::LayerArgs& a, hipStream_t st) {
-  ev_begin(ckv::kStageGather, st);
-  const hipError_t e = ckv::launch_gather(a, grid_gather(a), st);
+  const hipError_t e = ckv::launch_gather(a, grid_gather(a), st, timing(ckv::kStageGather, true, true));
   if (e != hipSuccess) return hip_fail(e);
-  ev_end(ckv::kStageGather, st);
   return CKV_OK;
 }
 

@@ -2,6 +2,8 @@
 // workgroup numbering, score keys, workgroup scans and the threshold search.
 #pragma once
 
+#include <hip/hip_ext.h>
+
 #include "ckv_internal.h"
 
 namespace ckv {
@@ -118,6 +120,18 @@ __device__ __forceinline__ void find_bin(int nbins, uint32_t need, Get get, uint
     }
   }
   __syncthreads();
+}
+
+// Launch kernel(a) on stream st, with its start and end times recorded into
+// tm's events when they are given.
+template <typename K>
+__host__ hipError_t launch(K kernel, int grid, int block, hipStream_t st, const Timing& tm,
+                           const LayerArgs& a) {
+  if (tm.start || tm.stop)
+    hipExtLaunchKernelGGL(kernel, dim3(grid), dim3(block), 0, st, tm.start, tm.stop, 0, a);
+  else
+    hipLaunchKernelGGL(kernel, dim3(grid), dim3(block), 0, st, a);
+  return hipGetLastError();
 }
 
 }  // namespace dev

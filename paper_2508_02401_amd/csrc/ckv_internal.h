@@ -90,15 +90,24 @@ struct LayerArgs {
   SeqArgs seq[kMaxSeqs];
 };
 
-// dtype codes match ckv_dtype.
-hipError_t launch_rowstats(int dtype, const LayerArgs& a, int grid, hipStream_t st);
-hipError_t launch_lse(const LayerArgs& a, int grid, hipStream_t st);
-hipError_t launch_score(int dtype, const LayerArgs& a, int grid, hipStream_t st);
-hipError_t launch_clear(const LayerArgs& a, int grid, hipStream_t st);
-hipError_t launch_hist(const LayerArgs& a, int grid, hipStream_t st);
-hipError_t launch_filter(const LayerArgs& a, int grid, hipStream_t st);
-hipError_t launch_resolve(const LayerArgs& a, int grid, hipStream_t st);
-hipError_t launch_compact(const LayerArgs& a, int grid, hipStream_t st);
-hipError_t launch_gather(const LayerArgs& a, int grid, hipStream_t st);
+// Optional timing of one launch: start receives the kernel's start time and
+// stop its end time (hipExtLaunchKernel events, which add no marker packets to
+// the stream). Either may be null.
+struct Timing {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
+
+// dtype codes match ckv_dtype. grid is the number of workgroups, except for
+// launch_lse, which takes the number of (prompt, group) pairs.
+hipError_t launch_rowstats(int dtype, const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
+hipError_t launch_lse(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
+hipError_t launch_score(int dtype, const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
+hipError_t launch_clear(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
+hipError_t launch_hist(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
+hipError_t launch_filter(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
+hipError_t launch_resolve(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
+hipError_t launch_compact(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
+hipError_t launch_gather(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
 
 }  // namespace ckv

@@ -347,26 +347,47 @@ __global__ __launch_bounds__(kThreads) void rowstats_kernel(const LayerArgs a) {
 
 // Merge chunk partials: lse[r] = log2(sum_j exp2(alpha * s_rj)) so that the
 // softmax probability is exp2(alpha * s - lse). Padding rows get +inf (p = 0).
-__global__ __launch_bounds__(kMaxRows) void lse_kernel(const LayerArgs a) {
-  const int s = blockIdx.x / a.n_kv, g = blockIdx.x - s * a.n_kv;
+// One workgroup per (prompt, group, 32-row block); the 8 lanes of a row merge
+// every 8th chunk each, then one lane merges their 8 results.
+constexpr int kLseRows = 32;
+constexpr int kLseLanes = kThreads / kLseRows;
+
+__device__ __forceinline__ void lse_merge(float& m, float& z, float m2, float z2, float alpha) {
+  const float mn = fmaxf(m, m2);
+  if (mn == -INFINITY) return;  // both empty
+  const float ms = mn * alpha;
+  z = z * fast_exp2(m * alpha - ms) + z2 * fast_exp2(m2 * alpha - ms);
+  m = mn;
+}
+
+__global__ __launch_bounds__(kThreads) void lse_kernel(const LayerArgs a) {
+  __shared__ float2 part[kLseLanes][kLseRows];
+  constexpr int kBlocks = kMaxRows / kLseRows;
+  const int sg = blockIdx.x / kBlocks, rb = blockIdx.x - sg * kBlocks;
+  const int s = sg / a.n_kv, g = sg - s * a.n_kv;
   const SeqArgs& sq = a.seq[s];
-  const int r = threadIdx.x;
+  const int lr = threadIdx.x % kLseRows, c0 = threadIdx.x / kLseRows;
+  const int r = rb * kLseRows + lr;
   const int n_sel = a.grp_off[g + 1] - a.grp_off[g];
   const int slot = r / a.w8, i = r - slot * a.w8;
-  float out = INFINITY;
-  if (slot < n_sel && i < a.w) {
+  const bool valid = slot < n_sel && i < a.w;
+  float m = -INFINITY, z = 0.f;
+  if (valid) {
     const float2* p = sq.partial + (int64_t)g * sq.n_chunks * kMaxRows + r;
-    float m = -INFINITY;
-    for (int c = 0; c < sq.n_chunks; ++c) m = fmaxf(m, p[(int64_t)c * kMaxRows].x);
-    const float ms = m * a.alpha;
-    float z = 0.f;
-    for (int c = 0; c < sq.n_chunks; ++c) {
+#pragma unroll 8
+    for (int c = c0; c < sq.n_chunks; c += kLseLanes) {
       const float2 v = p[(int64_t)c * kMaxRows];
-      z += v.y * fast_exp2(v.x * a.alpha - ms);
+      lse_merge(m, z, v.x, v.y, a.alpha);
     }
-    out = ms + log2f(z);
   }
-  sq.lse[(int64_t)g * kMaxRows + r] = out;
+  part[c0][lr] = make_float2(m, z);
+  __syncthreads();
+  if (threadIdx.x < kLseRows) {
+    float mm = -INFINITY, zz = 0.f;
+#pragma unroll
+    for (int c = 0; c < kLseLanes; ++c) lse_merge(mm, zz, part[c][lr].x, part[c][lr].y, a.alpha);
+    sq.lse[(int64_t)g * kMaxRows + r] = valid ? mm * a.alpha + log2f(zz) : INFINITY;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -527,29 +548,37 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const LayerArgs a) {
   else score_body<DT, D, 4, S, NS>(a, sq, g, tile, sel0, n_sel, nqb, slots, slot01, gsum);
 }
 
+template <template <int, int> class KernelOf>
+hipError_t launch_typed(int dtype, const LayerArgs& a, int grid, hipStream_t st, const Timing& tm) {
+  if (dtype == 0) return a.d == 64 ? launch(KernelOf<0, 64>::fn, grid, kThreads, st, tm, a)
+                                   : launch(KernelOf<0, 128>::fn, grid, kThreads, st, tm, a);
+  if (dtype == 1) return a.d == 64 ? launch(KernelOf<1, 64>::fn, grid, kThreads, st, tm, a)
+                                   : launch(KernelOf<1, 128>::fn, grid, kThreads, st, tm, a);
+  return a.d == 64 ? launch(KernelOf<2, 64>::fn, grid, kThreads, st, tm, a)
+                   : launch(KernelOf<2, 128>::fn, grid, kThreads, st, tm, a);
+}
+
+template <int DT, int D>
+struct RowStatsOf {
+  static constexpr auto fn = rowstats_kernel<DT, D>;
+};
+template <int DT, int D>
+struct ScoreOf {
+  static constexpr auto fn = score_kernel<DT, D>;
+};
+
 }  // namespace
 
-hipError_t launch_rowstats(int dtype, const LayerArgs& a, int grid, hipStream_t st) {
-#define CKV_RS(DT, D) hipLaunchKernelGGL((rowstats_kernel<DT, D>), dim3(grid), dim3(kThreads), 0, st, a)
-  if (dtype == 0) { if (a.d == 64) CKV_RS(0, 64); else CKV_RS(0, 128); }
-  else if (dtype == 1) { if (a.d == 64) CKV_RS(1, 64); else CKV_RS(1, 128); }
-  else { if (a.d == 64) CKV_RS(2, 64); else CKV_RS(2, 128); }
-#undef CKV_RS
-  return hipGetLastError();
+hipError_t launch_rowstats(int dtype, const LayerArgs& a, int grid, hipStream_t st, const Timing& tm) {
+  return launch_typed<RowStatsOf>(dtype, a, grid, st, tm);
 }
 
-hipError_t launch_lse(const LayerArgs& a, int grid, hipStream_t st) {
-  hipLaunchKernelGGL(lse_kernel, dim3(grid), dim3(kMaxRows), 0, st, a);
-  return hipGetLastError();
+hipError_t launch_lse(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm) {
+  return launch(lse_kernel, grid * (kMaxRows / kLseRows), kThreads, st, tm, a);
 }
 
-hipError_t launch_score(int dtype, const LayerArgs& a, int grid, hipStream_t st) {
-#define CKV_SC(DT, D) hipLaunchKernelGGL((score_kernel<DT, D>), dim3(grid), dim3(kThreads), 0, st, a)
-  if (dtype == 0) { if (a.d == 64) CKV_SC(0, 64); else CKV_SC(0, 128); }
-  else if (dtype == 1) { if (a.d == 64) CKV_SC(1, 64); else CKV_SC(1, 128); }
-  else { if (a.d == 64) CKV_SC(2, 64); else CKV_SC(2, 128); }
-#undef CKV_SC
-  return hipGetLastError();
+hipError_t launch_score(int dtype, const LayerArgs& a, int grid, hipStream_t st, const Timing& tm) {
+  return launch_typed<ScoreOf>(dtype, a, grid, st, tm);
 }
 
 }  // namespace ckv

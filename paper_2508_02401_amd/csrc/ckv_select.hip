@@ -362,34 +362,28 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const LayerArgs a) {
 
 }  // namespace
 
-hipError_t launch_clear(const LayerArgs& a, int grid, hipStream_t st) {
-  hipLaunchKernelGGL(clear_kernel, dim3(grid), dim3(kThreads), 0, st, a);
-  return hipGetLastError();
+hipError_t launch_clear(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm) {
+  return launch(clear_kernel, grid, kThreads, st, tm, a);
 }
 
-hipError_t launch_hist(const LayerArgs& a, int grid, hipStream_t st) {
-  hipLaunchKernelGGL(hist_kernel, dim3(grid), dim3(kThreads), 0, st, a);
-  return hipGetLastError();
+hipError_t launch_hist(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm) {
+  return launch(hist_kernel, grid, kThreads, st, tm, a);
 }
 
-hipError_t launch_filter(const LayerArgs& a, int grid, hipStream_t st) {
-  hipLaunchKernelGGL(filter_kernel, dim3(grid), dim3(kThreads), 0, st, a);
-  return hipGetLastError();
+hipError_t launch_filter(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm) {
+  return launch(filter_kernel, grid, kThreads, st, tm, a);
 }
 
-hipError_t launch_resolve(const LayerArgs& a, int grid, hipStream_t st) {
-  hipLaunchKernelGGL(resolve_kernel, dim3(grid), dim3(kThreads), 0, st, a);
-  return hipGetLastError();
+hipError_t launch_resolve(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm) {
+  return launch(resolve_kernel, grid, kThreads, st, tm, a);
 }
 
-hipError_t launch_compact(const LayerArgs& a, int grid, hipStream_t st) {
-  hipLaunchKernelGGL(compact_kernel, dim3(grid), dim3(kThreads), 0, st, a);
-  return hipGetLastError();
+hipError_t launch_compact(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm) {
+  return launch(compact_kernel, grid, kThreads, st, tm, a);
 }
 
-hipError_t launch_gather(const LayerArgs& a, int grid, hipStream_t st) {
-  hipLaunchKernelGGL(gather_kernel, dim3(grid), dim3(kThreads), 0, st, a);
-  return hipGetLastError();
+hipError_t launch_gather(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm) {
+  return launch(gather_kernel, grid, kThreads, st, tm, a);
 }
 
 }  // namespace ckv

@@ -38,8 +38,20 @@ def parse():
     p.add_argument("--layers", type=int, default=0, help="limit the layer count (0 = all)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-threads", type=int, default=0)
-    p.add_argument("--streams", type=int, default=2,
-                   help="layers are issued round-robin on this many streams (one workspace each)")
+    p.add_argument("--streams", type=int, default=1,
+                   help="layers are issued round-robin on this many streams (one workspace each); "
+                        "with more than one, launches overlap and per-launch times include it")
+    p.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                   help="first run an elementwise kernel that reads and writes MIB MiB (the "
+                        "reference for scaling FETCH_SIZE / WRITE_SIZE counters)")
+    p.add_argument("--summarize-trace", metavar="DIR",
+                   help="print a markdown summary of a rocprofv3 --kernel-trace --stats "
+                        "output directory and exit (no GPU needed)")
+    p.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                   help="print the calibrated per-launch HBM traffic from two rocprofv3 --pmc "
+                        "runs (FETCH_SIZE, WRITE_SIZE) and exit (no GPU needed)")
+    p.add_argument("--copy-mib", type=int, default=1024,
+                   help="size the calibration copy used, for --summarize-pmc")
     return p.parse_args()
 
 
@@ -71,12 +83,143 @@ class Hip:
         self.lib.hipEventDestroy(e)
 
 
+KERNEL_SOURCES = ("paper_2508_02401_amd/csrc/ckv_score.hip", "paper_2508_02401_amd/csrc/ckv_select.hip",
+                  "paper_2508_02401_amd/csrc/ckv_device.h", "paper_2508_02401_amd/csrc/ckv_internal.h",
+                  "paper_2508_02401_amd/build.py")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_llama8b-128k-stack.md")
+
+
+def kernel_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def committed_traffic(kernel: str):
+    """Counter-measured HBM bytes per launch of `kernel` from the committed
+    summary, or None when there is none or the kernel sources changed since."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            text = f.read()
+    except OSError:
+        return None
+    start = text.find("```json")
+    if start < 0:
+        return None
+    end = text.find("```", start + 7)
+    try:
+        data = json.loads(text[start + 7:end])
+    except ValueError:
+        return None
+    if data.get("source_sha256") != kernel_source_hash():
+        return None
+    entry = data.get("kernels", {}).get(kernel)
+    return None if entry is None else float(entry["traffic_bytes_per_launch"])
+
+
+def _kernel_short(name: str) -> str:
+    import re
+    m = re.search(r"ckv::\(anonymous namespace\)::(\w+)", name)
+    if m:
+        return m.group(1)
+    if "neg_kernel" in name:
+        return "calibration_copy(neg)"
+    return name[:60]
+
+
+def summarize_trace(d: str) -> None:
+    import csv
+    import glob
+    stats = glob.glob(os.path.join(d, "**", "*kernel_stats.csv"), recursive=True)
+    if not stats:
+        raise SystemExit("no kernel_stats.csv under " + d)
+    rows = list(csv.DictReader(open(stats[0])))
+    # this library's kernels (the torch kernels are the input draws, outside
+    # the timed region)
+    rows = [r for r in rows if _kernel_short(r["Name"]).endswith("_kernel")]
+    print("| kernel | calls | total ms | avg us | min us | max us | % of all GPU time |")
+    print("|---|---|---|---|---|---|---|")
+    for r in rows:
+        print("| %s | %s | %.3f | %.2f | %.2f | %.2f | %.2f |" % (
+            _kernel_short(r["Name"]), r["Calls"], float(r["TotalDurationNs"]) / 1e6,
+            float(r["AverageNs"]) / 1e3, float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3,
+            float(r["Percentage"])))
+
+
+def _pmc_means(d: str, counter: str):
+    import csv
+    import glob
+    import collections
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit("no counter_collection.csv under " + d)
+    vals = collections.defaultdict(list)
+    for r in csv.DictReader(open(files[0])):
+        if r["Counter_Name"] == counter:
+            vals[_kernel_short(r["Kernel_Name"])].append(float(r["Counter_Value"]))
+    return {k: (sum(v) / len(v), len(v)) for k, v in vals.items()}
+
+
+def summarize_pmc(fetch_dir: str, write_dir: str, copy_mib: int) -> None:
+    fetch = _pmc_means(fetch_dir, "FETCH_SIZE")
+    write = _pmc_means(write_dir, "WRITE_SIZE")
+    copy_bytes = copy_mib * 1024 * 1024
+    cal = "calibration_copy(neg)"
+    if cal not in fetch or cal not in write:
+        raise SystemExit("the calibration copy kernel is missing from the counter runs")
+    # counters are in KiB per dispatch; scale so that the copy reads and
+    # writes exactly copy_bytes
+    f_scale = copy_bytes / (fetch[cal][0] * 1024.0)
+    w_scale = copy_bytes / (write[cal][0] * 1024.0)
+    print("calibration: elementwise copy of %d MiB read %.1f KiB and wrote %.1f KiB per dispatch"
+          % (copy_mib, fetch[cal][0], write[cal][0]))
+    print("scale factors: FETCH_SIZE x %.4f, WRITE_SIZE x %.4f" % (f_scale, w_scale))
+    print()
+    print("| kernel | dispatches | FETCH_SIZE KiB | WRITE_SIZE KiB | calibrated HBM MB per launch |")
+    print("|---|---|---|---|---|")
+    out = {}
+    for k in sorted(fetch):
+        if k == cal or k not in write or not k.endswith("_kernel"):
+            continue  # only this library's kernels
+        t = fetch[k][0] * 1024.0 * f_scale + write[k][0] * 1024.0 * w_scale
+        out[k] = {"fetch_kib": fetch[k][0], "write_kib": write[k][0],
+                  "traffic_bytes_per_launch": t}
+        print("| %s | %d | %.1f | %.1f | %.2f |" % (k, fetch[k][1], fetch[k][0], write[k][0], t / 1e6))
+    print()
+    print("```json")
+    print(json.dumps({"source_sha256": kernel_source_hash(), "fetch_scale": f_scale,
+                      "write_scale": w_scale, "kernels": out}, indent=1))
+    print("```")
+
+
+def calibration_copy(mib: int) -> None:
+    import torch
+    n = mib * 1024 * 1024 // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    print("bench: calibration copy of %d MiB done" % mib, file=sys.stderr, flush=True)
+    del src, dst
+    torch.cuda.empty_cache()
+
+
 def main():
     args = parse()
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace)
+        return
+    if args.summarize_pmc:
+        summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.copy_mib)
+        return
     if args.gpus != 1:
-        print("bench.py runs on one GPU only: the eviction path has no multi-GPU mode in this "
-              "build (each KV head and layer is independent; see DESIGN.md for how it shards).",
-              file=sys.stderr)
+        print("bench.py runs on one GPU only: the eviction path has no multi-GPU mode (every KV "
+              "head, layer and prompt is independent, so a multi-GPU run would shard by KV head "
+              "or layer with no communication).", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
@@ -87,6 +230,8 @@ def main():
 
     ckv.load()
     dev = torch.device("cuda:0")
+    if args.calibrate_copy > 0:
+        calibration_copy(args.calibrate_copy)
     wl = synth.WORKLOADS[args.workload]
     n_layers = wl.n_layers if args.layers <= 0 else min(args.layers, wl.n_layers)
     desc = ckv.layer_desc(wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.window, wl.dtype, 0.0,
@@ -208,6 +353,7 @@ def main():
         flops.append(f)
     dom_tflops = float(np.mean(flops)) / (stage_avg[dom] / 1e3) / 1e12
 
+    traffic = committed_traffic(dom + "_kernel")  # counter-measured HBM bytes per launch
     result = {
         "metric": "prompt tokens compressed/sec per layer (L=32K/128K) + achieved HBM GB/s",
         "value": value,
@@ -233,7 +379,8 @@ def main():
         "stage_ms_avg": stage_avg,
         "roofline": {"kernel": dom + "_kernel", "bound": "hbm", "achieved": dom_gbs,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": dom_gbs / HBM_PEAK_GBS,
-                     "traffic": None, "avg_launch_ms": stage_avg[dom],
+                     "traffic": traffic, "traffic_gbs": None if traffic is None else
+                     traffic / (stage_avg[dom] / 1e3) / 1e9, "avg_launch_ms": stage_avg[dom],
                      "algorithmic_bytes_per_launch": float(np.mean(dom_bytes)),
                      "mfma_tflops": dom_tflops, "mfma_frac_bf16": dom_tflops / BF16_PEAK_TFLOPS},
         "wall_s_timed": wall,

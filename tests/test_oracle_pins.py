@@ -14,7 +14,9 @@ or index, transposed operand, off-by-one mask, mean vs sum, pool order)
 fails at least one test here.
 """
 import itertools
+import json
 import math
+import os
 from fractions import Fraction as F
 
 import numpy as np
@@ -27,23 +29,28 @@ import oracle
 LN2 = math.log(2.0)
 
 # ---------------------------------------------------------------------------
-# Hand-worked example (my own construction, exact in rationals).
-# One KV group of two query heads, d = 1, scale = 1, L = 6, w = 2 (prefix 4).
-# Keys k = [1, 0, 0, 2, 0, 0].
-#   head 0: both window rows q = ln 2  -> exp(s_j) = 2^{k_j} = [2,1,1,4,1,1]
-#   head 1: both window rows q = -ln 2 -> exp(s_j) = 2^{-k_j} = [1/2,1,1,1/4,1,1]
-# Window row i sits at position L-w+i and sees keys 0..L-w+i (causal).
-#   head 0, row 0: keys 0..4, Z = 9;  row 1: keys 0..5, Z = 10
-#     S0 = [2/9+2/10, 1/9+1/10, 1/9+1/10, 4/9+4/10, 1/9+1/10, 1/10]
-#        = [19/45, 19/90, 19/90, 38/45, 19/90, 1/10]   (total 2 = w)
-#   head 1, row 0: Z = 15/4; row 1: Z = 19/4
-#     S1 = [2/15+2/19, 4/15+4/19, 4/15+4/19, 1/15+1/19, 4/15+4/19, 4/19]
+# Hand-worked example (my own construction, exact in rationals); the values
+# and their derivation are in tests/golden/hand_example.json.
 # ---------------------------------------------------------------------------
-HW_K = np.array([[1.0], [0.0], [0.0], [2.0], [0.0], [0.0]])
-HW_Q = np.array([[[LN2], [LN2]], [[-LN2], [-LN2]]])  # [head, row, d]
-HW_S0 = [F(19, 45), F(19, 90), F(19, 90), F(38, 45), F(19, 90), F(1, 10)]
-HW_S1 = [F(2, 15) + F(2, 19), F(4, 15) + F(4, 19), F(4, 15) + F(4, 19),
-         F(1, 15) + F(1, 19), F(4, 15) + F(4, 19), F(4, 19)]
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _golden(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def _frac(text):
+    """'a/b+c/d' -> exact Fraction."""
+    return sum((F(t) for t in text.split("+")), F(0))
+
+
+HAND = _golden("hand_example.json")
+HW_K = np.array(HAND["K"], dtype=np.float64)[:, None]
+HW_Q = np.array([[[sg * LN2]] * HAND["window"] for sg in HAND["q_sign"]])  # [head, row, d]
+HW_S0 = [_frac(t) for t in HAND["window_sums"]["head0"]]
+HW_S1 = [_frac(t) for t in HAND["window_sums"]["head1"]]
+POOLS = {"avg": oracle.POOL_AVG, "max": oracle.POOL_MAX}
 
 
 def _close(x, fr, rel=1e-12):
@@ -60,43 +67,25 @@ def test_hand_example_window_sums_exact():
 
 
 def test_hand_example_head1_prefix_values():
-    # the prefix of head 1 reduces to [68, 136, 136, 34] / 285
-    assert HW_S1[:4] == [F(68, 285), F(136, 285), F(136, 285), F(34, 285)]
+    assert HW_S1[:4] == [_frac(t) for t in HAND["head1_prefix_reduced"]]
 
 
-@pytest.mark.parametrize("mask,kp,mode,budget,expect_idx,expect_scores", [
-    # head 0 alone, no pooling: prefix [19/45, 19/90, 19/90, 38/45] -> keep 3, 0
-    ([0], 1, oracle.POOL_AVG, 4, [0, 3, 4, 5], [F(19, 45), F(19, 90), F(19, 90), F(38, 45)]),
-    # avg pooling (kernel 3, zero padding, divide by 3) changes the answer
-    ([0], 3, oracle.POOL_AVG, 4, [2, 3, 4, 5], [F(19, 90), F(38, 135), F(19, 45), F(19, 54)]),
-    # max pooling makes plateaus; B = 4 keeps the upper plateau
-    ([0], 3, oracle.POOL_MAX, 4, [2, 3, 4, 5], [F(19, 45), F(19, 45), F(38, 45), F(38, 45)]),
-    # B = 5: the tie 0 vs 1 on the lower plateau goes to the lower index
-    ([0], 3, oracle.POOL_MAX, 5, [0, 2, 3, 4, 5], [F(19, 45), F(19, 45), F(38, 45), F(38, 45)]),
-    # both heads, no pooling: mean of the two prefixes; exact tie 1 vs 2 -> 1
-    ([0, 1], 1, oracle.POOL_AVG, 4, [1, 3, 4, 5],
-     [F(113, 342), F(1177, 3420), F(1177, 3420), F(412, 855)]),
-    # both heads, max pooling: pool each head, then average (not the reverse)
-    ([0, 1], 3, oracle.POOL_MAX, 4, [2, 3, 4, 5],
-     [F(769, 1710), F(769, 1710), F(113, 171), F(113, 171)]),
-    # budget >= L keeps everything
-    ([0, 1], 1, oracle.POOL_AVG, 6, [0, 1, 2, 3, 4, 5],
-     [F(113, 342), F(1177, 3420), F(1177, 3420), F(412, 855)]),
-    # budget == w keeps only the window
-    ([1], 1, oracle.POOL_AVG, 2, [4, 5], [F(68, 285), F(136, 285), F(136, 285), F(34, 285)]),
-])
-def test_hand_example_selection(mask, kp, mode, budget, expect_idx, expect_scores):
-    scores, idx, _ = oracle.select_group(HW_Q[mask], HW_K, 2, 1.0, mode, kp, budget)
-    assert idx.tolist() == expect_idx
+@pytest.mark.parametrize("case", HAND["selection"], ids=lambda c: c["why"][:40])
+def test_hand_example_selection(case):
+    mask = case["mask"]
+    scores, idx, _ = oracle.select_group(HW_Q[mask], HW_K, HAND["window"], 1.0, POOLS[case["pool"]],
+                                         case["kp"], case["budget"])
+    assert idx.tolist() == case["idx"]
     for j in range(4):
-        assert _close(scores[j], expect_scores[j]), (j, scores[j], expect_scores[j])
+        expect = _frac(case["scores"][j])
+        assert _close(scores[j], expect), (j, scores[j], expect)
 
 
 def test_hand_example_mean_then_pool_differs():
     # pinning reading R6: the mean-then-pool order would give these scores instead
     mean = [(a + b) / 2 for a, b in zip(HW_S0[:4], HW_S1[:4])]
     mtp = [max(mean[max(0, j - 1):j + 2]) for j in range(4)]
-    assert mtp == [F(1177, 3420), F(1177, 3420), F(412, 855), F(412, 855)]
+    assert mtp == [_frac(t) for t in HAND["mean_then_pool_max3"]]
     scores, _, _ = oracle.select_group(HW_Q, HW_K, 2, 1.0, oracle.POOL_MAX, 3, 4)
     assert not _close(scores[0], mtp[0], rel=1e-3)
 
@@ -372,22 +361,12 @@ def test_gather_rows_bitwise():
 # ---------------------------------------------------------------------------
 # Algorithm 1: hand-worked examples and invariants.
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("e,total,m,M,expect", [
-    # m=32: R = 204, shares 102, 61.2->61, 40.8->41; sum 300 at once
-    ([0.5, 0.3, 0.2], 300, 32, 300, [134, 93, 73]),
-    # R = 272: 263.84->264, 2.72->3 (x3) -> 401; one token leaves the
-    # lowest-error layer, ties to the lowest index (layer 1)
-    ([0.97, 0.01, 0.01, 0.01], 400, 32, 300, [296, 34, 35, 35]),
-    # 269.28->269 clips at M=300; 1.36->1, 1.36->1, 0 -> 398; two tokens go
-    # to the highest-error layer below M, both to layer 1 (tie, lowest index)
-    ([0.99, 0.005, 0.005, 0.0], 400, 32, 300, [300, 35, 33, 32]),
-    # R = 1, 0.5 rounds half to even -> 0; the one token goes to layer 0
-    ([0.5, 0.5], 65, 32, 97, [33, 32]),
-])
-def test_algorithm1_hand_examples(e, total, m, M, expect):
-    B, rc = oracle.allocate_budgets(e, total, m, M)
+@pytest.mark.parametrize("case", _golden("algorithm1_examples.json")["cases"],
+                         ids=lambda c: str(c["budgets"]))
+def test_algorithm1_hand_examples(case):
+    B, rc = oracle.allocate_budgets(case["e"], case["total"], case["m"], case["M"])
     assert rc == oracle.OK
-    assert B.tolist() == expect
+    assert B.tolist() == case["budgets"]
 
 
 @pytest.mark.parametrize("seed", range(40))

@@ -285,8 +285,9 @@ def main():
     torch.cuda.synchronize()
 
     hip = Hip()
-    # ev[step][layer] = (begin events, end events) of the four stages
-    ev = [[([hip.event() for _ in range(4)], [hip.event() for _ in range(4)])
+    # ev[step][layer] = (begin events, end events) of the stages
+    ns = ckv.CKV_NUM_STAGES
+    ev = [[([hip.event() for _ in range(ns)], [hip.event() for _ in range(ns)])
            for _ in range(n_layers)] for _ in range(args.steps)]
     t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -300,7 +301,7 @@ def main():
     ms_total = t_start.elapsed_time(t_end)
     ms_per_step = ms_total / args.steps
 
-    stage_names = ["rowstats", "score", "select", "gather"]
+    stage_names = list(ckv.STAGE_NAMES)
     stage_ms = {n: [] for n in stage_names}
     for k in range(args.steps):
         for li in range(n_layers):
@@ -336,11 +337,12 @@ def main():
         b = 0
         for L in wl.seq_lens:
             if dom == "rowstats":
-                # every key of the prompt, the chosen Q rows, chunk partials
+                # every key of the prompt and the chosen Q rows
                 b += n_kv * L * d * elt + n_chosen * w * d * elt
             else:
-                # prefix keys, chosen Q rows, row lse, scores written
-                b += n_kv * (L - w) * d * elt + n_chosen * w * d * elt + n_kv * (L - w) * 4
+                # prefix keys, chosen Q rows, and the window sum of every
+                # chosen head written per prefix token
+                b += n_kv * (L - w) * d * elt + n_chosen * w * d * elt + n_chosen * (L - w) * 4
         dom_bytes.append(b)
     dom_gbs = float(np.mean(dom_bytes)) / (stage_avg[dom] / 1e3) / 1e9
     # MFMA work of the dominant kernel (one logit pass over its keys)

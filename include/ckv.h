@@ -181,11 +181,12 @@ int ckv_last_hip_error(void);
  * each stage's first kernel launch records its start time into begin[s] and
  * its last kernel records its end time into end[s] (hipExtLaunchKernel events:
  * no marker packets are added to the stream, so the timing does not perturb
- * the launches). Stages: 0 row statistics (pass 1), 1 scoring (pass 2; the
- * small merge kernel between the passes is not covered), 2 selection
- * (threshold search), 3 compaction and gather. Arrays are hipEvent_t[4]
- * owned by the caller, created with timing enabled; pass NULL to stop. Per
- * host thread. */
+ * the launches). Stages: 0 row statistics (K pass 1), 1 window sums (K pass
+ * 2; the small merge kernel between the passes is not covered), 2 pooling,
+ * head mean and histogram, 3 selection (threshold search), 4 compaction and
+ * gather. Arrays are hipEvent_t[CKV_NUM_STAGES] owned by the caller, created
+ * with timing enabled; pass NULL to stop. Per host thread. */
+#define CKV_NUM_STAGES 5
 int ckv_set_stage_events(void *const *begin, void *const *end);
 
 #ifdef __cplusplus

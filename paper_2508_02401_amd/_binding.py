@@ -228,13 +228,19 @@ def ckv_allocate_budgets(err_norm, total: int, m: int, M: int):
     return out, st
 
 
+CKV_NUM_STAGES = 5
+STAGE_NAMES = ("rowstats", "score", "pool", "select", "gather")
+
+
 def ckv_set_stage_events(begin, end) -> None:
-    """begin/end: sequences of 4 raw hipEvent_t handles, or None to stop."""
+    """begin/end: sequences of CKV_NUM_STAGES raw hipEvent_t handles, or None to stop."""
     if begin is None or end is None:
         _check(load().ckv_set_stage_events(None, None), "ckv_set_stage_events")
         return
-    b = (ctypes.c_void_p * 4)(*begin)
-    e = (ctypes.c_void_p * 4)(*end)
+    if len(begin) != CKV_NUM_STAGES or len(end) != CKV_NUM_STAGES:
+        raise ValueError("ckv_set_stage_events: need %d begin and end events" % CKV_NUM_STAGES)
+    b = (ctypes.c_void_p * CKV_NUM_STAGES)(*begin)
+    e = (ctypes.c_void_p * CKV_NUM_STAGES)(*end)
     _check(load().ckv_set_stage_events(b, e), "ckv_set_stage_events")
 
 

@@ -12,8 +12,8 @@
 namespace {
 
 thread_local int g_last_hip_error = 0;
-thread_local hipEvent_t g_ev_begin[4] = {nullptr, nullptr, nullptr, nullptr};
-thread_local hipEvent_t g_ev_end[4] = {nullptr, nullptr, nullptr, nullptr};
+thread_local hipEvent_t g_ev_begin[ckv::kNumStages] = {};
+thread_local hipEvent_t g_ev_end[ckv::kNumStages] = {};
 thread_local bool g_events_on = false;
 
 constexpr size_t kAlign = 256;
@@ -30,21 +30,42 @@ int64_t range_size(int64_t Ls) {
   return per <= ckv::kRangeMin ? ckv::kRangeMin : ceil_div(per, ckv::kRangeMin) * ckv::kRangeMin;
 }
 
-// Per-prompt workspace, in order: chunk partials, row lse, scores, selection
-// control words, histograms, candidates, per-range counts/offsets.
+// K stages of one KV head of a prompt of seq_len tokens.
+int64_t k_stages(const ckv_layer_desc* d, int64_t seq_len) {
+  return ceil_div(seq_len, ckv::stage_tokens(d->head_dim * elt_bytes(d->dtype)));
+}
+
+// Most workgroups per KV head a K pass can use for this prompt.
+int64_t max_split(const ckv_layer_desc* d, int64_t seq_len) {
+  const int64_t p = ceil_div(k_stages(d, seq_len), ckv::kMinStagesPerWg);
+  return p < ckv::kMaxSplit ? p : ckv::kMaxSplit;
+}
+
+// Head slots per KV head in the window-sum buffer: every chosen head of a
+// group, at most G and at most kMaxRows / w8.
+int64_t wsum_heads(const ckv_layer_desc* d) {
+  const int64_t G = d->num_q_heads / d->num_kv_heads;
+  const int64_t by_rows = ckv::kMaxRows / ((d->window + 7) / 8 * 8);
+  const int64_t h = G < by_rows ? G : by_rows;
+  return h > 0 ? h : 1;
+}
+
+// Per-prompt workspace, in order: K-pass partials, row lse, head window
+// sums, scores, selection control words, histograms, candidates, per-range
+// counts/offsets.
 struct WsLayout {
-  size_t partial, lse, scores, ctl, hist, cand, rsure, roff, reqb, total;
+  size_t partial, lse, wsum, scores, ctl, hist, cand, rsure, roff, reqb, total;
 };
 
 WsLayout seq_ws_layout(const ckv_layer_desc* d, const ckv_seq* s) {
   const int64_t n_kv = d->num_kv_heads;
-  const int64_t n_chunks = ceil_div(s->seq_len, ckv::kChunk);
   const int64_t Ls = s->seq_len - d->window;
   const int64_t n_ranges = ceil_div(Ls, range_size(Ls));
   WsLayout w;
   size_t o = 0;
-  w.partial = o; o += align_up((size_t)n_kv * n_chunks * ckv::kMaxRows * sizeof(float2));
+  w.partial = o; o += align_up((size_t)n_kv * max_split(d, s->seq_len) * ckv::kMaxRows * sizeof(float2));
   w.lse = o;     o += align_up((size_t)n_kv * ckv::kMaxRows * sizeof(float));
+  w.wsum = o;    o += align_up((size_t)n_kv * wsum_heads(d) * Ls * sizeof(float));
   w.scores = o;  o += align_up((size_t)n_kv * Ls * sizeof(float));
   w.ctl = o;     o += align_up((size_t)n_kv * ckv::kCtlWords * sizeof(uint32_t));
   w.hist = o;    o += align_up((size_t)n_kv * ckv::kHistBins * sizeof(uint32_t));
@@ -145,7 +166,7 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
     a.grp_off[d->num_kv_heads] = (int16_t)off;
   }
   a.elt = elt_bytes(d->dtype);
-  int32_t blk_rows = 0, blk_score = 0, blk_sel = 0, blk_gather = 0;
+  int32_t blk_kpass = 0, blk_pool = 0, blk_sel = 0, blk_gather = 0;
   for (int32_t i = 0; i < n; ++i) {
     const ckv_seq& s = seqs[i];
     ckv::SeqArgs& q = a.seq[i];
@@ -164,23 +185,34 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
     q.idx = s.idx;
     q.k_out = s.k_out;
     q.v_out = s.v_out;
-    q.n_chunks = (int32_t)ceil_div(s.seq_len, ckv::kChunk);
-    q.n_tiles = (int32_t)ceil_div(Ls, ckv::kTileOut);
+    {
+      // K-pass workgroups of this prompt: about kTargetWgs over its KV
+      // heads, at least kMinStagesPerWg stages each. It depends on the prompt
+      // alone, so a prompt's results do not depend on the rest of the batch.
+      const int64_t n_st = k_stages(d, s.seq_len);
+      int64_t per_wg = ceil_div(d->num_kv_heads * n_st, ckv::kTargetWgs);
+      if (per_wg < ckv::kMinStagesPerWg) per_wg = ckv::kMinStagesPerWg;
+      const int64_t split = ceil_div(n_st, per_wg), cap = max_split(d, s.seq_len);
+      q.n_split = (int32_t)(split < cap ? split : cap);
+    }
+    q.wsum_heads = (int32_t)wsum_heads(d);
+    q.n_ptiles = (int32_t)ceil_div(Ls, ckv::kPoolTile);
     q.range = (int32_t)range_size(Ls);
     q.n_ranges = (int32_t)ceil_div(Ls, q.range);
     q.n_gblk = (int32_t)ceil_div(q.n_ret, ckv::kGatherRows);
-    q.blk_rows = blk_rows;
-    q.blk_score = blk_score;
+    q.blk_kpass = blk_kpass;
+    q.blk_pool = blk_pool;
     q.blk_sel = blk_sel;
     q.blk_gather = blk_gather;
-    blk_rows += q.n_chunks * d->num_kv_heads;
-    blk_score += q.n_tiles * d->num_kv_heads;
+    blk_kpass += q.n_split * d->num_kv_heads;
+    blk_pool += q.n_ptiles * d->num_kv_heads;
     blk_sel += q.n_ranges * d->num_kv_heads;
     blk_gather += q.n_gblk * d->num_kv_heads;
     if (ws) {
       const WsLayout l = seq_ws_layout(d, &s);
       q.partial = reinterpret_cast<float2*>(ws + l.partial);
       q.lse = reinterpret_cast<float*>(ws + l.lse);
+      q.wsum = reinterpret_cast<float*>(ws + l.wsum);
       if (scores_from_ws && !q.scores) q.scores = reinterpret_cast<float*>(ws + l.scores);
       q.ctl = reinterpret_cast<uint32_t*>(ws + l.ctl);
       q.hist = reinterpret_cast<uint32_t*>(ws + l.hist);
@@ -194,13 +226,13 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
   return CKV_OK;
 }
 
-int grid_rows(const ckv::LayerArgs& a) {
+int grid_kpass(const ckv::LayerArgs& a) {
   const ckv::SeqArgs& q = a.seq[a.num_seqs - 1];
-  return q.blk_rows + q.n_chunks * a.n_kv;
+  return q.blk_kpass + q.n_split * a.n_kv;
 }
-int grid_score(const ckv::LayerArgs& a) {
+int grid_pool(const ckv::LayerArgs& a) {
   const ckv::SeqArgs& q = a.seq[a.num_seqs - 1];
-  return q.blk_score + q.n_tiles * a.n_kv;
+  return q.blk_pool + q.n_ptiles * a.n_kv;
 }
 int grid_sel(const ckv::LayerArgs& a) {
   const ckv::SeqArgs& q = a.seq[a.num_seqs - 1];
@@ -230,12 +262,14 @@ ckv::Timing timing(int stage, bool first, bool last) {
 int run_score(const ckv_layer_desc* d, const ckv::LayerArgs& a, hipStream_t st) {
   hipError_t e;
   const ckv::Timing none;
-  if ((e = ckv::launch_rowstats(d->dtype, a, grid_rows(a), st,
+  if ((e = ckv::launch_rowstats(d->dtype, a, grid_kpass(a), st,
                                 timing(ckv::kStageRowStats, true, true))) != hipSuccess)
     return hip_fail(e);
   if ((e = ckv::launch_lse(a, a.num_seqs * a.n_kv, st, none)) != hipSuccess) return hip_fail(e);
-  if ((e = ckv::launch_score(d->dtype, a, grid_score(a), st,
+  if ((e = ckv::launch_score(d->dtype, a, grid_kpass(a), st,
                              timing(ckv::kStageScore, true, true))) != hipSuccess)
+    return hip_fail(e);
+  if ((e = ckv::launch_pool(a, grid_pool(a), st, timing(ckv::kStagePool, true, true))) != hipSuccess)
     return hip_fail(e);
   return CKV_OK;
 }
@@ -404,13 +438,16 @@ const char* ckv_status_string(int status) {
 
 int ckv_last_hip_error(void) { return g_last_hip_error; }
 
+static_assert(ckv::kNumStages == CKV_NUM_STAGES, "stage count of the C ABI");
+static_assert(sizeof(ckv::LayerArgs) <= 4096, "kernel argument block");
+
 int ckv_set_stage_events(void* const* begin, void* const* end) {
   if (!begin || !end) {
     g_events_on = false;
-    for (int i = 0; i < 4; ++i) g_ev_begin[i] = g_ev_end[i] = nullptr;
+    for (int i = 0; i < ckv::kNumStages; ++i) g_ev_begin[i] = g_ev_end[i] = nullptr;
     return CKV_OK;
   }
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < ckv::kNumStages; ++i) {
     g_ev_begin[i] = (hipEvent_t)begin[i];
     g_ev_end[i] = (hipEvent_t)end[i];
   }

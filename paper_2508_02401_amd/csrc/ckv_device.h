@@ -12,6 +12,7 @@ namespace dev {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
@@ -92,31 +93,38 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* wsum, 
   return before + x - v;
 }
 
-// Find, in a histogram of nbins bins read through `get(bin)`, the bin holding
+// Find, in a histogram of NBINS bins read through `get(bin)`, the bin holding
 // the need-th largest key (bins ordered by value, need >= 1 and <= total).
-// Each thread owns nbins/kThreads consecutive bins, walked from the top.
-// Returns (bin, keys in higher bins, keys in the bin) in res[0..2] for every
-// thread of the workgroup.
-template <typename Get>
-__device__ __forceinline__ void find_bin(int nbins, uint32_t need, Get get, uint32_t* wsum,
-                                         uint32_t* res) {
-  const int per = nbins / kThreads;  // nbins is a multiple of kThreads
-  const int top = nbins - 1 - per * (int)threadIdx.x;
+// Each thread owns NBINS/kThreads consecutive bins, walked from the top; the
+// reads are unrolled so that they are all in flight at once. Returns (bin,
+// keys in higher bins, keys in the bin) in res[0..2] for every thread of the
+// workgroup.
+template <int NBINS, typename Get>
+__device__ __forceinline__ void find_bin(uint32_t need, Get get, uint32_t* wsum, uint32_t* res) {
+  static_assert(NBINS % kThreads == 0, "bins per thread");
+  constexpr int kPer = NBINS / kThreads;
+  const int top = NBINS - 1 - kPer * (int)threadIdx.x;
+  uint32_t c[kPer];
   uint32_t local = 0;
-  for (int i = 0; i < per; ++i) local += get(top - i);
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    c[i] = get(top - i);
+    local += c[i];
+  }
   uint32_t tot;
   const uint32_t above = block_excl_scan<kThreads>(local, wsum, tot);
   if (above < need && need <= above + local) {
     uint32_t run = above;
-    for (int i = 0; i < per; ++i) {
-      const uint32_t c = get(top - i);
-      if (need <= run + c) {
+    bool found = false;
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      if (!found && need <= run + c[i]) {
         res[0] = (uint32_t)(top - i);
         res[1] = run;
-        res[2] = c;
-        break;
+        res[2] = c[i];
+        found = true;
       }
-      run += c;
+      run += c[i];
     }
   }
   __syncthreads();

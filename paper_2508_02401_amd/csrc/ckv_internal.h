@@ -11,10 +11,12 @@ constexpr int kMaxSeqs = 16;
 constexpr int kMaxQHeads = 128;
 constexpr int kMaxKvHeads = 64;
 constexpr int kMaxRows = 128;      // chosen-head rows per group after padding each head to 8
-constexpr int kChunk = 1024;       // tokens per row-statistics workgroup
-constexpr int kTileComp = 512;     // tokens whose logits one scoring workgroup computes
+constexpr int kStageBytes = 16384; // K bytes per LDS stage of the two K passes
+constexpr int kMaxSplit = 512;     // workgroups per (prompt, KV head) in a K pass
+constexpr int kMinStagesPerWg = 4; // K stages per workgroup (at least)
+constexpr int kTargetWgs = 512;    // K-pass workgroups per launch: 2 on each of 256 CUs
+constexpr int kPoolTile = 2048;    // scores per pooling workgroup
 constexpr int kHalo = 16;          // pooling halo on each side (pool kernel <= 2*16+1)
-constexpr int kTileOut = kTileComp - 2 * kHalo;  // scores one scoring workgroup writes
 constexpr int kGatherRows = 64;    // retained rows per gather workgroup
 constexpr int kHistBits = 12;      // first-level histogram: key bits 30..19
 constexpr int kHistBins = 1 << kHistBits;
@@ -34,7 +36,20 @@ enum Ctl {
   kCtlWords = 16
 };
 
-enum Stage { kStageRowStats = 0, kStageScore = 1, kStageSelect = 2, kStageGather = 3 };
+enum Stage {
+  kStageRowStats = 0,
+  kStageScore = 1,
+  kStagePool = 2,
+  kStageSelect = 3,
+  kStageGather = 4,
+  kNumStages = 5
+};
+
+// Tokens per K stage for rows of row_bytes: kStageBytes, or one 32-token
+// block of larger rows.
+constexpr int stage_tokens(int row_bytes) {
+  return 32 * row_bytes > kStageBytes ? 32 : kStageBytes / row_bytes;
+}
 
 // One prompt of the batch, in the form the kernels read.
 struct SeqArgs {
@@ -51,20 +66,22 @@ struct SeqArgs {
   void* k_out;             // [n_kv][n_ret][d]
   void* v_out;
   // workspace
-  float2* partial;         // [n_kv][n_chunks][kMaxRows]: (max logit, sum exp2) per chunk
+  float2* partial;         // [n_kv][n_split][kMaxRows]: (max logit, sum exp2) per workgroup
   float* lse;              // [n_kv][kMaxRows]: per-row log2-sum-exp2 in exp2 units
+  float* wsum;             // [n_kv][wsum_heads][L - w]: window sum of each chosen head
   uint32_t* ctl;           // [n_kv][kCtlWords]
   uint32_t* hist;          // [n_kv][kHistBins]
   uint2* cand;             // [n_kv][L - w]: (key, index) of threshold-bin candidates
   uint32_t* rsure;         // [n_kv][n_ranges]: keys above the threshold bin per range
   uint32_t* roff;          // [n_kv][n_ranges]: output offset of each range
   uint32_t* reqb;          // [n_kv][n_ranges]: threshold-equal keys before each range
-  int32_t n_chunks;        // ceil(L / kChunk)
-  int32_t n_tiles;         // ceil((L - w) / kTileOut)
+  int32_t n_split;         // P: workgroups per KV head in each K pass
+  int32_t wsum_heads;      // head slots per KV head in wsum
+  int32_t n_ptiles;        // ceil((L - w) / kPoolTile)
   int32_t n_ranges;        // ceil((L - w) / range)
   int32_t range;           // scores per selection range (multiple of kRangeMin)
-  int32_t blk_rows;        // first workgroup of this prompt in the row-statistics grid
-  int32_t blk_score;       // ... in the scoring grid
+  int32_t blk_kpass;       // first workgroup of this prompt in the two K-pass grids
+  int32_t blk_pool;        // ... in the pooling grid
   int32_t blk_sel;         // ... in the selection grids (n_kv * n_ranges per prompt)
   int32_t blk_gather;      // ... in the gather grid
   int32_t n_gblk;          // gather workgroups per KV head
@@ -103,6 +120,7 @@ struct Timing {
 hipError_t launch_rowstats(int dtype, const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
 hipError_t launch_lse(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
 hipError_t launch_score(int dtype, const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
+hipError_t launch_pool(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
 hipError_t launch_clear(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
 hipError_t launch_hist(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
 hipError_t launch_filter(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);

@@ -11,24 +11,29 @@
 //
 // The exact softmax needs each row's normaliser before the column sums, so
 // the logits are formed twice from K:
-//   rowstats_kernel  pass 1: per (group, 1024-token chunk) online max and
-//                    sum of exp2 for every chosen row;
-//   lse_kernel       merges the chunk partials into one log2-sum-exp2 per row;
-//   score_kernel     pass 2: exp2(alpha*s - lse), window sums per head,
-//                    pooling with a 16-token halo, head mean, and the
+//   rowstats_kernel  pass 1: online max and sum of exp2 of every chosen row,
+//                    one partial per workgroup;
+//   lse_kernel       merges the partials into one log2-sum-exp2 per row;
+//   score_kernel     pass 2: exp2(alpha*s - lse) summed over each chosen
+//                    head's window rows, written per head (S[h,j]);
+//   pool_kernel      pooling along the tokens, head mean, scores, and the
 //                    first-level histogram of the score keys that the
 //                    selection starts from.
 //
-// Work decomposition (both passes): a group's chosen rows are padded per head
-// to a multiple of 8 and split into 32-row query blocks. Each wave of a
-// workgroup owns one query block and keeps its query operand in registers for
-// its whole life. K is streamed once per workgroup through a ring of LDS
-// slots with direct global-to-LDS loads (global_load_lds_dwordx4): every load
-// instruction moves 1 KB of consecutive rows, so HBM sees whole lines, and the
-// loads of the next stages stay in flight (explicit partial vmcnt waits and a
-// plain s_barrier, since a fenced barrier would drain them). Rows land in LDS
-// with their 16-byte chunks XOR-swizzled so that the MFMA-layout reads (lane l
-// takes token l % 32) spread over all banks. Logits come from v_mfma 32x32x16.
+// Work decomposition of the two K passes: a group's chosen rows are padded
+// per head to a multiple of 8 and split into 32-row query blocks; each wave
+// keeps one query block's operand in registers for its whole life. K is cut
+// into 16 KB stages, and the P workgroups of a group take the stages
+// round-robin (workgroup p: stages p, p+P, p+2P, ...), so at any moment the
+// whole chip reads one compact window of each K head rather than hundreds of
+// scattered streams; this keeps HBM near its streaming rate. Stages go
+// through a ring of LDS slots filled by direct global-to-LDS loads
+// (global_load_lds_dwordx4): every load instruction moves 1 KB of consecutive
+// rows, and the loads of the next stages stay in flight (explicit partial
+// vmcnt waits and a plain s_barrier, since a fenced barrier would drain
+// them). Rows land in LDS with their 16-byte chunks XOR-swizzled so that the
+// MFMA-layout reads (lane l takes token l % 32) spread over all banks. Logits
+// come from v_mfma 32x32x16.
 #include <math.h>
 
 #include "ckv_device.h"
@@ -150,36 +155,40 @@ struct Stager {
   }
 };
 
-// Stage size: 16 KB (at least one 32-token block): with two blocks per stage
-// every wave has a block when a group has 2 query blocks.
+// Stage size: kStageBytes (at least one 32-token block).
 template <int DT, int D>
 constexpr int stage_bytes() {
-  return 32 * D * Elt<DT>::bytes > 16384 ? 32 * D * Elt<DT>::bytes : 16384;
+  return stage_tokens(D * Elt<DT>::bytes) * D * Elt<DT>::bytes;
 }
 
-// Wait until at most n_after of this wave's later stages are still loading.
+// Wait until at most n_after of this wave's later stages are still loading
+// (each stage is PT load instructions per wave; n_after <= MAXA).
 template <int PT, int MAXA>
 __device__ __forceinline__ void wait_stages(int n_after) {
-  static_assert(MAXA <= 2, "ring depth");
-  if (MAXA >= 2 && n_after >= 2) __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * PT));
+  static_assert(MAXA <= 6 && MAXA * PT <= 63, "vmcnt range");
+  if (MAXA >= 6 && n_after >= 6) __builtin_amdgcn_s_waitcnt(vmcnt_imm(6 * PT));
+  else if (MAXA >= 5 && n_after >= 5) __builtin_amdgcn_s_waitcnt(vmcnt_imm(5 * PT));
+  else if (MAXA >= 4 && n_after >= 4) __builtin_amdgcn_s_waitcnt(vmcnt_imm(4 * PT));
+  else if (MAXA >= 3 && n_after >= 3) __builtin_amdgcn_s_waitcnt(vmcnt_imm(3 * PT));
+  else if (MAXA >= 2 && n_after >= 2) __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * PT));
   else if (MAXA >= 1 && n_after >= 1) __builtin_amdgcn_s_waitcnt(vmcnt_imm(PT));
   else __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
 }
 
 // Stage loop shared by both passes over stages 0..ns-1 (stage k starts at
-// token t_first + k*ST, tokens clamped to [lo, hi]) with an NS-slot LDS ring
+// token t_first + k*stride, tokens clamped to [lo, hi]) with an NS-slot LDS ring
 // (slots are distinct LDS arrays so the compiler can tell the in-flight loads
 // from the slot being read). At step k: wait for stage k, barrier (stage k is
 // complete and every wave has finished with stage k-1's slot), issue stage
 // k+NS-1 into that freed slot, then body(slot, k) reduces stage k.
 template <class S, int NS, class Body>
 __device__ __forceinline__ void stage_loop(uint4* const* slot, const char* kbase, int64_t kv_st,
-                                           int64_t t_first, int ns, int64_t lo, int64_t hi,
-                                           int wave, Body body) {
+                                           int64_t t_first, int64_t stride, int ns, int64_t lo,
+                                           int64_t hi, int wave, Body body) {
   const typename S::Plan p = S::plan(wave, kv_st);
 #pragma unroll
   for (int j = 0; j < NS - 1; ++j)
-    if (j < ns) S::fetch(kbase, kv_st, t_first + (int64_t)j * S::ST, lo, hi, p, wave, slot[j]);
+    if (j < ns) S::fetch(kbase, kv_st, t_first + j * stride, lo, hi, p, wave, slot[j]);
   for (int k0 = 0; k0 < ns; k0 += NS) {
 #pragma unroll
     for (int j = 0; j < NS; ++j) {
@@ -189,7 +198,7 @@ __device__ __forceinline__ void stage_loop(uint4* const* slot, const char* kbase
         wait_stages<S::PT, NS - 2>(left < NS - 2 ? left : NS - 2);
         __builtin_amdgcn_s_barrier();
         if (k + NS - 1 < ns)
-          S::fetch(kbase, kv_st, t_first + (int64_t)(k + NS - 1) * S::ST, lo, hi, p, wave,
+          S::fetch(kbase, kv_st, t_first + (k + NS - 1) * stride, lo, hi, p, wave,
                    slot[(j + NS - 1) % NS]);
         body(slot[j], k);
       }
@@ -221,28 +230,45 @@ __device__ __forceinline__ void stage_tiles(const uint4* slot, const int* opoff,
   }
 }
 
+// Stages of workgroup p of P over n_tok tokens: p, p+P, ... (none if p is
+// past the last stage).
+__device__ __forceinline__ int stages_of(int64_t n_tok, int st, int p, int P) {
+  const int64_t n_st = (n_tok + st - 1) / st;
+  return p < n_st ? (int)((n_st - p + P - 1) / P) : 0;
+}
+
+// Prompt and local workgroup index of workgroup b in a grid laid out by the
+// per-prompt first-workgroup offsets off(t).
+template <class Off>
+__device__ __forceinline__ int find_seq(const LayerArgs& a, int b, Off off) {
+  int s = 0;
+  for (int t = 1; t < a.num_seqs; ++t)
+    if (b >= off(a.seq[t])) s = t;
+  return s;
+}
+
 // ---------------------------------------------------------------------------
-// Pass 1: per-chunk row statistics.
+// Pass 1: row statistics.
 // ---------------------------------------------------------------------------
 template <int DT, int D, int WPQ, class S, int NS>
-__device__ __forceinline__ void rowstats_body(const LayerArgs& a, const SeqArgs& sq, int g,
-                                              int chunk, int sel0, int n_sel, int nqb,
-                                              uint4* const* slots, float2 (*red)[32]) {
+__device__ __forceinline__ void rowstats_body(const LayerArgs& a, const SeqArgs& sq, int g, int p,
+                                              int sel0, int n_sel, int nqb, uint4* const* slots,
+                                              float2 (*red)[32]) {
   constexpr int NC = S::NC;
   constexpr int NB = (S::BLOCKS + WPQ - 1) / WPQ;
   const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int qb = wave / WPQ, sub = wave % WPQ;
   const bool active = qb < nqb;
-  const int w = a.w, w8 = a.w8;
-  const int L = (int)sq.L, Ls = L - w;
+  const int w8 = a.w8;
+  const int64_t L = sq.L, Ls = L - a.w;
+  const int P = sq.n_split;
+  const int64_t stride = (int64_t)P * S::ST;
   const float alpha = a.alpha;
   const char* kbase = static_cast<const char*>(sq.k) + (int64_t)g * sq.kv_sh * S::EB;
-  const int t_begin = chunk * kChunk;
-  const int n_tok = L - t_begin < kChunk ? L - t_begin : kChunk;
-  const int ns = (n_tok + S::ST - 1) / S::ST;
+  const int ns = stages_of(L, S::ST, p, P);
   // this lane's query row (column of the MFMA result) and its last visible key
-  const int last = Ls + (qb * 32 + l32) % w8;  // >= L for padding rows
+  const int64_t last = Ls + (qb * 32 + l32) % w8;  // >= L for padding rows
 
   uint4 q[NC];
   if (active) load_queries<NC, S::EB>(a, sq, sel0, n_sel, qb, l32, h, q);
@@ -252,9 +278,10 @@ __device__ __forceinline__ void rowstats_body(const LayerArgs& a, const SeqArgs&
   for (int c = 0; c < NC; ++c) opoff[c] += sub * 32 * S::ROWB;
   float m_run = -INFINITY, z_run = 0.f;
 
-  stage_loop<S, NS>(slots, kbase, sq.kv_st, t_begin, ns, 0, L - 1, wave, [&](const uint4* slot, int k) {
+  stage_loop<S, NS>(slots, kbase, sq.kv_st, (int64_t)p * S::ST, stride, ns, 0, L - 1, wave,
+                    [&](const uint4* slot, int k) {
     if (!active) return;
-    const int ts = t_begin + k * S::ST + sub * 32;  // token of this wave's first block
+    const int64_t ts = (int64_t)p * S::ST + k * stride + sub * 32;  // this wave's first block
     bool has[NB];
 #pragma unroll
     for (int i = 0; i < NB; ++i) has[i] = sub + i * WPQ < S::BLOCKS && ts + i * WPQ * 32 < L;
@@ -264,10 +291,10 @@ __device__ __forceinline__ void rowstats_body(const LayerArgs& a, const SeqArgs&
     for (int i = 0; i < NB; ++i) {
       if (!has[i]) continue;
       // acc[i][v]: key t0 + acc_row(v, h) of this lane's query row
-      const int t0 = ts + i * WPQ * 32;
+      const int64_t t0 = ts + i * WPQ * 32;
       if (t0 + 32 > Ls) {  // keys inside the window: causal mask (a uniform branch)
-        const int rel = last - t0;
-        const int lim = rel < -1 ? -1 : (rel > 32 ? 32 : rel);
+        const int64_t rel = last - t0;
+        const int lim = rel < -1 ? -1 : (rel > 32 ? 32 : (int)rel);
 #pragma unroll
         for (int v = 0; v < 16; ++v)
           if (acc_row(v, h) > lim) acc[i][v] = -INFINITY;
@@ -306,7 +333,7 @@ __device__ __forceinline__ void rowstats_body(const LayerArgs& a, const SeqArgs&
 #pragma unroll
     for (int sw = 0; sw < WPQ; ++sw)
       z += red[qq * WPQ + sw][r].y * fast_exp2(red[qq * WPQ + sw][r].x * alpha - ms);
-    sq.partial[((int64_t)g * sq.n_chunks + chunk) * kMaxRows + tid] = make_float2(m, z);
+    sq.partial[((int64_t)g * P + p) * kMaxRows + tid] = make_float2(m, z);
   }
 }
 
@@ -321,34 +348,31 @@ __global__ __launch_bounds__(kThreads) void rowstats_kernel(const LayerArgs a) {
   __shared__ float2 red[kWaves][32];
   uint4* const slots[NS] = {slot0, slot1, slot2, slot3};
 
-  const int b = xcd_remap(blockIdx.x, gridDim.x);
-  int s = 0;
-  for (int t = 1; t < a.num_seqs; ++t)
-    if (b >= a.seq[t].blk_rows) s = t;
-  const SeqArgs& sq = a.seq[s];
-  const int local = b - sq.blk_rows;
-  const int g = local / sq.n_chunks;
-  const int chunk = local - g * sq.n_chunks;
+  const int b = blockIdx.x;
+  const SeqArgs& sq = a.seq[find_seq(a, b, [](const SeqArgs& t) { return t.blk_kpass; })];
+  const int local = b - sq.blk_kpass;
+  const int g = local / sq.n_split;
+  const int p = local - g * sq.n_split;
   const int sel0 = a.grp_off[g], n_sel = a.grp_off[g + 1] - sel0;
   const int nqb = (n_sel * a.w8 + 31) >> 5;
 
   // the selection state of this group starts from zero in every call; the
-  // scoring kernel that accumulates into it runs after this one
-  if (chunk == 0 && a.do_hist) {
+  // pooling kernel that accumulates into it runs after this one
+  if (p == 0 && a.do_hist) {
     for (int i = threadIdx.x; i < kCtlWords; i += kThreads) sq.ctl[g * kCtlWords + i] = 0u;
     for (int i = threadIdx.x; i < kHistBins; i += kThreads)
       sq.hist[(int64_t)g * kHistBins + i] = 0u;
   }
   const int wpq = waves_per_qblock(nqb);
-  if (wpq == 1) rowstats_body<DT, D, 1, S, NS>(a, sq, g, chunk, sel0, n_sel, nqb, slots, red);
-  else if (wpq == 2) rowstats_body<DT, D, 2, S, NS>(a, sq, g, chunk, sel0, n_sel, nqb, slots, red);
-  else rowstats_body<DT, D, 4, S, NS>(a, sq, g, chunk, sel0, n_sel, nqb, slots, red);
+  if (wpq == 1) rowstats_body<DT, D, 1, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, red);
+  else if (wpq == 2) rowstats_body<DT, D, 2, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, red);
+  else rowstats_body<DT, D, 4, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, red);
 }
 
-// Merge chunk partials: lse[r] = log2(sum_j exp2(alpha * s_rj)) so that the
-// softmax probability is exp2(alpha * s - lse). Padding rows get +inf (p = 0).
-// One workgroup per (prompt, group, 32-row block); the 8 lanes of a row merge
-// every 8th chunk each, then one lane merges their 8 results.
+// Merge the workgroup partials: lse[r] = log2(sum_j exp2(alpha * s_rj)) so
+// that the softmax probability is exp2(alpha * s - lse). Padding rows get +inf
+// (p = 0). One workgroup per (prompt, group, 32-row block); the 8 lanes of a
+// row merge every 8th partial each, then one lane merges their 8 results.
 constexpr int kLseRows = 32;
 constexpr int kLseLanes = kThreads / kLseRows;
 
@@ -373,10 +397,10 @@ __global__ __launch_bounds__(kThreads) void lse_kernel(const LayerArgs a) {
   const bool valid = slot < n_sel && i < a.w;
   float m = -INFINITY, z = 0.f;
   if (valid) {
-    const float2* p = sq.partial + (int64_t)g * sq.n_chunks * kMaxRows + r;
+    const float2* pp = sq.partial + (int64_t)g * sq.n_split * kMaxRows + r;
 #pragma unroll 8
-    for (int c = c0; c < sq.n_chunks; c += kLseLanes) {
-      const float2 v = p[(int64_t)c * kMaxRows];
+    for (int c = c0; c < sq.n_split; c += kLseLanes) {
+      const float2 v = pp[(int64_t)c * kMaxRows];
       lse_merge(m, z, v.x, v.y, a.alpha);
     }
   }
@@ -391,30 +415,27 @@ __global__ __launch_bounds__(kThreads) void lse_kernel(const LayerArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Pass 2: probabilities, window sums, pooling, head mean.
+// Pass 2: probabilities and per-head window sums.
 // ---------------------------------------------------------------------------
 constexpr int kGroupRows = kMaxRows / 8;  // 8-row groups of one group's rows
 
 template <int DT, int D, int WPQ, class S, int NS>
-__device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq, int g, int tile,
+__device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq, int g, int p,
                                            int sel0, int n_sel, int nqb, uint4* const* slots,
-                                           uint4* slot01, float* gsum) {
+                                           float* gsum) {
   constexpr int NC = S::NC;
   constexpr int NB = (S::BLOCKS + WPQ - 1) / WPQ;
+  constexpr int ST = S::ST;
   const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int qb = wave / WPQ, sub = wave % WPQ;
   const bool active = qb < nqb;
-  const int w8 = a.w8;
-  const int Ls = (int)sq.L - a.w;
-  const int j0 = tile * kTileOut;
-  const int base = j0 - kHalo;  // token of computed column 0
+  const int64_t Ls = sq.L - a.w;
+  const int P = sq.n_split;
+  const int64_t stride = (int64_t)P * ST;
   const float alpha = a.alpha;
   const char* kbase = static_cast<const char*>(sq.k) + (int64_t)g * sq.kv_sh * S::EB;
-
-  // stages overlapping the prefix [0, Ls)
-  const int end_tok = base + kTileComp < Ls ? base + kTileComp : Ls;
-  const int ns = (end_tok - base + S::ST - 1) / S::ST;
+  const int ns = stages_of(Ls, ST, p, P);
 
   uint4 q[NC];
   float4 cv[4];  // lse of this lane's 16 result rows qb*32 + 8*a4 + 4*h + e (exp2 units)
@@ -429,23 +450,43 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
 #pragma unroll
   for (int c = 0; c < NC; ++c) opoff[c] += sub * 32 * S::ROWB;
 
-  stage_loop<S, NS>(slots, kbase, sq.kv_st, base, ns, 0, Ls - 1, wave, [&](const uint4* slot, int k) {
+  // Head window sums of stage kk: the head in slot hs owns 8-row groups
+  // [hs*w8/8, (hs+1)*w8/8) of gsum buffer kk % 2; their fixed-order sum is
+  // written to wsum[g][hs][token].
+  const int gph = a.w8 / 8;
+  float* wsum_g = sq.wsum + (int64_t)g * sq.wsum_heads * Ls;
+  auto fold = [&](int kk) {
+    const float* gb = gsum + (kk & 1) * (kGroupRows * ST);
+    const int64_t t0 = (int64_t)p * ST + kk * stride;
+    for (int e = tid; e < n_sel * ST; e += kThreads) {
+      const int hs = e / ST, c = e - hs * ST;
+      if (t0 + c >= Ls) continue;
+      float acc = gb[(hs * gph) * ST + c];
+      for (int r8 = 1; r8 < gph; ++r8) acc += gb[(hs * gph + r8) * ST + c];
+      wsum_g[(int64_t)hs * Ls + t0 + c] = acc;
+    }
+  };
+
+  stage_loop<S, NS>(slots, kbase, sq.kv_st, (int64_t)p * ST, stride, ns, 0, Ls - 1, wave,
+                    [&](const uint4* slot, int k) {
+    // the barrier before this step ordered every wave's gsum writes of stage
+    // k-1 before these reads, and this fold's reads before stage k+1 reuses
+    // the buffer
+    if (k > 0) fold(k - 1);
     if (!active) return;
-    const int cs = k * S::ST + sub * 32;  // computed column of this wave's first block
+    const int64_t ts = (int64_t)p * ST + k * stride + sub * 32;  // this wave's first block
     bool has[NB];
 #pragma unroll
-    for (int i = 0; i < NB; ++i) {
-      const int tb = base + cs + i * WPQ * 32;  // first token of block i
-      // blocks wholly before token 0 or at/after Ls are not needed
-      has[i] = sub + i * WPQ < S::BLOCKS && tb + 32 > 0 && tb < Ls;
-    }
+    for (int i = 0; i < NB; ++i) has[i] = sub + i * WPQ < S::BLOCKS && ts + i * WPQ * 32 < Ls;
     f32x16 acc[NB];
     stage_tiles<DT, S, WPQ, false>(slot, opoff, q, has, acc);
+    float* gb = gsum + (k & 1) * (kGroupRows * ST);
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
       if (!has[i]) continue;
-      // acc[i][v]: query row qb*32 + acc_row(v, h), key at computed column col;
-      // prefix keys are visible to every window row, so no mask is needed.
+      // acc[i][v]: query row qb*32 + acc_row(v, h), key (sub + i*WPQ)*32 + l32
+      // of the stage; prefix keys are visible to every window row, so no
+      // mask is needed (keys at or past Ls are never written out).
       float gs[4];
 #pragma unroll
       for (int a4 = 0; a4 < 4; ++a4)
@@ -455,60 +496,141 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
                  fast_exp2(fmaf(acc[i][4 * a4 + 3], alpha, -cv[a4].w));
 #pragma unroll
       for (int a4 = 0; a4 < 4; ++a4) gs[a4] += __shfl_xor(gs[a4], 32);
-      // lane half h stores groups a4 = h and h + 2
-      const int col = cs + i * WPQ * 32 + l32;
-      gsum[(qb * 4 + h) * kTileComp + col] = h ? gs[1] : gs[0];
-      gsum[(qb * 4 + 2 + h) * kTileComp + col] = h ? gs[3] : gs[2];
+      // lane half h stores 8-row groups a4 = h and h + 2
+      const int col = (sub + i * WPQ) * 32 + l32;
+      gb[(qb * 4 + h) * ST + col] = h ? gs[1] : gs[0];
+      gb[(qb * 4 + 2 + h) * ST + col] = h ? gs[3] : gs[2];
     }
   });
+  // stage_loop ended with a barrier: the last stage's sums are complete
+  if (ns > 0) fold(ns - 1);
+}
 
-  const bool do_hist = a.do_hist && sq.n_keep > 0;
-  uint32_t* hist_lds = reinterpret_cast<uint32_t*>(slot01);  // K stages are no longer read
-  if (do_hist)
-    for (int i = tid; i < kHistBins; i += kThreads) hist_lds[i] = 0u;
-  __syncthreads();
+template <int DT, int D>
+__global__ __launch_bounds__(kThreads) void score_kernel(const LayerArgs a) {
+  using S = Stager<DT, D, stage_bytes<DT, D>()>;
+  constexpr int NS = 4;  // 4-slot ring
+  __shared__ uint4 slot0[S::VEC];
+  __shared__ uint4 slot1[S::VEC];
+  __shared__ uint4 slot2[S::VEC];
+  __shared__ uint4 slot3[S::VEC];
+  // gsum[buf][r8][col]: sum over the 8 rows of 8-row group r8 of p at stage
+  // column col, double-buffered by stage parity
+  __shared__ float gsum[2 * kGroupRows * S::ST];
+  uint4* const slots[NS] = {slot0, slot1, slot2, slot3};
 
-  // head window sums: the head in slot hs owns 8-row groups
-  // [hs*w8/8, (hs+1)*w8/8); fold them into the slot's first group row
-  const int gph = w8 / 8;
-  for (int col = tid; col < kTileComp; col += kThreads) {
-    for (int hs = 0; hs < n_sel; ++hs) {
-      float acc = gsum[(hs * gph) * kTileComp + col];
-      for (int r8 = 1; r8 < gph; ++r8) acc += gsum[(hs * gph + r8) * kTileComp + col];
-      gsum[(hs * gph) * kTileComp + col] = acc;
+  const int b = blockIdx.x;
+  const SeqArgs& sq = a.seq[find_seq(a, b, [](const SeqArgs& t) { return t.blk_kpass; })];
+  const int local = b - sq.blk_kpass;
+  const int g = local / sq.n_split;
+  const int p = local - g * sq.n_split;
+  const int sel0 = a.grp_off[g], n_sel = a.grp_off[g + 1] - sel0;
+  const int nqb = (n_sel * a.w8 + 31) >> 5;
+  const int wpq = waves_per_qblock(nqb);
+  if (wpq == 1) score_body<DT, D, 1, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, gsum);
+  else if (wpq == 2) score_body<DT, D, 2, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, gsum);
+  else score_body<DT, D, 4, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, gsum);
+}
+
+// ---------------------------------------------------------------------------
+// Pooling along the tokens, head mean, scores and the selection histogram.
+// One workgroup per (prompt, group, kPoolTile scores); thread t owns the
+// kPoolPer consecutive scores starting at t * kPoolPer. The window sums of
+// two heads are staged in LDS per barrier, then every thread pools from a
+// register copy of its kPoolPer + 2*kHalo inputs, with the pool radius R a
+// template parameter so that only the needed taps are evaluated.
+// ---------------------------------------------------------------------------
+constexpr int kPoolPer = kPoolTile / kThreads;  // scores per thread
+constexpr int kPoolRow = kPoolTile + 2 * kHalo;
+constexpr int kPoolWin = kPoolPer + 2 * kHalo;  // inputs one thread pools from
+static_assert(kPoolPer % 4 == 0 && kHalo % 4 == 0, "float4 staging");
+
+// total[u] += pool over [u - R, u + R] of this thread's window x (avg: sum / kp).
+template <int R>
+__device__ __forceinline__ void pool_window(const float* x, bool is_max, float inv_kp,
+                                            float* total) {
+  static_assert(R <= kHalo, "pool radius within the halo");
+#pragma unroll
+  for (int u = 0; u < kPoolPer; ++u) {
+    float v = x[kHalo + u];
+#pragma unroll
+    for (int dt = 1; dt <= R; ++dt) {
+      const float lo = x[kHalo + u - dt], hi = x[kHalo + u + dt];
+      v = is_max ? fmaxf(v, fmaxf(lo, hi)) : v + (lo + hi);
     }
+    total[u] += is_max ? v : v * inv_kp;
   }
-  __syncthreads();
+}
 
-  const int r = a.kp >> 1;
-  const float kpf = (float)a.kp;
-  float* out = sq.scores + (int64_t)g * Ls;
-  for (int o = tid; o < kTileOut; o += kThreads) {
-    const int j = j0 + o;
-    if (j >= Ls) break;
-    const int lo = j < r ? -j : -r;
-    const int hi = Ls - 1 - j < r ? Ls - 1 - j : r;
-    const int tc = o + kHalo;
-    float total = 0.f;
-    for (int hs = 0; hs < n_sel; ++hs) {
-      const float* row = gsum + (hs * gph) * kTileComp + tc;
-      if (a.pool == 0) {
-        float acc = 0.f;
-        for (int dt = lo; dt <= hi; ++dt) acc += row[dt];
-        total += acc / kpf;
-      } else {
-        float m = row[lo];
-        for (int dt = lo + 1; dt <= hi; ++dt) m = fmaxf(m, row[dt]);
-        total += m;
+template <int R>
+__device__ __forceinline__ void pool_tile(const LayerArgs& a, const SeqArgs& sq, int g, int tile,
+                                          float (*row)[kPoolRow], uint32_t* hist_lds) {
+  const int tid = threadIdx.x;
+  const int64_t Ls = sq.L - a.w;
+  const int64_t j0 = (int64_t)tile * kPoolTile;
+  const int n_out = Ls - j0 < kPoolTile ? (int)(Ls - j0) : kPoolTile;
+  const int n_sel = a.grp_off[g + 1] - a.grp_off[g];
+  const bool is_max = a.pool != 0;
+  const float pad = is_max ? -INFINITY : 0.f;  // max ignores padding; avg counts it as 0
+  const float inv_kp = 1.f / (float)a.kp;
+  const bool do_hist = a.do_hist && sq.n_keep > 0;
+  const float* wsum_g = sq.wsum + (int64_t)g * sq.wsum_heads * Ls;
+
+  float total[kPoolPer];
+#pragma unroll
+  for (int u = 0; u < kPoolPer; ++u) total[u] = 0.f;
+  for (int hs0 = 0; hs0 < n_sel; hs0 += 2) {
+    const int nh = n_sel - hs0 < 2 ? n_sel - hs0 : 2;
+    if (hs0 > 0) __syncthreads();  // the previous rows' reads are done
+    // all loads of the (one or two) rows are issued before any is stored
+    constexpr int kLoads = (kPoolRow + kThreads - 1) / kThreads;
+    float v0[kLoads], v1[kLoads];
+    const float* src0 = wsum_g + (int64_t)hs0 * Ls;
+    const float* src1 = src0 + Ls;
+#pragma unroll
+    for (int i = 0; i < kLoads; ++i) {
+      const int64_t j = j0 - kHalo + tid + i * kThreads;
+      const bool in = j >= 0 && j < Ls;
+      v0[i] = in ? src0[j] : pad;
+      v1[i] = in && nh > 1 ? src1[j] : pad;
+    }
+#pragma unroll
+    for (int i = 0; i < kLoads; ++i) {
+      const int idx = tid + i * kThreads;
+      if (idx < kPoolRow) {
+        row[0][idx] = v0[i];
+        row[1][idx] = v1[i];
       }
     }
-    const float score = total / (float)n_sel;
-    out[j] = score;
+    if (hs0 == 0 && do_hist)
+      for (int i = tid; i < kHistBins; i += kThreads) hist_lds[i] = 0u;
+    __syncthreads();
+    for (int e = 0; e < nh; ++e) {
+      // x[i] = window sum at score index tid*kPoolPer - kHalo + i
+      float x[kPoolWin];
+      const float4* rp = reinterpret_cast<const float4*>(row[e] + tid * kPoolPer);
+#pragma unroll
+      for (int v = 0; v < kPoolWin / 4; ++v) {
+        const float4 t4 = rp[v];
+        x[4 * v] = t4.x;
+        x[4 * v + 1] = t4.y;
+        x[4 * v + 2] = t4.z;
+        x[4 * v + 3] = t4.w;
+      }
+      pool_window<R>(x, is_max, inv_kp, total);
+    }
+  }
+  const int o0 = tid * kPoolPer;
+  float* out = sq.scores + (int64_t)g * Ls + j0 + o0;
+#pragma unroll
+  for (int u = 0; u < kPoolPer; ++u) {
+    if (o0 + u >= n_out) break;
+    const float score = total[u] / (float)n_sel;
+    out[u] = score;
     if (do_hist) atomicAdd(&hist_lds[score_key(score) >> kHistShift], 1u);
   }
   if (!do_hist) return;
-
-  // first-level histogram of this tile's keys into the group's histogram
+  // this tile's part of the group's first-level histogram
   __syncthreads();
   uint32_t* ghist = sq.hist + (int64_t)g * kHistBins;
   for (int i = tid; i < kHistBins; i += kThreads) {
@@ -517,35 +639,26 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
   }
 }
 
-template <int DT, int D>
-__global__ __launch_bounds__(kThreads) void score_kernel(const LayerArgs a) {
-  using S = Stager<DT, D, stage_bytes<DT, D>()>;
-  constexpr int NS = 3;  // 3-slot ring
-  static_assert(kTileComp % S::ST == 0, "tile is whole stages");
-  static_assert(2 * S::VEC * 16 >= kHistBins * 4, "histogram reuses two K slots");
-  // slots 0 and 1 are adjacent so that the histogram can reuse them as one
-  __shared__ uint4 slot01[2 * S::VEC];
-  __shared__ uint4 slot2[S::VEC];
-  // gsum[r8][col]: sum over the 8 rows of 8-row group r8 of p at computed
-  // column col; rows of one head are whole groups, so a head's window sum is a
-  // fixed-order sum of its groups
-  __shared__ float gsum[kGroupRows * kTileComp];
-  uint4* const slots[NS] = {slot01, slot01 + S::VEC, slot2};
+template <int R>
+__device__ __forceinline__ void pool_dispatch(int r, const LayerArgs& a, const SeqArgs& sq, int g,
+                                              int tile, float (*row)[kPoolRow], uint32_t* hist) {
+  if constexpr (R > kHalo - 1) {
+    pool_tile<R>(a, sq, g, tile, row, hist);
+  } else {
+    if (r == R) pool_tile<R>(a, sq, g, tile, row, hist);
+    else pool_dispatch<R + 1>(r, a, sq, g, tile, row, hist);
+  }
+}
 
-  const int b = xcd_remap(blockIdx.x, gridDim.x);
-  int s = 0;
-  for (int t = 1; t < a.num_seqs; ++t)
-    if (b >= a.seq[t].blk_score) s = t;
-  const SeqArgs& sq = a.seq[s];
-  const int local = b - sq.blk_score;
-  const int g = local / sq.n_tiles;
-  const int tile = local - g * sq.n_tiles;
-  const int sel0 = a.grp_off[g], n_sel = a.grp_off[g + 1] - sel0;
-  const int nqb = (n_sel * a.w8 + 31) >> 5;
-  const int wpq = waves_per_qblock(nqb);
-  if (wpq == 1) score_body<DT, D, 1, S, NS>(a, sq, g, tile, sel0, n_sel, nqb, slots, slot01, gsum);
-  else if (wpq == 2) score_body<DT, D, 2, S, NS>(a, sq, g, tile, sel0, n_sel, nqb, slots, slot01, gsum);
-  else score_body<DT, D, 4, S, NS>(a, sq, g, tile, sel0, n_sel, nqb, slots, slot01, gsum);
+__global__ __launch_bounds__(kThreads) void pool_kernel(const LayerArgs a) {
+  __shared__ __align__(16) float row[2][kPoolRow];
+  __shared__ uint32_t hist_lds[kHistBins];
+  const int b = blockIdx.x;
+  const SeqArgs& sq = a.seq[find_seq(a, b, [](const SeqArgs& t) { return t.blk_pool; })];
+  const int local = b - sq.blk_pool;
+  const int g = local / sq.n_ptiles;
+  const int tile = local - g * sq.n_ptiles;
+  pool_dispatch<0>(a.kp >> 1, a, sq, g, tile, row, hist_lds);  // radius 0..15
 }
 
 template <template <int, int> class KernelOf>
@@ -579,6 +692,10 @@ hipError_t launch_lse(const LayerArgs& a, int grid, hipStream_t st, const Timing
 
 hipError_t launch_score(int dtype, const LayerArgs& a, int grid, hipStream_t st, const Timing& tm) {
   return launch_typed<ScoreOf>(dtype, a, grid, st, tm);
+}
+
+hipError_t launch_pool(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm) {
+  return launch(pool_kernel, grid, kThreads, st, tm, a);
 }
 
 }  // namespace ckv

@@ -18,6 +18,8 @@
 //      it), appends the window positions, and copies the kept K/V rows.
 // Each step is its own launch, so stream order makes every hand-off visible
 // without device-wide fences inside the kernels.
+#include <type_traits>
+
 #include "ckv_device.h"
 
 namespace ckv {
@@ -25,7 +27,9 @@ namespace {
 
 using namespace dev;
 
-constexpr int kStep = 4 * kThreads;  // scores per compaction step (4 per thread)
+constexpr int kCompactPer = 16;                      // scores per thread and compaction step
+constexpr int kCompactStep = kCompactPer * kThreads;  // scores per compaction step
+constexpr int kFilterPer = kRangeMin / kThreads;  // scores per thread loaded up front
 
 __device__ __forceinline__ int find_seq_sel(const LayerArgs& a, int b) {
   int s = 0;
@@ -34,39 +38,52 @@ __device__ __forceinline__ int find_seq_sel(const LayerArgs& a, int b) {
   return s;
 }
 
-// Copy n rows of K and V: row src0 + i -> output row dst0 + i (contiguous runs).
-__device__ __forceinline__ void copy_run(const LayerArgs& a, const SeqArgs& sq, int g, int64_t dst0,
-                                         int64_t src0, int64_t n) {
-  const int nv = a.d * a.elt / 16;
-  const char* kb = static_cast<const char*>(sq.k) + (int64_t)g * sq.kv_sh * a.elt;
-  const char* vb = static_cast<const char*>(sq.v) + (int64_t)g * sq.kv_sh * a.elt;
-  uint4* ko = static_cast<uint4*>(sq.k_out) + (int64_t)g * sq.n_ret * nv;
-  uint4* vo = static_cast<uint4*>(sq.v_out) + (int64_t)g * sq.n_ret * nv;
-  for (int64_t e = threadIdx.x; e < n * nv; e += kThreads) {
-    const int64_t i = e / nv;
-    const int c = (int)(e - i * nv);
-    const int64_t j = src0 + i, p = dst0 + i;
-    if (j < 0 || j >= sq.L || p < 0 || p >= sq.n_ret) continue;
-    ko[p * nv + c] = reinterpret_cast<const uint4*>(kb + j * sq.kv_st * a.elt)[c];
-    vo[p * nv + c] = reinterpret_cast<const uint4*>(vb + j * sq.kv_st * a.elt)[c];
+constexpr int kCopyBatch = 8;  // 16-byte K and V chunks in flight per thread
+
+// Copy n rows of K and V: source token src(i) -> output row dst(i), for i in
+// [0, n). Rows whose source or destination is out of range are skipped. The
+// loads of a batch are all issued before its stores.
+template <class Src, class Dst>
+__device__ __forceinline__ void copy_rows(const LayerArgs& a, const SeqArgs& sq, int g, int64_t n,
+                                          Src src, Dst dst) {
+  const int nv = a.d * a.elt / 16;  // 8, 16 or 32 chunks per row
+  const int nv_log2 = nv == 8 ? 3 : (nv == 16 ? 4 : 5);
+  // native vectors (not HIP's uint4 struct) so the batch stays in registers
+  const char* __restrict__ kb = static_cast<const char*>(sq.k) + (int64_t)g * sq.kv_sh * a.elt;
+  const char* __restrict__ vb = static_cast<const char*>(sq.v) + (int64_t)g * sq.kv_sh * a.elt;
+  u32x4* __restrict__ ko = static_cast<u32x4*>(sq.k_out) + (int64_t)g * sq.n_ret * nv;
+  u32x4* __restrict__ vo = static_cast<u32x4*>(sq.v_out) + (int64_t)g * sq.n_ret * nv;
+  const int64_t total = n << nv_log2;
+  for (int64_t e0 = 0; e0 < total; e0 += (int64_t)kThreads * kCopyBatch) {
+    u32x4 kr[kCopyBatch], vr[kCopyBatch];
+    int64_t to[kCopyBatch];
+#pragma unroll
+    for (int u = 0; u < kCopyBatch; ++u) {
+      const int64_t e = e0 + threadIdx.x + (int64_t)u * kThreads;
+      const int64_t i = e >> nv_log2;
+      const int c = (int)(e & (nv - 1));
+      const int64_t j = e < total ? src(i) : -1;
+      const int64_t p = e < total ? dst(i) : -1;
+      const bool ok = j >= 0 && j < sq.L && p >= 0 && p < sq.n_ret;
+      to[u] = ok ? (p << nv_log2) + c : -1;
+      const int64_t jj = ok ? j : 0;  // row 0 is a valid address for skipped lanes
+      kr[u] = reinterpret_cast<const u32x4*>(kb + jj * sq.kv_st * a.elt)[c];
+      vr[u] = reinterpret_cast<const u32x4*>(vb + jj * sq.kv_st * a.elt)[c];
+    }
+#pragma unroll
+    for (int u = 0; u < kCopyBatch; ++u) {
+      if (to[u] >= 0) {
+        ko[to[u]] = kr[u];
+        vo[to[u]] = vr[u];
+      }
+    }
   }
 }
 
-// Copy the listed rows: source token jl[i] -> output row pl[i].
-__device__ __forceinline__ void copy_list(const LayerArgs& a, const SeqArgs& sq, int g,
-                                          const int32_t* pl, const int32_t* jl, int n) {
-  const int nv = a.d * a.elt / 16;
-  const char* kb = static_cast<const char*>(sq.k) + (int64_t)g * sq.kv_sh * a.elt;
-  const char* vb = static_cast<const char*>(sq.v) + (int64_t)g * sq.kv_sh * a.elt;
-  uint4* ko = static_cast<uint4*>(sq.k_out) + (int64_t)g * sq.n_ret * nv;
-  uint4* vo = static_cast<uint4*>(sq.v_out) + (int64_t)g * sq.n_ret * nv;
-  for (int e = threadIdx.x; e < n * nv; e += kThreads) {
-    const int i = e / nv, c = e - i * nv;
-    const int64_t j = jl[i], p = pl[i];
-    if (j < 0 || j >= sq.L || p < 0 || p >= sq.n_ret) continue;
-    ko[p * nv + c] = reinterpret_cast<const uint4*>(kb + j * sq.kv_st * a.elt)[c];
-    vo[p * nv + c] = reinterpret_cast<const uint4*>(vb + j * sq.kv_st * a.elt)[c];
-  }
+// Contiguous run: row src0 + i -> output row dst0 + i.
+__device__ __forceinline__ void copy_run(const LayerArgs& a, const SeqArgs& sq, int g, int64_t dst0,
+                                         int64_t src0, int64_t n) {
+  copy_rows(a, sq, g, n, [=](int64_t i) { return src0 + i; }, [=](int64_t i) { return dst0 + i; });
 }
 
 // Zero the selection control words and histograms (ckv_select on caller
@@ -116,10 +133,10 @@ __device__ void resolve(const SeqArgs& sq, int g, int64_t Ls, uint32_t* ctl, uin
   uint32_t need = (uint32_t)sq.n_keep - ctl[kCtlAbove];
   int shift = kHistShift;
   // radix select on bits 18..9, then 8..0, among keys still matching prefix
-  for (int level = 0; level < 2; ++level) {
-    const int nb = level == 0 ? 10 : 9;
+  auto level = [&](auto nb_c) -> bool {
+    constexpr int nb = decltype(nb_c)::value;
+    constexpr int nbins = 1 << nb;
     const int nshift = shift - nb;
-    const int nbins = 1 << nb;
     for (int i = tid; i < nbins; i += kThreads) lds_a[i] = 0u;
     __syncthreads();
     for (uint32_t c = tid; c < n_cand; c += kThreads) {
@@ -127,14 +144,16 @@ __device__ void resolve(const SeqArgs& sq, int g, int64_t Ls, uint32_t* ctl, uin
       if ((key >> shift) == prefix) atomicAdd(&lds_a[(key >> nshift) & (nbins - 1)], 1u);
     }
     __syncthreads();
-    find_bin(nbins, need, [&](int bin) { return lds_a[bin]; }, wsum, res);
+    find_bin<nbins>(need, [&](int bin) { return lds_a[bin]; }, wsum, res);
     prefix = (prefix << nb) | res[0];
     need -= res[1];
     shift = nshift;
     const uint32_t cnt = res[2];
     __syncthreads();
-    if (cnt == need) break;  // every key of this bin is kept
-  }
+    return cnt == need;  // every key of this bin is kept
+  };
+  static_assert(kHistShift == 19, "radix levels cover bits 18..0");
+  if (!level(std::integral_constant<int, 10>{})) level(std::integral_constant<int, 9>{});
   // keys compare on key >> shift: above prefix kept, equal kept while need lasts
   const int n_ranges = sq.n_ranges;
   for (int i = tid; i < n_ranges; i += kThreads) {
@@ -194,19 +213,58 @@ __global__ __launch_bounds__(kThreads) void filter_kernel(const LayerArgs a) {
   const int64_t Ls = sq.L - a.w;
   uint32_t* ctl = sq.ctl + g * kCtlWords;
   const uint32_t* ghist = sq.hist + (int64_t)g * kHistBins;
-  find_bin(kHistBins, (uint32_t)sq.n_keep, [&](int bin) { return ghist[bin]; }, wsum, res);
+  const float* sc = sq.scores + (int64_t)g * Ls;
+  uint2* cands = sq.cand + (int64_t)g * Ls;
+  const int64_t j0 = (int64_t)r * sq.range;
+  const int64_t j1 = j0 + sq.range < Ls ? j0 + sq.range : Ls;
+  // this thread's first kFilterPer keys are loaded before the threshold
+  // search, so their latency overlaps it
+  uint32_t key0[kFilterPer];
+#pragma unroll
+  for (int e = 0; e < kFilterPer; ++e) {
+    const int64_t j = j0 + tid + (int64_t)e * kThreads;
+    key0[e] = j < j1 ? score_key(sc[j]) : 0u;
+  }
+  find_bin<kHistBins>((uint32_t)sq.n_keep, [&](int bin) { return ghist[bin]; }, wsum, res);
   const uint32_t bin = res[0];
   if (r == 0 && tid == 0) {
     ctl[kCtlBin] = res[0];
     ctl[kCtlAbove] = res[1];
     ctl[kCtlBinCount] = res[2];
   }
-  const float* sc = sq.scores + (int64_t)g * Ls;
-  uint2* cands = sq.cand + (int64_t)g * Ls;
-  const int64_t j0 = (int64_t)r * sq.range;
-  const int64_t j1 = j0 + sq.range < Ls ? j0 + sq.range : Ls;
   uint32_t sure = 0;
-  for (int64_t j = j0 + tid; j < j1; j += kThreads) {
+  // keys loaded up front: count, then one atomic per wave reserves the
+  // wave's candidate slots, written in lane order
+  {
+    uint32_t mine = 0;
+#pragma unroll
+    for (int e = 0; e < kFilterPer; ++e) {
+      const bool in = j0 + tid + (int64_t)e * kThreads < j1;
+      const uint32_t kb = key0[e] >> kHistShift;
+      sure += in && kb > bin;
+      mine += in && kb == bin;
+    }
+    uint32_t incl = mine;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const uint32_t y = __shfl_up(incl, off);
+      if (lane >= off) incl += y;
+    }
+    const uint32_t wave_total = __shfl(incl, 63);
+    if (wave_total) {
+      uint32_t base = 0;
+      if (lane == 63) base = atomicAdd(&ctl[kCtlNumCand], wave_total);
+      base = __shfl(base, 63);
+      uint32_t at = base + incl - mine;
+#pragma unroll
+      for (int e = 0; e < kFilterPer; ++e) {
+        const int64_t j = j0 + tid + (int64_t)e * kThreads;
+        if (j < j1 && (key0[e] >> kHistShift) == bin) cands[at++] = make_uint2(key0[e], (uint32_t)j);
+      }
+    }
+  }
+  // ranges longer than kFilterPer * kThreads scores
+  for (int64_t j = j0 + tid + (int64_t)kFilterPer * kThreads; j < j1; j += kThreads) {
     const uint32_t key = score_key(sc[j]);
     const uint32_t kb = key >> kHistShift;
     sure += kb > bin;
@@ -240,10 +298,13 @@ __global__ __launch_bounds__(kThreads) void resolve_kernel(const LayerArgs a) {
   resolve(sq, g, sq.L - a.w, sq.ctl + g * kCtlWords, lds_a, lds_b, wsum, res);
 }
 
+// Kept indices of one range, in ascending order at the range's output offset,
+// then the copies of their K/V rows. Thread t takes kCompactPer consecutive
+// scores per step, so a thread's kept tokens are consecutive in the output.
 __global__ __launch_bounds__(kThreads) void compact_kernel(const LayerArgs a) {
   __shared__ uint32_t wsum[kWaves];
-  __shared__ int32_t pos_l[kStep];
-  __shared__ int32_t tok_l[kStep];
+  __shared__ int32_t pos_l[kCompactStep];
+  __shared__ int32_t tok_l[kCompactStep];
   const int b = blockIdx.x;
   const int s = find_seq_sel(a, b);
   const SeqArgs& sq = a.seq[s];
@@ -273,51 +334,53 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const LayerArgs a) {
   }
   if (nk == 0) return;
   const uint32_t* ctl = sq.ctl + g * kCtlWords;
+  const uint32_t* roff = sq.roff + (int64_t)g * sq.n_ranges;
+  uint32_t pos_carry = roff[r];
+  uint32_t end = r + 1 < sq.n_ranges ? roff[r + 1] : nk;
+  uint32_t eq_carry = sq.reqb[(int64_t)g * sq.n_ranges + r];
   const uint32_t prefix = ctl[kCtlPrefix];
   const int shift = (int)ctl[kCtlShift];
   const uint32_t need = ctl[kCtlNeedEq];
-  const uint32_t* roff = sq.roff + (int64_t)g * sq.n_ranges;
-  uint32_t eq_carry = sq.reqb[(int64_t)g * sq.n_ranges + r];
-  uint32_t pos_carry = roff[r];
-  uint32_t end = r + 1 < sq.n_ranges ? roff[r + 1] : nk;
   end = end < nk ? end : nk;
   if (end == pos_carry) return;  // nothing kept in this range
   const float* sc = sq.scores + (int64_t)g * Ls;
-  for (int64_t base = j0; base < j1 && pos_carry < end; base += kStep) {
-    const int64_t jb = base + 4 * tid;
-    int f[4];
+  for (int64_t base = j0; base < j1 && pos_carry < end; base += kCompactStep) {
+    const int64_t jt = base + (int64_t)tid * kCompactPer;  // this thread's first score
+    // flag 1: above the threshold, 2: equal to it, 0: below
+    uint32_t key[kCompactPer];
+#pragma unroll
+    for (int e = 0; e < kCompactPer; ++e) key[e] = jt + e < j1 ? score_key(sc[jt + e]) : 0u;
+    int f[kCompactPer];
     uint32_t neq = 0;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      f[e] = 0;
-      if (jb + e < j1) {
-        const uint32_t p = score_key(sc[jb + e]) >> shift;
-        f[e] = p > prefix ? 1 : (p == prefix ? 2 : 0);
-      }
+    for (int e = 0; e < kCompactPer; ++e) {
+      const uint32_t p = key[e] >> shift;
+      f[e] = jt + e >= j1 ? 0 : (p > prefix ? 1 : (p == prefix ? 2 : 0));
       neq += f[e] == 2;
     }
     uint32_t tot_eq, tot_sel;
     uint32_t eq_rank = eq_carry + block_excl_scan<kThreads>(neq, wsum, tot_eq);
-    bool keep[4];
+    uint32_t kept = 0;  // bit e: score jt + e is kept
     uint32_t nsel = 0;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      keep[e] = f[e] == 1;
-      if (f[e] == 2) {
-        keep[e] = eq_rank < need;
+    for (int e = 0; e < kCompactPer; ++e) {
+      bool keep = f[e] == 1;
+      if (f[e] == 2) {  // equal keys: the lowest indices, while any are needed
+        keep = eq_rank < need;
         ++eq_rank;
       }
-      nsel += keep[e];
+      kept |= (uint32_t)keep << e;
+      nsel += keep;
     }
     const uint32_t first = block_excl_scan<kThreads>(nsel, wsum, tot_sel);
     uint32_t pos = pos_carry + first;
     uint32_t li = first;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      if (keep[e] && pos < end) {
-        out[pos] = (int32_t)(jb + e);
+    for (int e = 0; e < kCompactPer; ++e) {
+      if (((kept >> e) & 1u) && pos < end) {
+        out[pos] = (int32_t)(jt + e);
         pos_l[li] = (int32_t)pos;
-        tok_l[li] = (int32_t)(jb + e);
+        tok_l[li] = (int32_t)(jt + e);
         ++pos;
         ++li;
       }
@@ -325,7 +388,8 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const LayerArgs a) {
     if (a.do_gather) {
       __syncthreads();
       const uint32_t n = tot_sel < end - pos_carry ? tot_sel : end - pos_carry;
-      copy_list(a, sq, g, pos_l, tok_l, (int)n);
+      copy_rows(a, sq, g, n, [&](int64_t i) { return (int64_t)tok_l[i]; },
+                [&](int64_t i) { return (int64_t)pos_l[i]; });
       __syncthreads();
     }
     eq_carry += tot_eq;
@@ -333,8 +397,11 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const LayerArgs a) {
   }
 }
 
-// Standalone retain/evict (ckv_gather): rows idx[g, r] of K and V.
+// Standalone retain/evict (ckv_gather): rows idx[g, r] of K and V for the
+// kGatherRows output rows of this workgroup. An out-of-range index leaves its
+// output row untouched.
 __global__ __launch_bounds__(kThreads) void gather_kernel(const LayerArgs a) {
+  __shared__ int32_t tok_l[kGatherRows];
   const int b = blockIdx.x;
   int s = 0;
   for (int t = 1; t < a.num_seqs; ++t)
@@ -343,21 +410,12 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const LayerArgs a) {
   const int local = b - sq.blk_gather;
   const int g = local / sq.n_gblk;
   const int r0 = (local - g * sq.n_gblk) * kGatherRows;
-  const int nv = a.d * a.elt / 16;
+  const int n = sq.n_ret - r0 < kGatherRows ? sq.n_ret - r0 : kGatherRows;
   const int32_t* idx = sq.idx + (int64_t)g * sq.n_ret;
-  const char* kb = static_cast<const char*>(sq.k) + (int64_t)g * sq.kv_sh * a.elt;
-  const char* vb = static_cast<const char*>(sq.v) + (int64_t)g * sq.kv_sh * a.elt;
-  uint4* ko = static_cast<uint4*>(sq.k_out) + (int64_t)g * sq.n_ret * nv;
-  uint4* vo = static_cast<uint4*>(sq.v_out) + (int64_t)g * sq.n_ret * nv;
-  for (int e = threadIdx.x; e < kGatherRows * nv; e += kThreads) {
-    const int rr = e / nv, c = e - rr * nv;
-    const int r = r0 + rr;
-    if (r >= sq.n_ret) break;
-    const int64_t t = idx[r];
-    if (t < 0 || t >= sq.L) continue;  // out-of-range index: leave the row untouched
-    ko[(int64_t)r * nv + c] = reinterpret_cast<const uint4*>(kb + t * sq.kv_st * a.elt)[c];
-    vo[(int64_t)r * nv + c] = reinterpret_cast<const uint4*>(vb + t * sq.kv_st * a.elt)[c];
-  }
+  for (int i = threadIdx.x; i < n; i += kThreads) tok_l[i] = idx[r0 + i];
+  __syncthreads();
+  copy_rows(a, sq, g, n, [&](int64_t i) { return (int64_t)tok_l[i]; },
+            [&](int64_t i) { return r0 + i; });
 }
 
 }  // namespace

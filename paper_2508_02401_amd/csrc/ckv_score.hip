@@ -419,7 +419,11 @@ __global__ __launch_bounds__(kThreads) void lse_kernel(const LayerArgs a) {
 // ---------------------------------------------------------------------------
 constexpr int kGroupRows = kMaxRows / 8;  // 8-row groups of one group's rows
 
-template <int DT, int D, int WPQ, class S, int NS>
+// QM (query-block mode, when w8 is a multiple of 32): every 32-row query
+// block belongs to one head, so a lane sums its four 8-row groups in
+// registers and the block's column sums are one row of gsum; otherwise
+// gsum holds one row per 8-row group.
+template <int DT, int D, int WPQ, bool QM, class S, int NS>
 __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq, int g, int p,
                                            int sel0, int n_sel, int nqb, uint4* const* slots,
                                            float* gsum) {
@@ -450,10 +454,11 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
 #pragma unroll
   for (int c = 0; c < NC; ++c) opoff[c] += sub * 32 * S::ROWB;
 
-  // Head window sums of stage kk: the head in slot hs owns 8-row groups
-  // [hs*w8/8, (hs+1)*w8/8) of gsum buffer kk % 2; their fixed-order sum is
-  // written to wsum[g][hs][token].
-  const int gph = a.w8 / 8;
+  // Head window sums of stage kk: the head in slot hs owns gsum rows
+  // [hs*rph, (hs+1)*rph) of buffer kk % 2 (rph = its query blocks in QM, its
+  // 8-row groups otherwise); their fixed-order sum is written to
+  // wsum[g][hs][token].
+  const int rph = QM ? a.w8 / 32 : a.w8 / 8;
   float* wsum_g = sq.wsum + (int64_t)g * sq.wsum_heads * Ls;
   auto fold = [&](int kk) {
     const float* gb = gsum + (kk & 1) * (kGroupRows * ST);
@@ -461,8 +466,8 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
     for (int e = tid; e < n_sel * ST; e += kThreads) {
       const int hs = e / ST, c = e - hs * ST;
       if (t0 + c >= Ls) continue;
-      float acc = gb[(hs * gph) * ST + c];
-      for (int r8 = 1; r8 < gph; ++r8) acc += gb[(hs * gph + r8) * ST + c];
+      float acc = gb[(hs * rph) * ST + c];
+      for (int q8 = 1; q8 < rph; ++q8) acc += gb[(hs * rph + q8) * ST + c];
       wsum_g[(int64_t)hs * Ls + t0 + c] = acc;
     }
   };
@@ -494,12 +499,18 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
                  fast_exp2(fmaf(acc[i][4 * a4 + 1], alpha, -cv[a4].y)) +
                  fast_exp2(fmaf(acc[i][4 * a4 + 2], alpha, -cv[a4].z)) +
                  fast_exp2(fmaf(acc[i][4 * a4 + 3], alpha, -cv[a4].w));
-#pragma unroll
-      for (int a4 = 0; a4 < 4; ++a4) gs[a4] += __shfl_xor(gs[a4], 32);
-      // lane half h stores 8-row groups a4 = h and h + 2
       const int col = (sub + i * WPQ) * 32 + l32;
-      gb[(qb * 4 + h) * ST + col] = h ? gs[1] : gs[0];
-      gb[(qb * 4 + 2 + h) * ST + col] = h ? gs[3] : gs[2];
+      if (QM) {
+        float t = (gs[0] + gs[1]) + (gs[2] + gs[3]);
+        t += __shfl_xor(t, 32);
+        if (h == 0) gb[qb * ST + col] = t;
+      } else {
+#pragma unroll
+        for (int a4 = 0; a4 < 4; ++a4) gs[a4] += __shfl_xor(gs[a4], 32);
+        // lane half h stores 8-row groups a4 = h and h + 2
+        gb[(qb * 4 + h) * ST + col] = h ? gs[1] : gs[0];
+        gb[(qb * 4 + 2 + h) * ST + col] = h ? gs[3] : gs[2];
+      }
     }
   });
   // stage_loop ended with a barrier: the last stage's sums are complete
@@ -527,9 +538,15 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const LayerArgs a) {
   const int sel0 = a.grp_off[g], n_sel = a.grp_off[g + 1] - sel0;
   const int nqb = (n_sel * a.w8 + 31) >> 5;
   const int wpq = waves_per_qblock(nqb);
-  if (wpq == 1) score_body<DT, D, 1, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, gsum);
-  else if (wpq == 2) score_body<DT, D, 2, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, gsum);
-  else score_body<DT, D, 4, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, gsum);
+  if (a.w8 % 32 == 0) {
+    if (wpq == 1) score_body<DT, D, 1, true, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, gsum);
+    else if (wpq == 2) score_body<DT, D, 2, true, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, gsum);
+    else score_body<DT, D, 4, true, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, gsum);
+  } else {
+    if (wpq == 1) score_body<DT, D, 1, false, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, gsum);
+    else if (wpq == 2) score_body<DT, D, 2, false, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, gsum);
+    else score_body<DT, D, 4, false, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, gsum);
+  }
 }
 
 // ---------------------------------------------------------------------------

@@ -49,6 +49,13 @@ CASES = [
     ("f16-d64-G7", Case(28, 4, 64, 32, "max", 7, torch.float16), 2500, 2, 75),
     ("bf16-tile-boundary", Case(8, 2, 128, 32, "max", 7, torch.bfloat16), 992 * 3 + 32, 1, 500),
     ("bf16-chunk-boundary", Case(8, 2, 128, 32, "avg", 7, torch.bfloat16), 1024 * 2 + 1, 2, 100),
+    # one KV head: 257 workgroups share its 64-token stages round-robin
+    ("bf16-one-kv-head-many-splits", Case(4, 1, 128, 32, "max", 7, torch.bfloat16), 65536 + 17, 1,
+     256),
+    # prefix of 40 whole 64-token stages plus one token
+    ("bf16-stage-edge", Case(8, 2, 128, 32, "avg", 5, torch.bfloat16), 64 * 40 + 32 + 1, 2, 128),
+    # w8 = 48: query blocks straddle heads (8-row group sums)
+    ("bf16-w48-straddle", Case(8, 2, 128, 48, "max", 9, torch.bfloat16), 3333, 2, 200),
 ]
 
 

@@ -208,26 +208,28 @@ __device__ __forceinline__ void stage_loop(uint4* const* slot, const char* kbase
 }
 
 // Operand-reading and MFMA part shared by both passes: the wave's blocks of a
-// stage are sub, sub + WPQ, ... (NB of them at most); acc[i] receives the
-// 32x32 logit tile of block i, queries x keys when KEYS_AS_ROWS is false,
-// keys x queries otherwise. has[i] tells whether block i is computed.
+// stage are sub, sub + WPQ, ... (NB of them; the caller guarantees that they
+// lie inside the stage); acc[i] receives the 32x32 logit tile of block i,
+// queries x keys when KEYS_AS_ROWS is false, keys x queries otherwise. All
+// operands are read first and the NB accumulation chains are interleaved, so
+// the MFMA pipe never waits on a single dependent chain. Blocks past the
+// prompt are computed too (their LDS rows are clamped copies) and the caller
+// ignores them.
 template <int DT, class S, int WPQ, bool KEYS_AS_ROWS>
 __device__ __forceinline__ void stage_tiles(const uint4* slot, const int* opoff, const uint4* q,
-                                            const bool* has, f32x16* acc) {
+                                            f32x16* acc) {
   constexpr int NB = (S::BLOCKS + WPQ - 1) / WPQ;
   constexpr int NC = S::NC;
   uint4 kr[NB][NC];
 #pragma unroll
-  for (int i = 0; i < NB; ++i)
-    if (has[i]) S::operand(slot, i * WPQ, opoff, kr[i]);
+  for (int i = 0; i < NB; ++i) S::operand(slot, i * WPQ, opoff, kr[i]);
 #pragma unroll
-  for (int i = 0; i < NB; ++i) {
-    if (!has[i]) continue;
-    acc[i] = f32x16{};
+  for (int i = 0; i < NB; ++i) acc[i] = f32x16{};
 #pragma unroll
-    for (int c = 0; c < NC; ++c)
+  for (int c = 0; c < NC; ++c)
+#pragma unroll
+    for (int i = 0; i < NB; ++i)
       acc[i] = KEYS_AS_ROWS ? mfma_chunk<DT>(kr[i][c], q[c], acc[i]) : mfma_chunk<DT>(q[c], kr[i][c], acc[i]);
-  }
 }
 
 // Stages of workgroup p of P over n_tok tokens: p, p+P, ... (none if p is
@@ -280,19 +282,17 @@ __device__ __forceinline__ void rowstats_body(const LayerArgs& a, const SeqArgs&
 
   stage_loop<S, NS>(slots, kbase, sq.kv_st, (int64_t)p * S::ST, stride, ns, 0, L - 1, wave,
                     [&](const uint4* slot, int k) {
-    if (!active) return;
+    // waves past the stage's blocks (4 waves on a 2-block stage) sit out
+    if (!active || sub >= S::BLOCKS) return;
     const int64_t ts = (int64_t)p * S::ST + k * stride + sub * 32;  // this wave's first block
-    bool has[NB];
-#pragma unroll
-    for (int i = 0; i < NB; ++i) has[i] = sub + i * WPQ < S::BLOCKS && ts + i * WPQ * 32 < L;
     f32x16 acc[NB];
-    stage_tiles<DT, S, WPQ, true>(slot, opoff, q, has, acc);
+    stage_tiles<DT, S, WPQ, true>(slot, opoff, q, acc);
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
-      if (!has[i]) continue;
       // acc[i][v]: key t0 + acc_row(v, h) of this lane's query row
       const int64_t t0 = ts + i * WPQ * 32;
-      if (t0 + 32 > Ls) {  // keys inside the window: causal mask (a uniform branch)
+      if (t0 + 32 > Ls) {  // keys inside the window or past the prompt: causal
+                           // mask (a uniform branch; blocks past L mask all)
         const int64_t rel = last - t0;
         const int lim = rel < -1 ? -1 : (rel > 32 ? 32 : (int)rel);
 #pragma unroll
@@ -478,17 +478,14 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
     // k-1 before these reads, and this fold's reads before stage k+1 reuses
     // the buffer
     if (k > 0) fold(k - 1);
-    if (!active) return;
-    const int64_t ts = (int64_t)p * ST + k * stride + sub * 32;  // this wave's first block
-    bool has[NB];
-#pragma unroll
-    for (int i = 0; i < NB; ++i) has[i] = sub + i * WPQ < S::BLOCKS && ts + i * WPQ * 32 < Ls;
+    // waves past the stage's blocks (4 waves on a 2-block stage) sit out
+    if (!active || sub >= S::BLOCKS) return;
     f32x16 acc[NB];
-    stage_tiles<DT, S, WPQ, false>(slot, opoff, q, has, acc);
+    stage_tiles<DT, S, WPQ, false>(slot, opoff, q, acc);
     float* gb = gsum + (k & 1) * (kGroupRows * ST);
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
-      if (!has[i]) continue;
+      // columns at or past Ls get values too; the fold never writes them out
       // acc[i][v]: query row qb*32 + acc_row(v, h), key (sub + i*WPQ)*32 + l32
       // of the stage; prefix keys are visible to every window row, so no
       // mask is needed (keys at or past Ls are never written out).

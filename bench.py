@@ -1,9 +1,10 @@
 """Benchmark of the CompressKV prefill-end KV eviction path on one MI355X.
 
 One step = the whole path (score, select, gather) over every layer of the
-workload, one ckv_compress_layer call per layer (layers round-robin over a few
-streams, since they are independent), with all inputs
-already resident in HBM. Prints one JSON line.
+workload, with all inputs already resident in HBM: one ckv_compress_layer per
+layer on one stream by default. --pipeline instead runs ckv_score (both K
+passes and the pooling) of layer l+1 on one stream while ckv_select and
+ckv_gather of layer l run on another. Prints one JSON line.
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
 
@@ -39,8 +40,11 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-threads", type=int, default=0)
     p.add_argument("--streams", type=int, default=1,
-                   help="layers are issued round-robin on this many streams (one workspace each); "
-                        "with more than one, launches overlap and per-launch times include it")
+                   help="without --pipeline: layers are issued round-robin on this many streams "
+                        "(one workspace each); launches then overlap and per-launch times include it")
+    p.add_argument("--pipeline", action="store_true",
+                   help="two-stream pipeline (ckv_score of layer l+1 beside ckv_select and "
+                        "ckv_gather of layer l) instead of one ckv_compress_layer per layer")
     p.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                    help="first run an elementwise kernel that reads and writes MIB MiB (the "
                         "reference for scaling FETCH_SIZE / WRITE_SIZE counters)")
@@ -260,13 +264,49 @@ def main():
                 for s in range(len(wl.seq_lens))]
         layers.append((inp.mask, seqs))
     ws_bytes = max(ckv.ckv_workspace_bytes(desc, seqs) for _, seqs in layers)
-    n_streams = max(1, args.streams)
     main = torch.cuda.current_stream()
-    streams = [main] + [torch.cuda.Stream() for _ in range(n_streams - 1)]
-    wss = [torch.empty(ws_bytes, dtype=torch.uint8, device=dev) for _ in range(n_streams)]
+    if args.pipeline:
+        # Two-stream pipeline: stream A runs the scoring stages (ckv_score: both
+        # K passes and the pooling) of every layer in order, stream B the
+        # selection and gather (ckv_select, ckv_gather) of layer l while A
+        # scores layer l+1. Two workspaces and score buffers alternate; events
+        # keep A from reusing a slot before B is done with it.
+        n_streams = 2
+        side = torch.cuda.Stream()
+        streams = [main, side]
+        wss = [torch.empty(ws_bytes, dtype=torch.uint8, device=dev) for _ in range(2)]
+        score_bufs = [[torch.empty((wl.num_kv_heads, L - wl.window), dtype=torch.float32, device=dev)
+                       for L in wl.seq_lens] for _ in range(2)]
+        for li, (mask, seqs) in enumerate(layers):
+            for si, sq in enumerate(seqs):
+                sq.scores = score_bufs[li % 2][si]
+        scored = [torch.cuda.Event(enable_timing=False) for _ in range(2)]
+        selected = [torch.cuda.Event(enable_timing=False) for _ in range(2)]
+    else:
+        n_streams = max(1, args.streams)
+        streams = [main] + [torch.cuda.Stream() for _ in range(n_streams - 1)]
+        wss = [torch.empty(ws_bytes, dtype=torch.uint8, device=dev) for _ in range(n_streams)]
     torch.cuda.synchronize()
 
-    def step(events=None):
+    def step_pipeline(events=None):
+        side.wait_stream(main)
+        for li, (mask, seqs) in enumerate(layers):
+            slot = li % 2
+            if events is not None:
+                ckv.ckv_set_stage_events(events[li][0], events[li][1])
+            if li >= 2:
+                main.wait_event(selected[slot])  # layer li-2 is done with this slot
+            ckv.ckv_score(desc, mask, seqs, wss[slot], main)
+            scored[slot].record(main)
+            side.wait_event(scored[slot])
+            ckv.ckv_select(desc, seqs, wss[slot], side)
+            ckv.ckv_gather(desc, seqs, side)
+            selected[slot].record(side)
+        if events is not None:
+            ckv.ckv_set_stage_events(None, None)
+        main.wait_stream(side)
+
+    def step_layers(events=None):
         # every layer is independent: layer l runs on stream l % n_streams
         for st in streams[1:]:
             st.wait_stream(main)
@@ -280,15 +320,29 @@ def main():
         for st in streams[1:]:
             main.wait_stream(st)
 
+    step = step_pipeline if args.pipeline else step_layers
+
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
     hip = Hip()
-    # ev[step][layer] = (begin events, end events) of the stages
+    # Only the two K passes (the candidates for the dominant kernel) carry
+    # kernel start/end events: each timed launch costs a few microseconds of
+    # dispatch overlap, so the other stages are left untimed (their times are
+    # in the rocprofv3 kernel trace). ev[step][layer] = (begin, end) arrays.
+    timed = ("rowstats", "score")
     ns = ckv.CKV_NUM_STAGES
-    ev = [[([hip.event() for _ in range(ns)], [hip.event() for _ in range(ns)])
-           for _ in range(n_layers)] for _ in range(args.steps)]
+    idx = {n: ckv.STAGE_NAMES.index(n) for n in timed}
+    ev = []
+    for _ in range(args.steps):
+        per_layer = []
+        for _ in range(n_layers):
+            b, e = [None] * ns, [None] * ns
+            for n in timed:
+                b[idx[n]], e[idx[n]] = hip.event(), hip.event()
+            per_layer.append((b, e))
+        ev.append(per_layer)
     t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
@@ -301,17 +355,17 @@ def main():
     ms_total = t_start.elapsed_time(t_end)
     ms_per_step = ms_total / args.steps
 
-    stage_names = list(ckv.STAGE_NAMES)
-    stage_ms = {n: [] for n in stage_names}
+    stage_ms = {n: [] for n in timed}
     for k in range(args.steps):
         for li in range(n_layers):
             b, e = ev[k][li]
-            for si, n in enumerate(stage_names):
-                stage_ms[n].append(hip.elapsed_ms(b[si], e[si]))
+            for n in timed:
+                stage_ms[n].append(hip.elapsed_ms(b[idx[n]], e[idx[n]]))
     for k in range(args.steps):
         for li in range(n_layers):
             for x in ev[k][li][0] + ev[k][li][1]:
-                hip.destroy(x)
+                if x is not None:
+                    hip.destroy(x)
     stage_avg = {n: float(np.mean(v)) for n, v in stage_ms.items()}
 
     tokens_per_layer = sum(wl.seq_lens)
@@ -375,7 +429,10 @@ def main():
                    "window": w, "pool": "max" if wl.pool == 1 else "avg",
                    "pool_kernel": wl.pool_kernel, "heads_per_group": list(wl.n_sel_choices),
                    "budget_avg": float(np.mean(budgets)), "parallelism": "single GPU",
-                   "streams": n_streams},
+                   "streams": n_streams,
+                   "schedule": "pipeline: K passes + pooling on stream A, selection + gather on "
+                               "stream B, one layer apart" if args.pipeline else
+                               "ckv_compress_layer per layer, round-robin over streams"},
         "path_hbm_gbs": path_gbs,
         "path_hbm_frac": path_gbs / HBM_PEAK_GBS,
         "stage_ms_avg": stage_avg,

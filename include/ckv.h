@@ -185,7 +185,9 @@ int ckv_last_hip_error(void);
  * 2; the small merge kernel between the passes is not covered), 2 pooling,
  * head mean and histogram, 3 selection (threshold search), 4 compaction and
  * gather. Arrays are hipEvent_t[CKV_NUM_STAGES] owned by the caller, created
- * with timing enabled; pass NULL to stop. Per host thread. */
+ * with timing enabled; a NULL entry leaves that stage untimed (each timed
+ * launch costs a few microseconds of dispatch overlap); pass NULL arrays to
+ * stop. Per host thread. */
 #define CKV_NUM_STAGES 5
 int ckv_set_stage_events(void *const *begin, void *const *end);
 

@@ -233,7 +233,8 @@ STAGE_NAMES = ("rowstats", "score", "pool", "select", "gather")
 
 
 def ckv_set_stage_events(begin, end) -> None:
-    """begin/end: sequences of CKV_NUM_STAGES raw hipEvent_t handles, or None to stop."""
+    """begin/end: sequences of CKV_NUM_STAGES raw hipEvent_t handles (None entries
+    leave that stage untimed), or None to stop."""
     if begin is None or end is None:
         _check(load().ckv_set_stage_events(None, None), "ckv_set_stage_events")
         return

@@ -110,9 +110,20 @@ __global__ __launch_bounds__(kThreads) void hist_kernel(const LayerArgs a) {
   const float* sc = sq.scores + (int64_t)g * Ls;
   const int64_t j0 = (int64_t)r * sq.range;
   const int64_t j1 = j0 + sq.range < Ls ? j0 + sq.range : Ls;
+  // the first kFilterPer keys of this thread are loaded before the LDS
+  // histogram is cleared, all in flight at once
+  uint32_t key0[kFilterPer];
+#pragma unroll
+  for (int e = 0; e < kFilterPer; ++e) {
+    const int64_t j = j0 + tid + (int64_t)e * kThreads;
+    key0[e] = j < j1 ? score_key(sc[j]) : 0u;
+  }
   for (int i = tid; i < kHistBins; i += kThreads) hist_lds[i] = 0u;
   __syncthreads();
-  for (int64_t j = j0 + tid; j < j1; j += kThreads)
+#pragma unroll
+  for (int e = 0; e < kFilterPer; ++e)
+    if (j0 + tid + (int64_t)e * kThreads < j1) atomicAdd(&hist_lds[key0[e] >> kHistShift], 1u);
+  for (int64_t j = j0 + tid + (int64_t)kFilterPer * kThreads; j < j1; j += kThreads)
     atomicAdd(&hist_lds[score_key(sc[j]) >> kHistShift], 1u);
   __syncthreads();
   uint32_t* ghist = sq.hist + (int64_t)g * kHistBins;

@@ -50,11 +50,10 @@ int64_t wsum_heads(const ckv_layer_desc* d) {
   return h > 0 ? h : 1;
 }
 
-// Per-prompt workspace, in order: K-pass partials, row lse, head window
-// sums, scores, selection control words, histograms, candidates, per-range
+// Per-prompt workspace, in order: K-pass partials, head window sums, scores, selection control words, histograms, candidates, per-range
 // counts/offsets.
 struct WsLayout {
-  size_t partial, lse, wsum, scores, ctl, hist, cand, rsure, roff, reqb, total;
+  size_t partial, wsum, scores, ctl, hist, cand, rsure, roff, reqb, total;
 };
 
 WsLayout seq_ws_layout(const ckv_layer_desc* d, const ckv_seq* s) {
@@ -64,7 +63,6 @@ WsLayout seq_ws_layout(const ckv_layer_desc* d, const ckv_seq* s) {
   WsLayout w;
   size_t o = 0;
   w.partial = o; o += align_up((size_t)n_kv * max_split(d, s->seq_len) * ckv::kMaxRows * sizeof(float2));
-  w.lse = o;     o += align_up((size_t)n_kv * ckv::kMaxRows * sizeof(float));
   w.wsum = o;    o += align_up((size_t)n_kv * wsum_heads(d) * Ls * sizeof(float));
   w.scores = o;  o += align_up((size_t)n_kv * Ls * sizeof(float));
   w.ctl = o;     o += align_up((size_t)n_kv * ckv::kCtlWords * sizeof(uint32_t));
@@ -211,7 +209,6 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
     if (ws) {
       const WsLayout l = seq_ws_layout(d, &s);
       q.partial = reinterpret_cast<float2*>(ws + l.partial);
-      q.lse = reinterpret_cast<float*>(ws + l.lse);
       q.wsum = reinterpret_cast<float*>(ws + l.wsum);
       if (scores_from_ws && !q.scores) q.scores = reinterpret_cast<float*>(ws + l.scores);
       q.ctl = reinterpret_cast<uint32_t*>(ws + l.ctl);
@@ -261,11 +258,9 @@ ckv::Timing timing(int stage, bool first, bool last) {
 
 int run_score(const ckv_layer_desc* d, const ckv::LayerArgs& a, hipStream_t st) {
   hipError_t e;
-  const ckv::Timing none;
   if ((e = ckv::launch_rowstats(d->dtype, a, grid_kpass(a), st,
                                 timing(ckv::kStageRowStats, true, true))) != hipSuccess)
     return hip_fail(e);
-  if ((e = ckv::launch_lse(a, a.num_seqs * a.n_kv, st, none)) != hipSuccess) return hip_fail(e);
   if ((e = ckv::launch_score(d->dtype, a, grid_kpass(a), st,
                              timing(ckv::kStageScore, true, true))) != hipSuccess)
     return hip_fail(e);

@@ -67,7 +67,6 @@ struct SeqArgs {
   void* v_out;
   // workspace
   float2* partial;         // [n_kv][n_split][kMaxRows]: (max logit, sum exp2) per workgroup
-  float* lse;              // [n_kv][kMaxRows]: per-row log2-sum-exp2 in exp2 units
   float* wsum;             // [n_kv][wsum_heads][L - w]: window sum of each chosen head
   uint32_t* ctl;           // [n_kv][kCtlWords]
   uint32_t* hist;          // [n_kv][kHistBins]
@@ -115,10 +114,8 @@ struct Timing {
   hipEvent_t stop = nullptr;
 };
 
-// dtype codes match ckv_dtype. grid is the number of workgroups, except for
-// launch_lse, which takes the number of (prompt, group) pairs.
+// dtype codes match ckv_dtype. grid is the number of workgroups.
 hipError_t launch_rowstats(int dtype, const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
-hipError_t launch_lse(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
 hipError_t launch_score(int dtype, const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
 hipError_t launch_pool(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
 hipError_t launch_clear(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);

@@ -13,9 +13,9 @@
 // the logits are formed twice from K:
 //   rowstats_kernel  pass 1: online max and sum of exp2 of every chosen row,
 //                    one partial per workgroup;
-//   lse_kernel       merges the partials into one log2-sum-exp2 per row;
-//   score_kernel     pass 2: exp2(alpha*s - lse) summed over each chosen
-//                    head's window rows, written per head (S[h,j]);
+//   score_kernel     pass 2: merges those partials into one log2-sum-exp2
+//                    per row, then exp2(alpha*s - lse) summed over each
+//                    chosen head's window rows, written per head (S[h,j]);
 //   pool_kernel      pooling along the tokens, head mean, scores, and the
 //                    first-level histogram of the score keys that the
 //                    selection starts from.
@@ -178,17 +178,19 @@ __device__ __forceinline__ void wait_stages(int n_after) {
 // Stage loop shared by both passes over stages 0..ns-1 (stage k starts at
 // token t_first + k*stride, tokens clamped to [lo, hi]) with an NS-slot LDS ring
 // (slots are distinct LDS arrays so the compiler can tell the in-flight loads
-// from the slot being read). At step k: wait for stage k, barrier (stage k is
+// from the slot being read). After the first NS-1 stages are issued, pre()
+// runs while they load. At step k: wait for stage k, barrier (stage k is
 // complete and every wave has finished with stage k-1's slot), issue stage
 // k+NS-1 into that freed slot, then body(slot, k) reduces stage k.
-template <class S, int NS, class Body>
+template <class S, int NS, class Pre, class Body>
 __device__ __forceinline__ void stage_loop(uint4* const* slot, const char* kbase, int64_t kv_st,
                                            int64_t t_first, int64_t stride, int ns, int64_t lo,
-                                           int64_t hi, int wave, Body body) {
+                                           int64_t hi, int wave, Pre pre, Body body) {
   const typename S::Plan p = S::plan(wave, kv_st);
 #pragma unroll
   for (int j = 0; j < NS - 1; ++j)
     if (j < ns) S::fetch(kbase, kv_st, t_first + j * stride, lo, hi, p, wave, slot[j]);
+  pre();  // work that overlaps the first stages' loads
   for (int k0 = 0; k0 < ns; k0 += NS) {
 #pragma unroll
     for (int j = 0; j < NS; ++j) {
@@ -281,7 +283,7 @@ __device__ __forceinline__ void rowstats_body(const LayerArgs& a, const SeqArgs&
   float m_run = -INFINITY, z_run = 0.f;
 
   stage_loop<S, NS>(slots, kbase, sq.kv_st, (int64_t)p * S::ST, stride, ns, 0, L - 1, wave,
-                    [&](const uint4* slot, int k) {
+                    [] {}, [&](const uint4* slot, int k) {
     // waves past the stage's blocks (4 waves on a 2-block stage) sit out
     if (!active || sub >= S::BLOCKS) return;
     const int64_t ts = (int64_t)p * S::ST + k * stride + sub * 32;  // this wave's first block
@@ -369,13 +371,7 @@ __global__ __launch_bounds__(kThreads) void rowstats_kernel(const LayerArgs a) {
   else rowstats_body<DT, D, 4, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, red);
 }
 
-// Merge the workgroup partials: lse[r] = log2(sum_j exp2(alpha * s_rj)) so
-// that the softmax probability is exp2(alpha * s - lse). Padding rows get +inf
-// (p = 0). One workgroup per (prompt, group, 32-row block); the 8 lanes of a
-// row merge every 8th partial each, then one lane merges their 8 results.
-constexpr int kLseRows = 32;
-constexpr int kLseLanes = kThreads / kLseRows;
-
+// Online merge of (max logit, sum of exp2) pairs in exp2 units.
 __device__ __forceinline__ void lse_merge(float& m, float& z, float m2, float z2, float alpha) {
   const float mn = fmaxf(m, m2);
   if (mn == -INFINITY) return;  // both empty
@@ -384,40 +380,11 @@ __device__ __forceinline__ void lse_merge(float& m, float& z, float m2, float z2
   m = mn;
 }
 
-__global__ __launch_bounds__(kThreads) void lse_kernel(const LayerArgs a) {
-  __shared__ float2 part[kLseLanes][kLseRows];
-  constexpr int kBlocks = kMaxRows / kLseRows;
-  const int sg = blockIdx.x / kBlocks, rb = blockIdx.x - sg * kBlocks;
-  const int s = sg / a.n_kv, g = sg - s * a.n_kv;
-  const SeqArgs& sq = a.seq[s];
-  const int lr = threadIdx.x % kLseRows, c0 = threadIdx.x / kLseRows;
-  const int r = rb * kLseRows + lr;
-  const int n_sel = a.grp_off[g + 1] - a.grp_off[g];
-  const int slot = r / a.w8, i = r - slot * a.w8;
-  const bool valid = slot < n_sel && i < a.w;
-  float m = -INFINITY, z = 0.f;
-  if (valid) {
-    const float2* pp = sq.partial + (int64_t)g * sq.n_split * kMaxRows + r;
-#pragma unroll 8
-    for (int c = c0; c < sq.n_split; c += kLseLanes) {
-      const float2 v = pp[(int64_t)c * kMaxRows];
-      lse_merge(m, z, v.x, v.y, a.alpha);
-    }
-  }
-  part[c0][lr] = make_float2(m, z);
-  __syncthreads();
-  if (threadIdx.x < kLseRows) {
-    float mm = -INFINITY, zz = 0.f;
-#pragma unroll
-    for (int c = 0; c < kLseLanes; ++c) lse_merge(mm, zz, part[c][lr].x, part[c][lr].y, a.alpha);
-    sq.lse[(int64_t)g * kMaxRows + r] = valid ? mm * a.alpha + log2f(zz) : INFINITY;
-  }
-}
-
 // ---------------------------------------------------------------------------
 // Pass 2: probabilities and per-head window sums.
 // ---------------------------------------------------------------------------
 constexpr int kGroupRows = kMaxRows / 8;  // 8-row groups of one group's rows
+constexpr int kLseBatch = 16;             // partial loads in flight per thread
 
 // QM (query-block mode, when w8 is a multiple of 32): every 32-row query
 // block belongs to one head, so a lane sums its four 8-row groups in
@@ -442,13 +409,51 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
   const int ns = stages_of(Ls, ST, p, P);
 
   uint4 q[NC];
-  float4 cv[4];  // lse of this lane's 16 result rows qb*32 + 8*a4 + 4*h + e (exp2 units)
-  if (active) {
-    load_queries<NC, S::EB>(a, sq, sel0, n_sel, qb, l32, h, q);
-    const float4* lse4 = reinterpret_cast<const float4*>(sq.lse + (int64_t)g * kMaxRows + qb * 32);
+  if (active) load_queries<NC, S::EB>(a, sq, sel0, n_sel, qb, l32, h, q);
+  // lse of this lane's 16 result rows qb*32 + 8*a4 + 4*h + e, in exp2 units:
+  // merged from pass 1's per-workgroup partials while the first stages load
+  float4 cv[4];
+  auto merge_lse = [&] {
+    // two threads per row, each merging every other partial; results meet in
+    // LDS (the gsum buffers are not in use yet)
+    float2* part = reinterpret_cast<float2*>(gsum);  // [2][kMaxRows]
+    float* lse_l = gsum + 4 * kMaxRows;               // [kMaxRows]
+    const int r = tid % kMaxRows, half = tid / kMaxRows;
+    const int slot_h = r / a.w8, wrow = r - slot_h * a.w8;
+    const bool valid = r < nqb * 32 && slot_h < n_sel && wrow < a.w;
+    float m = -INFINITY, z = 0.f;
+    if (valid) {
+      const int P = sq.n_split;
+      const float2* pp = sq.partial + (int64_t)g * P * kMaxRows + r;
+      for (int c0 = half; c0 < P; c0 += 2 * kLseBatch) {
+        float2 v[kLseBatch];
 #pragma unroll
-    for (int a4 = 0; a4 < 4; ++a4) cv[a4] = lse4[2 * a4 + h];
-  }
+        for (int u = 0; u < kLseBatch; ++u) {
+          const int c = c0 + 2 * u;
+          v[u] = c < P ? pp[(int64_t)c * kMaxRows] : make_float2(-INFINITY, 0.f);
+        }
+#pragma unroll
+        for (int u = 0; u < kLseBatch; ++u) lse_merge(m, z, v[u].x, v[u].y, alpha);
+      }
+    }
+    part[half * kMaxRows + r] = make_float2(m, z);
+    __syncthreads();
+    if (tid < kMaxRows) {
+      float mm = part[r].x, zz = part[r].y;
+      lse_merge(mm, zz, part[kMaxRows + r].x, part[kMaxRows + r].y, alpha);
+      // padding rows: +inf, so their probabilities are 0
+      lse_l[r] = valid ? mm * alpha + log2f(zz) : INFINITY;
+    }
+    __syncthreads();
+    if (active) {
+#pragma unroll
+      for (int a4 = 0; a4 < 4; ++a4) {
+        const float* src = lse_l + qb * 32 + 8 * a4 + 4 * h;
+        cv[a4] = make_float4(src[0], src[1], src[2], src[3]);
+      }
+    }
+    __syncthreads();  // lse_l and part are gsum, which stage 0 overwrites
+  };
   int opoff[NC];
   S::operand_offsets(l32, h, opoff);
 #pragma unroll
@@ -473,7 +478,7 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
   };
 
   stage_loop<S, NS>(slots, kbase, sq.kv_st, (int64_t)p * ST, stride, ns, 0, Ls - 1, wave,
-                    [&](const uint4* slot, int k) {
+                    merge_lse, [&](const uint4* slot, int k) {
     // the barrier before this step ordered every wave's gsum writes of stage
     // k-1 before these reads, and this fold's reads before stage k+1 reuses
     // the buffer
@@ -524,7 +529,8 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const LayerArgs a) {
   __shared__ uint4 slot3[S::VEC];
   // gsum[buf][r8][col]: sum over the 8 rows of 8-row group r8 of p at stage
   // column col, double-buffered by stage parity
-  __shared__ float gsum[2 * kGroupRows * S::ST];
+  __shared__ __align__(16) float gsum[2 * kGroupRows * S::ST];
+  static_assert(2 * kGroupRows * S::ST >= 5 * kMaxRows, "the lse merge fits in gsum");
   uint4* const slots[NS] = {slot0, slot1, slot2, slot3};
 
   const int b = blockIdx.x;
@@ -698,10 +704,6 @@ struct ScoreOf {
 
 hipError_t launch_rowstats(int dtype, const LayerArgs& a, int grid, hipStream_t st, const Timing& tm) {
   return launch_typed<RowStatsOf>(dtype, a, grid, st, tm);
-}
-
-hipError_t launch_lse(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm) {
-  return launch(lse_kernel, grid * (kMaxRows / kLseRows), kThreads, st, tm, a);
 }
 
 hipError_t launch_score(int dtype, const LayerArgs& a, int grid, hipStream_t st, const Timing& tm) {

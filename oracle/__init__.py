@@ -75,6 +75,8 @@ def _load():
         lib.ckvo_select_layer.argtypes = [P(d), P(ctypes.c_uint8), i32, i32, P(d), i64, i32,
                                           i32, d, i32, i32, i64, P(d), P(i32), i32]
         lib.ckvo_select_layer.restype = i64
+        lib.ckvo_select_layer_shared.argtypes = lib.ckvo_select_layer.argtypes
+        lib.ckvo_select_layer_shared.restype = i64
         lib.ckvo_allocate_budgets.argtypes = [P(d), i32, i64, i64, i64, P(i64)]
         lib.ckvo_allocate_budgets.restype = ctypes.c_int
         _lib = lib
@@ -189,6 +191,28 @@ def select_layer(q, mask, k, w: int, scale: float, pool_mode: int, kp: int, budg
         _ptr(idx, ctypes.c_int32), n_threads)
     if n < 0:
         raise OracleError(int(n), "select_layer")
+    return scores, idx
+
+
+def select_layer_shared(q, mask, k, w: int, scale: float, pool_mode: int, kp: int, budget: int,
+                        n_threads: int = 0):
+    """The paper's layer-shared variant. q [H, w, d], mask [H], k [n_kv, L, d].
+
+    Returns (scores [L-w] fp64, idx [min(B, L)] int32), one index set for every
+    KV head of the layer."""
+    q, k = _f64(q), _f64(k)
+    mask = np.ascontiguousarray(np.asarray(mask, dtype=np.uint8))
+    H, w_, d = q.shape
+    n_kv, L, d2 = k.shape
+    assert w_ == w and d2 == d and mask.shape == (H,)
+    scores = np.empty(L - w, dtype=np.float64)
+    idx = np.empty(min(budget, L), dtype=np.int32)
+    n = _load().ckvo_select_layer_shared(
+        _ptr(q, ctypes.c_double), _ptr(mask, ctypes.c_uint8), H, n_kv, _ptr(k, ctypes.c_double),
+        L, d, w, scale, pool_mode, kp, budget, _ptr(scores, ctypes.c_double),
+        _ptr(idx, ctypes.c_int32), n_threads)
+    if n < 0:
+        raise OracleError(int(n), "select_layer_shared")
     return scores, idx
 
 

@@ -26,6 +26,10 @@
  *   R5 pooling: stride 1, half-width r = kp/2, window clipped to [0, L-w);
  *      average divides by kp (zero padding), max ignores padding.
  *   R6 pool each head, then average the pooled vectors over the heads.
+ *   R8 two head scopes: per KV group (each group's chosen heads pick that
+ *      group's tokens), or the paper's layer-shared form (the chosen heads of
+ *      the whole layer pick one index set for every head; the mean runs over
+ *      all chosen heads, each scored against its own group's keys).
  *   R9 the budget B counts the w window tokens, which are always kept; the
  *      other B-w come from the prefix; B >= L keeps every token.
  *   R10 equal scores: the lower token index wins.
@@ -267,6 +271,68 @@ int64_t ckvo_select_layer(const double *q, const uint8_t *mask, int32_t H,
     free(q_sel);
   }
   return status < 0 ? status : n_ret;
+}
+
+/* The paper's own variant of Sec. 3.3: the chosen retrieval heads of the
+ * whole layer (marked in mask, from any groups) decide one index set that
+ * every attention head of the layer shares. Each chosen head h is scored
+ * against the keys of its own group h / (H / n_kv) (R13): its window sums
+ * are pooled over the prefix (R6), the pooled vectors of all chosen heads
+ * are averaged, and the top-N of that single vector is kept. q is [H][w][d],
+ * k is [n_kv][L][d], scores is [L-w], idx gets min(budget, L) entries.
+ * n_threads <= 0 uses the OpenMP default (heads run in parallel; their sum is
+ * taken afterwards in head order). */
+int64_t ckvo_select_layer_shared(const double *q, const uint8_t *mask, int32_t H,
+                                 int32_t n_kv, const double *k, int64_t L, int32_t d,
+                                 int32_t w, double scale, int32_t pool_mode, int32_t kp,
+                                 int64_t budget, double *scores, int32_t *idx,
+                                 int32_t n_threads) {
+  if (!q || !mask || !k || !scores || !idx || H < 1 || n_kv < 1 || H % n_kv)
+    return CKVO_EINVAL;
+  if (L <= w || w < 1 || d < 1 || kp < 1 || (kp % 2) == 0) return CKVO_EINVAL;
+  if (budget < w) return CKVO_EBUDGET;
+  int32_t G = H / n_kv, n_chosen = 0;
+  for (int32_t h = 0; h < H; ++h) n_chosen += mask[h] != 0;
+  if (n_chosen == 0) return CKVO_EMASK;
+  int64_t Ls = L - w;
+  int32_t *heads = (int32_t *)malloc(sizeof(int32_t) * (size_t)n_chosen);
+  double *pooled = (double *)malloc(sizeof(double) * (size_t)n_chosen * (size_t)Ls);
+  if (!heads || !pooled) {
+    free(heads);
+    free(pooled);
+    return CKVO_ENOMEM;
+  }
+  for (int32_t h = 0, c = 0; h < H; ++h)
+    if (mask[h]) heads[c++] = h;
+  int64_t status = 0;
+#ifdef _OPENMP
+  if (n_threads <= 0) n_threads = omp_get_max_threads();
+#pragma omp parallel for schedule(dynamic, 1) num_threads(n_threads)
+#endif
+  for (int32_t c = 0; c < n_chosen; ++c) {
+    int32_t h = heads[c], g = h / G;
+    double *S = (double *)malloc(sizeof(double) * (size_t)L);
+    if (!S) {
+      status = CKVO_ENOMEM;
+      continue;
+    }
+    int rc = ckvo_window_sums(q + (int64_t)h * w * d, 1, k + (int64_t)g * L * d, L, d, w,
+                              scale, S);
+    if (rc == CKVO_OK) ckvo_pool(S, Ls, kp, pool_mode, pooled + (int64_t)c * Ls);
+    else status = rc;
+    free(S);
+  }
+  if (status == 0) {
+    for (int64_t j = 0; j < Ls; ++j) {
+      double acc = 0.0;
+      for (int32_t c = 0; c < n_chosen; ++c) acc += pooled[(int64_t)c * Ls + j];
+      scores[j] = acc / (double)n_chosen;
+    }
+  }
+  free(heads);
+  free(pooled);
+  if (status < 0) return status;
+  return ckvo_select_tokens(scores, L, w, budget, idx);
 }
 
 /* Algorithm 1 (error-aware layer-adaptive cache allocation), step by step:

@@ -388,3 +388,100 @@ def test_algorithm1_infeasible_reports_shortfall():
     assert rc == oracle.EBUDGET and B.tolist() == [100, 100]
     B, rc = oracle.allocate_budgets([0.5, 0.5], 10, 32, 100)
     assert rc == oracle.EBUDGET and B.tolist() == [32, 32]
+
+
+# ---------------------------------------------------------------------------
+# Layer-shared selection (the paper's own variant of Sec. 3.3).
+# ---------------------------------------------------------------------------
+SHARED = HAND["shared"]
+
+
+@pytest.mark.parametrize("case", SHARED["cases"], ids=lambda c: c["why"][:40])
+def test_shared_hand_example(case):
+    k = np.array(SHARED["K"], dtype=np.float64)[:, :, None]          # [n_kv, L, 1]
+    q = np.full((2, SHARED["window"], 1), LN2)                        # [H, w, 1]
+    scores, idx = oracle.select_layer_shared(q, [1, 1], k, SHARED["window"], 1.0,
+                                             POOLS[case["pool"]], case["kp"], case["budget"])
+    assert idx.tolist() == case["idx"]
+    for j, t in enumerate(case["scores"]):
+        assert _close(scores[j], _frac(t)), (j, scores[j], t)
+
+
+def test_shared_hand_example_differs_from_each_group():
+    k = np.array(SHARED["K"], dtype=np.float64)[:, :, None]
+    q = np.full((1, 2, 1), LN2)
+    per_group = [oracle.select_group(q, k[g], 2, 1.0, oracle.POOL_AVG, 1, 4)[1].tolist()
+                 for g in range(2)]
+    assert per_group == [[0, 3, 4, 5], [0, 1, 4, 5]]
+
+
+def _layer_case(seed, H=8, n_kv=2, L=97, w=5, d=6):
+    rng = np.random.default_rng(seed)
+    return rng.standard_normal((H, w, d)), rng.standard_normal((n_kv, L, d)), w
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_shared_one_group_reduces_to_group_selection(seed):
+    # every chosen head in one group: the shared set is that group's selection
+    q, k, w = _layer_case(seed)
+    G = q.shape[0] // k.shape[0]
+    g = seed % k.shape[0]
+    mask = np.zeros(q.shape[0], np.uint8)
+    mask[g * G: g * G + 1 + seed % G] = 1
+    chosen = np.nonzero(mask)[0]
+    s_sh, i_sh = oracle.select_layer_shared(q, mask, k, w, 0.4, oracle.POOL_MAX, 5, 20)
+    s_g, i_g, _ = oracle.select_group(q[chosen], k[g], w, 0.4, oracle.POOL_MAX, 5, 20)
+    np.testing.assert_allclose(s_sh, s_g, rtol=1e-14, atol=0)
+    assert i_sh.tolist() == i_g.tolist()
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_shared_is_head_weighted_mean_of_group_scores(seed):
+    # the mean runs over all chosen heads, so a group with more chosen heads
+    # weighs more: shared = sum_g n_g * A_g / sum_g n_g
+    q, k, w = _layer_case(seed + 100, H=12, n_kv=3)
+    G = 4
+    rng = np.random.default_rng(seed)
+    mask = np.zeros(12, np.uint8)
+    counts = []
+    for g in range(3):
+        n = int(rng.integers(1, G + 1))
+        mask[g * G + rng.choice(G, n, replace=False)] = 1
+        counts.append(n)
+    s_sh, _ = oracle.select_layer_shared(q, mask, k, w, 0.3, oracle.POOL_AVG, 3, 30)
+    s_groups, _ = oracle.select_layer(q, mask, k, w, 0.3, oracle.POOL_AVG, 3, 30)
+    expect = sum(n * s_groups[g] for g, n in enumerate(counts)) / sum(counts)
+    np.testing.assert_allclose(s_sh, expect, rtol=1e-12, atol=1e-15)
+    # and not the plain mean of the group means (unless the counts are equal)
+    if len(set(counts)) > 1:
+        assert not np.allclose(s_sh, s_groups.mean(axis=0), rtol=1e-6, atol=0)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_shared_library_route(seed):
+    # per head: dense scipy softmax rows over the visible keys of its own
+    # group, window sum, torch max pooling, then the mean over all chosen heads
+    q, k, w = _layer_case(seed + 200, H=6, n_kv=3, L=64, w=4, d=5)
+    mask = np.array([1, 0, 1, 1, 0, 1], np.uint8)
+    G, L, scale, kp = 2, k.shape[1], 0.7, 5
+    pooled = []
+    for h in np.nonzero(mask)[0]:
+        kg = k[h // G]
+        S = np.zeros(L)
+        for i in range(w):
+            vis = L - w + i + 1
+            S[:vis] += scipy.special.softmax(scale * (kg[:vis] @ q[h, i]))
+        x = torch.from_numpy(S[:L - w])[None, None]
+        pooled.append(torch.nn.functional.max_pool1d(x, kp, 1, kp // 2)[0, 0].numpy())
+    expect = np.mean(pooled, axis=0)
+    s_sh, idx = oracle.select_layer_shared(q, mask, k, w, scale, oracle.POOL_MAX, kp, 12)
+    np.testing.assert_allclose(s_sh, expect, rtol=1e-12, atol=1e-15)
+    order = np.lexsort((np.arange(L - w), -expect))[:12 - w]
+    assert idx.tolist() == sorted(order.tolist()) + list(range(L - w, L))
+
+
+def test_shared_rejects_empty_mask():
+    q, k, w = _layer_case(7)
+    with pytest.raises(oracle.OracleError):
+        oracle.select_layer_shared(q, np.zeros(q.shape[0], np.uint8), k, w, 0.3,
+                                   oracle.POOL_AVG, 3, 20)

@@ -44,7 +44,7 @@ extern "C" {
 #define CKV_ERR_INVALID_ARG (-1) /* null pointer, bad size/stride/alignment, even pool kernel */
 #define CKV_ERR_UNSUPPORTED (-2) /* dtype, head_dim, window or head count outside the built set */
 #define CKV_ERR_BUDGET (-3)      /* budget below the window; Algorithm 1 could not meet the total */
-#define CKV_ERR_MASK (-4)        /* a KV group has no chosen query head */
+#define CKV_ERR_MASK (-4)        /* a KV group has no chosen query head (per-group scope), or no head at all */
 #define CKV_ERR_WORKSPACE (-5)   /* workspace missing or smaller than ckv_workspace_bytes() */
 #define CKV_ERR_HIP (-6)         /* a HIP runtime call failed; see ckv_last_hip_error() */
 
@@ -54,6 +54,14 @@ typedef enum { CKV_POOL_AVG = 0, CKV_POOL_MAX = 1 } ckv_pool;
 
 /* flags */
 #define CKV_KEEP_WINDOW (1u << 0) /* required: the w window tokens are always kept and count in B */
+/* Head scope of the selection (paper Sec. 3.3). Without this flag every KV
+ * group g ranks its tokens with its own chosen heads and keeps its own index
+ * set. With it, the chosen heads of the whole layer (any groups; a group may
+ * have none) rank the tokens together: each chosen head is scored against
+ * its own group's keys, the pooled vectors of all chosen heads are averaged
+ * (each head weighs the same), and one index set is kept for every KV head,
+ * as the paper describes. Shapes that change under this flag are noted below. */
+#define CKV_SHARE_LAYER (1u << 1)
 
 /* Limits of this build (larger values return CKV_ERR_UNSUPPORTED). */
 #define CKV_MAX_Q_HEADS 128
@@ -76,7 +84,7 @@ typedef enum { CKV_POOL_AVG = 0, CKV_POOL_MAX = 1 } ckv_pool;
  *                CKV_POOL_MAX (padding ignored); pool_kernel odd, 1..31
  *                (1 = no pooling). Stride 1; the neighbourhood of token j is
  *                [j - k/2, j + k/2] clipped to the ranked prefix [0, L - w).
- *   flags        must contain CKV_KEEP_WINDOW.
+ *   flags        must contain CKV_KEEP_WINDOW; may contain CKV_SHARE_LAYER.
  */
 typedef struct {
   int32_t num_q_heads;
@@ -103,14 +111,17 @@ typedef struct {
  *   budget  B, tokens kept per KV head including the w window tokens
  *           (B >= w). B >= L keeps every token. The top B - w of the prefix
  *           [0, L - w) are kept; ties go to the lower index.
- *   scores  [n_kv, L - w] fp32: the averaged score of every prefix token.
- *           Written by ckv_score, read by ckv_select; may be NULL for
- *           ckv_compress_layer (the workspace holds it then).
- *   idx     [n_kv, min(B, L)] int32: retained token positions per KV head in
+ *   scores  [n_kv, L - w] fp32 ([L - w] under CKV_SHARE_LAYER): the averaged
+ *           score of every prefix token. Written by ckv_score, read by
+ *           ckv_select; may be NULL for ckv_compress_layer (the workspace holds
+ *           it then).
+ *   idx     [n_kv, min(B, L)] int32 ([min(B, L)] under CKV_SHARE_LAYER):
+ *           retained token positions per KV head (or for every head) in
  *           ascending order (the last w are L-w..L-1). Written by ckv_select,
  *           read by ckv_gather.
  *   k_out, v_out [n_kv, min(B, L), d] contiguous, dtype of the layer: the
- *           compact cache, row r of head g is K[g, idx[g, r], :].
+ *           compact cache, row r of head g is K[g, idx[g, r], :] (idx[r] under
+ *           CKV_SHARE_LAYER).
  */
 typedef struct {
   const void *q_win;
@@ -136,7 +147,9 @@ size_t ckv_workspace_bytes(const ckv_layer_desc *desc, const ckv_seq *seqs, int3
 /* Token scoring, paper Sec. 3.3 (the chosen heads' attention-score matrices
  * over the observation window, summed over the window, pooled along the token
  * axis, averaged over the chosen heads). head_mask is a host array [H]; nonzero
- * marks a chosen head and every KV group needs at least one. Writes
+ * marks a chosen head. Every KV group needs at least one, except under
+ * CKV_SHARE_LAYER, where at least one head of the layer must be chosen and
+ * groups without one are not read. Writes
  * seqs[s].scores for every prompt s. Window row i (position L-w+i) attends to
  * keys 0..L-w+i; its softmax runs over all of them, and only the prefix
  * columns [0, L-w) are scored. */

@@ -29,6 +29,7 @@ CKV_ERR_HIP = -6
 CKV_BF16, CKV_F16, CKV_F32 = 0, 1, 2
 CKV_POOL_AVG, CKV_POOL_MAX = 0, 1
 CKV_KEEP_WINDOW = 1
+CKV_SHARE_LAYER = 2
 CKV_MAX_SEQS = 16
 
 EXPORTED = ("ckv_workspace_bytes", "ckv_score", "ckv_select", "ckv_gather", "ckv_compress_layer",
@@ -249,14 +250,16 @@ def ckv_set_stage_events(begin, end) -> None:
 # output allocation (plumbing)
 # --------------------------------------------------------------------------
 def alloc_outputs(desc: ckv_layer_desc, s: Seq, with_scores: bool = True) -> Seq:
-    """Allocate scores/idx/k_out/v_out for one prompt on the device of s.k."""
+    """Allocate scores/idx/k_out/v_out for one prompt on the device of s.k
+    (one score row and one index row under CKV_SHARE_LAYER)."""
     L = s.k.shape[1] if s.seq_len is None else s.seq_len
     n_kv, d = desc.num_kv_heads, desc.head_dim
+    n_sg = 1 if desc.flags & CKV_SHARE_LAYER else n_kv
     n_ret = min(int(s.budget), L)
     dev = s.k.device
     if with_scores:
-        s.scores = torch.empty((n_kv, L - desc.window), dtype=torch.float32, device=dev)
-    s.idx = torch.empty((n_kv, n_ret), dtype=torch.int32, device=dev)
+        s.scores = torch.empty((n_sg, L - desc.window), dtype=torch.float32, device=dev)
+    s.idx = torch.empty((n_sg, n_ret), dtype=torch.int32, device=dev)
     s.k_out = torch.empty((n_kv, n_ret, d), dtype=s.k.dtype, device=dev)
     s.v_out = torch.empty((n_kv, n_ret, d), dtype=s.k.dtype, device=dev)
     return s

@@ -30,6 +30,11 @@ int64_t range_size(int64_t Ls) {
   return per <= ckv::kRangeMin ? ckv::kRangeMin : ceil_div(per, ckv::kRangeMin) * ckv::kRangeMin;
 }
 
+// Selections per prompt: one per KV group, or one for the layer.
+int64_t sel_groups(const ckv_layer_desc* d) {
+  return (d->flags & CKV_SHARE_LAYER) ? 1 : d->num_kv_heads;
+}
+
 // K stages of one KV head of a prompt of seq_len tokens.
 int64_t k_stages(const ckv_layer_desc* d, int64_t seq_len) {
   return ceil_div(seq_len, ckv::stage_tokens(d->head_dim * elt_bytes(d->dtype)));
@@ -57,20 +62,20 @@ struct WsLayout {
 };
 
 WsLayout seq_ws_layout(const ckv_layer_desc* d, const ckv_seq* s) {
-  const int64_t n_kv = d->num_kv_heads;
+  const int64_t n_kv = d->num_kv_heads, n_sg = sel_groups(d);
   const int64_t Ls = s->seq_len - d->window;
   const int64_t n_ranges = ceil_div(Ls, range_size(Ls));
   WsLayout w;
   size_t o = 0;
   w.partial = o; o += align_up((size_t)n_kv * max_split(d, s->seq_len) * ckv::kMaxRows * sizeof(float2));
   w.wsum = o;    o += align_up((size_t)n_kv * wsum_heads(d) * Ls * sizeof(float));
-  w.scores = o;  o += align_up((size_t)n_kv * Ls * sizeof(float));
-  w.ctl = o;     o += align_up((size_t)n_kv * ckv::kCtlWords * sizeof(uint32_t));
-  w.hist = o;    o += align_up((size_t)n_kv * ckv::kHistBins * sizeof(uint32_t));
-  w.cand = o;    o += align_up((size_t)n_kv * Ls * sizeof(uint2));
-  w.rsure = o;   o += align_up((size_t)n_kv * n_ranges * sizeof(uint32_t));
-  w.roff = o;    o += align_up((size_t)n_kv * n_ranges * sizeof(uint32_t));
-  w.reqb = o;    o += align_up((size_t)n_kv * n_ranges * sizeof(uint32_t));
+  w.scores = o;  o += align_up((size_t)n_sg * Ls * sizeof(float));
+  w.ctl = o;     o += align_up((size_t)n_sg * ckv::kCtlWords * sizeof(uint32_t));
+  w.hist = o;    o += align_up((size_t)n_sg * ckv::kHistBins * sizeof(uint32_t));
+  w.cand = o;    o += align_up((size_t)n_sg * Ls * sizeof(uint2));
+  w.rsure = o;   o += align_up((size_t)n_sg * n_ranges * sizeof(uint32_t));
+  w.roff = o;    o += align_up((size_t)n_sg * n_ranges * sizeof(uint32_t));
+  w.reqb = o;    o += align_up((size_t)n_sg * n_ranges * sizeof(uint32_t));
   w.total = o;
   return w;
 }
@@ -92,7 +97,8 @@ int check_desc(const ckv_layer_desc* d) {
   if (d->pool != CKV_POOL_AVG && d->pool != CKV_POOL_MAX) return CKV_ERR_INVALID_ARG;
   if (d->pool_kernel < 1 || d->pool_kernel % 2 == 0) return CKV_ERR_INVALID_ARG;
   if (d->pool_kernel > CKV_MAX_POOL_KERNEL) return CKV_ERR_UNSUPPORTED;
-  if (!(d->flags & CKV_KEEP_WINDOW) || (d->flags & ~CKV_KEEP_WINDOW)) return CKV_ERR_UNSUPPORTED;
+  if (!(d->flags & CKV_KEEP_WINDOW) || (d->flags & ~(CKV_KEEP_WINDOW | CKV_SHARE_LAYER)))
+    return CKV_ERR_UNSUPPORTED;
   if (!(d->scale > 0.f) && !(d->scale <= 0.f)) return CKV_ERR_INVALID_ARG;  // NaN
   if (isinf(d->scale)) return CKV_ERR_INVALID_ARG;
   return CKV_OK;
@@ -142,6 +148,8 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
   a.alpha = (float)((double)scale * 1.4426950408889634);  // log2(e)
   a.pool = d->pool;
   a.kp = d->pool_kernel;
+  a.shared = (d->flags & CKV_SHARE_LAYER) ? 1 : 0;
+  a.n_sg = (int32_t)sel_groups(d);
   if (mask) {
     const int G = d->num_q_heads / d->num_kv_heads;
     const int max_rows = ckv::kMaxRows;
@@ -153,15 +161,19 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
       for (int t = 0; t < G; ++t) {
         const int h = g * G + t;
         if (mask[h]) {
+          a.sel_grp[off] = (uint8_t)g;
           a.sel[off++] = (uint8_t)h;
           ++cnt;
         }
       }
-      if (cnt == 0) return CKV_ERR_MASK;
+      // per-group scope: every group selects with its own heads; shared
+      // scope: a group may have none (it is not read)
+      if (cnt == 0 && !a.shared) return CKV_ERR_MASK;
       if (cnt * a.w8 > max_rows) return CKV_ERR_UNSUPPORTED;
       if (cnt > a.max_sel) a.max_sel = cnt;
     }
     a.grp_off[d->num_kv_heads] = (int16_t)off;
+    if (off == 0) return CKV_ERR_MASK;
   }
   a.elt = elt_bytes(d->dtype);
   int32_t blk_kpass = 0, blk_pool = 0, blk_sel = 0, blk_gather = 0;
@@ -203,8 +215,8 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
     q.blk_sel = blk_sel;
     q.blk_gather = blk_gather;
     blk_kpass += q.n_split * d->num_kv_heads;
-    blk_pool += q.n_ptiles * d->num_kv_heads;
-    blk_sel += q.n_ranges * d->num_kv_heads;
+    blk_pool += q.n_ptiles * a.n_sg;
+    blk_sel += q.n_ranges * a.n_sg;
     blk_gather += q.n_gblk * d->num_kv_heads;
     if (ws) {
       const WsLayout l = seq_ws_layout(d, &s);
@@ -229,11 +241,11 @@ int grid_kpass(const ckv::LayerArgs& a) {
 }
 int grid_pool(const ckv::LayerArgs& a) {
   const ckv::SeqArgs& q = a.seq[a.num_seqs - 1];
-  return q.blk_pool + q.n_ptiles * a.n_kv;
+  return q.blk_pool + q.n_ptiles * a.n_sg;
 }
 int grid_sel(const ckv::LayerArgs& a) {
   const ckv::SeqArgs& q = a.seq[a.num_seqs - 1];
-  return q.blk_sel + q.n_ranges * a.n_kv;
+  return q.blk_sel + q.n_ranges * a.n_sg;
 }
 int grid_gather(const ckv::LayerArgs& a) {
   const ckv::SeqArgs& q = a.seq[a.num_seqs - 1];
@@ -277,7 +289,7 @@ int run_select(const ckv::LayerArgs& a, bool caller_scores, hipStream_t st) {
   const int gs = grid_sel(a);
   const ckv::Timing none;
   if (caller_scores) {
-    if ((e = ckv::launch_clear(a, a.num_seqs * a.n_kv, st, timing(ckv::kStageSelect, true, false))) !=
+    if ((e = ckv::launch_clear(a, a.num_seqs * a.n_sg, st, timing(ckv::kStageSelect, true, false))) !=
         hipSuccess)
       return hip_fail(e);
     if ((e = ckv::launch_hist(a, gs, st, none)) != hipSuccess) return hip_fail(e);
@@ -285,7 +297,7 @@ int run_select(const ckv::LayerArgs& a, bool caller_scores, hipStream_t st) {
   if ((e = ckv::launch_filter(a, gs, st, timing(ckv::kStageSelect, !caller_scores, false))) !=
       hipSuccess)
     return hip_fail(e);
-  if ((e = ckv::launch_resolve(a, a.num_seqs * a.n_kv, st, timing(ckv::kStageSelect, false, true))) !=
+  if ((e = ckv::launch_resolve(a, a.num_seqs * a.n_sg, st, timing(ckv::kStageSelect, false, true))) !=
       hipSuccess)
     return hip_fail(e);
   if ((e = ckv::launch_compact(a, gs, st, timing(ckv::kStageGather, true, true))) != hipSuccess)

@@ -101,8 +101,11 @@ struct LayerArgs {
   int32_t elt;             // bytes per element of Q/K/V
   int32_t do_hist;         // scoring also builds the selection histogram
   int32_t do_gather;       // compaction also copies the kept K/V rows
+  int32_t shared;          // one selection per prompt from the layer's chosen heads
+  int32_t n_sg;            // selection groups per prompt: n_kv, or 1 when shared
   int16_t grp_off[kMaxKvHeads + 1];  // chosen heads of group g: sel[grp_off[g] .. grp_off[g+1])
   uint8_t sel[kMaxQHeads];
+  uint8_t sel_grp[kMaxQHeads];       // KV group of chosen head t (sel[t] / G)
   SeqArgs seq[kMaxSeqs];
 };
 

@@ -358,13 +358,15 @@ __global__ __launch_bounds__(kThreads) void rowstats_kernel(const LayerArgs a) {
   const int sel0 = a.grp_off[g], n_sel = a.grp_off[g + 1] - sel0;
   const int nqb = (n_sel * a.w8 + 31) >> 5;
 
-  // the selection state of this group starts from zero in every call; the
-  // pooling kernel that accumulates into it runs after this one
-  if (p == 0 && a.do_hist) {
+  // the selection state starts from zero in every call (one per group, or
+  // one per prompt when shared); the pooling kernel that accumulates into it
+  // runs after this one
+  if (p == 0 && a.do_hist && g < a.n_sg) {
     for (int i = threadIdx.x; i < kCtlWords; i += kThreads) sq.ctl[g * kCtlWords + i] = 0u;
     for (int i = threadIdx.x; i < kHistBins; i += kThreads)
       sq.hist[(int64_t)g * kHistBins + i] = 0u;
   }
+  if (n_sel == 0) return;  // a group without chosen heads (shared scope) is not read
   const int wpq = waves_per_qblock(nqb);
   if (wpq == 1) rowstats_body<DT, D, 1, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, red);
   else if (wpq == 2) rowstats_body<DT, D, 2, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, red);
@@ -539,6 +541,7 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const LayerArgs a) {
   const int g = local / sq.n_split;
   const int p = local - g * sq.n_split;
   const int sel0 = a.grp_off[g], n_sel = a.grp_off[g + 1] - sel0;
+  if (n_sel == 0) return;  // a group without chosen heads (shared scope) is not read
   const int nqb = (n_sel * a.w8 + 31) >> 5;
   const int wpq = waves_per_qblock(nqb);
   if (a.w8 % 32 == 0) {
@@ -554,7 +557,9 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const LayerArgs a) {
 
 // ---------------------------------------------------------------------------
 // Pooling along the tokens, head mean, scores and the selection histogram.
-// One workgroup per (prompt, group, kPoolTile scores); thread t owns the
+// One workgroup per (prompt, selection group, kPoolTile scores), where the
+// selection group is the KV group, or the whole layer when the selection is
+// shared (then the mean runs over every chosen head); thread t owns the
 // kPoolPer consecutive scores starting at t * kPoolPer. The window sums of
 // two heads are staged in LDS per barrier, then every thread pools from a
 // register copy of its kPoolPer + 2*kHalo inputs, with the pool radius R a
@@ -582,35 +587,40 @@ __device__ __forceinline__ void pool_window(const float* x, bool is_max, float i
   }
 }
 
-template <int R>
-__device__ __forceinline__ void pool_tile(const LayerArgs& a, const SeqArgs& sq, int g, int tile,
-                                          float (*row)[kPoolRow], uint32_t* hist_lds) {
-  const int tid = threadIdx.x;
-  const int64_t Ls = sq.L - a.w;
-  const int64_t j0 = (int64_t)tile * kPoolTile;
-  const int n_out = Ls - j0 < kPoolTile ? (int)(Ls - j0) : kPoolTile;
-  const int n_sel = a.grp_off[g + 1] - a.grp_off[g];
-  const bool is_max = a.pool != 0;
-  const float pad = is_max ? -INFINITY : 0.f;  // max ignores padding; avg counts it as 0
-  const float inv_kp = 1.f / (float)a.kp;
-  const bool do_hist = a.do_hist && sq.n_keep > 0;
-  const float* wsum_g = sq.wsum + (int64_t)g * sq.wsum_heads * Ls;
+// What one pooling workgroup needs, resolved from the argument block in the
+// kernel itself (passing the block by reference down the radius dispatch
+// would make the compiler copy it to scratch memory).
+struct PoolJob {
+  const float* const* rows;  // LDS table: window sums of the heads averaged
+  int n_heads;
+  int64_t Ls, j0;            // prefix length, first score of the tile
+  int n_out;                 // scores in this tile
+  bool is_max, do_hist;
+  float inv_kp;
+  float* out;                // scores of the tile
+  uint32_t* ghist;           // the selection group's histogram
+};
 
+template <int R>
+__device__ __forceinline__ void pool_tile(const PoolJob& jb, float (*row)[kPoolRow],
+                                          uint32_t* hist_lds) {
+  const int tid = threadIdx.x;
+  const float pad = jb.is_max ? -INFINITY : 0.f;  // max ignores padding; avg counts it as 0
   float total[kPoolPer];
 #pragma unroll
   for (int u = 0; u < kPoolPer; ++u) total[u] = 0.f;
-  for (int hs0 = 0; hs0 < n_sel; hs0 += 2) {
-    const int nh = n_sel - hs0 < 2 ? n_sel - hs0 : 2;
-    if (hs0 > 0) __syncthreads();  // the previous rows' reads are done
+  for (int tp = 0; tp < jb.n_heads; tp += 2) {
+    const int nh = jb.n_heads - tp < 2 ? jb.n_heads - tp : 2;
+    if (tp > 0) __syncthreads();  // the previous rows' reads are done
     // all loads of the (one or two) rows are issued before any is stored
     constexpr int kLoads = (kPoolRow + kThreads - 1) / kThreads;
     float v0[kLoads], v1[kLoads];
-    const float* src0 = wsum_g + (int64_t)hs0 * Ls;
-    const float* src1 = src0 + Ls;
+    const float* src0 = jb.rows[tp];
+    const float* src1 = jb.rows[nh > 1 ? tp + 1 : tp];
 #pragma unroll
     for (int i = 0; i < kLoads; ++i) {
-      const int64_t j = j0 - kHalo + tid + i * kThreads;
-      const bool in = j >= 0 && j < Ls;
+      const int64_t j = jb.j0 - kHalo + tid + i * kThreads;
+      const bool in = j >= 0 && j < jb.Ls;
       v0[i] = in ? src0[j] : pad;
       v1[i] = in && nh > 1 ? src1[j] : pad;
     }
@@ -622,7 +632,7 @@ __device__ __forceinline__ void pool_tile(const LayerArgs& a, const SeqArgs& sq,
         row[1][idx] = v1[i];
       }
     }
-    if (hs0 == 0 && do_hist)
+    if (tp == 0 && jb.do_hist)
       for (int i = tid; i < kHistBins; i += kThreads) hist_lds[i] = 0u;
     __syncthreads();
     for (int e = 0; e < nh; ++e) {
@@ -637,48 +647,68 @@ __device__ __forceinline__ void pool_tile(const LayerArgs& a, const SeqArgs& sq,
         x[4 * v + 2] = t4.z;
         x[4 * v + 3] = t4.w;
       }
-      pool_window<R>(x, is_max, inv_kp, total);
+      pool_window<R>(x, jb.is_max, jb.inv_kp, total);
     }
   }
   const int o0 = tid * kPoolPer;
-  float* out = sq.scores + (int64_t)g * Ls + j0 + o0;
 #pragma unroll
   for (int u = 0; u < kPoolPer; ++u) {
-    if (o0 + u >= n_out) break;
-    const float score = total[u] / (float)n_sel;
-    out[u] = score;
-    if (do_hist) atomicAdd(&hist_lds[score_key(score) >> kHistShift], 1u);
+    if (o0 + u >= jb.n_out) break;
+    const float score = total[u] / (float)jb.n_heads;
+    jb.out[o0 + u] = score;
+    if (jb.do_hist) atomicAdd(&hist_lds[score_key(score) >> kHistShift], 1u);
   }
-  if (!do_hist) return;
-  // this tile's part of the group's first-level histogram
+  if (!jb.do_hist) return;
+  // this tile's part of the selection group's first-level histogram
   __syncthreads();
-  uint32_t* ghist = sq.hist + (int64_t)g * kHistBins;
   for (int i = tid; i < kHistBins; i += kThreads) {
     const uint32_t c = hist_lds[i];
-    if (c) atomicAdd(&ghist[i], c);
+    if (c) atomicAdd(&jb.ghist[i], c);
   }
 }
 
 template <int R>
-__device__ __forceinline__ void pool_dispatch(int r, const LayerArgs& a, const SeqArgs& sq, int g,
-                                              int tile, float (*row)[kPoolRow], uint32_t* hist) {
+__device__ __forceinline__ void pool_dispatch(int r, const PoolJob& jb, float (*row)[kPoolRow],
+                                              uint32_t* hist) {
   if constexpr (R > kHalo - 1) {
-    pool_tile<R>(a, sq, g, tile, row, hist);
+    pool_tile<R>(jb, row, hist);
   } else {
-    if (r == R) pool_tile<R>(a, sq, g, tile, row, hist);
-    else pool_dispatch<R + 1>(r, a, sq, g, tile, row, hist);
+    if (r == R) pool_tile<R>(jb, row, hist);
+    else pool_dispatch<R + 1>(r, jb, row, hist);
   }
 }
 
 __global__ __launch_bounds__(kThreads) void pool_kernel(const LayerArgs a) {
   __shared__ __align__(16) float row[2][kPoolRow];
   __shared__ uint32_t hist_lds[kHistBins];
+  __shared__ const float* rows[kMaxQHeads];
   const int b = blockIdx.x;
   const SeqArgs& sq = a.seq[find_seq(a, b, [](const SeqArgs& t) { return t.blk_pool; })];
   const int local = b - sq.blk_pool;
-  const int g = local / sq.n_ptiles;
+  const int g = local / sq.n_ptiles;  // selection group (0 when shared)
   const int tile = local - g * sq.n_ptiles;
-  pool_dispatch<0>(a.kp >> 1, a, sq, g, tile, row, hist_lds);  // radius 0..15
+  const int64_t Ls = sq.L - a.w;
+  // the heads averaged here: the group's chosen heads, or every chosen head
+  // of the layer when the selection is shared
+  const int t0 = a.shared ? 0 : a.grp_off[g];
+  const int t1 = a.shared ? a.grp_off[a.n_kv] : a.grp_off[g + 1];
+  for (int t = t0 + (int)threadIdx.x; t < t1; t += kThreads) {
+    const int gt = a.sel_grp[t];  // head t - grp_off[gt] of group gt
+    rows[t - t0] = sq.wsum + ((int64_t)gt * sq.wsum_heads + (t - a.grp_off[gt])) * Ls;
+  }
+  __syncthreads();
+  PoolJob jb;
+  jb.rows = rows;
+  jb.n_heads = t1 - t0;
+  jb.Ls = Ls;
+  jb.j0 = (int64_t)tile * kPoolTile;
+  jb.n_out = Ls - jb.j0 < kPoolTile ? (int)(Ls - jb.j0) : kPoolTile;
+  jb.is_max = a.pool != 0;
+  jb.do_hist = a.do_hist && sq.n_keep > 0;
+  jb.inv_kp = 1.f / (float)a.kp;
+  jb.out = sq.scores + (int64_t)g * Ls + jb.j0;
+  jb.ghist = sq.hist + (int64_t)g * kHistBins;
+  pool_dispatch<0>(a.kp >> 1, jb, row, hist_lds);  // radius 0..15
 }
 
 template <template <int, int> class KernelOf>

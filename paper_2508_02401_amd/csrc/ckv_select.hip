@@ -16,6 +16,8 @@
 //   4. compact_kernel: every range writes its kept indices in ascending order
 //      at its offset (keys above the threshold, then the first keys equal to
 //      it), appends the window positions, and copies the kept K/V rows.
+// With the layer-shared scope there is one selection per prompt (selection
+// group 0) and its rows are copied for every KV head.
 // Each step is its own launch, so stream order makes every hand-off visible
 // without device-wide fences inside the kernels.
 #include <type_traits>
@@ -89,7 +91,7 @@ __device__ __forceinline__ void copy_run(const LayerArgs& a, const SeqArgs& sq, 
 // Zero the selection control words and histograms (ckv_select on caller
 // scores; ckv_compress_layer clears them in the row-statistics kernel).
 __global__ __launch_bounds__(kThreads) void clear_kernel(const LayerArgs a) {
-  const int s = blockIdx.x / a.n_kv, g = blockIdx.x - s * a.n_kv;
+  const int s = blockIdx.x / a.n_sg, g = blockIdx.x - s * a.n_sg;
   const SeqArgs& sq = a.seq[s];
   for (int i = threadIdx.x; i < kCtlWords; i += kThreads) sq.ctl[g * kCtlWords + i] = 0u;
   for (int i = threadIdx.x; i < kHistBins; i += kThreads)
@@ -303,7 +305,7 @@ __global__ __launch_bounds__(kThreads) void resolve_kernel(const LayerArgs a) {
   __shared__ uint32_t lds_b[kMaxRanges];
   __shared__ uint32_t wsum[kWaves];
   __shared__ uint32_t res[3];
-  const int s = blockIdx.x / a.n_kv, g = blockIdx.x - s * a.n_kv;
+  const int s = blockIdx.x / a.n_sg, g = blockIdx.x - s * a.n_sg;
   const SeqArgs& sq = a.seq[s];
   if (sq.n_keep <= 0) return;
   resolve(sq, g, sq.L - a.w, sq.ctl + g * kCtlWords, lds_a, lds_b, wsum, res);
@@ -328,20 +330,27 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const LayerArgs a) {
   const int64_t j0 = (int64_t)r * sq.range;
   const int64_t j1 = j0 + sq.range < Ls ? j0 + sq.range : Ls;
 
+  // the KV heads whose rows this selection keeps: its own, or all of them
+  // when the selection is shared (g is then 0)
+  const int gk0 = a.shared ? 0 : g, gk1 = a.shared ? a.n_kv : g + 1;
+
   if (sq.n_keep < 0) {  // budget >= L: every token stays, in order
     for (int64_t j = j0 + tid; j < j1; j += kThreads) out[j] = (int32_t)j;
     if (r == 0)
       for (int i = tid; i < w; i += kThreads) out[Ls + i] = (int32_t)(Ls + i);
     if (a.do_gather) {
-      copy_run(a, sq, g, j0, j0, j1 - j0);
-      if (r == 0) copy_run(a, sq, g, Ls, Ls, w);
+      for (int gk = gk0; gk < gk1; ++gk) {
+        copy_run(a, sq, gk, j0, j0, j1 - j0);
+        if (r == 0) copy_run(a, sq, gk, Ls, Ls, w);
+      }
     }
     return;
   }
   const uint32_t nk = (uint32_t)sq.n_keep;
   if (r == 0) {  // the window is always kept, after the prefix tokens
     for (int i = tid; i < w; i += kThreads) out[nk + i] = (int32_t)(Ls + i);
-    if (a.do_gather) copy_run(a, sq, g, nk, Ls, w);
+    if (a.do_gather)
+      for (int gk = gk0; gk < gk1; ++gk) copy_run(a, sq, gk, nk, Ls, w);
   }
   if (nk == 0) return;
   const uint32_t* ctl = sq.ctl + g * kCtlWords;
@@ -399,8 +408,9 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const LayerArgs a) {
     if (a.do_gather) {
       __syncthreads();
       const uint32_t n = tot_sel < end - pos_carry ? tot_sel : end - pos_carry;
-      copy_rows(a, sq, g, n, [&](int64_t i) { return (int64_t)tok_l[i]; },
-                [&](int64_t i) { return (int64_t)pos_l[i]; });
+      for (int gk = gk0; gk < gk1; ++gk)
+        copy_rows(a, sq, gk, n, [&](int64_t i) { return (int64_t)tok_l[i]; },
+                  [&](int64_t i) { return (int64_t)pos_l[i]; });
       __syncthreads();
     }
     eq_carry += tot_eq;
@@ -422,7 +432,8 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const LayerArgs a) {
   const int g = local / sq.n_gblk;
   const int r0 = (local - g * sq.n_gblk) * kGatherRows;
   const int n = sq.n_ret - r0 < kGatherRows ? sq.n_ret - r0 : kGatherRows;
-  const int32_t* idx = sq.idx + (int64_t)g * sq.n_ret;
+  // the head's own index row, or the layer's one row when shared
+  const int32_t* idx = sq.idx + (a.shared ? 0 : (int64_t)g * sq.n_ret);
   for (int i = threadIdx.x; i < n; i += kThreads) tok_l[i] = idx[r0 + i];
   __syncthreads();
   copy_rows(a, sq, g, n, [&](int64_t i) { return (int64_t)tok_l[i]; },

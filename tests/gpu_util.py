@@ -26,10 +26,12 @@ class Case:
     pool: str
     kp: int
     dtype: torch.dtype
+    shared: bool = False  # layer-shared selection (CKV_SHARE_LAYER)
 
     def desc(self):
+        flags = ckv.CKV_KEEP_WINDOW | (ckv.CKV_SHARE_LAYER if self.shared else 0)
         return ckv.layer_desc(self.H, self.n_kv, self.d, self.w, self.dtype, 0.0, POOL[self.pool],
-                              self.kp)
+                              self.kp, flags)
 
     @property
     def scale(self) -> float:
@@ -69,9 +71,26 @@ def oracle_group(case: Case, mask, q: torch.Tensor, k: torch.Tensor, g: int, bud
     return scores, idx
 
 
+def oracle_shared(case: Case, mask, q: torch.Tensor, k: torch.Tensor, budget: int):
+    """The layer-shared selection of the oracle: (scores [L-w], idx [min(B, L)])."""
+    return oracle.select_layer_shared(q.double().cpu().numpy(), mask, k.double().cpu().numpy(),
+                                      case.w, case.scale, ORACLE_POOL[case.pool], case.kp,
+                                      int(budget))
+
+
+def check_shared(case: Case, gpu: dict, ref_scores, ref_idx, k: torch.Tensor, v: torch.Tensor,
+                 label: str = ""):
+    """Assert parity of a layer-shared selection: the one score and index row,
+    and every KV head's compact rows at those indices."""
+    rel, swaps = check_group(case, gpu, 0, ref_scores, ref_idx, k, v, label, heads=range(k.shape[0]))
+    return rel, swaps
+
+
 def check_group(case: Case, gpu: dict, g: int, ref_scores, ref_idx, k: torch.Tensor,
-                v: torch.Tensor, label: str = ""):
-    """Assert parity of KV head g of one prompt. Returns (max rel err, swaps)."""
+                v: torch.Tensor, label: str = "", heads=None):
+    """Assert parity of selection row g of one prompt (KV head g, or the shared
+    row 0) and of the compact rows of `heads` (default: head g) at its indices.
+    Returns (max rel err, swaps)."""
     L = k.shape[1]
     gs = gpu["scores"][g] if gpu["scores"] is not None else None
     if gs is not None:
@@ -89,8 +108,9 @@ def check_group(case: Case, gpu: dict, g: int, ref_scores, ref_idx, k: torch.Ten
         np.testing.assert_array_equal(gi[:n_keep], own, err_msg="%s group %d own top-N" % (label, g))
     # compact cache: bit-exact rows of the input at the GPU's indices
     ii = torch.from_numpy(gi.astype(np.int64))
-    assert torch.equal(gpu["k_out"][g], k[g].cpu()[ii]), "%s group %d k_out" % (label, g)
-    assert torch.equal(gpu["v_out"][g], v[g].cpu()[ii]), "%s group %d v_out" % (label, g)
+    for h in (heads if heads is not None else [g]):
+        assert torch.equal(gpu["k_out"][h], k[h].cpu()[ii]), "%s head %d k_out" % (label, h)
+        assert torch.equal(gpu["v_out"][h], v[h].cpu()[ii]), "%s head %d v_out" % (label, h)
     return rel, swaps
 
 

@@ -238,3 +238,48 @@ def test_synth_tiny_inputs_on_cpu():
         logit = (a.k[0][g].double() @ qbar) / 8.0
         assert 2.5 < float(logit[planted].mean()) < 3.5
         assert abs(float(logit[others].mean())) < 0.5
+
+
+def test_shared_scope_mask_rules():
+    # layer-shared scope: a layer with no chosen head at all is rejected before
+    # any launch; an unknown flag bit is unsupported
+    shared = _desc(flags=ckv.CKV_KEEP_WINDOW | ckv.CKV_SHARE_LAYER)
+    for fn in ("score", "compress"):
+        assert _call(fn, shared, _seq(), mask=[0] * 8) == ckv.CKV_ERR_MASK
+        assert _call(fn, _desc(flags=ckv.CKV_KEEP_WINDOW | 4), _seq()) == ckv.CKV_ERR_UNSUPPORTED
+    # rows per group are still limited: 3 heads of one group x window 64 > 128
+    assert _call("score", _desc(window=64, flags=ckv.CKV_KEEP_WINDOW | ckv.CKV_SHARE_LAYER),
+                 _seq(budget=80), mask=[1, 1, 1, 0, 0, 0, 0, 0]) == ckv.CKV_ERR_UNSUPPORTED
+
+
+def test_shared_scope_workspace_is_smaller():
+    # one selection per prompt instead of one per KV group
+    per_group = ckv.layer_desc(32, 8, 128, 32, torch.bfloat16, 0.0, ckv.CKV_POOL_MAX, 7)
+    shared = ckv.layer_desc(32, 8, 128, 32, torch.bfloat16, 0.0, ckv.CKV_POOL_MAX, 7,
+                            ckv.CKV_KEEP_WINDOW | ckv.CKV_SHARE_LAYER)
+    s = ckv.Seq(None, None, None, 512, seq_len=65536)
+    assert 0 < ckv.ckv_workspace_bytes(shared, [s]) < ckv.ckv_workspace_bytes(per_group, [s])
+
+
+def test_kernels_use_no_scratch_memory():
+    # every hot kernel keeps its arrays in registers and LDS; per-lane scratch
+    # (a register array the compiler could not promote, or the argument block
+    # copied to private memory) is a large silent slowdown
+    import re
+    import subprocess
+    from paper_2508_02401_amd import build as B
+
+    procs = {}
+    for src in ("ckv_score.hip", "ckv_select.hip"):  # compiled side by side
+        cmd = [B.HIPCC, "-x", "hip"] + B.COMMON + [
+            "--cuda-device-only", "-c", os.path.join(B.CSRC, src), "-o", os.devnull,
+            "-Rpass-analysis=kernel-resource-usage"]
+        procs[src] = subprocess.Popen(cmd, stdout=subprocess.DEVNULL, stderr=subprocess.PIPE,
+                                      text=True)
+    for src, proc in procs.items():
+        out = proc.communicate(timeout=600)[1]
+        kernels = re.findall(r"Function Name: (\S+)", out)
+        scratch = [int(x) for x in re.findall(r"ScratchSize \[bytes/lane\]: (\d+)", out)]
+        assert kernels and len(kernels) == len(scratch), src
+        bad = [k for k, n in zip(kernels, scratch) if n]
+        assert not bad, "%s: kernels with scratch memory: %s" % (src, bad)

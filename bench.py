@@ -42,6 +42,9 @@ def parse():
     p.add_argument("--streams", type=int, default=1,
                    help="without --pipeline: layers are issued round-robin on this many streams "
                         "(one workspace each); launches then overlap and per-launch times include it")
+    p.add_argument("--scope", choices=("group", "shared"), default="group",
+                   help="group: the workload's per-group head mask (default); shared: the "
+                        "paper's layer-shared selection with 4 retrieval heads per layer")
     p.add_argument("--pipeline", action="store_true",
                    help="two-stream pipeline (ckv_score of layer l+1 beside ckv_select and "
                         "ckv_gather of layer l) instead of one ckv_compress_layer per layer")
@@ -238,8 +241,10 @@ def main():
         calibration_copy(args.calibrate_copy)
     wl = synth.WORKLOADS[args.workload]
     n_layers = wl.n_layers if args.layers <= 0 else min(args.layers, wl.n_layers)
+    shared = args.scope == "shared"
     desc = ckv.layer_desc(wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.window, wl.dtype, 0.0,
-                          wl.pool, wl.pool_kernel)
+                          wl.pool, wl.pool_kernel,
+                          ckv.CKV_KEEP_WINDOW | (ckv.CKV_SHARE_LAYER if shared else 0))
     elt = torch.tensor([], dtype=wl.dtype).element_size()
 
     # budgets per layer and prompt (Algorithm 1 on the host, or the fixed budget)
@@ -262,7 +267,7 @@ def main():
         seqs = [ckv.alloc_outputs(desc, ckv.Seq(inp.q_win[s], inp.k[s], inp.v[s], budgets[s][l]),
                                   with_scores=False)
                 for s in range(len(wl.seq_lens))]
-        layers.append((inp.mask, seqs))
+        layers.append((synth.shared_head_mask(wl, l) if shared else inp.mask, seqs))
     ws_bytes = max(ckv.ckv_workspace_bytes(desc, seqs) for _, seqs in layers)
     main = torch.cuda.current_stream()
     if args.pipeline:
@@ -374,13 +379,20 @@ def main():
     # algorithmic bytes of the whole path per layer (K once, chosen Q rows,
     # retained K/V read + written, indices) and of the dominant kernel
     n_kv, d, w = wl.num_kv_heads, wl.head_dim, wl.window
+    G = wl.num_q_heads // n_kv
+
+    def groups_read(mask):
+        # KV heads whose keys are streamed: those with a chosen query head
+        return len(set((np.nonzero(mask)[0] // G).tolist()))
+
+    n_sg = 1 if shared else n_kv  # index rows written per prompt
     path_bytes = 0
     for li, (mask, seqs) in enumerate(layers):
         n_chosen = int(np.count_nonzero(mask))
         for s, L in enumerate(wl.seq_lens):
             n_ret = min(budgets[s][li], L)
-            path_bytes += n_kv * L * d * elt + n_chosen * w * d * elt + 4 * n_kv * n_ret * d * elt \
-                + 4 * n_kv * n_ret
+            path_bytes += groups_read(mask) * L * d * elt + n_chosen * w * d * elt \
+                + 4 * n_kv * n_ret * d * elt + 4 * n_sg * n_ret
     path_gbs = path_bytes / (ms_per_step / 1e3) / 1e9
 
     # dominant kernel: the one with the largest share of the step
@@ -390,13 +402,14 @@ def main():
         n_chosen = int(np.count_nonzero(mask))
         b = 0
         for L in wl.seq_lens:
+            n_rd = groups_read(mask)
             if dom == "rowstats":
                 # every key of the prompt and the chosen Q rows
-                b += n_kv * L * d * elt + n_chosen * w * d * elt
+                b += n_rd * L * d * elt + n_chosen * w * d * elt
             else:
                 # prefix keys, chosen Q rows, and the window sum of every
                 # chosen head written per prefix token
-                b += n_kv * (L - w) * d * elt + n_chosen * w * d * elt + n_chosen * (L - w) * 4
+                b += n_rd * (L - w) * d * elt + n_chosen * w * d * elt + n_chosen * (L - w) * 4
         dom_bytes.append(b)
     dom_gbs = float(np.mean(dom_bytes)) / (stage_avg[dom] / 1e3) / 1e9
     # MFMA work of the dominant kernel (one logit pass over its keys)
@@ -429,6 +442,8 @@ def main():
                    "window": w, "pool": "max" if wl.pool == 1 else "avg",
                    "pool_kernel": wl.pool_kernel, "heads_per_group": list(wl.n_sel_choices),
                    "budget_avg": float(np.mean(budgets)), "parallelism": "single GPU",
+                   "head_scope": "layer-shared, 4 heads per layer" if shared else
+                                 "per KV group",
                    "streams": n_streams,
                    "schedule": "pipeline: K passes + pooling on stream A, selection + gather on "
                                "stream B, one layer apart" if args.pipeline else

@@ -175,6 +175,12 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
     a.grp_off[d->num_kv_heads] = (int16_t)off;
     if (off == 0) return CKV_ERR_MASK;
   }
+  // KV heads the K passes stream (the others have no chosen head)
+  int64_t n_read = d->num_kv_heads;
+  if (mask) {
+    n_read = 0;
+    for (int g = 0; g < d->num_kv_heads; ++g) n_read += a.grp_off[g + 1] > a.grp_off[g];
+  }
   a.elt = elt_bytes(d->dtype);
   int32_t blk_kpass = 0, blk_pool = 0, blk_sel = 0, blk_gather = 0;
   for (int32_t i = 0; i < n; ++i) {
@@ -196,11 +202,12 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
     q.k_out = s.k_out;
     q.v_out = s.v_out;
     {
-      // K-pass workgroups of this prompt: about kTargetWgs over its KV
-      // heads, at least kMinStagesPerWg stages each. It depends on the prompt
-      // alone, so a prompt's results do not depend on the rest of the batch.
+      // K-pass workgroups of this prompt: about kTargetWgs over the KV
+      // heads it reads, at least kMinStagesPerWg stages each. It depends on
+      // the prompt and the mask alone, so a prompt's results do not depend on
+      // the rest of the batch.
       const int64_t n_st = k_stages(d, s.seq_len);
-      int64_t per_wg = ceil_div(d->num_kv_heads * n_st, ckv::kTargetWgs);
+      int64_t per_wg = ceil_div(n_read * n_st, ckv::kTargetWgs);
       if (per_wg < ckv::kMinStagesPerWg) per_wg = ckv::kMinStagesPerWg;
       const int64_t split = ceil_div(n_st, per_wg), cap = max_split(d, s.seq_len);
       q.n_split = (int32_t)(split < cap ? split : cap);

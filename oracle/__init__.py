@@ -77,6 +77,13 @@ def _load():
         lib.ckvo_select_layer.restype = i64
         lib.ckvo_select_layer_shared.argtypes = lib.ckvo_select_layer.argtypes
         lib.ckvo_select_layer_shared.restype = i64
+        lib.ckvo_decode_attention.argtypes = [P(d), P(d), P(d), i32, i32, i64, i32, d, P(d)]
+        lib.ckvo_decode_attention.restype = ctypes.c_int
+        lib.ckvo_layer_error.argtypes = [P(d), i32, i32, i32, i32, P(d), P(d), i64, P(d), P(d),
+                                         i64, P(d), i32, d, d, P(d), P(d)]
+        lib.ckvo_layer_error.restype = ctypes.c_int
+        lib.ckvo_normalize_errors.argtypes = [P(d), i32, i32, P(d)]
+        lib.ckvo_normalize_errors.restype = ctypes.c_int
         lib.ckvo_allocate_budgets.argtypes = [P(d), i32, i64, i64, i64, P(i64)]
         lib.ckvo_allocate_budgets.restype = ctypes.c_int
         _lib = lib
@@ -214,6 +221,53 @@ def select_layer_shared(q, mask, k, w: int, scale: float, pool_mode: int, kp: in
     if n < 0:
         raise OracleError(int(n), "select_layer_shared")
     return scores, idx
+
+
+def decode_attention(q, k, v, scale: float):
+    """Decode attention, one query per head. q [H, d], k/v [n_kv, n, d] -> [H, d]."""
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    H, d = q.shape
+    n_kv, n, d2 = k.shape
+    assert d2 == d and v.shape == k.shape
+    out = np.empty((H, d), dtype=np.float64)
+    rc = _load().ckvo_decode_attention(_ptr(q, ctypes.c_double), _ptr(k, ctypes.c_double),
+                                       _ptr(v, ctypes.c_double), H, n_kv, n, d, scale,
+                                       _ptr(out, ctypes.c_double))
+    if rc != OK:
+        raise OracleError(rc, "decode_attention")
+    return out
+
+
+def layer_error(q_dec, k, v, k_comp, v_comp, w_o, scale: float, eps: float = 1e-6):
+    """Eq. 6-8 for one layer. q_dec [T, H, d]; k/v [n_kv, L, d]; k_comp/v_comp
+    [n_kv, n_c, d]; w_o [D, H*d]. Returns (e, per-step terms [T])."""
+    q_dec, k, v, kc, vc, w_o = map(_f64, (q_dec, k, v, k_comp, v_comp, w_o))
+    T, H, d = q_dec.shape
+    n_kv, L, _ = k.shape
+    n_c = kc.shape[1]
+    D = w_o.shape[0]
+    assert w_o.shape[1] == H * d and kc.shape == vc.shape and kc.shape[0] == n_kv
+    ratio = np.empty(T, dtype=np.float64)
+    e = np.empty(1, dtype=np.float64)
+    rc = _load().ckvo_layer_error(_ptr(q_dec, ctypes.c_double), T, H, n_kv, d,
+                                  _ptr(k, ctypes.c_double), _ptr(v, ctypes.c_double), L,
+                                  _ptr(kc, ctypes.c_double), _ptr(vc, ctypes.c_double), n_c,
+                                  _ptr(w_o, ctypes.c_double), D, scale, eps,
+                                  _ptr(ratio, ctypes.c_double), _ptr(e, ctypes.c_double))
+    if rc != OK:
+        raise OracleError(rc, "layer_error")
+    return float(e[0]), ratio
+
+
+def normalize_errors(e):
+    """Eq. 10-12: e [n_sets, n_layers] -> e_tilde [n_layers]."""
+    e = _f64(np.atleast_2d(e))
+    out = np.empty(e.shape[1], dtype=np.float64)
+    rc = _load().ckvo_normalize_errors(_ptr(e, ctypes.c_double), e.shape[0], e.shape[1],
+                                       _ptr(out, ctypes.c_double))
+    if rc != OK:
+        raise OracleError(rc, "normalize_errors")
+    return out
 
 
 def allocate_budgets(e, total: int, m: int, M: int):

@@ -16,7 +16,10 @@
  *     usual 1/sqrt(d) factor passed in as `scale`.
  *   - Hyper-parameters (window, pooling kernel, average pooling) from the
  *     appendix "More Implementation Details".
- *   - Layer budgets: Algorithm 1 (error-aware layer-adaptive allocation).
+ *   - Layer budgets: Algorithm 1 (error-aware layer-adaptive allocation), fed
+ *     by the compression error of every layer (Eq. 6-8: decode attention
+ *     with the full and the compressed cache, projected by W_O) normalised
+ *     over profiling sets (Eq. 10-12).
  *
  * Readings of points the paper leaves open (each is listed in the design notes):
  *   R1 scale = 1/sqrt(d) unless given (Eq. 2 omits it).
@@ -37,6 +40,11 @@
  *   R13 query head h belongs to KV group h / (H / n_kv).
  *   R14 Algorithm 1's round() is round-half-to-even; R15 its argmax/argmin
  *      ties go to the lowest layer index.
+ *   R17 the attention of Eq. 6-7 is decode attention with the scale of R1
+ *      and the GQA map of R13, the heads' outputs concatenated head-major;
+ *      R18 a one-token output's Frobenius norm is its 2-norm; R19 the decode
+ *      queries attend to the prompt's cache only (tokens generated while
+ *      profiling are not appended).
  *
  * Everything is fp64 with plain loops; no blocking, fusion or reordering.
  * OpenMP only runs independent KV groups on separate threads.
@@ -333,6 +341,100 @@ int64_t ckvo_select_layer_shared(const double *q, const uint8_t *mask, int32_t H
   free(pooled);
   if (status < 0) return status;
   return ckvo_select_tokens(scores, L, w, budget, idx);
+}
+
+/* Decode attention (Eq. 2 for one query per head): head h attends to the
+ * cache of its group g = h / (H / n_kv) (R13), out[h] = sum_j p_j v[g][j]
+ * with p the softmax over all n cached keys of scale * <q[h], k[g][j]>.
+ * q is [H][d], k and v are [n_kv][n][d], out is [H][d]. */
+int ckvo_decode_attention(const double *q, const double *k, const double *v, int32_t H,
+                          int32_t n_kv, int64_t n, int32_t d, double scale, double *out) {
+  if (!q || !k || !v || !out || H < 1 || n_kv < 1 || H % n_kv || n < 1 || d < 1)
+    return CKVO_EINVAL;
+  int32_t G = H / n_kv;
+  double *p = (double *)malloc(sizeof(double) * (size_t)n);
+  if (!p) return CKVO_ENOMEM;
+  for (int32_t h = 0; h < H; ++h) {
+    const double *kg = k + (int64_t)(h / G) * n * d;
+    const double *vg = v + (int64_t)(h / G) * n * d;
+    ckvo_attention_row(q + (int64_t)h * d, kg, n, d, scale, p);
+    for (int32_t c = 0; c < d; ++c) {
+      double acc = 0.0;
+      for (int64_t j = 0; j < n; ++j) acc += p[j] * vg[j * d + c];
+      out[(int64_t)h * d + c] = acc;
+    }
+  }
+  free(p);
+  return CKVO_OK;
+}
+
+/* Compression error of one layer (Eq. 6-8): for every decoding step t the
+ * attention outputs of all heads, concatenated head-major into an H*d vector,
+ * are taken with the full cache and with the compressed cache and projected
+ * by W_O ([D][H*d], row-major); the step's term is
+ *   || W_O (A_comp,t - A_full,t) || / (|| W_O A_full,t || + eps)
+ * (the Frobenius norm of a one-token output is its 2-norm), and e is their
+ * sum over the T steps. q_dec is [T][H][d]; k, v [n_kv][L][d]; kc, vc
+ * [n_kv][n_c][d]. ratio (optional) receives the T terms. */
+int ckvo_layer_error(const double *q_dec, int32_t T, int32_t H, int32_t n_kv, int32_t d,
+                     const double *k, const double *v, int64_t L, const double *kc,
+                     const double *vc, int64_t n_c, const double *w_o, int32_t D,
+                     double scale, double eps, double *ratio, double *e) {
+  if (!q_dec || !k || !v || !kc || !vc || !w_o || !e || T < 1 || D < 1) return CKVO_EINVAL;
+  int64_t hd = (int64_t)H * d;
+  double *af = (double *)malloc(sizeof(double) * (size_t)hd);
+  double *ac = (double *)malloc(sizeof(double) * (size_t)hd);
+  if (!af || !ac) {
+    free(af);
+    free(ac);
+    return CKVO_ENOMEM;
+  }
+  double total = 0.0;
+  int rc = CKVO_OK;
+  for (int32_t t = 0; t < T && rc == CKVO_OK; ++t) {
+    const double *qt = q_dec + (int64_t)t * hd;
+    rc = ckvo_decode_attention(qt, k, v, H, n_kv, L, d, scale, af);
+    if (rc == CKVO_OK) rc = ckvo_decode_attention(qt, kc, vc, H, n_kv, n_c, d, scale, ac);
+    if (rc != CKVO_OK) break;
+    double num = 0.0, den = 0.0;
+    for (int32_t r = 0; r < D; ++r) {
+      const double *wr = w_o + (int64_t)r * hd;
+      double yf = 0.0, yd = 0.0;
+      for (int64_t c = 0; c < hd; ++c) {
+        yf += wr[c] * af[c];
+        yd += wr[c] * (ac[c] - af[c]);
+      }
+      num += yd * yd;
+      den += yf * yf;
+    }
+    double term = sqrt(num) / (sqrt(den) + eps);
+    if (ratio) ratio[t] = term;
+    total += term;
+  }
+  free(af);
+  free(ac);
+  if (rc != CKVO_OK) return rc;
+  *e = total;
+  return CKVO_OK;
+}
+
+/* Normalised layer errors from profiling sets (Eq. 10-12): e is
+ * [n_sets][n_layers]; each set is L1-normalised over its layers, the sets
+ * are averaged, and the average is L1-normalised again into e_tilde. */
+int ckvo_normalize_errors(const double *e, int32_t n_sets, int32_t n_layers, double *e_tilde) {
+  if (!e || !e_tilde || n_sets < 1 || n_layers < 1) return CKVO_EINVAL;
+  for (int32_t l = 0; l < n_layers; ++l) e_tilde[l] = 0.0;
+  for (int32_t s = 0; s < n_sets; ++s) {
+    double sum = 0.0;
+    for (int32_t l = 0; l < n_layers; ++l) sum += e[(int64_t)s * n_layers + l];
+    if (!(sum > 0.0)) return CKVO_EINVAL;
+    for (int32_t l = 0; l < n_layers; ++l)
+      e_tilde[l] += e[(int64_t)s * n_layers + l] / sum / (double)n_sets;
+  }
+  double sum = 0.0;
+  for (int32_t l = 0; l < n_layers; ++l) sum += e_tilde[l];
+  for (int32_t l = 0; l < n_layers; ++l) e_tilde[l] /= sum;
+  return CKVO_OK;
 }
 
 /* Algorithm 1 (error-aware layer-adaptive cache allocation), step by step:

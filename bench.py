@@ -1,10 +1,13 @@
 """Benchmark of the CompressKV prefill-end KV eviction path on one MI355X.
 
 One step = the whole path (score, select, gather) over every layer of the
-workload, with all inputs already resident in HBM: one ckv_compress_layer per
-layer on one stream by default. --pipeline instead runs ckv_score (both K
-passes and the pooling) of layer l+1 on one stream while ckv_select and
-ckv_gather of layer l run on another. Prints one JSON line.
+workload, with all inputs already resident in HBM. By default one
+ckv_compress_stack call runs all layers: the two K passes of every layer on the
+main stream, the pooling, selection and gather of layer l on a side stream
+while layer l+1's K passes run. --schedule layers issues one
+ckv_compress_layer per layer instead; --pipeline runs ckv_score (both K passes
+and the pooling) of layer l+1 on one stream while ckv_select and ckv_gather of
+layer l run on another. Prints one JSON line.
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
 
@@ -39,8 +42,16 @@ def parse():
     p.add_argument("--layers", type=int, default=0, help="limit the layer count (0 = all)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-threads", type=int, default=0)
+    p.add_argument("--time-every", type=int, default=4, metavar="N",
+                   help="K-pass launches of every N-th layer carry start/end events (the layer "
+                        "offset rotates with the step, so every layer is sampled); each timed "
+                        "launch delays its neighbours' dispatch by a few microseconds")
+    p.add_argument("--schedule", choices=("stack", "layers"), default="stack",
+                   help="stack: one ckv_compress_stack call over all layers, the selection of "
+                        "layer l on a side stream beside the K passes of layer l+1 (default); "
+                        "layers: one ckv_compress_layer per layer (see --streams)")
     p.add_argument("--streams", type=int, default=1,
-                   help="without --pipeline: layers are issued round-robin on this many streams "
+                   help="--schedule layers: layers are issued round-robin on this many streams "
                         "(one workspace each); launches then overlap and per-launch times include it")
     p.add_argument("--scope", choices=("group", "shared"), default="group",
                    help="group: the workload's per-group head mask (default); shared: the "
@@ -270,7 +281,17 @@ def main():
         layers.append((synth.shared_head_mask(wl, l) if shared else inp.mask, seqs))
     ws_bytes = max(ckv.ckv_workspace_bytes(desc, seqs) for _, seqs in layers)
     main = torch.cuda.current_stream()
-    if args.pipeline:
+    stack = args.schedule == "stack" and not args.pipeline
+    if stack:
+        # one call for the whole stack: the K passes on the main stream, the
+        # selection stages on a side stream one layer behind
+        n_streams = 2
+        side = torch.cuda.Stream()
+        streams = [main, side]
+        ws_stack = torch.empty(2 * ws_bytes, dtype=torch.uint8, device=dev)
+        stack_masks = np.stack([m for m, _ in layers])
+        stack_seqs = [sq for _, sq in layers]
+    elif args.pipeline:
         # Two-stream pipeline: stream A runs the scoring stages (ckv_score: both
         # K passes and the pooling) of every layer in order, stream B the
         # selection and gather (ckv_select, ckv_gather) of layer l while A
@@ -298,7 +319,10 @@ def main():
         for li, (mask, seqs) in enumerate(layers):
             slot = li % 2
             if events is not None:
-                ckv.ckv_set_stage_events(events[li][0], events[li][1])
+                if events[li] is None:
+                    ckv.ckv_set_stage_events(None, None)
+                else:
+                    ckv.ckv_set_stage_events(events[li][0], events[li][1])
             if li >= 2:
                 main.wait_event(selected[slot])  # layer li-2 is done with this slot
             ckv.ckv_score(desc, mask, seqs, wss[slot], main)
@@ -318,14 +342,27 @@ def main():
         for li, (mask, seqs) in enumerate(layers):
             si = li % n_streams
             if events is not None:
-                ckv.ckv_set_stage_events(events[li][0], events[li][1])
+                if events[li] is None:
+                    ckv.ckv_set_stage_events(None, None)
+                else:
+                    ckv.ckv_set_stage_events(events[li][0], events[li][1])
             ckv.ckv_compress_layer(desc, mask, seqs, wss[si], streams[si])
         if events is not None:
             ckv.ckv_set_stage_events(None, None)
         for st in streams[1:]:
             main.wait_stream(st)
 
-    step = step_pipeline if args.pipeline else step_layers
+    def step_stack(events=None):
+        if events is not None:
+            ns_ = ckv.CKV_NUM_STAGES
+            ckv.ckv_set_stack_stage_events(
+                [[None] * ns_ if x is None else x[0] for x in events],
+                [[None] * ns_ if x is None else x[1] for x in events])
+        ckv.ckv_compress_stack(desc, stack_masks, stack_seqs, ws_stack, main, side)
+        if events is not None:
+            ckv.ckv_set_stack_stage_events(None, None)
+
+    step = step_stack if stack else (step_pipeline if args.pipeline else step_layers)
 
     for _ in range(args.warmup):
         step()
@@ -333,16 +370,22 @@ def main():
 
     hip = Hip()
     # Only the two K passes (the candidates for the dominant kernel) carry
-    # kernel start/end events: each timed launch costs a few microseconds of
-    # dispatch overlap, so the other stages are left untimed (their times are
-    # in the rocprofv3 kernel trace). ev[step][layer] = (begin, end) arrays.
+    # kernel start/end events, and only on every N-th layer of a step (the
+    # offset rotates with the step): each timed launch delays the dispatch of
+    # its neighbours by a few microseconds, so the other stages and layers are
+    # left untimed (their times are in the rocprofv3 kernel trace).
+    # ev[step][layer] = (begin, end) arrays, or None for an untimed layer.
     timed = ("rowstats", "score")
     ns = ckv.CKV_NUM_STAGES
     idx = {n: ckv.STAGE_NAMES.index(n) for n in timed}
+    every = max(1, args.time_every)
     ev = []
-    for _ in range(args.steps):
+    for k in range(args.steps):
         per_layer = []
-        for _ in range(n_layers):
+        for li in range(n_layers):
+            if (li + k) % every != 0:
+                per_layer.append(None)
+                continue
             b, e = [None] * ns, [None] * ns
             for n in timed:
                 b[idx[n]], e[idx[n]] = hip.event(), hip.event()
@@ -361,14 +404,16 @@ def main():
     ms_per_step = ms_total / args.steps
 
     stage_ms = {n: [] for n in timed}
+    sampled = []  # layer of every timed launch pair
     for k in range(args.steps):
         for li in range(n_layers):
+            if ev[k][li] is None:
+                continue
             b, e = ev[k][li]
+            sampled.append(li)
             for n in timed:
                 stage_ms[n].append(hip.elapsed_ms(b[idx[n]], e[idx[n]]))
-    for k in range(args.steps):
-        for li in range(n_layers):
-            for x in ev[k][li][0] + ev[k][li][1]:
+            for x in b + e:
                 if x is not None:
                     hip.destroy(x)
     stage_avg = {n: float(np.mean(v)) for n, v in stage_ms.items()}
@@ -398,7 +443,8 @@ def main():
     # dominant kernel: the one with the largest share of the step
     dom = max(("rowstats", "score"), key=lambda n: stage_avg[n])
     dom_bytes = []
-    for li, (mask, seqs) in enumerate(layers):
+    for li in sampled:
+        mask = layers[li][0]
         n_chosen = int(np.count_nonzero(mask))
         b = 0
         for L in wl.seq_lens:
@@ -414,7 +460,8 @@ def main():
     dom_gbs = float(np.mean(dom_bytes)) / (stage_avg[dom] / 1e3) / 1e9
     # MFMA work of the dominant kernel (one logit pass over its keys)
     flops = []
-    for li, (mask, seqs) in enumerate(layers):
+    for li in sampled:
+        mask = layers[li][0]
         n_chosen = int(np.count_nonzero(mask))
         f = 0
         for L in wl.seq_lens:
@@ -445,9 +492,11 @@ def main():
                    "head_scope": "layer-shared, 4 heads per layer" if shared else
                                  "per KV group",
                    "streams": n_streams,
-                   "schedule": "pipeline: K passes + pooling on stream A, selection + gather on "
-                               "stream B, one layer apart" if args.pipeline else
-                               "ckv_compress_layer per layer, round-robin over streams"},
+                   "schedule": "ckv_compress_stack: K passes on the main stream, pooling + "
+                               "selection + gather on a side stream one layer behind" if stack else
+                               ("pipeline: K passes + pooling on stream A, selection + gather on "
+                                "stream B, one layer apart" if args.pipeline else
+                                "ckv_compress_layer per layer, round-robin over streams")},
         "path_hbm_gbs": path_gbs,
         "path_hbm_frac": path_gbs / HBM_PEAK_GBS,
         "stage_ms_avg": stage_avg,
@@ -456,6 +505,7 @@ def main():
                      "traffic": traffic, "traffic_gbs": None if traffic is None else
                      traffic / (stage_avg[dom] / 1e3) / 1e9, "avg_launch_ms": stage_avg[dom],
                      "algorithmic_bytes_per_launch": float(np.mean(dom_bytes)),
+                     "timed_launches": len(sampled),
                      "mfma_tflops": dom_tflops, "mfma_frac_bf16": dom_tflops / BF16_PEAK_TFLOPS},
         "wall_s_timed": wall,
     }

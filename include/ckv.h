@@ -26,8 +26,9 @@
  *     surface at the caller's next synchronisation. Calls that share one
  *     workspace must be ordered (same stream or synchronised).
  *   - The library keeps no state between calls apart from cached device
- *     properties; it is safe to call from several host threads with distinct
- *     workspaces.
+ *     properties and, for ckv_compress_stack, a few synchronisation events
+ *     per host thread and device; it is safe to call from several host
+ *     threads with distinct workspaces.
  */
 #ifndef CKV_H_
 #define CKV_H_
@@ -174,6 +175,30 @@ int ckv_gather(const ckv_layer_desc *desc, const ckv_seq *seqs, int32_t num_seqs
 int ckv_compress_layer(const ckv_layer_desc *desc, const uint8_t *head_mask, const ckv_seq *seqs,
                        int32_t num_seqs, void *workspace, size_t workspace_bytes, void *stream);
 
+/* The whole path over a stack of layers that share one descriptor (every
+ * layer of a model at the end of prefill), paper Sec. 3.3 applied per layer.
+ *   head_masks [n_layers][H]: layer l's mask at head_masks + l * H.
+ *   seqs [n_layers][num_seqs]: layer l's prompts at seqs + l * num_seqs, with
+ *       that layer's inputs, budgets and outputs (scores may be NULL); every
+ *       layer has the same prompt lengths.
+ * Every layer's results are those of ckv_compress_layer on it. With
+ * side_stream non-NULL and different from stream, the selection stages of
+ * layer l (pooling, top-N, compaction with the gather) run on side_stream
+ * while the two K passes of layer l+1 run on stream: the latency-bound
+ * selection kernels then hide behind the bandwidth-bound K passes. The call
+ * forks side_stream from stream and joins it back, so all its work is
+ * ordered after earlier work on stream and before later work on stream, and
+ * side_stream is only ordered after its own earlier work besides. The
+ * workspace then holds two layer slots: workspace_bytes must be at least
+ * 2 * ckv_workspace_bytes(desc, seqs, num_seqs) (once without a side
+ * stream). On first use with a side stream the library creates 6 events for
+ * the calling host thread and device and keeps them until the process ends.
+ * If a launch fails mid-way (CKV_ERR_HIP) the layers before it are enqueued
+ * and the fork may be left open: synchronise both streams before reuse. */
+int ckv_compress_stack(const ckv_layer_desc *desc, int32_t n_layers, const uint8_t *head_masks,
+                       const ckv_seq *seqs, int32_t num_seqs, void *workspace,
+                       size_t workspace_bytes, void *stream, void *side_stream);
+
 /* Algorithm 1 (error-aware layer-adaptive cache allocation), host only,
  * synchronous. err_norm [n_layers] are the normalised per-layer errors,
  * total is B_total, [m, M] the per-layer bounds. out [n_layers] receives the
@@ -203,6 +228,15 @@ int ckv_last_hip_error(void);
  * stop. Per host thread. */
 #define CKV_NUM_STAGES 5
 int ckv_set_stage_events(void *const *begin, void *const *end);
+
+/* Per-layer stage timing of ckv_compress_stack: begin/end hold
+ * n_layers * CKV_NUM_STAGES events (layer l, stage s at index
+ * l * CKV_NUM_STAGES + s; NULL entries untimed) and apply to layers
+ * 0..n_layers-1 of the following ckv_compress_stack calls on this host thread,
+ * in place of the ckv_set_stage_events ones; NULL arrays stop it. The arrays
+ * are read at each call, not copied: keep them alive while set. Stages 0-1
+ * run on the stream, stages 2-4 on the side stream when there is one. */
+int ckv_set_stack_stage_events(void *const *begin, void *const *end, int32_t n_layers);
 
 #ifdef __cplusplus
 }

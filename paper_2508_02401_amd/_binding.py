@@ -33,8 +33,8 @@ CKV_SHARE_LAYER = 2
 CKV_MAX_SEQS = 16
 
 EXPORTED = ("ckv_workspace_bytes", "ckv_score", "ckv_select", "ckv_gather", "ckv_compress_layer",
-            "ckv_allocate_budgets", "ckv_status_string", "ckv_last_hip_error",
-            "ckv_set_stage_events")
+            "ckv_compress_stack", "ckv_allocate_budgets", "ckv_status_string",
+            "ckv_last_hip_error", "ckv_set_stage_events", "ckv_set_stack_stage_events")
 
 _DTYPE_CODE = {torch.bfloat16: CKV_BF16, torch.float16: CKV_F16, torch.float32: CKV_F32}
 
@@ -84,6 +84,9 @@ def load() -> ctypes.CDLL:
         lib.ckv_gather.argtypes = [D, S, ctypes.c_int32, vp]
         lib.ckv_compress_layer.argtypes = [D, P(ctypes.c_uint8), S, ctypes.c_int32, vp,
                                            ctypes.c_size_t, vp]
+        lib.ckv_compress_stack.argtypes = [D, ctypes.c_int32, P(ctypes.c_uint8), S, ctypes.c_int32,
+                                           vp, ctypes.c_size_t, vp, vp]
+        lib.ckv_set_stack_stage_events.argtypes = [P(vp), P(vp), ctypes.c_int32]
         lib.ckv_allocate_budgets.argtypes = [P(ctypes.c_double), ctypes.c_int32, ctypes.c_int64,
                                              ctypes.c_int32, ctypes.c_int32, P(ctypes.c_int32)]
         lib.ckv_status_string.argtypes = [ctypes.c_int]
@@ -91,7 +94,8 @@ def load() -> ctypes.CDLL:
         lib.ckv_last_hip_error.argtypes = []
         lib.ckv_set_stage_events.argtypes = [P(vp), P(vp)]
         for name in ("ckv_score", "ckv_select", "ckv_gather", "ckv_compress_layer",
-                     "ckv_allocate_budgets", "ckv_last_hip_error", "ckv_set_stage_events"):
+                     "ckv_compress_stack", "ckv_allocate_budgets", "ckv_last_hip_error",
+                     "ckv_set_stage_events", "ckv_set_stack_stage_events"):
             getattr(lib, name).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -217,6 +221,28 @@ def ckv_compress_layer(desc, head_mask, seqs: Sequence[Seq], workspace: torch.Te
                                      _stream(stream)), "ckv_compress_layer")
 
 
+def ckv_compress_stack(desc, head_masks, seqs: Sequence[Sequence[Seq]], workspace: torch.Tensor,
+                       stream=None, side_stream=None) -> None:
+    """head_masks [n_layers][H]; seqs[l] is layer l's list of prompts (the same
+    lengths in every layer). With a side stream the workspace holds two layer
+    slots (2 * ckv_workspace_bytes of one layer)."""
+    n_layers = len(seqs)
+    num_seqs = len(seqs[0]) if n_layers else 0
+    if any(len(x) != num_seqs for x in seqs):
+        raise ValueError("ckv_compress_stack: every layer needs the same number of prompts")
+    flat = [s for layer in seqs for s in layer]
+    arr = _seq_array(flat)
+    m = np.ascontiguousarray(np.asarray(head_masks, dtype=np.uint8)).reshape(-1)
+    if m.size != n_layers * desc.num_q_heads:
+        raise ValueError("ckv_compress_stack: head_masks must be [n_layers][H]")
+    masks = (ctypes.c_uint8 * m.size).from_buffer_copy(m.tobytes())
+    side = None if side_stream is None else _stream(side_stream)
+    _check(load().ckv_compress_stack(ctypes.byref(desc), n_layers, masks, arr, num_seqs,
+                                     workspace.data_ptr(),
+                                     workspace.numel() * workspace.element_size(),
+                                     _stream(stream), side), "ckv_compress_stack")
+
+
 def ckv_allocate_budgets(err_norm, total: int, m: int, M: int):
     """Algorithm 1 on the host. Returns (budgets int32 array, status)."""
     e = np.ascontiguousarray(np.asarray(err_norm, dtype=np.float64))
@@ -244,6 +270,27 @@ def ckv_set_stage_events(begin, end) -> None:
     b = (ctypes.c_void_p * CKV_NUM_STAGES)(*begin)
     e = (ctypes.c_void_p * CKV_NUM_STAGES)(*end)
     _check(load().ckv_set_stage_events(b, e), "ckv_set_stage_events")
+
+
+_stack_events = None  # keeps the arrays passed to ckv_set_stack_stage_events alive
+
+
+def ckv_set_stack_stage_events(begin, end) -> None:
+    """begin/end: [n_layers][CKV_NUM_STAGES] raw hipEvent_t handles (None entries
+    untimed) for the layers of the following ckv_compress_stack calls, or None
+    to stop."""
+    global _stack_events
+    if begin is None or end is None:
+        _check(load().ckv_set_stack_stage_events(None, None, 0), "ckv_set_stack_stage_events")
+        _stack_events = None
+        return
+    n = len(begin)
+    if len(end) != n or any(len(x) != CKV_NUM_STAGES for x in list(begin) + list(end)):
+        raise ValueError("ckv_set_stack_stage_events: need [n_layers][%d] events" % CKV_NUM_STAGES)
+    b = (ctypes.c_void_p * (n * CKV_NUM_STAGES))(*[x for row in begin for x in row])
+    e = (ctypes.c_void_p * (n * CKV_NUM_STAGES))(*[x for row in end for x in row])
+    _stack_events = (b, e)
+    _check(load().ckv_set_stack_stage_events(b, e, n), "ckv_set_stack_stage_events")
 
 
 # --------------------------------------------------------------------------

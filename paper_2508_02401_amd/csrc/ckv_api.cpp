@@ -15,6 +15,14 @@ thread_local int g_last_hip_error = 0;
 thread_local hipEvent_t g_ev_begin[ckv::kNumStages] = {};
 thread_local hipEvent_t g_ev_end[ckv::kNumStages] = {};
 thread_local bool g_events_on = false;
+// ckv_compress_stack: per-layer stage events, and the fork/join events of its
+// side stream per device (created on first use, kept for the process)
+thread_local void* const* g_stack_begin = nullptr;
+thread_local void* const* g_stack_end = nullptr;
+thread_local int32_t g_stack_layers = 0;
+constexpr int kMaxDevices = 16;
+enum SyncEvent { kEvFork = 0, kEvJoin = 1, kEvScored = 2, kEvSelected = 4, kNumSyncEvents = 6 };
+thread_local hipEvent_t g_sync_ev[kMaxDevices][kNumSyncEvents] = {};
 
 constexpr size_t kAlign = 256;
 
@@ -55,6 +63,10 @@ int64_t wsum_heads(const ckv_layer_desc* d) {
   return h > 0 ? h : 1;
 }
 
+// Floats per window-sum row: the prefix length rounded up to 4, so that every
+// row starts 16-byte aligned.
+int64_t ws_stride(int64_t Ls) { return (Ls + 3) / 4 * 4; }
+
 // Per-prompt workspace, in order: K-pass partials, head window sums, scores, selection control words, histograms, candidates, per-range
 // counts/offsets.
 struct WsLayout {
@@ -68,7 +80,7 @@ WsLayout seq_ws_layout(const ckv_layer_desc* d, const ckv_seq* s) {
   WsLayout w;
   size_t o = 0;
   w.partial = o; o += align_up((size_t)n_kv * max_split(d, s->seq_len) * ckv::kMaxRows * sizeof(float2));
-  w.wsum = o;    o += align_up((size_t)n_kv * wsum_heads(d) * Ls * sizeof(float));
+  w.wsum = o;    o += align_up((size_t)n_kv * wsum_heads(d) * ws_stride(Ls) * sizeof(float));
   w.scores = o;  o += align_up((size_t)n_sg * Ls * sizeof(float));
   w.ctl = o;     o += align_up((size_t)n_sg * ckv::kCtlWords * sizeof(uint32_t));
   w.hist = o;    o += align_up((size_t)n_sg * ckv::kHistBins * sizeof(uint32_t));
@@ -213,6 +225,7 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
       q.n_split = (int32_t)(split < cap ? split : cap);
     }
     q.wsum_heads = (int32_t)wsum_heads(d);
+    q.ws_stride = ws_stride(Ls);
     q.n_ptiles = (int32_t)ceil_div(Ls, ckv::kPoolTile);
     q.range = (int32_t)range_size(Ls);
     q.n_ranges = (int32_t)ceil_div(Ls, q.range);
@@ -275,7 +288,8 @@ ckv::Timing timing(int stage, bool first, bool last) {
   return t;
 }
 
-int run_score(const ckv_layer_desc* d, const ckv::LayerArgs& a, hipStream_t st) {
+// The two K passes (row statistics, then window sums).
+int run_kpasses(const ckv_layer_desc* d, const ckv::LayerArgs& a, hipStream_t st) {
   hipError_t e;
   if ((e = ckv::launch_rowstats(d->dtype, a, grid_kpass(a), st,
                                 timing(ckv::kStageRowStats, true, true))) != hipSuccess)
@@ -283,9 +297,17 @@ int run_score(const ckv_layer_desc* d, const ckv::LayerArgs& a, hipStream_t st) 
   if ((e = ckv::launch_score(d->dtype, a, grid_kpass(a), st,
                              timing(ckv::kStageScore, true, true))) != hipSuccess)
     return hip_fail(e);
-  if ((e = ckv::launch_pool(a, grid_pool(a), st, timing(ckv::kStagePool, true, true))) != hipSuccess)
-    return hip_fail(e);
   return CKV_OK;
+}
+
+int run_pool(const ckv::LayerArgs& a, hipStream_t st) {
+  const hipError_t e = ckv::launch_pool(a, grid_pool(a), st, timing(ckv::kStagePool, true, true));
+  return e == hipSuccess ? CKV_OK : hip_fail(e);
+}
+
+int run_score(const ckv_layer_desc* d, const ckv::LayerArgs& a, hipStream_t st) {
+  const int rc = run_kpasses(d, a, st);
+  return rc != CKV_OK ? rc : run_pool(a, st);
 }
 
 // Selection on scores already in place. With caller scores (ckv_select) the
@@ -395,6 +417,111 @@ int ckv_compress_layer(const ckv_layer_desc* desc, const uint8_t* head_mask, con
   return run_select(a, false, st);
 }
 
+int ckv_compress_stack(const ckv_layer_desc* desc, int32_t n_layers, const uint8_t* head_masks,
+                       const ckv_seq* seqs, int32_t num_seqs, void* workspace,
+                       size_t workspace_bytes, void* stream, void* side_stream) {
+  int rc = check_desc(desc);
+  if (rc != CKV_OK) return rc;
+  if (n_layers < 1 || !head_masks || !seqs) return CKV_ERR_INVALID_ARG;
+  if (num_seqs < 1) return CKV_ERR_INVALID_ARG;
+  if (num_seqs > CKV_MAX_SEQS) return CKV_ERR_UNSUPPORTED;
+  const hipStream_t st = (hipStream_t)stream;
+  const hipStream_t side = (hipStream_t)side_stream;
+  const bool two = side != nullptr && side != st;
+  // every layer is validated before anything is enqueued
+  const size_t slot_bytes = ckv_workspace_bytes(desc, seqs, num_seqs);
+  if (slot_bytes == 0) return CKV_ERR_INVALID_ARG;
+  for (int32_t l = 0; l < n_layers; ++l) {
+    const ckv_seq* ls = seqs + (int64_t)l * num_seqs;
+    if ((rc = check_seqs(desc, ls, num_seqs, kNeedQ | kNeedK | kNeedV | kNeedIdx | kNeedOut)) !=
+        CKV_OK)
+      return rc;
+    for (int32_t i = 0; i < num_seqs; ++i) {
+      if (ls[i].seq_len != seqs[i].seq_len) return CKV_ERR_INVALID_ARG;
+      if (ls[i].scores && !aligned16(ls[i].scores)) return CKV_ERR_INVALID_ARG;
+    }
+    ckv::LayerArgs probe;
+    if ((rc = build_args(desc, head_masks + (int64_t)l * desc->num_q_heads, ls, num_seqs, nullptr,
+                         true, probe)) != CKV_OK)
+      return rc;
+  }
+  if (!workspace || !aligned16(workspace) || workspace_bytes < (two ? 2 : 1) * slot_bytes)
+    return CKV_ERR_WORKSPACE;
+  // fork/join and hand-off events of this thread on the current device
+  hipEvent_t* ev = nullptr;
+  if (two) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e);
+    if (dev < 0 || dev >= kMaxDevices) return CKV_ERR_UNSUPPORTED;
+    ev = g_sync_ev[dev];
+    for (int i = 0; i < kNumSyncEvents; ++i)
+      if (!ev[i] && (e = hipEventCreateWithFlags(&ev[i], hipEventDisableTiming)) != hipSuccess)
+        return hip_fail(e);
+    if ((e = hipEventRecord(ev[kEvFork], st)) != hipSuccess) return hip_fail(e);
+    if ((e = hipStreamWaitEvent(side, ev[kEvFork], 0)) != hipSuccess) return hip_fail(e);
+  }
+  // per-layer stage events replace the per-call ones for the duration
+  const bool saved_on = g_events_on;
+  hipEvent_t saved_b[ckv::kNumStages], saved_e[ckv::kNumStages];
+  for (int i = 0; i < ckv::kNumStages; ++i) {
+    saved_b[i] = g_ev_begin[i];
+    saved_e[i] = g_ev_end[i];
+  }
+  const bool stack_timed = g_stack_begin != nullptr;
+  for (int32_t l = 0; l < n_layers && rc == CKV_OK; ++l) {
+    const int slot = two ? (l & 1) : 0;
+    char* ws = static_cast<char*>(workspace) + slot * slot_bytes;
+    ckv::LayerArgs a;
+    if ((rc = build_args(desc, head_masks + (int64_t)l * desc->num_q_heads,
+                         seqs + (int64_t)l * num_seqs, num_seqs, ws, true, a)) != CKV_OK)
+      break;
+    a.do_hist = 1;
+    a.do_gather = 1;
+    if (stack_timed) {
+      g_events_on = l < g_stack_layers;
+      for (int i = 0; i < ckv::kNumStages; ++i) {
+        g_ev_begin[i] = g_events_on ? (hipEvent_t)g_stack_begin[l * ckv::kNumStages + i] : nullptr;
+        g_ev_end[i] = g_events_on ? (hipEvent_t)g_stack_end[l * ckv::kNumStages + i] : nullptr;
+      }
+    }
+    hipError_t e;
+    // the selection of layer l-2 used this slot: wait until it is done
+    if (two && l >= 2 && (e = hipStreamWaitEvent(st, ev[kEvSelected + slot], 0)) != hipSuccess) {
+      rc = hip_fail(e);
+      break;
+    }
+    if ((rc = run_kpasses(desc, a, st)) != CKV_OK) break;
+    hipStream_t sel = st;
+    if (two) {
+      if ((e = hipEventRecord(ev[kEvScored + slot], st)) != hipSuccess ||
+          (e = hipStreamWaitEvent(side, ev[kEvScored + slot], 0)) != hipSuccess) {
+        rc = hip_fail(e);
+        break;
+      }
+      sel = side;
+    }
+    if ((rc = run_pool(a, sel)) != CKV_OK) break;
+    if ((rc = run_select(a, false, sel)) != CKV_OK) break;
+    if (two && (e = hipEventRecord(ev[kEvSelected + slot], side)) != hipSuccess) {
+      rc = hip_fail(e);
+      break;
+    }
+  }
+  g_events_on = saved_on;
+  for (int i = 0; i < ckv::kNumStages; ++i) {
+    g_ev_begin[i] = saved_b[i];
+    g_ev_end[i] = saved_e[i];
+  }
+  if (rc != CKV_OK) return rc;
+  if (two) {
+    hipError_t e;
+    if ((e = hipEventRecord(ev[kEvJoin], side)) != hipSuccess) return hip_fail(e);
+    if ((e = hipStreamWaitEvent(st, ev[kEvJoin], 0)) != hipSuccess) return hip_fail(e);
+  }
+  return CKV_OK;
+}
+
 int ckv_allocate_budgets(const double* err_norm, int32_t n_layers, int64_t total, int32_t m,
                          int32_t M, int32_t* out) {
   if (!err_norm || !out || n_layers < 1 || m < 0 || M < m) return CKV_ERR_INVALID_ARG;
@@ -454,6 +581,18 @@ int ckv_last_hip_error(void) { return g_last_hip_error; }
 
 static_assert(ckv::kNumStages == CKV_NUM_STAGES, "stage count of the C ABI");
 static_assert(sizeof(ckv::LayerArgs) <= 4096, "kernel argument block");
+
+int ckv_set_stack_stage_events(void* const* begin, void* const* end, int32_t n_layers) {
+  if (!begin || !end || n_layers <= 0) {
+    g_stack_begin = g_stack_end = nullptr;
+    g_stack_layers = 0;
+    return CKV_OK;
+  }
+  g_stack_begin = begin;
+  g_stack_end = end;
+  g_stack_layers = n_layers;
+  return CKV_OK;
+}
 
 int ckv_set_stage_events(void* const* begin, void* const* end) {
   if (!begin || !end) {

@@ -16,13 +16,13 @@ constexpr int kMaxSplit = 512;     // workgroups per (prompt, KV head) in a K pa
 constexpr int kMinStagesPerWg = 4; // K stages per workgroup (at least)
 constexpr int kTargetWgs = 512;    // K-pass workgroups per launch: 2 on each of 256 CUs
 constexpr int kPoolTile = 2048;    // scores per pooling workgroup
-constexpr int kHalo = 16;          // pooling halo on each side (pool kernel <= 2*16+1)
+constexpr int kMaxPoolRadius = 15; // pool kernel <= 2*15+1
 constexpr int kGatherRows = 64;    // retained rows per gather workgroup
 constexpr int kHistBits = 12;      // first-level histogram: key bits 30..19
 constexpr int kHistBins = 1 << kHistBits;
 constexpr int kHistShift = 31 - kHistBits;
 constexpr int kRangeMin = 4096;    // scores per selection workgroup (at least)
-constexpr int kMaxRanges = 2048;   // selection ranges per KV head (at most)
+constexpr int kMaxRanges = 1024;   // selection ranges per KV head (at most)
 
 // Per-(prompt, KV head) control words of the selection, in the workspace.
 enum Ctl {
@@ -67,7 +67,7 @@ struct SeqArgs {
   void* v_out;
   // workspace
   float2* partial;         // [n_kv][n_split][kMaxRows]: (max logit, sum exp2) per workgroup
-  float* wsum;             // [n_kv][wsum_heads][L - w]: window sum of each chosen head
+  float* wsum;             // [n_kv][wsum_heads][ws_stride]: window sum of each chosen head
   uint32_t* ctl;           // [n_kv][kCtlWords]
   uint32_t* hist;          // [n_kv][kHistBins]
   uint2* cand;             // [n_kv][L - w]: (key, index) of threshold-bin candidates
@@ -75,6 +75,7 @@ struct SeqArgs {
   uint32_t* roff;          // [n_kv][n_ranges]: output offset of each range
   uint32_t* reqb;          // [n_kv][n_ranges]: threshold-equal keys before each range
   int32_t n_split;         // P: workgroups per KV head in each K pass
+  int64_t ws_stride;       // floats per window-sum row: L - w rounded up to 4
   int32_t wsum_heads;      // head slots per KV head in wsum
   int32_t n_ptiles;        // ceil((L - w) / kPoolTile)
   int32_t n_ranges;        // ceil((L - w) / range)

@@ -466,7 +466,7 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
   // 8-row groups otherwise); their fixed-order sum is written to
   // wsum[g][hs][token].
   const int rph = QM ? a.w8 / 32 : a.w8 / 8;
-  float* wsum_g = sq.wsum + (int64_t)g * sq.wsum_heads * Ls;
+  float* wsum_g = sq.wsum + (int64_t)g * sq.wsum_heads * sq.ws_stride;
   auto fold = [&](int kk) {
     const float* gb = gsum + (kk & 1) * (kGroupRows * ST);
     const int64_t t0 = (int64_t)p * ST + kk * stride;
@@ -475,7 +475,7 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
       if (t0 + c >= Ls) continue;
       float acc = gb[(hs * rph) * ST + c];
       for (int q8 = 1; q8 < rph; ++q8) acc += gb[(hs * rph + q8) * ST + c];
-      wsum_g[(int64_t)hs * Ls + t0 + c] = acc;
+      wsum_g[(int64_t)hs * sq.ws_stride + t0 + c] = acc;
     }
   };
 
@@ -560,32 +560,17 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const LayerArgs a) {
 // One workgroup per (prompt, selection group, kPoolTile scores), where the
 // selection group is the KV group, or the whole layer when the selection is
 // shared (then the mean runs over every chosen head); thread t owns the
-// kPoolPer consecutive scores starting at t * kPoolPer. The window sums of
-// two heads are staged in LDS per barrier, then every thread pools from a
-// register copy of its kPoolPer + 2*kHalo inputs, with the pool radius R a
-// template parameter so that only the needed taps are evaluated.
+// kPoolPer consecutive scores starting at t * kPoolPer. Window-sum rows are
+// padded to a multiple of 4 floats, so a thread reads its scores and an
+// R-wide halo on each side (rounded up to 4) with aligned 16-byte loads
+// straight from global memory, the pool radius R being a template parameter
+// so that only the needed taps are evaluated. The workgroup's histogram
+// lives in LDS as packed 16-bit counters (a tile has at most 2048 scores),
+// which keeps the kernel small enough in LDS to share a CU with two K-pass
+// workgroups.
 // ---------------------------------------------------------------------------
 constexpr int kPoolPer = kPoolTile / kThreads;  // scores per thread
-constexpr int kPoolRow = kPoolTile + 2 * kHalo;
-constexpr int kPoolWin = kPoolPer + 2 * kHalo;  // inputs one thread pools from
-static_assert(kPoolPer % 4 == 0 && kHalo % 4 == 0, "float4 staging");
-
-// total[u] += pool over [u - R, u + R] of this thread's window x (avg: sum / kp).
-template <int R>
-__device__ __forceinline__ void pool_window(const float* x, bool is_max, float inv_kp,
-                                            float* total) {
-  static_assert(R <= kHalo, "pool radius within the halo");
-#pragma unroll
-  for (int u = 0; u < kPoolPer; ++u) {
-    float v = x[kHalo + u];
-#pragma unroll
-    for (int dt = 1; dt <= R; ++dt) {
-      const float lo = x[kHalo + u - dt], hi = x[kHalo + u + dt];
-      v = is_max ? fmaxf(v, fmaxf(lo, hi)) : v + (lo + hi);
-    }
-    total[u] += is_max ? v : v * inv_kp;
-  }
-}
+static_assert(kPoolPer == 8 && kPoolTile <= 65535, "8 scores per thread, 16-bit bin counts");
 
 // What one pooling workgroup needs, resolved from the argument block in the
 // kernel itself (passing the block by reference down the radius dispatch
@@ -601,86 +586,90 @@ struct PoolJob {
   uint32_t* ghist;           // the selection group's histogram
 };
 
+// x[i] = row[o0 - HW + i] for i in [0, 8 + 2*HW); inputs outside [0, Ls)
+// read as pad. Aligned 16-byte loads when the window lies inside the row
+// (o0 - HW is a multiple of 4 and rows start 16-byte aligned).
+template <int HW>
+__device__ __forceinline__ void pool_inputs(const float* row, int64_t o0, int64_t Ls, float pad,
+                                            float* x) {
+  constexpr int NX = kPoolPer + 2 * HW;
+  const int64_t lo = o0 - HW;
+  if (lo >= 0 && lo + NX <= Ls) {
+    const float4* src = reinterpret_cast<const float4*>(row + lo);
+#pragma unroll
+    for (int v = 0; v < NX / 4; ++v) {
+      const float4 t = src[v];
+      x[4 * v] = t.x;
+      x[4 * v + 1] = t.y;
+      x[4 * v + 2] = t.z;
+      x[4 * v + 3] = t.w;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < NX; ++i) {
+      const int64_t j = lo + i;
+      x[i] = j >= 0 && j < Ls ? row[j] : pad;
+    }
+  }
+}
+
 template <int R>
-__device__ __forceinline__ void pool_tile(const PoolJob& jb, float (*row)[kPoolRow],
-                                          uint32_t* hist_lds) {
+__device__ __forceinline__ void pool_tile(const PoolJob& jb, uint32_t* hist_lds) {
+  constexpr int HW = (R + 3) / 4 * 4;  // halo loaded on each side
+  constexpr int NX = kPoolPer + 2 * HW;
   const int tid = threadIdx.x;
   const float pad = jb.is_max ? -INFINITY : 0.f;  // max ignores padding; avg counts it as 0
+  const int64_t o0 = jb.j0 + (int64_t)tid * kPoolPer;
   float total[kPoolPer];
 #pragma unroll
   for (int u = 0; u < kPoolPer; ++u) total[u] = 0.f;
-  for (int tp = 0; tp < jb.n_heads; tp += 2) {
-    const int nh = jb.n_heads - tp < 2 ? jb.n_heads - tp : 2;
-    if (tp > 0) __syncthreads();  // the previous rows' reads are done
-    // all loads of the (one or two) rows are issued before any is stored
-    constexpr int kLoads = (kPoolRow + kThreads - 1) / kThreads;
-    float v0[kLoads], v1[kLoads];
-    const float* src0 = jb.rows[tp];
-    const float* src1 = jb.rows[nh > 1 ? tp + 1 : tp];
+  for (int hh = 0; hh < jb.n_heads; ++hh) {
+    float x[NX];
+    pool_inputs<HW>(jb.rows[hh], o0, jb.Ls, pad, x);
 #pragma unroll
-    for (int i = 0; i < kLoads; ++i) {
-      const int64_t j = jb.j0 - kHalo + tid + i * kThreads;
-      const bool in = j >= 0 && j < jb.Ls;
-      v0[i] = in ? src0[j] : pad;
-      v1[i] = in && nh > 1 ? src1[j] : pad;
-    }
+    for (int u = 0; u < kPoolPer; ++u) {
+      float v = x[HW + u];
 #pragma unroll
-    for (int i = 0; i < kLoads; ++i) {
-      const int idx = tid + i * kThreads;
-      if (idx < kPoolRow) {
-        row[0][idx] = v0[i];
-        row[1][idx] = v1[i];
+      for (int dt = 1; dt <= R; ++dt) {
+        const float lo = x[HW + u - dt], hi = x[HW + u + dt];
+        v = jb.is_max ? fmaxf(v, fmaxf(lo, hi)) : v + (lo + hi);
       }
-    }
-    if (tp == 0 && jb.do_hist)
-      for (int i = tid; i < kHistBins; i += kThreads) hist_lds[i] = 0u;
-    __syncthreads();
-    for (int e = 0; e < nh; ++e) {
-      // x[i] = window sum at score index tid*kPoolPer - kHalo + i
-      float x[kPoolWin];
-      const float4* rp = reinterpret_cast<const float4*>(row[e] + tid * kPoolPer);
-#pragma unroll
-      for (int v = 0; v < kPoolWin / 4; ++v) {
-        const float4 t4 = rp[v];
-        x[4 * v] = t4.x;
-        x[4 * v + 1] = t4.y;
-        x[4 * v + 2] = t4.z;
-        x[4 * v + 3] = t4.w;
-      }
-      pool_window<R>(x, jb.is_max, jb.inv_kp, total);
+      total[u] += jb.is_max ? v : v * jb.inv_kp;
     }
   }
-  const int o0 = tid * kPoolPer;
+  const int n_mine = jb.n_out - tid * kPoolPer;  // scores of this thread inside the tile
 #pragma unroll
   for (int u = 0; u < kPoolPer; ++u) {
-    if (o0 + u >= jb.n_out) break;
+    if (u >= n_mine) break;
     const float score = total[u] / (float)jb.n_heads;
-    jb.out[o0 + u] = score;
-    if (jb.do_hist) atomicAdd(&hist_lds[score_key(score) >> kHistShift], 1u);
+    jb.out[tid * kPoolPer + u] = score;
+    if (jb.do_hist) {
+      const uint32_t bin = score_key(score) >> kHistShift;
+      atomicAdd(&hist_lds[bin >> 1], 1u << ((bin & 1u) * 16u));
+    }
   }
   if (!jb.do_hist) return;
   // this tile's part of the selection group's first-level histogram
   __syncthreads();
-  for (int i = tid; i < kHistBins; i += kThreads) {
+  for (int i = tid; i < kHistBins / 2; i += kThreads) {
     const uint32_t c = hist_lds[i];
-    if (c) atomicAdd(&jb.ghist[i], c);
+    if (c & 0xFFFFu) atomicAdd(&jb.ghist[2 * i], c & 0xFFFFu);
+    if (c >> 16) atomicAdd(&jb.ghist[2 * i + 1], c >> 16);
   }
 }
 
 template <int R>
-__device__ __forceinline__ void pool_dispatch(int r, const PoolJob& jb, float (*row)[kPoolRow],
-                                              uint32_t* hist) {
-  if constexpr (R > kHalo - 1) {
-    pool_tile<R>(jb, row, hist);
+__device__ __forceinline__ void pool_dispatch(int r, const PoolJob& jb, uint32_t* hist) {
+  if constexpr (R >= kMaxPoolRadius) {
+    pool_tile<R>(jb, hist);
   } else {
-    if (r == R) pool_tile<R>(jb, row, hist);
-    else pool_dispatch<R + 1>(r, jb, row, hist);
+    if (r == R) pool_tile<R>(jb, hist);
+    else pool_dispatch<R + 1>(r, jb, hist);
   }
 }
 
 __global__ __launch_bounds__(kThreads) void pool_kernel(const LayerArgs a) {
-  __shared__ __align__(16) float row[2][kPoolRow];
-  __shared__ uint32_t hist_lds[kHistBins];
+  __shared__ uint32_t hist_lds[kHistBins / 2];  // two 16-bit counts per word
   __shared__ const float* rows[kMaxQHeads];
   const int b = blockIdx.x;
   const SeqArgs& sq = a.seq[find_seq(a, b, [](const SeqArgs& t) { return t.blk_pool; })];
@@ -694,8 +683,11 @@ __global__ __launch_bounds__(kThreads) void pool_kernel(const LayerArgs a) {
   const int t1 = a.shared ? a.grp_off[a.n_kv] : a.grp_off[g + 1];
   for (int t = t0 + (int)threadIdx.x; t < t1; t += kThreads) {
     const int gt = a.sel_grp[t];  // head t - grp_off[gt] of group gt
-    rows[t - t0] = sq.wsum + ((int64_t)gt * sq.wsum_heads + (t - a.grp_off[gt])) * Ls;
+    rows[t - t0] = sq.wsum + ((int64_t)gt * sq.wsum_heads + (t - a.grp_off[gt])) * sq.ws_stride;
   }
+  const bool do_hist = a.do_hist && sq.n_keep > 0;
+  if (do_hist)
+    for (int i = threadIdx.x; i < kHistBins / 2; i += kThreads) hist_lds[i] = 0u;
   __syncthreads();
   PoolJob jb;
   jb.rows = rows;
@@ -704,11 +696,11 @@ __global__ __launch_bounds__(kThreads) void pool_kernel(const LayerArgs a) {
   jb.j0 = (int64_t)tile * kPoolTile;
   jb.n_out = Ls - jb.j0 < kPoolTile ? (int)(Ls - jb.j0) : kPoolTile;
   jb.is_max = a.pool != 0;
-  jb.do_hist = a.do_hist && sq.n_keep > 0;
+  jb.do_hist = do_hist;
   jb.inv_kp = 1.f / (float)a.kp;
   jb.out = sq.scores + (int64_t)g * Ls + jb.j0;
   jb.ghist = sq.hist + (int64_t)g * kHistBins;
-  pool_dispatch<0>(a.kp >> 1, jb, row, hist_lds);  // radius 0..15
+  pool_dispatch<0>(a.kp >> 1, jb, hist_lds);  // radius 0..kMaxPoolRadius
 }
 
 template <template <int, int> class KernelOf>

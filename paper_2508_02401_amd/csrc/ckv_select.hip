@@ -32,6 +32,7 @@ using namespace dev;
 constexpr int kCompactPer = 16;                      // scores per thread and compaction step
 constexpr int kCompactStep = kCompactPer * kThreads;  // scores per compaction step
 constexpr int kFilterPer = kRangeMin / kThreads;  // scores per thread loaded up front
+constexpr int kCopyList = 1024;                   // kept rows listed in LDS per copy round
 
 __device__ __forceinline__ int find_seq_sel(const LayerArgs& a, int b) {
   int s = 0;
@@ -316,8 +317,8 @@ __global__ __launch_bounds__(kThreads) void resolve_kernel(const LayerArgs a) {
 // scores per step, so a thread's kept tokens are consecutive in the output.
 __global__ __launch_bounds__(kThreads) void compact_kernel(const LayerArgs a) {
   __shared__ uint32_t wsum[kWaves];
-  __shared__ int32_t pos_l[kCompactStep];
-  __shared__ int32_t tok_l[kCompactStep];
+  __shared__ int32_t pos_l[kCopyList];
+  __shared__ int32_t tok_l[kCopyList];
   const int b = blockIdx.x;
   const int s = find_seq_sel(a, b);
   const SeqArgs& sq = a.seq[s];
@@ -393,25 +394,36 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const LayerArgs a) {
       nsel += keep;
     }
     const uint32_t first = block_excl_scan<kThreads>(nsel, wsum, tot_sel);
-    uint32_t pos = pos_carry + first;
-    uint32_t li = first;
+    {
+      uint32_t pos = pos_carry + first;
 #pragma unroll
-    for (int e = 0; e < kCompactPer; ++e) {
-      if (((kept >> e) & 1u) && pos < end) {
-        out[pos] = (int32_t)(jt + e);
-        pos_l[li] = (int32_t)pos;
-        tok_l[li] = (int32_t)(jt + e);
-        ++pos;
-        ++li;
+      for (int e = 0; e < kCompactPer; ++e) {
+        if (((kept >> e) & 1u) && pos < end) out[pos++] = (int32_t)(jt + e);
       }
     }
     if (a.do_gather) {
-      __syncthreads();
+      // the step's kept rows in rounds of kCopyList: this thread's kept
+      // tokens have list numbers first, first + 1, ...
       const uint32_t n = tot_sel < end - pos_carry ? tot_sel : end - pos_carry;
-      for (int gk = gk0; gk < gk1; ++gk)
-        copy_rows(a, sq, gk, n, [&](int64_t i) { return (int64_t)tok_l[i]; },
-                  [&](int64_t i) { return (int64_t)pos_l[i]; });
-      __syncthreads();
+      for (uint32_t r0 = 0; r0 < n; r0 += kCopyList) {
+        uint32_t li = first;
+#pragma unroll
+        for (int e = 0; e < kCompactPer; ++e) {
+          if ((kept >> e) & 1u) {
+            if (li >= r0 && li < r0 + kCopyList && li < n) {
+              pos_l[li - r0] = (int32_t)(pos_carry + li);
+              tok_l[li - r0] = (int32_t)(jt + e);
+            }
+            ++li;
+          }
+        }
+        __syncthreads();
+        const uint32_t m = n - r0 < (uint32_t)kCopyList ? n - r0 : (uint32_t)kCopyList;
+        for (int gk = gk0; gk < gk1; ++gk)
+          copy_rows(a, sq, gk, m, [&](int64_t i) { return (int64_t)tok_l[i]; },
+                    [&](int64_t i) { return (int64_t)pos_l[i]; });
+        __syncthreads();
+      }
     }
     eq_carry += tot_eq;
     pos_carry += tot_sel;

@@ -283,3 +283,75 @@ def test_kernels_use_no_scratch_memory():
         assert kernels and len(kernels) == len(scratch), src
         bad = [k for k, n in zip(kernels, scratch) if n]
         assert not bad, "%s: kernels with scratch memory: %s" % (src, bad)
+
+
+# ---------------------------------------------------------------------------
+# ckv_compress_stack: every layer is validated before anything is enqueued.
+# ---------------------------------------------------------------------------
+def _stack_call(desc, layers, masks, ws_bytes=1 << 40, side=None):
+    """layers: list of per-layer ckv_seq lists; masks: [n_layers][H]."""
+    lib = ckv.load()
+    flat = [s for layer in layers for s in layer]
+    arr = (ckv._binding.ckv_seq * max(1, len(flat)))(*flat)
+    m = np.asarray(masks, np.uint8).reshape(-1)
+    mm = (ctypes.c_uint8 * max(1, m.size))(*m.tolist())
+    return lib.ckv_compress_stack(ctypes.byref(desc), len(layers), mm, arr,
+                                  len(layers[0]) if layers else 1, _BASE + 32768, ws_bytes, None,
+                                  side)
+
+
+def test_stack_rejects_bad_layers():
+    d, ok_mask = _desc(), [1] * 8
+    three = [[_seq()], [_seq()], [_seq()]]
+    assert _stack_call(d, [], [ok_mask]) == ckv.CKV_ERR_INVALID_ARG
+    # a later layer with another prompt length, budget below the window, a
+    # null output, or a group without a chosen head
+    assert _stack_call(d, [[_seq()], [_seq(seq_len=99)]], [ok_mask] * 2) == ckv.CKV_ERR_INVALID_ARG
+    assert _stack_call(d, [[_seq()], [_seq(budget=3)]], [ok_mask] * 2) == ckv.CKV_ERR_BUDGET
+    assert _stack_call(d, [[_seq()], [_seq(k_out=None)]], [ok_mask] * 2) == ckv.CKV_ERR_INVALID_ARG
+    assert _stack_call(d, three, [ok_mask, ok_mask, [1, 0, 0, 0, 0, 0, 0, 0]]) == ckv.CKV_ERR_MASK
+    assert _stack_call(_desc(pool_kernel=4), three, [ok_mask] * 3) == ckv.CKV_ERR_INVALID_ARG
+
+
+def test_stack_workspace_holds_two_slots_with_a_side_stream():
+    lib = ckv.load()
+    d = _desc()
+    arr = (ckv._binding.ckv_seq * 1)(_seq())
+    one = lib.ckv_workspace_bytes(ctypes.byref(d), arr, 1)
+    # a side stream needs two layer slots; the (fake) stream handle is never
+    # touched because the size check fails first
+    assert _stack_call(d, [[_seq()], [_seq()]], [[1] * 8] * 2, ws_bytes=2 * one - 1,
+                       side=0x1000) == ckv.CKV_ERR_WORKSPACE
+    assert _stack_call(d, [[_seq()], [_seq()]], [[1] * 8] * 2, ws_bytes=0,
+                       side=None) == ckv.CKV_ERR_WORKSPACE
+
+
+def test_selection_kernels_fit_beside_two_k_pass_workgroups():
+    # ckv_compress_stack overlaps the selection kernels with the K passes: each
+    # must fit in the LDS that two K-pass workgroups leave free on a CU (160 KB)
+    import re
+    import subprocess
+    from paper_2508_02401_amd import build as B
+
+    lds = {}
+    procs = {}
+    for src in ("ckv_score.hip", "ckv_select.hip"):
+        cmd = [B.HIPCC, "-x", "hip"] + B.COMMON + [
+            "--cuda-device-only", "-c", os.path.join(B.CSRC, src), "-o", os.devnull,
+            "-Rpass-analysis=kernel-resource-usage"]
+        procs[src] = subprocess.Popen(cmd, stdout=subprocess.DEVNULL, stderr=subprocess.PIPE,
+                                      text=True)
+    for src, proc in procs.items():
+        out = proc.communicate(timeout=600)[1]
+        names = re.findall(r"Function Name: (\S+)", out)
+        sizes = [int(x) for x in re.findall(r"LDS Size \[bytes/block\]: (\d+)", out)]
+        assert names and len(names) == len(sizes)
+        lds.update(zip(names, sizes))
+    # the K-pass kernels of 16-bit d = 128 layers (the Llama / Qwen shapes)
+    kpass = max(v for k, v in lds.items()
+                if ("rowstats_kernel" in k or "score_kernel" in k) and ("ILi0ELi128" in k or "ILi1ELi128" in k))
+    free = 160 * 1024 - 2 * kpass
+    for k in ("pool_kernel", "filter_kernel", "resolve_kernel", "compact_kernel"):
+        size = max(v for n, v in lds.items() if k in n)
+        assert size <= free, "%s uses %d B of LDS, %d B are free beside two K-pass workgroups" % (
+            k, size, free)

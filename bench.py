@@ -41,6 +41,9 @@ def parse():
     p.add_argument("--workload", default="llama8b-128k-stack")
     p.add_argument("--layers", type=int, default=0, help="limit the layer count (0 = all)")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-lse-variant", action="store_true",
+                   help="skip the second measurement, with the window rows' log-sum-exp supplied "
+                        "by the caller (one pass over K)")
     p.add_argument("--cpu-threads", type=int, default=0)
     p.add_argument("--time-every", type=int, default=4, metavar="N",
                    help="K-pass launches of every N-th layer carry start/end events (the layer "
@@ -364,59 +367,61 @@ def main():
 
     step = step_stack if stack else (step_pipeline if args.pipeline else step_layers)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-
     hip = Hip()
-    # Only the two K passes (the candidates for the dominant kernel) carry
-    # kernel start/end events, and only on every N-th layer of a step (the
-    # offset rotates with the step): each timed launch delays the dispatch of
-    # its neighbours by a few microseconds, so the other stages and layers are
-    # left untimed (their times are in the rocprofv3 kernel trace).
-    # ev[step][layer] = (begin, end) arrays, or None for an untimed layer.
-    timed = ("rowstats", "score")
-    ns = ckv.CKV_NUM_STAGES
-    idx = {n: ckv.STAGE_NAMES.index(n) for n in timed}
-    every = max(1, args.time_every)
-    ev = []
-    for k in range(args.steps):
-        per_layer = []
-        for li in range(n_layers):
-            if (li + k) % every != 0:
-                per_layer.append(None)
-                continue
-            b, e = [None] * ns, [None] * ns
-            for n in timed:
-                b[idx[n]], e[idx[n]] = hip.event(), hip.event()
-            per_layer.append((b, e))
-        ev.append(per_layer)
-    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    t_start.record(main)
-    for k in range(args.steps):
-        step(ev[k])
-    t_end.record(main)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    ms_total = t_start.elapsed_time(t_end)
-    ms_per_step = ms_total / args.steps
 
-    stage_ms = {n: [] for n in timed}
-    sampled = []  # layer of every timed launch pair
-    for k in range(args.steps):
-        for li in range(n_layers):
-            if ev[k][li] is None:
-                continue
-            b, e = ev[k][li]
-            sampled.append(li)
-            for n in timed:
-                stage_ms[n].append(hip.elapsed_ms(b[idx[n]], e[idx[n]]))
-            for x in b + e:
-                if x is not None:
-                    hip.destroy(x)
-    stage_avg = {n: float(np.mean(v)) for n, v in stage_ms.items()}
+    def timed_run(timed):
+        """Warm up, then time args.steps steps. Only the stages in `timed` (K
+        passes) carry kernel start/end events, and only on every N-th layer of
+        a step (the offset rotates with the step): each timed launch delays
+        the dispatch of its neighbours by a few microseconds, so the other
+        stages and layers are left untimed (their times are in the rocprofv3
+        kernel trace). Returns (ms per step, mean launch ms per timed stage,
+        layer of every timed launch, wall seconds)."""
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+        ns = ckv.CKV_NUM_STAGES
+        idx = {n: ckv.STAGE_NAMES.index(n) for n in timed}
+        every = max(1, args.time_every)
+        ev = []  # ev[step][layer] = (begin, end) arrays, or None for an untimed layer
+        for k in range(args.steps):
+            per_layer = []
+            for li in range(n_layers):
+                if (li + k) % every != 0:
+                    per_layer.append(None)
+                    continue
+                b, e = [None] * ns, [None] * ns
+                for n in timed:
+                    b[idx[n]], e[idx[n]] = hip.event(), hip.event()
+                per_layer.append((b, e))
+            ev.append(per_layer)
+        t_start = torch.cuda.Event(enable_timing=True)
+        t_end = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        wall0 = time.perf_counter()
+        t_start.record(main)
+        for k in range(args.steps):
+            step(ev[k])
+        t_end.record(main)
+        torch.cuda.synchronize()
+        wall_s = time.perf_counter() - wall0
+        ms = t_start.elapsed_time(t_end) / args.steps
+        stage_ms = {n: [] for n in timed}
+        sampled_layers = []
+        for k in range(args.steps):
+            for li in range(n_layers):
+                if ev[k][li] is None:
+                    continue
+                b, e = ev[k][li]
+                sampled_layers.append(li)
+                for n in timed:
+                    stage_ms[n].append(hip.elapsed_ms(b[idx[n]], e[idx[n]]))
+                for x in b + e:
+                    if x is not None:
+                        hip.destroy(x)
+        return ms, {n: float(np.mean(v)) for n, v in stage_ms.items()}, sampled_layers, wall_s
+
+    ms_per_step, stage_avg, sampled, wall = timed_run(("rowstats", "score"))
 
     tokens_per_layer = sum(wl.seq_lens)
     value = tokens_per_layer * n_layers / (ms_per_step / 1e3)
@@ -510,48 +515,79 @@ def main():
         "wall_s_timed": wall,
     }
 
+    if not args.no_lse_variant:
+        # The same step with the window rows' log-sum-exp supplied by the
+        # caller (a causal prefill attention kernel keeps it per query row):
+        # the row-statistics pass is skipped and K is read once. The values
+        # are computed here beforehand (fp32 logits of the chosen heads, a
+        # causal mask and a log-sum-exp), outside the timed region.
+        scale = 1.0 / float(np.sqrt(d))
+        for mask, seqs in layers:
+            for sq in seqs:
+                L = sq.k.shape[1]
+                lse = torch.full((wl.num_q_heads, w), float("nan"), dtype=torch.float32, device=dev)
+                causal = (torch.arange(L, device=dev)[None, :]
+                          > (L - w + torch.arange(w, device=dev))[:, None])
+                for g in range(n_kv):
+                    heads = [int(h) for h in np.nonzero(mask)[0] if int(h) // G == g]
+                    if not heads:
+                        continue
+                    kt = sq.k[g].float().t().contiguous()  # [d, L]
+                    for h in heads:
+                        logits = (sq.q_win[h].float() @ kt) * scale
+                        lse[h] = torch.logsumexp(logits.masked_fill(causal, float("-inf")), dim=1)
+                    del kt
+                sq.lse = lse
+        torch.cuda.synchronize()
+        ms_lse, stage_lse, _, _ = timed_run(("score",))
+        for mask, seqs in layers:
+            for sq in seqs:
+                sq.lse = None
+        result["caller_lse_variant"] = {
+            "what": "same step with the window rows' log-sum-exp supplied by the caller's prefill "
+                    "attention: no row-statistics pass, K read once",
+            "ms_per_step": ms_lse, "value": tokens_per_layer * n_layers / (ms_lse / 1e3),
+            "path_hbm_gbs": path_bytes / (ms_lse / 1e3) / 1e9,
+            "path_hbm_frac": path_bytes / (ms_lse / 1e3) / 1e9 / HBM_PEAK_GBS,
+            "score_kernel_avg_us": stage_lse["score"] * 1e3}
+
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_threads)
     print(json.dumps(result), flush=True)
 
 
-def cpu_baseline(wl, threads: int):
-    """The fp64 oracle on one layer of the workload (a bounded sample)."""
+def cpu_baseline(wl, threads: int, min_seconds: float = 10.0):
+    """The fp64 oracle on a bounded sample of the workload: whole layers, in
+    order, until about min_seconds of oracle time have been spent (at most
+    every layer)."""
     import numpy as np
-    import torch
 
     import oracle
     from paper_2508_02401_amd import synth
 
     n_threads = threads if threads > 0 else min(os.cpu_count() or 1, 16)
-    L = wl.seq_lens[0]
-    inp = synth.layer_inputs(wl, 0, "cpu", seq_lens=(L,), with_v=False)
-    q = inp.q_win[0].double().numpy()
-    k = inp.k[0].double().numpy()
+    n_kv, G = wl.num_kv_heads, wl.num_q_heads // wl.num_kv_heads
+    scale = 1.0 / np.sqrt(wl.head_dim)
+    pool = oracle.POOL_MAX if wl.pool == 1 else oracle.POOL_AVG
     b = wl.budget if wl.budget is not None else 2 * wl.window
-    # a single layer takes tens of seconds at L=128K; sample KV heads so the
-    # run stays around 10-30 s, and scale to a full layer
-    n_kv = wl.num_kv_heads
-    heads = list(range(n_kv))
-    G = wl.num_q_heads // n_kv
-    t0 = time.perf_counter()
-    sub_mask = inp.mask.reshape(n_kv, G)
-    budget_kv = n_kv
-    if L >= 65536:
-        budget_kv = min(n_kv, max(1, n_threads))
-        heads = heads[:budget_kv]
-    qs = q.reshape(n_kv, G, wl.window, wl.head_dim)[heads].reshape(-1, wl.window, wl.head_dim)
-    ms = sub_mask[heads].reshape(-1)
-    oracle.select_layer(qs, ms, k[heads], wl.window, 1.0 / np.sqrt(wl.head_dim),
-                        oracle.POOL_MAX if wl.pool == 1 else oracle.POOL_AVG, wl.pool_kernel, b,
-                        n_threads)
-    dt = time.perf_counter() - t0
-    layer_time = dt * n_kv / len(heads)
-    return {"value": L / layer_time, "unit": "tokens/s", "cores": min(n_threads, len(heads)),
+    spent, tokens, layers_done = 0.0, 0, 0
+    for layer in range(wl.n_layers):
+        inp = synth.layer_inputs(wl, layer, "cpu", with_v=False)
+        for s, L in enumerate(wl.seq_lens):
+            q = inp.q_win[s].double().numpy()
+            k = inp.k[s].double().numpy()
+            t0 = time.perf_counter()
+            oracle.select_layer(q, inp.mask, k, wl.window, scale, pool, wl.pool_kernel, b,
+                                n_threads)
+            spent += time.perf_counter() - t0
+            tokens += L
+        layers_done += 1
+        if spent >= min_seconds:
+            break
+    return {"value": tokens / spent, "unit": "tokens/s", "cores": min(n_threads, n_kv),
             "kind": "oracle",
-            "sample": "layer 0 of %s, %d of %d KV heads at L=%d (fp64 C oracle, OpenMP over KV "
-                      "heads), scaled to a full layer; %.1f s wall"
-                      % (wl.name, len(heads), n_kv, L, dt)}
+            "sample": "layers 0-%d of %s, every KV head and prompt (fp64 C oracle, OpenMP over "
+                      "KV heads); %.1f s of oracle time" % (layers_done - 1, wl.name, spent)}
 
 
 if __name__ == "__main__":

@@ -123,6 +123,15 @@ typedef struct {
  *   k_out, v_out [n_kv, min(B, L), d] contiguous, dtype of the layer: the
  *           compact cache, row r of head g is K[g, idx[g, r], :] (idx[r] under
  *           CKV_SHARE_LAYER).
+ *   lse     optional fp32 [H, w]: the natural-log log-sum-exp of every window
+ *           row's scaled logits over its visible keys (row i of head h at
+ *           lse + h*lse_stride_head + i), i.e. log of the softmax normaliser of
+ *           paper Eq. 2 for that row, as a causal prefill attention kernel
+ *           leaves it behind. Only the chosen heads' rows are read. When given
+ *           (for every prompt of the call, or for none), the scoring skips its
+ *           first pass over K (the row statistics) and takes these values
+ *           instead, so K is read once. lse_stride_head >= w when w > 1;
+ *           4-byte aligned. Values must be finite; they are not checked.
  */
 typedef struct {
   const void *q_win;
@@ -139,6 +148,8 @@ typedef struct {
   int32_t *idx;
   void *k_out;
   void *v_out;
+  const float *lse;
+  int64_t lse_stride_head;
 } ckv_seq;
 
 /* Bytes of device workspace the calls below need for this layer and batch

@@ -63,6 +63,8 @@ def _load():
         lib.ckvo_attention_row.restype = ctypes.c_int
         lib.ckvo_window_sums.argtypes = [P(d), i32, P(d), i64, i32, i32, d, P(d)]
         lib.ckvo_window_sums.restype = ctypes.c_int
+        lib.ckvo_window_lse.argtypes = [P(d), i32, P(d), i64, i32, i32, d, P(d)]
+        lib.ckvo_window_lse.restype = ctypes.c_int
         lib.ckvo_pool.argtypes = [P(d), i64, i32, i32, P(d)]
         lib.ckvo_pool.restype = ctypes.c_int
         lib.ckvo_select_tokens.argtypes = [P(d), i64, i32, i64, P(i32)]
@@ -127,6 +129,20 @@ def window_sums(q_sel, k, scale: float) -> np.ndarray:
     if rc != OK:
         raise OracleError(rc, "window_sums")
     return S
+
+
+def window_lse(q_sel, k, scale: float) -> np.ndarray:
+    """Natural-log softmax normaliser of every window row (Eq. 2), [n_sel, w].
+    q_sel [n_sel, w, d], k [L, d]; row i sees keys 0..L-w+i."""
+    q_sel, k = _f64(q_sel), _f64(k)
+    n_sel, w, d = q_sel.shape
+    L = k.shape[0]
+    out = np.empty((n_sel, w), dtype=np.float64)
+    rc = _load().ckvo_window_lse(_ptr(q_sel, ctypes.c_double), n_sel, _ptr(k, ctypes.c_double),
+                                 L, d, w, scale, _ptr(out, ctypes.c_double))
+    if rc != OK:
+        raise OracleError(rc, "window_lse")
+    return out
 
 
 def pool(x, kp: int, mode: int) -> np.ndarray:

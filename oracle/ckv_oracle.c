@@ -111,6 +111,34 @@ int ckvo_window_sums(const double *q_sel, int32_t n_sel, const double *k,
   return CKVO_OK;
 }
 
+/* The softmax normaliser of every window row (Eq. 2), as its natural log:
+ * lse[h][i] = log sum_{j <= L-w+i} exp(scale * <q_i, k_j>), the quantity a
+ * causal prefill attention kernel keeps per query row. Computed max-shifted:
+ * m + log sum exp(s_j - m). q_sel [n_sel][w][d], k [L][d], lse [n_sel][w]. */
+int ckvo_window_lse(const double *q_sel, int32_t n_sel, const double *k, int64_t L, int32_t d,
+                    int32_t w, double scale, double *lse) {
+  if (!q_sel || !k || !lse || n_sel < 1 || w < 1 || L <= w || d < 1) return CKVO_EINVAL;
+  double *row = (double *)malloc(sizeof(double) * (size_t)L);
+  if (!row) return CKVO_ENOMEM;
+  for (int32_t h = 0; h < n_sel; ++h)
+    for (int32_t i = 0; i < w; ++i) {
+      const int64_t n_visible = L - w + i + 1; /* R2: causal inside the window */
+      const double *qi = q_sel + ((int64_t)h * w + i) * d;
+      double m = -INFINITY;
+      for (int64_t j = 0; j < n_visible; ++j) {
+        double dot = 0.0;
+        for (int32_t c = 0; c < d; ++c) dot += qi[c] * k[j * (int64_t)d + c];
+        row[j] = scale * dot;
+        if (row[j] > m) m = row[j];
+      }
+      double z = 0.0;
+      for (int64_t j = 0; j < n_visible; ++j) z += exp(row[j] - m);
+      lse[(int64_t)h * w + i] = m + log(z);
+    }
+  free(row);
+  return CKVO_OK;
+}
+
 /* 1-D pooling along the token axis (Sec. 3.3; kernel size and average pooling
  * from the appendix). Stride 1, odd kernel kp, half-width r = kp/2; the
  * neighbourhood of j is [j-r, j+r] clipped to [0, n). */

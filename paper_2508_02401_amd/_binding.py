@@ -53,7 +53,8 @@ class ckv_seq(ctypes.Structure):
                 ("kv_stride_head", ctypes.c_int64), ("kv_stride_tok", ctypes.c_int64),
                 ("seq_len", ctypes.c_int64), ("budget", ctypes.c_int32),
                 ("reserved", ctypes.c_int32), ("scores", ctypes.c_void_p),
-                ("idx", ctypes.c_void_p), ("k_out", ctypes.c_void_p), ("v_out", ctypes.c_void_p)]
+                ("idx", ctypes.c_void_p), ("k_out", ctypes.c_void_p), ("v_out", ctypes.c_void_p),
+                ("lse", ctypes.c_void_p), ("lse_stride_head", ctypes.c_int64)]
 
 
 class CkvError(RuntimeError):
@@ -126,7 +127,9 @@ def layer_desc(num_q_heads: int, num_kv_heads: int, head_dim: int, window: int,
 @dataclass
 class Seq:
     """One prompt. q_win [H, w, d], k/v [n_kv, L, d] (last axis contiguous),
-    outputs as in include/ckv.h (None where a call does not need them)."""
+    outputs as in include/ckv.h (None where a call does not need them). lse
+    [H, w] fp32 (window axis contiguous) optionally carries the window rows'
+    log-sum-exp from the caller's prefill attention."""
     q_win: Optional[torch.Tensor]
     k: Optional[torch.Tensor]
     v: Optional[torch.Tensor]
@@ -136,6 +139,7 @@ class Seq:
     k_out: Optional[torch.Tensor] = None
     v_out: Optional[torch.Tensor] = None
     seq_len: Optional[int] = None
+    lse: Optional[torch.Tensor] = None
 
 
 def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
@@ -164,6 +168,10 @@ def _seq_array(seqs: Sequence[Seq]):
         c.budget = int(s.budget)
         c.scores, c.idx = _ptr(s.scores), _ptr(s.idx)
         c.k_out, c.v_out = _ptr(s.k_out), _ptr(s.v_out)
+        if s.lse is not None:
+            if s.lse.dtype != torch.float32 or s.lse.dim() != 2 or s.lse.stride(1) != 1:
+                raise ValueError("lse must be fp32 [H, w] with the window axis contiguous")
+            c.lse, c.lse_stride_head = s.lse.data_ptr(), s.lse.stride(0)
     return arr
 
 

@@ -67,10 +67,10 @@ int64_t wsum_heads(const ckv_layer_desc* d) {
 // row starts 16-byte aligned.
 int64_t ws_stride(int64_t Ls) { return (Ls + 3) / 4 * 4; }
 
-// Per-prompt workspace, in order: K-pass partials, head window sums, scores, selection control words, histograms, candidates, per-range
-// counts/offsets.
+// Per-prompt workspace, in order: K-pass partials, head window sums, scores,
+// selection control words, histograms, candidates, per-range counts/offsets.
 struct WsLayout {
-  size_t partial, wsum, scores, ctl, hist, cand, rsure, roff, reqb, total;
+  size_t partial, wsum, scores, ctl, hist, cand, rsure, total;
 };
 
 WsLayout seq_ws_layout(const ckv_layer_desc* d, const ckv_seq* s) {
@@ -85,9 +85,7 @@ WsLayout seq_ws_layout(const ckv_layer_desc* d, const ckv_seq* s) {
   w.ctl = o;     o += align_up((size_t)n_sg * ckv::kCtlWords * sizeof(uint32_t));
   w.hist = o;    o += align_up((size_t)n_sg * ckv::kHistBins * sizeof(uint32_t));
   w.cand = o;    o += align_up((size_t)n_sg * Ls * sizeof(uint2));
-  w.rsure = o;   o += align_up((size_t)n_sg * n_ranges * sizeof(uint32_t));
-  w.roff = o;    o += align_up((size_t)n_sg * n_ranges * sizeof(uint32_t));
-  w.reqb = o;    o += align_up((size_t)n_sg * n_ranges * sizeof(uint32_t));
+  w.rsure = o;   o += align_up((size_t)3 * n_sg * n_ranges * sizeof(uint32_t));
   w.total = o;
   return w;
 }
@@ -143,6 +141,13 @@ int check_seqs(const ckv_layer_desc* d, const ckv_seq* seqs, int32_t n, unsigned
     if ((need & kNeedIdx) && !s.idx) return CKV_ERR_INVALID_ARG;
     if ((need & kNeedOut) && (!s.k_out || !s.v_out || !aligned16(s.k_out) || !aligned16(s.v_out)))
       return CKV_ERR_INVALID_ARG;
+    if (need & kNeedQ) {
+      // caller row statistics: for every prompt or for none
+      if ((s.lse != nullptr) != (seqs[0].lse != nullptr)) return CKV_ERR_INVALID_ARG;
+      if (s.lse && (((uintptr_t)s.lse & 3u) || s.lse_stride_head < 0 ||
+                    (d->window > 1 && s.lse_stride_head < d->window)))
+        return CKV_ERR_INVALID_ARG;
+    }
   }
   return CKV_OK;
 }
@@ -162,6 +167,7 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
   a.kp = d->pool_kernel;
   a.shared = (d->flags & CKV_SHARE_LAYER) ? 1 : 0;
   a.n_sg = (int32_t)sel_groups(d);
+  a.lse_given = seqs[0].lse != nullptr;
   if (mask) {
     const int G = d->num_q_heads / d->num_kv_heads;
     const int max_rows = ckv::kMaxRows;
@@ -187,12 +193,13 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
     a.grp_off[d->num_kv_heads] = (int16_t)off;
     if (off == 0) return CKV_ERR_MASK;
   }
-  // KV heads the K passes stream (the others have no chosen head)
-  int64_t n_read = d->num_kv_heads;
-  if (mask) {
-    n_read = 0;
-    for (int g = 0; g < d->num_kv_heads; ++g) n_read += a.grp_off[g + 1] > a.grp_off[g];
-  }
+  // weight of the K-pass work: nqb + kSplitBias for every group read (the
+  // others have no chosen head and are not read)
+  if (mask)
+    for (int g = 0; g < d->num_kv_heads; ++g) {
+      const int nqb = ((a.grp_off[g + 1] - a.grp_off[g]) * a.w8 + 31) / 32;
+      if (nqb > 0) a.split_w += nqb + ckv::kSplitBias;
+    }
   a.elt = elt_bytes(d->dtype);
   int32_t blk_kpass = 0, blk_pool = 0, blk_sel = 0, blk_gather = 0;
   for (int32_t i = 0; i < n; ++i) {
@@ -213,17 +220,18 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
     q.idx = s.idx;
     q.k_out = s.k_out;
     q.v_out = s.v_out;
-    {
-      // K-pass workgroups of this prompt: about kTargetWgs over the KV
-      // heads it reads, at least kMinStagesPerWg stages each. It depends on
-      // the prompt and the mask alone, so a prompt's results do not depend on
-      // the rest of the batch.
-      const int64_t n_st = k_stages(d, s.seq_len);
-      int64_t per_wg = ceil_div(n_read * n_st, ckv::kTargetWgs);
-      if (per_wg < ckv::kMinStagesPerWg) per_wg = ckv::kMinStagesPerWg;
-      const int64_t split = ceil_div(n_st, per_wg), cap = max_split(d, s.seq_len);
-      q.n_split = (int32_t)(split < cap ? split : cap);
-    }
+    q.lse = s.lse;
+    q.lse_sh = s.lse_stride_head;
+    // K-pass workgroups of this prompt: about kTargetWgs over the KV heads it
+    // reads, shared out by group_split, at least kMinStagesPerWg stages each.
+    // They depend on the prompt and the mask alone, so a prompt's results do
+    // not depend on the rest of the batch.
+    q.n_split = (int32_t)max_split(d, s.seq_len);
+    q.n_kpass = 0;
+    if (mask)
+      for (int g = 0; g < d->num_kv_heads; ++g)
+        q.n_kpass += ckv::group_split(((a.grp_off[g + 1] - a.grp_off[g]) * a.w8 + 31) / 32,
+                                      a.split_w, q.n_split);
     q.wsum_heads = (int32_t)wsum_heads(d);
     q.ws_stride = ws_stride(Ls);
     q.n_ptiles = (int32_t)ceil_div(Ls, ckv::kPoolTile);
@@ -234,7 +242,7 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
     q.blk_pool = blk_pool;
     q.blk_sel = blk_sel;
     q.blk_gather = blk_gather;
-    blk_kpass += q.n_split * d->num_kv_heads;
+    blk_kpass += q.n_kpass;
     blk_pool += q.n_ptiles * a.n_sg;
     blk_sel += q.n_ranges * a.n_sg;
     blk_gather += q.n_gblk * d->num_kv_heads;
@@ -247,8 +255,6 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
       q.hist = reinterpret_cast<uint32_t*>(ws + l.hist);
       q.cand = reinterpret_cast<uint2*>(ws + l.cand);
       q.rsure = reinterpret_cast<uint32_t*>(ws + l.rsure);
-      q.roff = reinterpret_cast<uint32_t*>(ws + l.roff);
-      q.reqb = reinterpret_cast<uint32_t*>(ws + l.reqb);
       ws += l.total;
     }
   }
@@ -257,7 +263,7 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
 
 int grid_kpass(const ckv::LayerArgs& a) {
   const ckv::SeqArgs& q = a.seq[a.num_seqs - 1];
-  return q.blk_kpass + q.n_split * a.n_kv;
+  return q.blk_kpass + q.n_kpass;
 }
 int grid_pool(const ckv::LayerArgs& a) {
   const ckv::SeqArgs& q = a.seq[a.num_seqs - 1];
@@ -288,11 +294,13 @@ ckv::Timing timing(int stage, bool first, bool last) {
   return t;
 }
 
-// The two K passes (row statistics, then window sums).
+// The two K passes (row statistics, then window sums); with caller row
+// statistics only the second.
 int run_kpasses(const ckv_layer_desc* d, const ckv::LayerArgs& a, hipStream_t st) {
   hipError_t e;
-  if ((e = ckv::launch_rowstats(d->dtype, a, grid_kpass(a), st,
-                                timing(ckv::kStageRowStats, true, true))) != hipSuccess)
+  if (!a.lse_given && (e = ckv::launch_rowstats(d->dtype, a, grid_kpass(a), st,
+                                                timing(ckv::kStageRowStats, true, true))) !=
+                          hipSuccess)
     return hip_fail(e);
   if ((e = ckv::launch_score(d->dtype, a, grid_kpass(a), st,
                              timing(ckv::kStageScore, true, true))) != hipSuccess)

@@ -16,6 +16,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
+constexpr int kKpWaves = kKpThreads / 64;  // waves per K-pass workgroup
 
 template <int DT>
 struct Elt {

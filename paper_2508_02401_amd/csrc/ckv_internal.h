@@ -11,10 +11,12 @@ constexpr int kMaxSeqs = 16;
 constexpr int kMaxQHeads = 128;
 constexpr int kMaxKvHeads = 64;
 constexpr int kMaxRows = 128;      // chosen-head rows per group after padding each head to 8
+constexpr int kKpThreads = 256;    // threads per K-pass workgroup
 constexpr int kStageBytes = 16384; // K bytes per LDS stage of the two K passes
 constexpr int kMaxSplit = 512;     // workgroups per (prompt, KV head) in a K pass
-constexpr int kMinStagesPerWg = 4; // K stages per workgroup (at least)
-constexpr int kTargetWgs = 512;    // K-pass workgroups per launch: 2 on each of 256 CUs
+constexpr int kMinStagesPerWg = 65536 / kStageBytes; // K stages per workgroup (at least 64 KB)
+constexpr int kTargetWgs = 512;    // K-pass workgroups per prompt: 2 on each of 256 CUs
+constexpr int kCUs = 256;          // compute units of the MI355X
 constexpr int kPoolTile = 2048;    // scores per pooling workgroup
 constexpr int kMaxPoolRadius = 15; // pool kernel <= 2*15+1
 constexpr int kGatherRows = 64;    // retained rows per gather workgroup
@@ -45,6 +47,21 @@ enum Stage {
   kNumStages = 5
 };
 
+// K-pass workgroups of one KV group (a prompt's groups together get at most
+// kTargetWgs, rounded down: one workgroup past what the CUs hold at once
+// would run after the others and double the launch). A stage costs a fixed
+// part plus a part per 32-row query block of the group's chosen rows, so
+// groups get workgroups in proportion to nqb + kSplitBias; w_total is that
+// weight summed over the groups read, and cap bounds the count by the
+// prompt's stages. A group without chosen heads (nqb == 0, shared scope only)
+// gets one workgroup, which reads nothing.
+constexpr int kSplitBias = 3;
+__host__ __device__ inline int group_split(int nqb, int w_total, int cap) {
+  if (nqb == 0) return 1;
+  const int p = (int)((int64_t)kTargetWgs * (nqb + kSplitBias) / w_total);
+  return p < 1 ? 1 : (p > cap ? cap : p);
+}
+
 // Tokens per K stage for rows of row_bytes: kStageBytes, or one 32-token
 // block of larger rows.
 constexpr int stage_tokens(int row_bytes) {
@@ -65,16 +82,18 @@ struct SeqArgs {
   int32_t* idx;            // [n_kv][n_ret]
   void* k_out;             // [n_kv][n_ret][d]
   void* v_out;
+  const float* lse;        // caller's window-row log-sum-exp [H][w] (natural log), or null
+  int64_t lse_sh;          // its head stride
   // workspace
   float2* partial;         // [n_kv][n_split][kMaxRows]: (max logit, sum exp2) per workgroup
   float* wsum;             // [n_kv][wsum_heads][ws_stride]: window sum of each chosen head
   uint32_t* ctl;           // [n_kv][kCtlWords]
   uint32_t* hist;          // [n_kv][kHistBins]
   uint2* cand;             // [n_kv][L - w]: (key, index) of threshold-bin candidates
-  uint32_t* rsure;         // [n_kv][n_ranges]: keys above the threshold bin per range
-  uint32_t* roff;          // [n_kv][n_ranges]: output offset of each range
-  uint32_t* reqb;          // [n_kv][n_ranges]: threshold-equal keys before each range
-  int32_t n_split;         // P: workgroups per KV head in each K pass
+  uint32_t* rsure;         // [3][n_sg][n_ranges], per range: keys above the threshold bin;
+                           // then the output offset; then threshold-equal keys before it
+  int32_t n_split;         // most K-pass workgroups of one KV head (group_split's cap)
+  int32_t n_kpass;         // K-pass workgroups of this prompt (all KV heads)
   int64_t ws_stride;       // floats per window-sum row: L - w rounded up to 4
   int32_t wsum_heads;      // head slots per KV head in wsum
   int32_t n_ptiles;        // ceil((L - w) / kPoolTile)
@@ -85,7 +104,6 @@ struct SeqArgs {
   int32_t blk_sel;         // ... in the selection grids (n_kv * n_ranges per prompt)
   int32_t blk_gather;      // ... in the gather grid
   int32_t n_gblk;          // gather workgroups per KV head
-  int32_t pad;
 };
 
 // One layer call.
@@ -104,6 +122,8 @@ struct LayerArgs {
   int32_t do_gather;       // compaction also copies the kept K/V rows
   int32_t shared;          // one selection per prompt from the layer's chosen heads
   int32_t n_sg;            // selection groups per prompt: n_kv, or 1 when shared
+  int32_t split_w;         // sum over the groups read of nqb + kSplitBias (group_split)
+  int32_t lse_given;       // every prompt carries lse: the row-statistics pass is skipped
   int16_t grp_off[kMaxKvHeads + 1];  // chosen heads of group g: sel[grp_off[g] .. grp_off[g+1])
   uint8_t sel[kMaxQHeads];
   uint8_t sel_grp[kMaxQHeads];       // KV group of chosen head t (sel[t] / G)

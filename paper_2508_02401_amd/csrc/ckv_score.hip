@@ -43,9 +43,10 @@ namespace {
 
 using namespace dev;
 
-// Waves per query block when a workgroup's 4 waves share nqb blocks.
+// Waves per query block when a K-pass workgroup's waves share nqb blocks
+// (nqb <= 4; 3 blocks use the 4-block split and leave the last waves idle).
 __device__ __forceinline__ int waves_per_qblock(int nqb) {
-  return nqb == 1 ? 4 : (nqb == 2 ? 2 : 1);
+  return nqb == 1 ? kKpWaves : (nqb == 2 ? kKpWaves / 2 : kKpWaves / 4);
 }
 
 // This lane's query operand for query block qb, straight from global memory:
@@ -85,9 +86,9 @@ struct Stager {
   static constexpr int NC = ROWB / 32;           // MFMA operand chunks per lane
   static constexpr int ST = SB / ROWB;           // tokens per stage
   static constexpr int VEC = SB / 16;            // 16-byte vectors per stage
-  static constexpr int PT = VEC / kThreads;      // load instructions per wave per stage
+  static constexpr int PT = VEC / kKpThreads;    // load instructions per wave per stage
   static constexpr int BLOCKS = ST / 32;
-  static_assert(ST % 32 == 0 && VEC % kThreads == 0, "stage shape");
+  static_assert(ST % 32 == 0 && VEC % kKpThreads == 0, "stage shape");
 
   // Rows of 256 B or more start on the same bank: spread chunks by t % 16.
   // 128-byte rows alternate halves of the banks: spread by (t / 2) % 8.
@@ -106,7 +107,7 @@ struct Stager {
     const int lane = threadIdx.x & 63;
 #pragma unroll
     for (int k = 0; k < PT; ++k) {
-      const int e = (k * kWaves + wave) * 64 + lane;
+      const int e = (k * kKpWaves + wave) * 64 + lane;
       const int t = e / NV, pos = e - t * NV;
       p.tok[k] = t;
       p.chunk[k] = pos ^ swz(t);
@@ -126,14 +127,14 @@ struct Stager {
 #pragma unroll
       for (int k = 0; k < PT; ++k)
         __builtin_amdgcn_global_load_lds(reinterpret_cast<const uint4*>(sb + p.off[k]),
-                                         slot + (k * kWaves + wave) * 64, 16, 0, 0);
+                                         slot + (k * kKpWaves + wave) * 64, 16, 0, 0);
     } else {
 #pragma unroll
       for (int k = 0; k < PT; ++k) {
         int64_t tok = t0 + p.tok[k];
         tok = tok < lo ? lo : (tok > hi ? hi : tok);
         const uint4* src = reinterpret_cast<const uint4*>(kbase + tok * kv_st * EB) + p.chunk[k];
-        __builtin_amdgcn_global_load_lds(src, slot + (k * kWaves + wave) * 64, 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(src, slot + (k * kKpWaves + wave) * 64, 16, 0, 0);
       }
     }
   }
@@ -187,6 +188,13 @@ __device__ __forceinline__ void stage_loop(uint4* const* slot, const char* kbase
                                            int64_t t_first, int64_t stride, int ns, int64_t lo,
                                            int64_t hi, int wave, Pre pre, Body body) {
   const typename S::Plan p = S::plan(wave, kv_st);
+  // Two workgroups share each CU; the one dispatched second is the younger,
+  // and the SIMDs issue the older one's waves first, so it would finish
+  // well after its partner and leave the CU half idle. It runs its first
+  // 3/8 of the stages at a raised wave priority to even them out (a hint
+  // only: results do not depend on it).
+  const int prio_until = ((blockIdx.x / kCUs) & 1) ? ns * 3 / 8 : 0;
+  if (prio_until > 0) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
   for (int j = 0; j < NS - 1; ++j)
     if (j < ns) S::fetch(kbase, kv_st, t_first + j * stride, lo, hi, p, wave, slot[j]);
@@ -197,6 +205,7 @@ __device__ __forceinline__ void stage_loop(uint4* const* slot, const char* kbase
       const int k = k0 + j;
       if (k < ns) {
         const int left = ns - 1 - k;
+        if (k == prio_until && prio_until > 0) __builtin_amdgcn_s_setprio(0);
         wait_stages<S::PT, NS - 2>(left < NS - 2 ? left : NS - 2);
         __builtin_amdgcn_s_barrier();
         if (k + NS - 1 < ns)
@@ -251,13 +260,27 @@ __device__ __forceinline__ int find_seq(const LayerArgs& a, int b, Off off) {
   return s;
 }
 
+// KV group g, its workgroup index p and its workgroup count P of K-pass
+// workgroup `local` of a prompt (groups are laid out in order, group_split
+// workgroups each).
+__device__ __forceinline__ void kpass_locate(const LayerArgs& a, const SeqArgs& sq, int local,
+                                             int& g, int& p, int& P) {
+  int base = 0;
+  for (g = 0;; ++g) {
+    P = group_split(((a.grp_off[g + 1] - a.grp_off[g]) * a.w8 + 31) >> 5, a.split_w, sq.n_split);
+    if (local < base + P || g == a.n_kv - 1) break;
+    base += P;
+  }
+  p = local - base;
+}
+
 // ---------------------------------------------------------------------------
 // Pass 1: row statistics.
 // ---------------------------------------------------------------------------
 template <int DT, int D, int WPQ, class S, int NS>
 __device__ __forceinline__ void rowstats_body(const LayerArgs& a, const SeqArgs& sq, int g, int p,
-                                              int sel0, int n_sel, int nqb, uint4* const* slots,
-                                              float2 (*red)[32]) {
+                                              int P, int sel0, int n_sel, int nqb,
+                                              uint4* const* slots, float2 (*red)[32]) {
   constexpr int NC = S::NC;
   constexpr int NB = (S::BLOCKS + WPQ - 1) / WPQ;
   const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
@@ -266,7 +289,6 @@ __device__ __forceinline__ void rowstats_body(const LayerArgs& a, const SeqArgs&
   const bool active = qb < nqb;
   const int w8 = a.w8;
   const int64_t L = sq.L, Ls = L - a.w;
-  const int P = sq.n_split;
   const int64_t stride = (int64_t)P * S::ST;
   const float alpha = a.alpha;
   const char* kbase = static_cast<const char*>(sq.k) + (int64_t)g * sq.kv_sh * S::EB;
@@ -335,26 +357,25 @@ __device__ __forceinline__ void rowstats_body(const LayerArgs& a, const SeqArgs&
 #pragma unroll
     for (int sw = 0; sw < WPQ; ++sw)
       z += red[qq * WPQ + sw][r].y * fast_exp2(red[qq * WPQ + sw][r].x * alpha - ms);
-    sq.partial[((int64_t)g * P + p) * kMaxRows + tid] = make_float2(m, z);
+    sq.partial[((int64_t)g * sq.n_split + p) * kMaxRows + tid] = make_float2(m, z);
   }
 }
 
 template <int DT, int D>
-__global__ __launch_bounds__(kThreads) void rowstats_kernel(const LayerArgs a) {
+__global__ __launch_bounds__(kKpThreads) void rowstats_kernel(const LayerArgs a) {
   using S = Stager<DT, D, stage_bytes<DT, D>()>;
   constexpr int NS = 4;  // 4-slot ring
   __shared__ uint4 slot0[S::VEC];
   __shared__ uint4 slot1[S::VEC];
   __shared__ uint4 slot2[S::VEC];
   __shared__ uint4 slot3[S::VEC];
-  __shared__ float2 red[kWaves][32];
+  __shared__ float2 red[kKpWaves][32];
   uint4* const slots[NS] = {slot0, slot1, slot2, slot3};
 
   const int b = blockIdx.x;
   const SeqArgs& sq = a.seq[find_seq(a, b, [](const SeqArgs& t) { return t.blk_kpass; })];
-  const int local = b - sq.blk_kpass;
-  const int g = local / sq.n_split;
-  const int p = local - g * sq.n_split;
+  int g, p, P;
+  kpass_locate(a, sq, b - sq.blk_kpass, g, p, P);
   const int sel0 = a.grp_off[g], n_sel = a.grp_off[g + 1] - sel0;
   const int nqb = (n_sel * a.w8 + 31) >> 5;
 
@@ -362,15 +383,16 @@ __global__ __launch_bounds__(kThreads) void rowstats_kernel(const LayerArgs a) {
   // one per prompt when shared); the pooling kernel that accumulates into it
   // runs after this one
   if (p == 0 && a.do_hist && g < a.n_sg) {
-    for (int i = threadIdx.x; i < kCtlWords; i += kThreads) sq.ctl[g * kCtlWords + i] = 0u;
-    for (int i = threadIdx.x; i < kHistBins; i += kThreads)
+    for (int i = threadIdx.x; i < kCtlWords; i += kKpThreads) sq.ctl[g * kCtlWords + i] = 0u;
+    for (int i = threadIdx.x; i < kHistBins; i += kKpThreads)
       sq.hist[(int64_t)g * kHistBins + i] = 0u;
   }
   if (n_sel == 0) return;  // a group without chosen heads (shared scope) is not read
   const int wpq = waves_per_qblock(nqb);
-  if (wpq == 1) rowstats_body<DT, D, 1, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, red);
-  else if (wpq == 2) rowstats_body<DT, D, 2, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, red);
-  else rowstats_body<DT, D, 4, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, red);
+  constexpr int W1 = kKpWaves, W2 = kKpWaves / 2, W4 = kKpWaves / 4;
+  if (wpq == W4) rowstats_body<DT, D, W4, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, red);
+  else if (wpq == W2) rowstats_body<DT, D, W2, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, red);
+  else rowstats_body<DT, D, W1, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, red);
 }
 
 // Online merge of (max logit, sum of exp2) pairs in exp2 units.
@@ -387,6 +409,7 @@ __device__ __forceinline__ void lse_merge(float& m, float& z, float m2, float z2
 // ---------------------------------------------------------------------------
 constexpr int kGroupRows = kMaxRows / 8;  // 8-row groups of one group's rows
 constexpr int kLseBatch = 16;             // partial loads in flight per thread
+constexpr int kMergeLanes = kKpThreads / kMaxRows;  // threads per row in the lse merge
 
 // QM (query-block mode, when w8 is a multiple of 32): every 32-row query
 // block belongs to one head, so a lane sums its four 8-row groups in
@@ -394,8 +417,8 @@ constexpr int kLseBatch = 16;             // partial loads in flight per thread
 // gsum holds one row per 8-row group.
 template <int DT, int D, int WPQ, bool QM, class S, int NS>
 __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq, int g, int p,
-                                           int sel0, int n_sel, int nqb, uint4* const* slots,
-                                           float* gsum) {
+                                           int P, int sel0, int n_sel, int nqb,
+                                           uint4* const* slots, float* gsum) {
   constexpr int NC = S::NC;
   constexpr int NB = (S::BLOCKS + WPQ - 1) / WPQ;
   constexpr int ST = S::ST;
@@ -404,7 +427,6 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
   const int qb = wave / WPQ, sub = wave % WPQ;
   const bool active = qb < nqb;
   const int64_t Ls = sq.L - a.w;
-  const int P = sq.n_split;
   const int64_t stride = (int64_t)P * ST;
   const float alpha = a.alpha;
   const char* kbase = static_cast<const char*>(sq.k) + (int64_t)g * sq.kv_sh * S::EB;
@@ -416,22 +438,22 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
   // merged from pass 1's per-workgroup partials while the first stages load
   float4 cv[4];
   auto merge_lse = [&] {
-    // two threads per row, each merging every other partial; results meet in
-    // LDS (the gsum buffers are not in use yet)
-    float2* part = reinterpret_cast<float2*>(gsum);  // [2][kMaxRows]
-    float* lse_l = gsum + 4 * kMaxRows;               // [kMaxRows]
+    // kMergeLanes threads per row, thread j merging partials j, j + kMergeLanes,
+    // ...; their results meet in LDS in a fixed order (the gsum buffers are
+    // not in use yet)
+    float2* part = reinterpret_cast<float2*>(gsum);      // [kMergeLanes][kMaxRows]
+    float* lse_l = gsum + 2 * kMergeLanes * kMaxRows;     // [kMaxRows]
     const int r = tid % kMaxRows, half = tid / kMaxRows;
     const int slot_h = r / a.w8, wrow = r - slot_h * a.w8;
     const bool valid = r < nqb * 32 && slot_h < n_sel && wrow < a.w;
     float m = -INFINITY, z = 0.f;
-    if (valid) {
-      const int P = sq.n_split;
-      const float2* pp = sq.partial + (int64_t)g * P * kMaxRows + r;
-      for (int c0 = half; c0 < P; c0 += 2 * kLseBatch) {
+    if (valid && !a.lse_given) {
+      const float2* pp = sq.partial + (int64_t)g * sq.n_split * kMaxRows + r;
+      for (int c0 = half; c0 < P; c0 += kMergeLanes * kLseBatch) {
         float2 v[kLseBatch];
 #pragma unroll
         for (int u = 0; u < kLseBatch; ++u) {
-          const int c = c0 + 2 * u;
+          const int c = c0 + kMergeLanes * u;
           v[u] = c < P ? pp[(int64_t)c * kMaxRows] : make_float2(-INFINITY, 0.f);
         }
 #pragma unroll
@@ -442,9 +464,17 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
     __syncthreads();
     if (tid < kMaxRows) {
       float mm = part[r].x, zz = part[r].y;
-      lse_merge(mm, zz, part[kMaxRows + r].x, part[kMaxRows + r].y, alpha);
-      // padding rows: +inf, so their probabilities are 0
-      lse_l[r] = valid ? mm * alpha + log2f(zz) : INFINITY;
+#pragma unroll
+      for (int j = 1; j < kMergeLanes; ++j)
+        lse_merge(mm, zz, part[j * kMaxRows + r].x, part[j * kMaxRows + r].y, alpha);
+      // padding rows: +inf, so their probabilities are 0. Caller row
+      // statistics are natural logs of the scaled logits' normaliser:
+      // log2(e) times that is the same quantity in exp2 units.
+      float v = INFINITY;
+      if (valid)
+        v = a.lse_given ? sq.lse[(int64_t)a.sel[sel0 + slot_h] * sq.lse_sh + wrow] * 1.4426950408889634f
+                        : mm * alpha + log2f(zz);
+      lse_l[r] = v;
     }
     __syncthreads();
     if (active) {
@@ -470,7 +500,7 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
   auto fold = [&](int kk) {
     const float* gb = gsum + (kk & 1) * (kGroupRows * ST);
     const int64_t t0 = (int64_t)p * ST + kk * stride;
-    for (int e = tid; e < n_sel * ST; e += kThreads) {
+    for (int e = tid; e < n_sel * ST; e += kKpThreads) {
       const int hs = e / ST, c = e - hs * ST;
       if (t0 + c >= Ls) continue;
       float acc = gb[(hs * rph) * ST + c];
@@ -522,7 +552,7 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
 }
 
 template <int DT, int D>
-__global__ __launch_bounds__(kThreads) void score_kernel(const LayerArgs a) {
+__global__ __launch_bounds__(kKpThreads) void score_kernel(const LayerArgs a) {
   using S = Stager<DT, D, stage_bytes<DT, D>()>;
   constexpr int NS = 4;  // 4-slot ring
   __shared__ uint4 slot0[S::VEC];
@@ -532,26 +562,33 @@ __global__ __launch_bounds__(kThreads) void score_kernel(const LayerArgs a) {
   // gsum[buf][r8][col]: sum over the 8 rows of 8-row group r8 of p at stage
   // column col, double-buffered by stage parity
   __shared__ __align__(16) float gsum[2 * kGroupRows * S::ST];
-  static_assert(2 * kGroupRows * S::ST >= 5 * kMaxRows, "the lse merge fits in gsum");
+  static_assert(2 * kGroupRows * S::ST >= (2 * kMergeLanes + 1) * kMaxRows, "the lse merge fits in gsum");
   uint4* const slots[NS] = {slot0, slot1, slot2, slot3};
 
   const int b = blockIdx.x;
   const SeqArgs& sq = a.seq[find_seq(a, b, [](const SeqArgs& t) { return t.blk_kpass; })];
-  const int local = b - sq.blk_kpass;
-  const int g = local / sq.n_split;
-  const int p = local - g * sq.n_split;
+  int g, p, P;
+  kpass_locate(a, sq, b - sq.blk_kpass, g, p, P);
   const int sel0 = a.grp_off[g], n_sel = a.grp_off[g + 1] - sel0;
+  // without the row-statistics pass, this pass starts the selection state
+  // from zero (the pooling kernel that accumulates into it runs after it)
+  if (a.lse_given && p == 0 && a.do_hist && g < a.n_sg) {
+    for (int i = threadIdx.x; i < kCtlWords; i += kKpThreads) sq.ctl[g * kCtlWords + i] = 0u;
+    for (int i = threadIdx.x; i < kHistBins; i += kKpThreads)
+      sq.hist[(int64_t)g * kHistBins + i] = 0u;
+  }
   if (n_sel == 0) return;  // a group without chosen heads (shared scope) is not read
   const int nqb = (n_sel * a.w8 + 31) >> 5;
   const int wpq = waves_per_qblock(nqb);
+  constexpr int W1 = kKpWaves, W2 = kKpWaves / 2, W4 = kKpWaves / 4;
   if (a.w8 % 32 == 0) {
-    if (wpq == 1) score_body<DT, D, 1, true, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, gsum);
-    else if (wpq == 2) score_body<DT, D, 2, true, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, gsum);
-    else score_body<DT, D, 4, true, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, gsum);
+    if (wpq == W4) score_body<DT, D, W4, true, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
+    else if (wpq == W2) score_body<DT, D, W2, true, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
+    else score_body<DT, D, W1, true, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
   } else {
-    if (wpq == 1) score_body<DT, D, 1, false, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, gsum);
-    else if (wpq == 2) score_body<DT, D, 2, false, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, gsum);
-    else score_body<DT, D, 4, false, S, NS>(a, sq, g, p, sel0, n_sel, nqb, slots, gsum);
+    if (wpq == W4) score_body<DT, D, W4, false, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
+    else if (wpq == W2) score_body<DT, D, W2, false, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
+    else score_body<DT, D, W1, false, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
   }
 }
 
@@ -705,12 +742,12 @@ __global__ __launch_bounds__(kThreads) void pool_kernel(const LayerArgs a) {
 
 template <template <int, int> class KernelOf>
 hipError_t launch_typed(int dtype, const LayerArgs& a, int grid, hipStream_t st, const Timing& tm) {
-  if (dtype == 0) return a.d == 64 ? launch(KernelOf<0, 64>::fn, grid, kThreads, st, tm, a)
-                                   : launch(KernelOf<0, 128>::fn, grid, kThreads, st, tm, a);
-  if (dtype == 1) return a.d == 64 ? launch(KernelOf<1, 64>::fn, grid, kThreads, st, tm, a)
-                                   : launch(KernelOf<1, 128>::fn, grid, kThreads, st, tm, a);
-  return a.d == 64 ? launch(KernelOf<2, 64>::fn, grid, kThreads, st, tm, a)
-                   : launch(KernelOf<2, 128>::fn, grid, kThreads, st, tm, a);
+  if (dtype == 0) return a.d == 64 ? launch(KernelOf<0, 64>::fn, grid, kKpThreads, st, tm, a)
+                                   : launch(KernelOf<0, 128>::fn, grid, kKpThreads, st, tm, a);
+  if (dtype == 1) return a.d == 64 ? launch(KernelOf<1, 64>::fn, grid, kKpThreads, st, tm, a)
+                                   : launch(KernelOf<1, 128>::fn, grid, kKpThreads, st, tm, a);
+  return a.d == 64 ? launch(KernelOf<2, 64>::fn, grid, kKpThreads, st, tm, a)
+                   : launch(KernelOf<2, 128>::fn, grid, kKpThreads, st, tm, a);
 }
 
 template <int DT, int D>

@@ -138,8 +138,8 @@ __global__ __launch_bounds__(kThreads) void hist_kernel(const LayerArgs a) {
 
 // Exact threshold among the candidates, then per-range kept counts and output
 // offsets.
-__device__ void resolve(const SeqArgs& sq, int g, int64_t Ls, uint32_t* ctl, uint32_t* lds_a,
-                        uint32_t* lds_b, uint32_t* wsum, uint32_t* res) {
+__device__ void resolve(const SeqArgs& sq, int n_sg, int g, int64_t Ls, uint32_t* ctl,
+                        uint32_t* lds_a, uint32_t* lds_b, uint32_t* wsum, uint32_t* res) {
   const int tid = threadIdx.x;
   const uint32_t n_cand = ctl[kCtlNumCand];
   const uint2* cands = sq.cand + (int64_t)g * Ls;
@@ -184,8 +184,8 @@ __device__ void resolve(const SeqArgs& sq, int g, int64_t Ls, uint32_t* ctl, uin
   }
   __syncthreads();
   const uint32_t* rsure = sq.rsure + (int64_t)g * n_ranges;
-  uint32_t* roff = sq.roff + (int64_t)g * n_ranges;
-  uint32_t* reqb = sq.reqb + (int64_t)g * n_ranges;
+  uint32_t* roff = sq.rsure + ((int64_t)n_sg + g) * n_ranges;
+  uint32_t* reqb = sq.rsure + (2 * (int64_t)n_sg + g) * n_ranges;
   uint32_t eq_carry = 0, off_carry = 0;
   for (int base = 0; base < n_ranges; base += kThreads) {
     const int r = base + tid;
@@ -309,7 +309,7 @@ __global__ __launch_bounds__(kThreads) void resolve_kernel(const LayerArgs a) {
   const int s = blockIdx.x / a.n_sg, g = blockIdx.x - s * a.n_sg;
   const SeqArgs& sq = a.seq[s];
   if (sq.n_keep <= 0) return;
-  resolve(sq, g, sq.L - a.w, sq.ctl + g * kCtlWords, lds_a, lds_b, wsum, res);
+  resolve(sq, a.n_sg, g, sq.L - a.w, sq.ctl + g * kCtlWords, lds_a, lds_b, wsum, res);
 }
 
 // Kept indices of one range, in ascending order at the range's output offset,
@@ -355,10 +355,10 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const LayerArgs a) {
   }
   if (nk == 0) return;
   const uint32_t* ctl = sq.ctl + g * kCtlWords;
-  const uint32_t* roff = sq.roff + (int64_t)g * sq.n_ranges;
+  const uint32_t* roff = sq.rsure + ((int64_t)a.n_sg + g) * sq.n_ranges;
   uint32_t pos_carry = roff[r];
   uint32_t end = r + 1 < sq.n_ranges ? roff[r + 1] : nk;
-  uint32_t eq_carry = sq.reqb[(int64_t)g * sq.n_ranges + r];
+  uint32_t eq_carry = sq.rsure[(2 * (int64_t)a.n_sg + g) * sq.n_ranges + r];
   const uint32_t prefix = ctl[kCtlPrefix];
   const int shift = (int)ctl[kCtlShift];
   const uint32_t need = ctl[kCtlNeedEq];

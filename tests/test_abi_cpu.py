@@ -355,3 +355,33 @@ def test_selection_kernels_fit_beside_two_k_pass_workgroups():
         size = max(v for n, v in lds.items() if k in n)
         assert size <= free, "%s uses %d B of LDS, %d B are free beside two K-pass workgroups" % (
             k, size, free)
+
+
+# ---- caller row statistics (the lse field) --------------------------------
+@pytest.mark.parametrize("fn", ["score", "compress"])
+@pytest.mark.parametrize("bad", [
+    dict(lse=_BASE + 40962),                        # not 4-byte aligned
+    dict(lse=_BASE + 40960, lse_stride_head=3),     # head stride below the window of 4
+    dict(lse=_BASE + 40960, lse_stride_head=-4),
+])
+def test_bad_lse(fn, bad):
+    assert _call(fn, _desc(), _seq(**bad)) == ckv.CKV_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("fn", ["score", "compress"])
+def test_lse_for_some_prompts_only_is_rejected(fn):
+    lib = ckv.load()
+    arr = (ckv._binding.ckv_seq * 2)(_seq(lse=_BASE + 40960, lse_stride_head=4), _seq())
+    m = (ctypes.c_uint8 * 8)(*([1] * 8))
+    f = lib.ckv_score if fn == "score" else lib.ckv_compress_layer
+    assert f(ctypes.byref(_desc()), m, arr, 2, _BASE + 32768, 1 << 40, None) == \
+        ckv.CKV_ERR_INVALID_ARG
+
+
+def test_lse_binding_rejects_wrong_layout():
+    s = ckv.Seq(None, None, None, 16, lse=torch.zeros(4, 8, dtype=torch.float64))
+    with pytest.raises(ValueError):
+        ckv._binding._seq_array([s])
+    s = ckv.Seq(None, None, None, 16, lse=torch.zeros(8, 4).t())
+    with pytest.raises(ValueError):
+        ckv._binding._seq_array([s])

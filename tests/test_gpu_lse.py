@@ -1,0 +1,148 @@
+"""GPU parity of the path with caller row statistics: the window rows'
+log-sum-exp comes from the caller (as a causal prefill attention kernel leaves
+it), the row-statistics pass over K is skipped, and the scores, indices and
+compact K/V must still match the fp64 oracle. The supplied values come from
+the oracle's own window_lse; rows of heads that are not chosen hold NaN, so a
+read of any of them would poison the scores."""
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2508_02401_amd as ckv
+from paper_2508_02401_amd import synth
+from tests.gpu_util import (Case, check_group, check_shared, chosen_heads, oracle_group,
+                            oracle_shared, random_inputs)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    ckv.load()
+    return torch.device("cuda:0")
+
+
+def _oracle_lse(case, mask, q, k, pad_stride=0):
+    """[H, w + pad_stride] fp32: the oracle's window-row lse for chosen heads in
+    the first w columns, NaN elsewhere (the padding makes the head stride
+    exceed w once the caller narrows it on the device)."""
+    lse = torch.full((case.H, case.w + pad_stride), float("nan"), dtype=torch.float32)
+    G = case.H // case.n_kv
+    for g in range(case.n_kv):
+        heads = chosen_heads(mask, case.H, case.n_kv, g)
+        if not heads:
+            continue
+        vals = oracle.window_lse(q[heads].double().numpy(), k[g].double().numpy(), case.scale)
+        for t, h in enumerate(heads):
+            lse[h, :case.w] = torch.from_numpy(vals[t]).float()
+    return lse
+
+
+def _run(case, mask, qs, ks, vs, lses, budgets, dev, fn="compress"):
+    desc = case.desc()
+    seqs = []
+    for q, k, v, lse, b in zip(qs, ks, vs, lses, budgets):
+        s = ckv.Seq(q.to(dev), k.to(dev), v.to(dev), int(b), lse=lse.to(dev)[:, :case.w])
+        ckv.alloc_outputs(desc, s)
+        seqs.append(s)
+    ws = ckv.alloc_workspace(desc, seqs, dev)
+    if fn == "compress":
+        ckv.ckv_compress_layer(desc, mask, seqs, ws)
+    else:  # the three stages as separate calls
+        ckv.ckv_score(desc, mask, seqs, ws)
+        ckv.ckv_select(desc, seqs, ws)
+        ckv.ckv_gather(desc, seqs)
+    torch.cuda.synchronize()
+    return [dict(scores=s.scores.cpu().numpy(), idx=s.idx.cpu().numpy(), k_out=s.k_out.cpu(),
+                 v_out=s.v_out.cpu()) for s in seqs]
+
+
+CASES = [
+    ("bf16-d128-G4-ragged", Case(32, 8, 128, 32, "max", 7, torch.bfloat16), 4095, 2, 512),
+    ("bf16-d64-paper-defaults", Case(8, 2, 64, 8, "avg", 5, torch.bfloat16), 257, 1, 64),
+    ("f16-w13-3heads", Case(8, 1, 128, 13, "max", 3, torch.float16), 2000, 3, 100),
+    ("bf16-w64-128rows", Case(8, 2, 128, 64, "max", 7, torch.bfloat16), 3000, 2, 300),
+    ("f32-d64", Case(8, 2, 64, 16, "avg", 7, torch.float32), 1024, 1, 128),
+    ("bf16-w48-straddle", Case(8, 2, 128, 48, "max", 9, torch.bfloat16), 3333, 2, 200),
+    ("bf16-w1-k31", Case(16, 4, 128, 1, "avg", 31, torch.bfloat16), 5000, 4, 1000),
+]
+
+
+@pytest.mark.parametrize("fn", ["compress", "split-calls"])
+@pytest.mark.parametrize("label,case,L,n_sel,budget", CASES, ids=[c[0] for c in CASES])
+def test_lse_parity(dev, label, case, L, n_sel, budget, fn):
+    q, k, v, mask = random_inputs(case, L, seed=zlib.crc32(label.encode()) % 10000, device="cpu",
+                                  n_sel=n_sel)
+    print("case", label, fn, "L", L, flush=True)
+    lse = _oracle_lse(case, mask, q, k, pad_stride=3)
+    out = _run(case, mask, [q], [k], [v], [lse], [budget], dev, fn)[0]
+    for g in range(case.n_kv):
+        rs, ri = oracle_group(case, mask, q, k, g, budget)
+        check_group(case, out, g, rs, ri, k, v, label)
+
+
+@pytest.mark.parametrize("budget", [32, 33, 1000])
+def test_lse_edge_budgets(dev, budget):
+    case = Case(8, 2, 128, 32, "max", 7, torch.bfloat16)
+    q, k, v, mask = random_inputs(case, 33, seed=5, device="cpu", n_sel=2)
+    out = _run(case, mask, [q], [k], [v], [_oracle_lse(case, mask, q, k)], [budget], dev)[0]
+    for g in range(case.n_kv):
+        rs, ri = oracle_group(case, mask, q, k, g, budget)
+        check_group(case, out, g, rs, ri, k, v, "lse-edge-%d" % budget)
+
+
+def test_lse_shared_scope(dev):
+    case = Case(32, 8, 128, 32, "max", 7, torch.bfloat16, shared=True)
+    L, budget = 3000, 256
+    q, k, v, _ = random_inputs(case, L, seed=77, device="cpu", n_sel=1)
+    mask = np.zeros(32, np.uint8)
+    mask[[1, 6, 13, 30]] = 1  # four retrieval heads in three groups
+    out = _run(case, mask, [q], [k], [v], [_oracle_lse(case, mask, q, k)], [budget], dev)[0]
+    rs, ri = oracle_shared(case, mask, q, k, budget)
+    check_shared(case, out, rs, ri, k, v, "lse-shared")
+
+
+def test_lse_ragged_batch(dev):
+    case = Case(28, 4, 128, 32, "max", 7, torch.bfloat16)
+    lens, budgets = (700, 2100, 1500), (100, 300, 64)
+    qs, ks, vs, lses = [], [], [], []
+    mask = None
+    for i, L in enumerate(lens):
+        q, k, v, m = random_inputs(case, L, seed=300 + i, device="cpu", n_sel=2, mask=mask)
+        mask = m
+        qs.append(q), ks.append(k), vs.append(v), lses.append(_oracle_lse(case, mask, q, k))
+    outs = _run(case, mask, qs, ks, vs, lses, budgets, dev)
+    for i, out in enumerate(outs):
+        for g in range(case.n_kv):
+            rs, ri = oracle_group(case, mask, qs[i], ks[i], g, budgets[i])
+            check_group(case, out, g, rs, ri, ks[i], vs[i], "lse-batch-%d" % i)
+
+
+def test_lse_full_size_128k_sampled_heads(dev):
+    # one layer of the 128K Llama workload; the supplied lse of every chosen
+    # head is computed on the host in fp64 (a matmul and a log-sum-exp), and
+    # two sampled KV heads are checked in full against the oracle
+    wl = synth.WORKLOADS["llama8b-128k-stack"]
+    inp = synth.layer_inputs(wl, 3, dev)
+    case = Case(wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.window, "max", wl.pool_kernel,
+                wl.dtype)
+    q, k, v = inp.q_win[0], inp.k[0], inp.v[0]
+    L = k.shape[1]
+    lse = torch.full((case.H, case.w), float("nan"), dtype=torch.float32)
+    qc, kc = q.double().cpu(), k.double().cpu()
+    pos = torch.arange(L)[None, :]
+    rows = (L - case.w + torch.arange(case.w))[:, None]
+    for h in np.nonzero(inp.mask)[0]:
+        g = int(h) // (case.H // case.n_kv)
+        logits = case.scale * (qc[h] @ kc[g].T)
+        logits = torch.where(pos <= rows, logits, torch.tensor(float("-inf"), dtype=torch.float64))
+        lse[h] = torch.logsumexp(logits, dim=1).float()
+    out = _run(case, inp.mask, [q], [k], [v], [lse], [192], dev)[0]
+    for g in (2, 7):
+        rs, ri = oracle_group(case, inp.mask, q.cpu(), k.cpu(), g, 192)
+        check_group(case, out, g, rs, ri, k.cpu(), v.cpu(), "lse-128k")

@@ -156,6 +156,50 @@ def test_window_sums_total_mass_is_w(seed):
     assert np.all(S[:, L - 1] <= 1 + 1e-15)
 
 
+# ---------------------------------------------------------------------------
+# Window-row log-sum-exp (the softmax normaliser of Eq. 2, natural log).
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("seed,n_sel,w,d,L", [(11, 1, 1, 3, 7), (12, 2, 4, 5, 19), (13, 3, 6, 8, 50)])
+def test_window_lse_library_route(seed, n_sel, w, d, L):
+    rng = np.random.default_rng(seed)
+    q = rng.standard_normal((n_sel, w, d)) * 2
+    k = rng.standard_normal((L, d))
+    scale = 0.61
+    lse = oracle.window_lse(q, k, scale)
+    for h in range(n_sel):
+        for i in range(w):
+            n_vis = L - w + i + 1
+            ref = scipy.special.logsumexp(scale * (k[:n_vis] @ q[h, i]))
+            assert abs(lse[h, i] - ref) <= 1e-12 * max(1.0, abs(ref))
+
+
+def test_window_lse_hand_example_and_softmax_identity():
+    # head 0 of the hand example: exp(s) over keys 0..4 sums to 9 (row 0) and
+    # over keys 0..5 to 10 (row 1), so lse = ln 9, ln 10
+    lse = oracle.window_lse(HW_Q, HW_K, 1.0)
+    assert abs(lse[0, 0] - math.log(9.0)) < 1e-14 and abs(lse[0, 1] - math.log(10.0)) < 1e-14
+    # exp(s - lse) is the attention row, whatever the row
+    rng = np.random.default_rng(14)
+    q = rng.standard_normal((1, 3, 4))
+    k = rng.standard_normal((12, 4))
+    lse = oracle.window_lse(q, k, 0.8)
+    for i in range(3):
+        n_vis = 12 - 3 + i + 1
+        p = oracle.attention_row(q[0, i], k, n_vis, 0.8)
+        np.testing.assert_allclose(np.exp(0.8 * (k[:n_vis] @ q[0, i]) - lse[0, i]), p,
+                                   rtol=1e-12, atol=1e-16)
+
+
+def test_window_lse_constant_keys_closed_form():
+    # every visible logit equal to c: lse = c + ln(number of visible keys)
+    w, L, d = 4, 13, 3
+    q = np.ones((1, w, d))
+    k = np.ones((L, d)) * 0.5
+    lse = oracle.window_lse(q, k, 2.0)
+    for i in range(w):
+        assert abs(lse[0, i] - (2.0 * 1.5 + math.log(L - w + i + 1))) < 1e-13
+
+
 @pytest.mark.parametrize("w,L", [(1, 5), (3, 10), (8, 64)])
 def test_window_sums_constant_keys_closed_form(w, L):
     # identical keys give uniform rows: row i spreads 1 over L-w+i+1 keys, so a

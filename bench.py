@@ -49,6 +49,13 @@ def parse():
                    help="K-pass launches of every N-th layer carry start/end events (the layer "
                         "offset rotates with the step, so every layer is sampled); each timed "
                         "launch delays its neighbours' dispatch by a few microseconds")
+    p.add_argument("--stack-slots", type=int, default=0,
+                   help="--schedule stack: layer slots of workspace (0 = one per layer); the "
+                        "selection stages run in launches covering that many layers (half as many "
+                        "with --stack-side)")
+    p.add_argument("--stack-side", type=int, default=0,
+                   help="--schedule stack: 1 runs a batch's selection stages on a side stream "
+                        "beside the next batch's K passes")
     p.add_argument("--schedule", choices=("stack", "layers"), default="stack",
                    help="stack: one ckv_compress_stack call over all layers, the selection of "
                         "layer l on a side stream beside the K passes of layer l+1 (default); "
@@ -160,7 +167,7 @@ def summarize_trace(d: str) -> None:
     rows = list(csv.DictReader(open(stats[0])))
     # this library's kernels (the torch kernels are the input draws, outside
     # the timed region)
-    rows = [r for r in rows if _kernel_short(r["Name"]).endswith("_kernel")]
+    rows = [r for r in rows if _kernel_short(r["Name"]).endswith(("_kernel", "_kernel_multi"))]
     print("| kernel | calls | total ms | avg us | min us | max us | % of all GPU time |")
     print("|---|---|---|---|---|---|---|")
     for r in rows:
@@ -286,12 +293,18 @@ def main():
     main = torch.cuda.current_stream()
     stack = args.schedule == "stack" and not args.pipeline
     if stack:
-        # one call for the whole stack: the K passes on the main stream, the
-        # selection stages on a side stream one layer behind
-        n_streams = 2
-        side = torch.cuda.Stream()
-        streams = [main, side]
-        ws_stack = torch.empty(2 * ws_bytes, dtype=torch.uint8, device=dev)
+        # one call for the whole stack: the K passes layer by layer, the
+        # selection stages in launches covering a batch of layers
+        stack_slots = args.stack_slots if args.stack_slots > 0 else n_layers
+        if args.stack_side:
+            stack_slots = max(2, stack_slots)
+            side = torch.cuda.Stream()
+            streams = [main, side]
+        else:
+            side = None
+            streams = [main]
+        n_streams = len(streams)
+        ws_stack = torch.empty(stack_slots * ws_bytes, dtype=torch.uint8, device=dev)
         stack_masks = np.stack([m for m, _ in layers])
         stack_seqs = [sq for _, sq in layers]
     elif args.pipeline:
@@ -497,8 +510,11 @@ def main():
                    "head_scope": "layer-shared, 4 heads per layer" if shared else
                                  "per KV group",
                    "streams": n_streams,
-                   "schedule": "ckv_compress_stack: K passes on the main stream, pooling + "
-                               "selection + gather on a side stream one layer behind" if stack else
+                   "schedule": ("ckv_compress_stack: the two K passes layer by layer, then "
+                                "pooling + selection + gather as four launches per batch of %d "
+                                "layers%s" % (stack_slots // (2 if args.stack_side else 1),
+                                              ", on a side stream beside the next batch's K passes"
+                                              if args.stack_side else "")) if stack else
                                ("pipeline: K passes + pooling on stream A, selection + gather on "
                                 "stream B, one layer apart" if args.pipeline else
                                 "ckv_compress_layer per layer, round-robin over streams")},

@@ -192,17 +192,20 @@ int ckv_compress_layer(const ckv_layer_desc *desc, const uint8_t *head_mask, con
  *   seqs [n_layers][num_seqs]: layer l's prompts at seqs + l * num_seqs, with
  *       that layer's inputs, budgets and outputs (scores may be NULL); every
  *       layer has the same prompt lengths.
- * Every layer's results are those of ckv_compress_layer on it. With
- * side_stream non-NULL and different from stream, the selection stages of
- * layer l (pooling, top-N, compaction with the gather) run on side_stream
- * while the two K passes of layer l+1 run on stream: the latency-bound
- * selection kernels then hide behind the bandwidth-bound K passes. The call
- * forks side_stream from stream and joins it back, so all its work is
- * ordered after earlier work on stream and before later work on stream, and
- * side_stream is only ordered after its own earlier work besides. The
- * workspace then holds two layer slots: workspace_bytes must be at least
- * 2 * ckv_workspace_bytes(desc, seqs, num_seqs) (once without a side
- * stream). On first use with a side stream the library creates 6 events for
+ * Every layer's results are those of ckv_compress_layer on it. The workspace
+ * is cut into slots of S = ckv_workspace_bytes(desc, seqs, num_seqs) bytes
+ * (n = workspace_bytes / S of them, at least 1, or 2 with a side stream).
+ * Layers go in batches of n (n / 2 with a side stream): the two K passes of
+ * each layer of a batch run in order on stream, then the batch's selection
+ * stages (pooling, top-N, compaction with the gather) run as four launches
+ * that each cover the whole batch; a slot per layer of the batch keeps its
+ * window sums and selection state meanwhile. With side_stream non-NULL and
+ * different from stream, a batch's selection stages run on side_stream while
+ * the next batch's K passes run on stream (the slots then form two halves
+ * used in turn). The call forks side_stream from stream and joins it back, so
+ * all its work is ordered after earlier work on stream and before later work
+ * on stream, and side_stream is only ordered after its own earlier work
+ * besides. On first use with a side stream the library creates 6 events for
  * the calling host thread and device and keeps them until the process ends.
  * If a launch fails mid-way (CKV_ERR_HIP) the layers before it are enqueued
  * and the fork may be left open: synchronise both streams before reuse. */
@@ -246,7 +249,9 @@ int ckv_set_stage_events(void *const *begin, void *const *end);
  * 0..n_layers-1 of the following ckv_compress_stack calls on this host thread,
  * in place of the ckv_set_stage_events ones; NULL arrays stop it. The arrays
  * are read at each call, not copied: keep them alive while set. Stages 0-1
- * run on the stream, stages 2-4 on the side stream when there is one. */
+ * are per layer, on the stream; stages 2-4 cover a whole batch of layers and
+ * use the entries of the batch's first layer (on the side stream when there
+ * is one). */
 int ckv_set_stack_stage_events(void *const *begin, void *const *end, int32_t n_layers);
 
 #ifdef __cplusplus

@@ -92,6 +92,11 @@ WsLayout seq_ws_layout(const ckv_layer_desc* d, const ckv_seq* s) {
 
 size_t seq_ws_bytes(const ckv_layer_desc* d, const ckv_seq* s) { return seq_ws_layout(d, s).total; }
 
+// A call's workspace starts with room for its kernel argument block (the
+// multi-layer selection launches of ckv_compress_stack read it from there),
+// then holds every prompt's sections in order.
+const size_t kWsHeader = align_up(sizeof(ckv::LayerArgs));
+
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 int check_desc(const ckv_layer_desc* d) {
@@ -202,6 +207,7 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
     }
   a.elt = elt_bytes(d->dtype);
   int32_t blk_kpass = 0, blk_pool = 0, blk_sel = 0, blk_gather = 0;
+  if (ws) ws += kWsHeader;
   for (int32_t i = 0; i < n; ++i) {
     const ckv_seq& s = seqs[i];
     ckv::SeqArgs& q = a.seq[i];
@@ -354,7 +360,7 @@ extern "C" {
 
 size_t ckv_workspace_bytes(const ckv_layer_desc* desc, const ckv_seq* seqs, int32_t num_seqs) {
   if (check_desc(desc) != CKV_OK || !seqs || num_seqs < 1 || num_seqs > CKV_MAX_SEQS) return 0;
-  size_t total = 0;
+  size_t total = kWsHeader;
   for (int32_t i = 0; i < num_seqs; ++i) {
     if (seqs[i].seq_len <= desc->window || seqs[i].seq_len >= ((int64_t)1 << 31)) return 0;
     total += seq_ws_bytes(desc, &seqs[i]);
@@ -453,8 +459,16 @@ int ckv_compress_stack(const ckv_layer_desc* desc, int32_t n_layers, const uint8
                          true, probe)) != CKV_OK)
       return rc;
   }
-  if (!workspace || !aligned16(workspace) || workspace_bytes < (two ? 2 : 1) * slot_bytes)
-    return CKV_ERR_WORKSPACE;
+  // Layers go in batches of `batch`, one workspace slot per layer of a batch:
+  // the K passes of the batch's layers on the stream, then its selection
+  // stages as four launches that each cover the whole batch. With a side
+  // stream the slots form two halves, and the selection of one batch runs
+  // there while the K passes of the next run on the stream.
+  const size_t n_slots = workspace ? workspace_bytes / slot_bytes : 0;
+  if (!workspace || !aligned16(workspace) || n_slots < (two ? 2u : 1u)) return CKV_ERR_WORKSPACE;
+  int32_t batch = (int32_t)((two ? n_slots / 2 : n_slots) < (size_t)n_layers
+                                ? (two ? n_slots / 2 : n_slots)
+                                : (size_t)n_layers);
   // fork/join and hand-off events of this thread on the current device
   hipEvent_t* ev = nullptr;
   if (two) {
@@ -477,41 +491,74 @@ int ckv_compress_stack(const ckv_layer_desc* desc, int32_t n_layers, const uint8
     saved_e[i] = g_ev_end[i];
   }
   const bool stack_timed = g_stack_begin != nullptr;
-  for (int32_t l = 0; l < n_layers && rc == CKV_OK; ++l) {
-    const int slot = two ? (l & 1) : 0;
-    char* ws = static_cast<char*>(workspace) + slot * slot_bytes;
-    ckv::LayerArgs a;
-    if ((rc = build_args(desc, head_masks + (int64_t)l * desc->num_q_heads,
-                         seqs + (int64_t)l * num_seqs, num_seqs, ws, true, a)) != CKV_OK)
-      break;
-    a.do_hist = 1;
-    a.do_gather = 1;
-    if (stack_timed) {
-      g_events_on = l < g_stack_layers;
-      for (int i = 0; i < ckv::kNumStages; ++i) {
-        g_ev_begin[i] = g_events_on ? (hipEvent_t)g_stack_begin[l * ckv::kNumStages + i] : nullptr;
-        g_ev_end[i] = g_events_on ? (hipEvent_t)g_stack_end[l * ckv::kNumStages + i] : nullptr;
-      }
+  auto use_layer_events = [&](int32_t l) {
+    if (!stack_timed) return;
+    g_events_on = l < g_stack_layers;
+    for (int i = 0; i < ckv::kNumStages; ++i) {
+      g_ev_begin[i] = g_events_on ? (hipEvent_t)g_stack_begin[l * ckv::kNumStages + i] : nullptr;
+      g_ev_end[i] = g_events_on ? (hipEvent_t)g_stack_end[l * ckv::kNumStages + i] : nullptr;
     }
+  };
+  for (int32_t b0 = 0, j = 0; b0 < n_layers && rc == CKV_OK; b0 += batch, ++j) {
+    const int half = two ? (j & 1) : 0;
+    const int32_t nb = n_layers - b0 < batch ? n_layers - b0 : batch;
+    char* base = static_cast<char*>(workspace) + (size_t)half * batch * slot_bytes;
     hipError_t e;
-    // the selection of layer l-2 used this slot: wait until it is done
-    if (two && l >= 2 && (e = hipStreamWaitEvent(st, ev[kEvSelected + slot], 0)) != hipSuccess) {
+    // the selection of batch j-2 used these slots: wait until it is done
+    if (two && j >= 2 && (e = hipStreamWaitEvent(st, ev[kEvSelected + half], 0)) != hipSuccess) {
       rc = hip_fail(e);
       break;
     }
-    if ((rc = run_kpasses(desc, a, st)) != CKV_OK) break;
+    ckv::LayerArgs a;
+    for (int32_t i = 0; i < nb && rc == CKV_OK; ++i) {
+      const int32_t l = b0 + i;
+      char* ws = base + (size_t)i * slot_bytes;
+      if ((rc = build_args(desc, head_masks + (int64_t)l * desc->num_q_heads,
+                           seqs + (int64_t)l * num_seqs, num_seqs, ws, true, a)) != CKV_OK)
+        break;
+      a.do_hist = 1;
+      a.do_gather = 1;
+      a.table_out = ws;  // the argument block the selection launches read
+      use_layer_events(l);
+      rc = run_kpasses(desc, a, st);
+    }
+    if (rc != CKV_OK) break;
     hipStream_t sel = st;
     if (two) {
-      if ((e = hipEventRecord(ev[kEvScored + slot], st)) != hipSuccess ||
-          (e = hipStreamWaitEvent(side, ev[kEvScored + slot], 0)) != hipSuccess) {
+      if ((e = hipEventRecord(ev[kEvScored + half], st)) != hipSuccess ||
+          (e = hipStreamWaitEvent(side, ev[kEvScored + half], 0)) != hipSuccess) {
         rc = hip_fail(e);
         break;
       }
       sel = side;
     }
-    if ((rc = run_pool(a, sel)) != CKV_OK) break;
-    if ((rc = run_select(a, false, sel)) != CKV_OK) break;
-    if (two && (e = hipEventRecord(ev[kEvSelected + slot], side)) != hipSuccess) {
+    // the batch's selection stages in two launches: the pooling (with the
+    // scores and histograms), then one workgroup per selection unit (layer,
+    // prompt, selection group) from the threshold to the gathered rows;
+    // timed on the events of the batch's first layer
+    use_layer_events(b0);
+    ckv::MultiArgs m;
+    m.table = base;
+    m.stride = (int64_t)slot_bytes;
+    m.n_layers = nb;
+    m.per_layer = 0;
+    for (int i = 0; i < a.num_seqs; ++i)
+      m.per_layer += a.n_sg * (int32_t)ceil_div(a.seq[i].n_ptiles, ckv::kUnitPoolTiles);
+    if ((e = ckv::launch_pool_units(m, sel, timing(ckv::kStagePool, true, true))) != hipSuccess) {
+      rc = hip_fail(e);
+      break;
+    }
+    m.per_layer = a.num_seqs * a.n_sg;
+    ckv::Timing tm;
+    if (g_events_on) {
+      tm.start = g_ev_begin[ckv::kStageSelect];
+      tm.stop = g_ev_end[ckv::kStageGather];
+    }
+    if ((e = ckv::launch_select_units(m, sel, tm)) != hipSuccess) {
+      rc = hip_fail(e);
+      break;
+    }
+    if (two && (e = hipEventRecord(ev[kEvSelected + half], side)) != hipSuccess) {
       rc = hip_fail(e);
       break;
     }

@@ -13,6 +13,21 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Pointers read from memory (argument blocks in device memory, LDS tables)
+// are generic, and generic (flat) loads count against the LDS wait counter
+// too, so every LDS access would also wait for them. Casting a pointer known
+// to address global memory lets the compiler issue global loads instead.
+#define CKV_GLOBAL __attribute__((address_space(1)))
+template <class T>
+__device__ __forceinline__ const CKV_GLOBAL T* to_global(const T* p) {
+  return (const CKV_GLOBAL T*)p;
+}
+template <class T>
+__device__ __forceinline__ CKV_GLOBAL T* to_global(T* p) {
+  return (CKV_GLOBAL T*)p;
+}
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
@@ -133,14 +148,100 @@ __device__ __forceinline__ void find_bin(uint32_t need, Get get, uint32_t* wsum,
 
 // Launch kernel(a) on stream st, with its start and end times recorded into
 // tm's events when they are given.
-template <typename K>
+template <typename K, typename A>
 __host__ hipError_t launch(K kernel, int grid, int block, hipStream_t st, const Timing& tm,
-                           const LayerArgs& a) {
+                           const A& a) {
   if (tm.start || tm.stop)
     hipExtLaunchKernelGGL(kernel, dim3(grid), dim3(block), 0, st, tm.start, tm.stop, 0, a);
   else
     hipLaunchKernelGGL(kernel, dim3(grid), dim3(block), 0, st, a);
   return hipGetLastError();
+}
+
+constexpr int kPoolPer = 8;  // consecutive scores pooled per thread
+
+// x[i] = row[o0 - HW + i] for i in [0, 8 + 2*HW); inputs outside [0, Ls)
+// read as pad. Aligned 16-byte loads when the window lies inside the row
+// (o0 - HW is a multiple of 4 and rows start 16-byte aligned).
+template <int HW>
+__device__ __forceinline__ void pool_inputs(const float* row_p, int64_t o0, int64_t Ls, float pad,
+                                            float* x) {
+  const CKV_GLOBAL float* row = to_global(row_p);
+  constexpr int NX = kPoolPer + 2 * HW;
+  const int64_t lo = o0 - HW;
+  if (lo >= 0 && lo + NX <= Ls) {
+    const CKV_GLOBAL f32x4* src = (const CKV_GLOBAL f32x4*)(row + lo);
+#pragma unroll
+    for (int v = 0; v < NX / 4; ++v) {
+      const f32x4 t = src[v];
+      x[4 * v] = t.x;
+      x[4 * v + 1] = t.y;
+      x[4 * v + 2] = t.z;
+      x[4 * v + 3] = t.w;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < NX; ++i) {
+      const int64_t j = lo + i;
+      x[i] = j >= 0 && j < Ls ? row[j] : pad;
+    }
+  }
+}
+
+constexpr int kCopyBatch = 8;  // 16-byte K and V chunks in flight per thread
+
+// Copy n rows of K and V: source token src(i) -> output row dst(i), for i in
+// [0, n). Rows whose source or destination is out of range are skipped. The
+// loads of a batch are all issued before its stores.
+template <int NT, class Src, class Dst>
+__device__ __forceinline__ void copy_rows(const LayerArgs& a, const SeqArgs& sq, int g, int64_t n,
+                                          Src src, Dst dst) {
+  const int nv = a.d * a.elt / 16;  // 8, 16 or 32 chunks per row
+  const int nv_log2 = nv == 8 ? 3 : (nv == 16 ? 4 : 5);
+  // native vectors (not HIP's uint4 struct) so the batch stays in registers
+  const CKV_GLOBAL char* __restrict__ kb =
+      to_global(static_cast<const char*>(sq.k)) + (int64_t)g * sq.kv_sh * a.elt;
+  const CKV_GLOBAL char* __restrict__ vb =
+      to_global(static_cast<const char*>(sq.v)) + (int64_t)g * sq.kv_sh * a.elt;
+  CKV_GLOBAL u32x4* __restrict__ ko = to_global(static_cast<u32x4*>(sq.k_out)) + (int64_t)g * sq.n_ret * nv;
+  CKV_GLOBAL u32x4* __restrict__ vo = to_global(static_cast<u32x4*>(sq.v_out)) + (int64_t)g * sq.n_ret * nv;
+  const int64_t total = n << nv_log2;
+  for (int64_t e0 = 0; e0 < total; e0 += (int64_t)NT * kCopyBatch) {
+    u32x4 kr[kCopyBatch], vr[kCopyBatch];
+    int64_t to[kCopyBatch];
+#pragma unroll
+    for (int u = 0; u < kCopyBatch; ++u) {
+      const int64_t e = e0 + threadIdx.x + (int64_t)u * NT;
+      const int64_t i = e >> nv_log2;
+      const int c = (int)(e & (nv - 1));
+      const int64_t j = e < total ? src(i) : -1;
+      const int64_t p = e < total ? dst(i) : -1;
+      const bool ok = j >= 0 && j < sq.L && p >= 0 && p < sq.n_ret;
+      to[u] = ok ? (p << nv_log2) + c : -1;
+      const int64_t jj = ok ? j : 0;  // row 0 is a valid address for skipped lanes
+      kr[u] = ((const CKV_GLOBAL u32x4*)(kb + jj * sq.kv_st * a.elt))[c];
+      vr[u] = ((const CKV_GLOBAL u32x4*)(vb + jj * sq.kv_st * a.elt))[c];
+    }
+#pragma unroll
+    for (int u = 0; u < kCopyBatch; ++u) {
+      if (to[u] >= 0) {
+        ko[to[u]] = kr[u];
+        vo[to[u]] = vr[u];
+      }
+    }
+  }
+}
+
+// Contiguous run: row src0 + i -> output row dst0 + i.
+template <int NT>
+__device__ __forceinline__ void copy_run(const LayerArgs& a, const SeqArgs& sq, int g, int64_t dst0,
+                                         int64_t src0, int64_t n) {
+  copy_rows<NT>(a, sq, g, n, [=](int64_t i) { return src0 + i; }, [=](int64_t i) { return dst0 + i; });
+}
+
+// Layer l's argument block of a multi-layer launch.
+__device__ __forceinline__ const LayerArgs& layer_args(const MultiArgs& m, int l) {
+  return *reinterpret_cast<const LayerArgs*>(m.table + (int64_t)l * m.stride);
 }
 
 }  // namespace dev

@@ -18,6 +18,7 @@ constexpr int kMinStagesPerWg = 65536 / kStageBytes; // K stages per workgroup (
 constexpr int kTargetWgs = 512;    // K-pass workgroups per prompt: 2 on each of 256 CUs
 constexpr int kCUs = 256;          // compute units of the MI355X
 constexpr int kPoolTile = 2048;    // scores per pooling workgroup
+constexpr int kUnitPoolTiles = 8;  // tiles per pooling workgroup of ckv_compress_stack
 constexpr int kMaxPoolRadius = 15; // pool kernel <= 2*15+1
 constexpr int kGatherRows = 64;    // retained rows per gather workgroup
 constexpr int kHistBits = 12;      // first-level histogram: key bits 30..19
@@ -124,10 +125,21 @@ struct LayerArgs {
   int32_t n_sg;            // selection groups per prompt: n_kv, or 1 when shared
   int32_t split_w;         // sum over the groups read of nqb + kSplitBias (group_split)
   int32_t lse_given;       // every prompt carries lse: the row-statistics pass is skipped
+  void* table_out;         // the scoring kernel copies this block here (device), or null
   int16_t grp_off[kMaxKvHeads + 1];  // chosen heads of group g: sel[grp_off[g] .. grp_off[g+1])
   uint8_t sel[kMaxQHeads];
   uint8_t sel_grp[kMaxQHeads];       // KV group of chosen head t (sel[t] / G)
   SeqArgs seq[kMaxSeqs];
+};
+
+// Several layers' selection stages in one launch: layer l's argument block is
+// in device memory at table + l * stride (the scoring kernel of that layer put
+// it there), and every layer has per_layer workgroups.
+struct MultiArgs {
+  const char* table;
+  int64_t stride;
+  int32_t per_layer;
+  int32_t n_layers;
 };
 
 // Optional timing of one launch: start receives the kernel's start time and
@@ -148,5 +160,12 @@ hipError_t launch_filter(const LayerArgs& a, int grid, hipStream_t st, const Tim
 hipError_t launch_resolve(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
 hipError_t launch_compact(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
 hipError_t launch_gather(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
+// pooling, head mean, scores and histograms of a batch of layers
+// (per_layer = sum over prompts of selection groups * ceil(n_ptiles /
+// kUnitPoolTiles)), then the top-N through compaction and gather of every
+// selection unit (layer, prompt, selection group), one workgroup each
+// (per_layer = prompts * selection groups)
+hipError_t launch_pool_units(const MultiArgs& m, hipStream_t st, const Timing& tm);
+hipError_t launch_select_units(const MultiArgs& m, hipStream_t st, const Timing& tm);
 
 }  // namespace ckv

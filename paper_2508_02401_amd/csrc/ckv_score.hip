@@ -567,6 +567,14 @@ __global__ __launch_bounds__(kKpThreads) void score_kernel(const LayerArgs a) {
 
   const int b = blockIdx.x;
   const SeqArgs& sq = a.seq[find_seq(a, b, [](const SeqArgs& t) { return t.blk_kpass; })];
+  // the selection stages of a multi-layer launch read this layer's argument
+  // block from device memory: workgroup 0 puts it there
+  if (a.table_out && b == 0) {
+    static_assert(sizeof(LayerArgs) % 16 == 0, "argument block in 16-byte words");
+    const uint4* src = reinterpret_cast<const uint4*>(&a);
+    uint4* dst = static_cast<uint4*>(a.table_out);
+    for (int i = threadIdx.x; i < (int)(sizeof(LayerArgs) / 16); i += kKpThreads) dst[i] = src[i];
+  }
   int g, p, P;
   kpass_locate(a, sq, b - sq.blk_kpass, g, p, P);
   const int sel0 = a.grp_off[g], n_sel = a.grp_off[g + 1] - sel0;
@@ -606,8 +614,8 @@ __global__ __launch_bounds__(kKpThreads) void score_kernel(const LayerArgs a) {
 // which keeps the kernel small enough in LDS to share a CU with two K-pass
 // workgroups.
 // ---------------------------------------------------------------------------
-constexpr int kPoolPer = kPoolTile / kThreads;  // scores per thread
-static_assert(kPoolPer == 8 && kPoolTile <= 65535, "8 scores per thread, 16-bit bin counts");
+static_assert(kPoolPer * kThreads == kPoolTile && kUnitPoolTiles * kPoolTile <= 65535,
+              "8 scores per thread, 16-bit bin counts");
 
 // What one pooling workgroup needs, resolved from the argument block in the
 // kernel itself (passing the block by reference down the radius dispatch
@@ -615,40 +623,14 @@ static_assert(kPoolPer == 8 && kPoolTile <= 65535, "8 scores per thread, 16-bit 
 struct PoolJob {
   const float* const* rows;  // LDS table: window sums of the heads averaged
   int n_heads;
-  int64_t Ls, j0;            // prefix length, first score of the tile
-  int n_out;                 // scores in this tile
+  int64_t Ls, j0;            // prefix length, first score of the first tile
+  int n_out;                 // scores in this workgroup's tiles
+  int n_tiles;               // consecutive tiles of kPoolTile scores
   bool is_max, do_hist;
   float inv_kp;
-  float* out;                // scores of the tile
+  CKV_GLOBAL float* out;     // scores of the first tile
   uint32_t* ghist;           // the selection group's histogram
 };
-
-// x[i] = row[o0 - HW + i] for i in [0, 8 + 2*HW); inputs outside [0, Ls)
-// read as pad. Aligned 16-byte loads when the window lies inside the row
-// (o0 - HW is a multiple of 4 and rows start 16-byte aligned).
-template <int HW>
-__device__ __forceinline__ void pool_inputs(const float* row, int64_t o0, int64_t Ls, float pad,
-                                            float* x) {
-  constexpr int NX = kPoolPer + 2 * HW;
-  const int64_t lo = o0 - HW;
-  if (lo >= 0 && lo + NX <= Ls) {
-    const float4* src = reinterpret_cast<const float4*>(row + lo);
-#pragma unroll
-    for (int v = 0; v < NX / 4; ++v) {
-      const float4 t = src[v];
-      x[4 * v] = t.x;
-      x[4 * v + 1] = t.y;
-      x[4 * v + 2] = t.z;
-      x[4 * v + 3] = t.w;
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < NX; ++i) {
-      const int64_t j = lo + i;
-      x[i] = j >= 0 && j < Ls ? row[j] : pad;
-    }
-  }
-}
 
 template <int R>
 __device__ __forceinline__ void pool_tile(const PoolJob& jb, uint32_t* hist_lds) {
@@ -656,33 +638,36 @@ __device__ __forceinline__ void pool_tile(const PoolJob& jb, uint32_t* hist_lds)
   constexpr int NX = kPoolPer + 2 * HW;
   const int tid = threadIdx.x;
   const float pad = jb.is_max ? -INFINITY : 0.f;  // max ignores padding; avg counts it as 0
-  const int64_t o0 = jb.j0 + (int64_t)tid * kPoolPer;
-  float total[kPoolPer];
+  for (int tile = 0; tile < jb.n_tiles; ++tile) {
+    const int t_off = tile * kPoolTile + tid * kPoolPer;  // first score of this thread
+    const int64_t o0 = jb.j0 + t_off;
+    float total[kPoolPer];
 #pragma unroll
-  for (int u = 0; u < kPoolPer; ++u) total[u] = 0.f;
-  for (int hh = 0; hh < jb.n_heads; ++hh) {
-    float x[NX];
-    pool_inputs<HW>(jb.rows[hh], o0, jb.Ls, pad, x);
+    for (int u = 0; u < kPoolPer; ++u) total[u] = 0.f;
+    for (int hh = 0; hh < jb.n_heads; ++hh) {
+      float x[NX];
+      pool_inputs<HW>(jb.rows[hh], o0, jb.Ls, pad, x);
+#pragma unroll
+      for (int u = 0; u < kPoolPer; ++u) {
+        float v = x[HW + u];
+#pragma unroll
+        for (int dt = 1; dt <= R; ++dt) {
+          const float lo = x[HW + u - dt], hi = x[HW + u + dt];
+          v = jb.is_max ? fmaxf(v, fmaxf(lo, hi)) : v + (lo + hi);
+        }
+        total[u] += jb.is_max ? v : v * jb.inv_kp;
+      }
+    }
+    const int n_mine = jb.n_out - t_off;  // scores of this thread inside the tile
 #pragma unroll
     for (int u = 0; u < kPoolPer; ++u) {
-      float v = x[HW + u];
-#pragma unroll
-      for (int dt = 1; dt <= R; ++dt) {
-        const float lo = x[HW + u - dt], hi = x[HW + u + dt];
-        v = jb.is_max ? fmaxf(v, fmaxf(lo, hi)) : v + (lo + hi);
+      if (u >= n_mine) break;
+      const float score = total[u] / (float)jb.n_heads;
+      jb.out[t_off + u] = score;
+      if (jb.do_hist) {
+        const uint32_t bin = score_key(score) >> kHistShift;
+        atomicAdd(&hist_lds[bin >> 1], 1u << ((bin & 1u) * 16u));
       }
-      total[u] += jb.is_max ? v : v * jb.inv_kp;
-    }
-  }
-  const int n_mine = jb.n_out - tid * kPoolPer;  // scores of this thread inside the tile
-#pragma unroll
-  for (int u = 0; u < kPoolPer; ++u) {
-    if (u >= n_mine) break;
-    const float score = total[u] / (float)jb.n_heads;
-    jb.out[tid * kPoolPer + u] = score;
-    if (jb.do_hist) {
-      const uint32_t bin = score_key(score) >> kHistShift;
-      atomicAdd(&hist_lds[bin >> 1], 1u << ((bin & 1u) * 16u));
     }
   }
   if (!jb.do_hist) return;
@@ -705,10 +690,9 @@ __device__ __forceinline__ void pool_dispatch(int r, const PoolJob& jb, uint32_t
   }
 }
 
-__global__ __launch_bounds__(kThreads) void pool_kernel(const LayerArgs a) {
+__device__ __forceinline__ void pool_body(const LayerArgs& a, int b) {
   __shared__ uint32_t hist_lds[kHistBins / 2];  // two 16-bit counts per word
   __shared__ const float* rows[kMaxQHeads];
-  const int b = blockIdx.x;
   const SeqArgs& sq = a.seq[find_seq(a, b, [](const SeqArgs& t) { return t.blk_pool; })];
   const int local = b - sq.blk_pool;
   const int g = local / sq.n_ptiles;  // selection group (0 when shared)
@@ -732,13 +716,64 @@ __global__ __launch_bounds__(kThreads) void pool_kernel(const LayerArgs a) {
   jb.Ls = Ls;
   jb.j0 = (int64_t)tile * kPoolTile;
   jb.n_out = Ls - jb.j0 < kPoolTile ? (int)(Ls - jb.j0) : kPoolTile;
+  jb.n_tiles = 1;
   jb.is_max = a.pool != 0;
   jb.do_hist = do_hist;
   jb.inv_kp = 1.f / (float)a.kp;
-  jb.out = sq.scores + (int64_t)g * Ls + jb.j0;
+  jb.out = to_global(sq.scores) + (int64_t)g * Ls + jb.j0;
   jb.ghist = sq.hist + (int64_t)g * kHistBins;
   pool_dispatch<0>(a.kp >> 1, jb, hist_lds);  // radius 0..kMaxPoolRadius
 }
+
+__global__ __launch_bounds__(kThreads) void pool_kernel(const LayerArgs a) { pool_body(a, blockIdx.x); }
+
+// Pooling, head mean, scores and the first-level histogram of several layers
+// at once (ckv_compress_stack): layer l's argument block is read from device
+// memory, and each workgroup covers kUnitPoolTiles consecutive tiles of one
+// (prompt, selection group), merging its histogram once.
+__global__ __launch_bounds__(kThreads) void pool_units_kernel(const MultiArgs m) {
+  __shared__ uint32_t hist_lds[kHistBins / 2];  // two 16-bit counts per word
+  __shared__ const float* rows[kMaxQHeads];
+  const int l = blockIdx.x / m.per_layer;
+  const LayerArgs& a = layer_args(m, l);
+  int local = blockIdx.x - l * m.per_layer;
+  int s = 0;
+  for (; s < a.num_seqs - 1; ++s) {
+    const int n = a.n_sg * ((a.seq[s].n_ptiles + kUnitPoolTiles - 1) / kUnitPoolTiles);
+    if (local < n) break;
+    local -= n;
+  }
+  const SeqArgs& sq = a.seq[s];
+  const int per_g = (sq.n_ptiles + kUnitPoolTiles - 1) / kUnitPoolTiles;
+  const int g = local / per_g;
+  const int chunk = local - g * per_g;
+  const int64_t Ls = sq.L - a.w;
+  const int t0 = a.shared ? 0 : a.grp_off[g];
+  const int t1 = a.shared ? a.grp_off[a.n_kv] : a.grp_off[g + 1];
+  for (int t = t0 + (int)threadIdx.x; t < t1; t += kThreads) {
+    const int gt = a.sel_grp[t];
+    rows[t - t0] = sq.wsum + ((int64_t)gt * sq.wsum_heads + (t - a.grp_off[gt])) * sq.ws_stride;
+  }
+  const bool do_hist = a.do_hist && sq.n_keep > 0;
+  if (do_hist)
+    for (int i = threadIdx.x; i < kHistBins / 2; i += kThreads) hist_lds[i] = 0u;
+  __syncthreads();
+  PoolJob jb;
+  jb.rows = rows;
+  jb.n_heads = t1 - t0;
+  jb.Ls = Ls;
+  jb.j0 = (int64_t)chunk * kUnitPoolTiles * kPoolTile;
+  const int64_t left = Ls - jb.j0;
+  jb.n_out = left < (int64_t)kUnitPoolTiles * kPoolTile ? (int)left : kUnitPoolTiles * kPoolTile;
+  jb.n_tiles = (jb.n_out + kPoolTile - 1) / kPoolTile;
+  jb.is_max = a.pool != 0;
+  jb.do_hist = do_hist;
+  jb.inv_kp = 1.f / (float)a.kp;
+  jb.out = to_global(sq.scores) + (int64_t)g * Ls + jb.j0;
+  jb.ghist = sq.hist + (int64_t)g * kHistBins;
+  pool_dispatch<0>(a.kp >> 1, jb, hist_lds);
+}
+
 
 template <template <int, int> class KernelOf>
 hipError_t launch_typed(int dtype, const LayerArgs& a, int grid, hipStream_t st, const Timing& tm) {
@@ -772,5 +807,10 @@ hipError_t launch_score(int dtype, const LayerArgs& a, int grid, hipStream_t st,
 hipError_t launch_pool(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm) {
   return launch(pool_kernel, grid, kThreads, st, tm, a);
 }
+
+hipError_t launch_pool_units(const MultiArgs& m, hipStream_t st, const Timing& tm) {
+  return launch(pool_units_kernel, m.n_layers * m.per_layer, kThreads, st, tm, m);
+}
+
 
 }  // namespace ckv

@@ -41,54 +41,6 @@ __device__ __forceinline__ int find_seq_sel(const LayerArgs& a, int b) {
   return s;
 }
 
-constexpr int kCopyBatch = 8;  // 16-byte K and V chunks in flight per thread
-
-// Copy n rows of K and V: source token src(i) -> output row dst(i), for i in
-// [0, n). Rows whose source or destination is out of range are skipped. The
-// loads of a batch are all issued before its stores.
-template <class Src, class Dst>
-__device__ __forceinline__ void copy_rows(const LayerArgs& a, const SeqArgs& sq, int g, int64_t n,
-                                          Src src, Dst dst) {
-  const int nv = a.d * a.elt / 16;  // 8, 16 or 32 chunks per row
-  const int nv_log2 = nv == 8 ? 3 : (nv == 16 ? 4 : 5);
-  // native vectors (not HIP's uint4 struct) so the batch stays in registers
-  const char* __restrict__ kb = static_cast<const char*>(sq.k) + (int64_t)g * sq.kv_sh * a.elt;
-  const char* __restrict__ vb = static_cast<const char*>(sq.v) + (int64_t)g * sq.kv_sh * a.elt;
-  u32x4* __restrict__ ko = static_cast<u32x4*>(sq.k_out) + (int64_t)g * sq.n_ret * nv;
-  u32x4* __restrict__ vo = static_cast<u32x4*>(sq.v_out) + (int64_t)g * sq.n_ret * nv;
-  const int64_t total = n << nv_log2;
-  for (int64_t e0 = 0; e0 < total; e0 += (int64_t)kThreads * kCopyBatch) {
-    u32x4 kr[kCopyBatch], vr[kCopyBatch];
-    int64_t to[kCopyBatch];
-#pragma unroll
-    for (int u = 0; u < kCopyBatch; ++u) {
-      const int64_t e = e0 + threadIdx.x + (int64_t)u * kThreads;
-      const int64_t i = e >> nv_log2;
-      const int c = (int)(e & (nv - 1));
-      const int64_t j = e < total ? src(i) : -1;
-      const int64_t p = e < total ? dst(i) : -1;
-      const bool ok = j >= 0 && j < sq.L && p >= 0 && p < sq.n_ret;
-      to[u] = ok ? (p << nv_log2) + c : -1;
-      const int64_t jj = ok ? j : 0;  // row 0 is a valid address for skipped lanes
-      kr[u] = reinterpret_cast<const u32x4*>(kb + jj * sq.kv_st * a.elt)[c];
-      vr[u] = reinterpret_cast<const u32x4*>(vb + jj * sq.kv_st * a.elt)[c];
-    }
-#pragma unroll
-    for (int u = 0; u < kCopyBatch; ++u) {
-      if (to[u] >= 0) {
-        ko[to[u]] = kr[u];
-        vo[to[u]] = vr[u];
-      }
-    }
-  }
-}
-
-// Contiguous run: row src0 + i -> output row dst0 + i.
-__device__ __forceinline__ void copy_run(const LayerArgs& a, const SeqArgs& sq, int g, int64_t dst0,
-                                         int64_t src0, int64_t n) {
-  copy_rows(a, sq, g, n, [=](int64_t i) { return src0 + i; }, [=](int64_t i) { return dst0 + i; });
-}
-
 // Zero the selection control words and histograms (ckv_select on caller
 // scores; ckv_compress_layer clears them in the row-statistics kernel).
 __global__ __launch_bounds__(kThreads) void clear_kernel(const LayerArgs a) {
@@ -214,10 +166,9 @@ __device__ void resolve(const SeqArgs& sq, int n_sg, int g, int64_t Ls, uint32_t
 // Every range finds the threshold bin from the group's histogram (the range 0
 // workgroup records it), counts its keys above the bin and appends the keys
 // inside it to the candidate list.
-__global__ __launch_bounds__(kThreads) void filter_kernel(const LayerArgs a) {
+__device__ __forceinline__ void filter_body(const LayerArgs& a, int b) {
   __shared__ uint32_t wsum[kWaves];
   __shared__ uint32_t res[3];
-  const int b = blockIdx.x;
   const int s = find_seq_sel(a, b);
   const SeqArgs& sq = a.seq[s];
   const int local = b - sq.blk_sel;
@@ -300,26 +251,35 @@ __global__ __launch_bounds__(kThreads) void filter_kernel(const LayerArgs a) {
   if (tid == 0) sq.rsure[(int64_t)g * sq.n_ranges + r] = total;
 }
 
+__global__ __launch_bounds__(kThreads) void filter_kernel(const LayerArgs a) {
+  filter_body(a, blockIdx.x);
+}
+
+
 // One workgroup per (prompt, group): exact threshold and range offsets.
-__global__ __launch_bounds__(kThreads) void resolve_kernel(const LayerArgs a) {
+__device__ __forceinline__ void resolve_body(const LayerArgs& a, int b) {
   __shared__ uint32_t lds_a[kMaxRanges];
   __shared__ uint32_t lds_b[kMaxRanges];
   __shared__ uint32_t wsum[kWaves];
   __shared__ uint32_t res[3];
-  const int s = blockIdx.x / a.n_sg, g = blockIdx.x - s * a.n_sg;
+  const int s = b / a.n_sg, g = b - s * a.n_sg;
   const SeqArgs& sq = a.seq[s];
   if (sq.n_keep <= 0) return;
   resolve(sq, a.n_sg, g, sq.L - a.w, sq.ctl + g * kCtlWords, lds_a, lds_b, wsum, res);
 }
 
+__global__ __launch_bounds__(kThreads) void resolve_kernel(const LayerArgs a) {
+  resolve_body(a, blockIdx.x);
+}
+
+
 // Kept indices of one range, in ascending order at the range's output offset,
 // then the copies of their K/V rows. Thread t takes kCompactPer consecutive
 // scores per step, so a thread's kept tokens are consecutive in the output.
-__global__ __launch_bounds__(kThreads) void compact_kernel(const LayerArgs a) {
+__device__ __forceinline__ void compact_body(const LayerArgs& a, int b) {
   __shared__ uint32_t wsum[kWaves];
   __shared__ int32_t pos_l[kCopyList];
   __shared__ int32_t tok_l[kCopyList];
-  const int b = blockIdx.x;
   const int s = find_seq_sel(a, b);
   const SeqArgs& sq = a.seq[s];
   const int local = b - sq.blk_sel;
@@ -341,8 +301,8 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const LayerArgs a) {
       for (int i = tid; i < w; i += kThreads) out[Ls + i] = (int32_t)(Ls + i);
     if (a.do_gather) {
       for (int gk = gk0; gk < gk1; ++gk) {
-        copy_run(a, sq, gk, j0, j0, j1 - j0);
-        if (r == 0) copy_run(a, sq, gk, Ls, Ls, w);
+        copy_run<kThreads>(a, sq, gk, j0, j0, j1 - j0);
+        if (r == 0) copy_run<kThreads>(a, sq, gk, Ls, Ls, w);
       }
     }
     return;
@@ -351,7 +311,7 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const LayerArgs a) {
   if (r == 0) {  // the window is always kept, after the prefix tokens
     for (int i = tid; i < w; i += kThreads) out[nk + i] = (int32_t)(Ls + i);
     if (a.do_gather)
-      for (int gk = gk0; gk < gk1; ++gk) copy_run(a, sq, gk, nk, Ls, w);
+      for (int gk = gk0; gk < gk1; ++gk) copy_run<kThreads>(a, sq, gk, nk, Ls, w);
   }
   if (nk == 0) return;
   const uint32_t* ctl = sq.ctl + g * kCtlWords;
@@ -420,7 +380,7 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const LayerArgs a) {
         __syncthreads();
         const uint32_t m = n - r0 < (uint32_t)kCopyList ? n - r0 : (uint32_t)kCopyList;
         for (int gk = gk0; gk < gk1; ++gk)
-          copy_rows(a, sq, gk, m, [&](int64_t i) { return (int64_t)tok_l[i]; },
+          copy_rows<kThreads>(a, sq, gk, m, [&](int64_t i) { return (int64_t)tok_l[i]; },
                     [&](int64_t i) { return (int64_t)pos_l[i]; });
         __syncthreads();
       }
@@ -429,6 +389,11 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const LayerArgs a) {
     pos_carry += tot_sel;
   }
 }
+
+__global__ __launch_bounds__(kThreads) void compact_kernel(const LayerArgs a) {
+  compact_body(a, blockIdx.x);
+}
+
 
 // Standalone retain/evict (ckv_gather): rows idx[g, r] of K and V for the
 // kGatherRows output rows of this workgroup. An out-of-range index leaves its
@@ -448,7 +413,7 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const LayerArgs a) {
   const int32_t* idx = sq.idx + (a.shared ? 0 : (int64_t)g * sq.n_ret);
   for (int i = threadIdx.x; i < n; i += kThreads) tok_l[i] = idx[r0 + i];
   __syncthreads();
-  copy_rows(a, sq, g, n, [&](int64_t i) { return (int64_t)tok_l[i]; },
+  copy_rows<kThreads>(a, sq, g, n, [&](int64_t i) { return (int64_t)tok_l[i]; },
             [&](int64_t i) { return r0 + i; });
 }
 
@@ -477,5 +442,8 @@ hipError_t launch_compact(const LayerArgs& a, int grid, hipStream_t st, const Ti
 hipError_t launch_gather(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm) {
   return launch(gather_kernel, grid, kThreads, st, tm, a);
 }
+
+
+
 
 }  // namespace ckv

@@ -1,8 +1,10 @@
-"""GPU parity of ckv_compress_stack (the whole path over a stack of layers,
-with the selection of layer l on a side stream beside the K passes of layer
-l+1): every layer's scores, indices and compact K/V equal those of
-ckv_compress_layer on the same inputs bit for bit, with and without the side
-stream, and match the fp64 oracle under the rules in tests/parity.py."""
+"""GPU parity of ckv_compress_stack (the whole path over a stack of layers:
+the K passes layer by layer, the selection stages in launches that cover a
+batch of layers, on a side stream beside the next batch's K passes or on the
+same stream): every layer's scores, indices and compact K/V equal those of
+ckv_compress_layer on the same inputs bit for bit, for several batch sizes
+with and without the side stream, and match the fp64 oracle under the rules
+in tests/parity.py."""
 import numpy as np
 import pytest
 import torch
@@ -36,10 +38,13 @@ def _outputs(desc, layer_inputs):
     return out
 
 
-def _run_stack(desc, layer_inputs, dev, side):
+def _run_stack(desc, layer_inputs, dev, side, slots=None):
+    """ckv_compress_stack with `slots` layer slots of workspace (default: the
+    fewest the schedule accepts; more slots mean larger selection batches)."""
     seqs = _outputs(desc, layer_inputs)
     one = ckv.ckv_workspace_bytes(desc, seqs[0])
-    ws = torch.empty((2 if side else 1) * one, dtype=torch.uint8, device=dev)
+    slots = slots if slots is not None else (2 if side else 1)
+    ws = torch.empty(slots * one + 100, dtype=torch.uint8, device=dev)
     masks = np.stack([li[0] for li in layer_inputs])
     side_stream = torch.cuda.Stream() if side else None
     ckv.ckv_compress_stack(desc, masks, seqs, ws, torch.cuda.current_stream(), side_stream)
@@ -69,8 +74,11 @@ def _as_dict(s):
                 v_out=s.v_out.cpu())
 
 
-@pytest.mark.parametrize("side", [True, False], ids=["side-stream", "one-stream"])
-def test_small_stack_matches_layer_calls_and_oracle(dev, side):
+@pytest.mark.parametrize("side,slots", [(True, 2), (False, 1), (False, 2), (False, 5),
+                                        (True, 4), (True, 10)],
+                         ids=["side-batch1", "one-batch1", "one-batch2-ragged", "one-batch5",
+                              "side-batch2-ragged", "side-batch5"])
+def test_small_stack_matches_layer_calls_and_oracle(dev, side, slots):
     case = Case(16, 4, 128, 32, "max", 7, torch.bfloat16)
     lens = (3000, 1100)
     # per-layer budgets per prompt: ordinary, the window alone, keep-all,
@@ -88,7 +96,7 @@ def test_small_stack_matches_layer_calls_and_oracle(dev, side):
             vs.append(v.to(dev))
         layer_inputs.append((mask, qs, ks, vs, bl))
     desc = case.desc()
-    got = _run_stack(desc, layer_inputs, dev, side)
+    got = _run_stack(desc, layer_inputs, dev, side, slots)
     ref = _run_layers(desc, layer_inputs, dev)
     _assert_same(got, ref, "stack vs layer calls")
     for l, (mask, qs, ks, vs, bl) in enumerate(layer_inputs):
@@ -116,6 +124,9 @@ def test_full_size_stack_128k(dev):
         layer_inputs.append((inp.mask, inp.q_win, inp.k, inp.v, [int(budgets[l])]))
     desc = case.desc()
     print("stack of 4 layers at L=131072", flush=True)
+    got = _run_stack(desc, layer_inputs, dev, False, slots=4)
+    ref = _run_layers(desc, layer_inputs, dev)
+    _assert_same(got, ref, "128k stack (one batch) vs layer calls")
     got = _run_stack(desc, layer_inputs, dev, True)
     ref = _run_layers(desc, layer_inputs, dev)
     _assert_same(got, ref, "128k stack vs layer calls")
@@ -145,3 +156,41 @@ def test_stack_rejects_a_bad_layer_before_launching(dev):
     torch.cuda.synchronize()
     for layer in seqs:  # nothing was launched: the sentinels are intact
         assert bool((layer[0].idx == -7).all()) and bool((layer[0].scores == -1.0).all())
+
+
+def test_stack_ties_long_prompts_and_big_budgets(dev):
+    # The stack's selection (one workgroup per layer and KV head) against the
+    # per-layer kernels and the oracle where its rarer paths run:
+    #   layer 0: constant keys, so every prefix score ties; the threshold bin
+    #            holds all 139968 keys and is ranked by histogram passes down
+    #            to the exact key, and the lowest indices win;
+    #   layer 1: random keys with a budget of 20000 (kept rows copied in many
+    #            rounds), the output in two 131072-token segments;
+    #   layer 2: constant keys plus a planted high-scoring span, so the span
+    #            is kept and the remaining slots go to the lowest indices.
+    case = Case(8, 2, 128, 32, "max", 7, torch.bfloat16)
+    L = 140000
+    layer_inputs = []
+    for l, budget in enumerate((10032, 20000, 6000)):
+        q, k, v, mask = random_inputs(case, L, seed=900 + l, device="cpu", n_sel=2)
+        if l != 1:
+            k = k[:, :1, :].expand(-1, L, -1).contiguous()
+        if l == 2:
+            G = case.H // case.n_kv
+            for g in range(case.n_kv):
+                qbar = q[g * G:(g + 1) * G].float().mean(dim=(0, 1))
+                k[g, 50000:50400] = (k[g, 50000:50400].float()
+                                     + 4.0 * qbar / qbar.norm() ** 2 * case.d ** 0.5).to(k.dtype)
+        layer_inputs.append((mask, [q.to(dev)], [k.to(dev)], [v.to(dev)], [budget]))
+    desc = case.desc()
+    print("stack of 3 layers at L=140000", flush=True)
+    got = _run_stack(desc, layer_inputs, dev, False, slots=3)
+    ref = _run_layers(desc, layer_inputs, dev)
+    _assert_same(got, ref, "ties/long stack vs layer calls")
+    for l, (mask, qs, ks, vs, bl) in enumerate(layer_inputs):
+        g = l % case.n_kv
+        k_cpu = ks[0].cpu()
+        rs, ri = oracle_group(case, mask, qs[0].cpu(), k_cpu, g, bl[0])
+        check_group(case, _as_dict(got[l][0]), g, rs, ri, k_cpu, vs[0].cpu(), "ties layer %d" % l)
+    # the tie rule itself: with constant keys the kept prefix is 0..n_keep-1
+    assert np.array_equal(got[0][0].idx.cpu().numpy()[0, :10000], np.arange(10000))

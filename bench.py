@@ -41,6 +41,9 @@ def parse():
     p.add_argument("--workload", default="llama8b-128k-stack")
     p.add_argument("--layers", type=int, default=0, help="limit the layer count (0 = all)")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-profile-variant", action="store_true",
+                   help="skip the timing of the layer-error profile (decode attention over the "
+                        "full and the compact cache, W_O projection)")
     p.add_argument("--no-lse-variant", action="store_true",
                    help="skip the second measurement, with the window rows' log-sum-exp supplied "
                         "by the caller (one pass over K)")
@@ -567,9 +570,64 @@ def main():
             "path_hbm_frac": path_bytes / (ms_lse / 1e3) / 1e9 / HBM_PEAK_GBS,
             "score_kernel_avg_us": stage_lse["score"] * 1e3}
 
+    if not args.no_profile_variant:
+        result["error_profile"] = error_profile(args, wl, layers, dev, hip)
+
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_threads)
     print(json.dumps(result), flush=True)
+
+
+def error_profile(args, wl, layers, dev, hip, T: int = 16, n_layers: int = 8, reps: int = 3):
+    """Time ckv_layer_error (Eq. 6-8) on the first layers of the workload: T
+    synthetic decode queries per layer, attention over the full prompt cache and
+    over the compact cache the timed step just wrote, a random W_O of the model's
+    shape (D = H * d). Bytes: K and V of the full cache read once, the compact
+    cache, and W_O."""
+    import numpy as np
+    import torch
+
+    import paper_2508_02401_amd as ckv
+
+    n_layers = min(n_layers, len(layers))
+    H, n_kv, d = wl.num_q_heads, wl.num_kv_heads, wl.head_dim
+    D = H * d
+    desc = ckv.attn_desc(H, n_kv, d, wl.dtype)
+    gen = torch.Generator(device=dev).manual_seed(7)
+    q_dec = torch.randn((T, H, d), generator=gen, device=dev).to(wl.dtype)
+    w_o = (torch.randn((D, H * d), generator=gen, device=dev) / float(np.sqrt(H * d))).to(wl.dtype)
+    jobs = []
+    for mask, seqs in layers[:n_layers]:
+        sq = seqs[0]
+        full, comp = ckv.kv_cache(sq.k, sq.v), ckv.kv_cache(sq.k_out, sq.v_out)
+        jobs.append((full, comp, sq.k.shape[1], sq.k_out.shape[1]))
+    ws = torch.empty(max(ckv.ckv_layer_error_workspace_bytes(desc, T, n, nc, D) for _, _, n, nc in jobs),
+                     dtype=torch.uint8, device=dev)
+    ratio = torch.empty((n_layers, T), dtype=torch.float32, device=dev)
+    e = torch.empty(n_layers, dtype=torch.float32, device=dev)
+
+    def run():
+        for i, (full, comp, _, _) in enumerate(jobs):
+            ckv.ckv_layer_error(desc, q_dec, full, comp, w_o, 1e-6, ratio[i], e[i:i + 1], ws)
+
+    run()
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(reps):
+        run()
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / (reps * n_layers)
+    elt = torch.tensor([], dtype=wl.dtype).element_size()
+    n, nc = jobs[0][2], jobs[0][3]
+    bytes_layer = 2 * n_kv * (n + nc) * d * elt + D * H * d * elt
+    return {"what": "ckv_layer_error per layer: decode attention of %d synthetic queries over the "
+                    "full %d-token cache and the compact cache, W_O [%d x %d] projection, ratios "
+                    "(Eq. 6-8); %d layers x %d reps" % (T, n, D, H * d, n_layers, reps),
+            "ms_per_layer": ms, "hbm_gbs": bytes_layer / (ms / 1e3) / 1e9,
+            "hbm_frac": bytes_layer / (ms / 1e3) / 1e9 / HBM_PEAK_GBS,
+            "e_first_layers": [float(x) for x in e.cpu()]}
 
 
 def cpu_baseline(wl, threads: int, min_seconds: float = 10.0):

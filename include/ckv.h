@@ -223,6 +223,66 @@ int ckv_compress_stack(const ckv_layer_desc *desc, int32_t n_layers, const uint8
 int ckv_allocate_budgets(const double *err_norm, int32_t n_layers, int64_t total, int32_t m,
                          int32_t M, int32_t *out);
 
+/* ---- compression-error profile (paper Sec. 3.4) -------------------------
+ * The per-layer errors that Algorithm 1 allocates by: decode attention of T
+ * query tokens over the full cache and over the compressed one (Eq. 3-4 for
+ * one query row per head, Eq. 2's softmax over every cached key), the
+ * attention outputs of all heads concatenated head-major and projected by
+ * W_O, and per decoding step t the ratio
+ *   || W_O (A_comp,t - A_full,t) || / (|| W_O A_full,t || + eps)      (Eq. 6-8)
+ * summed over the steps. Everything accumulates in fp32. */
+typedef struct {
+  int32_t num_q_heads;  /* H; head h reads KV head h / (H / n_kv) */
+  int32_t num_kv_heads;
+  int32_t head_dim;     /* 64 or 128 */
+  int32_t dtype;        /* ckv_dtype of queries, caches and W_O */
+  float scale;          /* <= 0 selects 1/sqrt(head_dim) */
+  int32_t reserved;
+} ckv_attn_desc;
+
+/* One KV cache [n_kv][n][d] (d contiguous; pointers 16-byte aligned, strides in
+ * elements and multiples of 16 bytes), e.g. a prompt's cache or the compact
+ * cache ckv_compress_layer wrote (then n = min(B, L), stride_tok = d,
+ * stride_head = n * d). */
+typedef struct {
+  const void *k;
+  const void *v;
+  int64_t stride_head;
+  int64_t stride_tok;
+  int64_t n;  /* cached tokens, >= 1 */
+} ckv_kv_cache;
+
+/* Workspace of ckv_decode_attention for T query tokens over n cached tokens
+ * (0 on invalid input). */
+size_t ckv_decode_workspace_bytes(const ckv_attn_desc *desc, int32_t T, int64_t n);
+
+/* out[t][h][:] (fp32, [T][H][d] contiguous) = softmax over the n cached keys
+ * of scale * <q[t][h], k[g][j]> applied to v[g][j], g = h / (H / n_kv).
+ * q: token t, head h at q + t * q_stride_t + h * q_stride_h (elements; d
+ * contiguous). Needs (H / n_kv) * T <= 128. Asynchronous on stream. */
+int ckv_decode_attention(const ckv_attn_desc *desc, const void *q, int64_t q_stride_t,
+                         int64_t q_stride_h, int32_t T, const ckv_kv_cache *cache, float *out,
+                         void *workspace, size_t workspace_bytes, void *stream);
+
+/* Workspace of ckv_layer_error (0 on invalid input). */
+size_t ckv_layer_error_workspace_bytes(const ckv_attn_desc *desc, int32_t T, int64_t n_full,
+                                       int64_t n_comp, int32_t D);
+
+/* One layer's error (Eq. 6-8) for T decoding steps with queries q (as in
+ * ckv_decode_attention): W_O is [D][H*d] (row r at w_o + r * w_o_stride,
+ * dtype of desc), eps the paper's 1e-6 or any >= 0. Writes ratio[T] (the
+ * per-step terms) and e[0] (their sum), both fp32 device memory. */
+int ckv_layer_error(const ckv_attn_desc *desc, const void *q, int64_t q_stride_t,
+                    int64_t q_stride_h, int32_t T, const ckv_kv_cache *full,
+                    const ckv_kv_cache *comp, const void *w_o, int64_t w_o_stride, int32_t D,
+                    float eps, float *ratio, float *e, void *workspace, size_t workspace_bytes,
+                    void *stream);
+
+/* Eq. 10-12 on the host: e [n_sets][n_layers] (each set's layer errors, > 0
+ * in sum) -> e_tilde [n_layers]: every set normalised to sum 1, the sets
+ * averaged, the average normalised to sum 1. CKV_OK or CKV_ERR_INVALID_ARG. */
+int ckv_normalize_errors(const double *e, int32_t n_sets, int32_t n_layers, double *e_tilde);
+
 /* Static description of a status code. */
 const char *ckv_status_string(int status);
 

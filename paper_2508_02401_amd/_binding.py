@@ -34,7 +34,9 @@ CKV_MAX_SEQS = 16
 
 EXPORTED = ("ckv_workspace_bytes", "ckv_score", "ckv_select", "ckv_gather", "ckv_compress_layer",
             "ckv_compress_stack", "ckv_allocate_budgets", "ckv_status_string",
-            "ckv_last_hip_error", "ckv_set_stage_events", "ckv_set_stack_stage_events")
+            "ckv_last_hip_error", "ckv_set_stage_events", "ckv_set_stack_stage_events",
+            "ckv_decode_workspace_bytes", "ckv_decode_attention", "ckv_layer_error_workspace_bytes",
+            "ckv_layer_error", "ckv_normalize_errors")
 
 _DTYPE_CODE = {torch.bfloat16: CKV_BF16, torch.float16: CKV_F16, torch.float32: CKV_F32}
 
@@ -55,6 +57,17 @@ class ckv_seq(ctypes.Structure):
                 ("reserved", ctypes.c_int32), ("scores", ctypes.c_void_p),
                 ("idx", ctypes.c_void_p), ("k_out", ctypes.c_void_p), ("v_out", ctypes.c_void_p),
                 ("lse", ctypes.c_void_p), ("lse_stride_head", ctypes.c_int64)]
+
+
+class ckv_attn_desc(ctypes.Structure):
+    _fields_ = [("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("scale", ctypes.c_float), ("reserved", ctypes.c_int32)]
+
+
+class ckv_kv_cache(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("stride_head", ctypes.c_int64),
+                ("stride_tok", ctypes.c_int64), ("n", ctypes.c_int64)]
 
 
 class CkvError(RuntimeError):
@@ -90,6 +103,21 @@ def load() -> ctypes.CDLL:
         lib.ckv_set_stack_stage_events.argtypes = [P(vp), P(vp), ctypes.c_int32]
         lib.ckv_allocate_budgets.argtypes = [P(ctypes.c_double), ctypes.c_int32, ctypes.c_int64,
                                              ctypes.c_int32, ctypes.c_int32, P(ctypes.c_int32)]
+        AD, KC = P(ckv_attn_desc), P(ckv_kv_cache)
+        lib.ckv_decode_workspace_bytes.argtypes = [AD, ctypes.c_int32, ctypes.c_int64]
+        lib.ckv_decode_workspace_bytes.restype = ctypes.c_size_t
+        lib.ckv_decode_attention.argtypes = [AD, vp, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
+                                             KC, vp, vp, ctypes.c_size_t, vp]
+        lib.ckv_layer_error_workspace_bytes.argtypes = [AD, ctypes.c_int32, ctypes.c_int64,
+                                                        ctypes.c_int64, ctypes.c_int32]
+        lib.ckv_layer_error_workspace_bytes.restype = ctypes.c_size_t
+        lib.ckv_layer_error.argtypes = [AD, vp, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, KC,
+                                        KC, vp, ctypes.c_int64, ctypes.c_int32, ctypes.c_float,
+                                        vp, vp, vp, ctypes.c_size_t, vp]
+        lib.ckv_normalize_errors.argtypes = [P(ctypes.c_double), ctypes.c_int32, ctypes.c_int32,
+                                             P(ctypes.c_double)]
+        for name in ("ckv_decode_attention", "ckv_layer_error", "ckv_normalize_errors"):
+            getattr(lib, name).restype = ctypes.c_int
         lib.ckv_status_string.argtypes = [ctypes.c_int]
         lib.ckv_status_string.restype = ctypes.c_char_p
         lib.ckv_last_hip_error.argtypes = []
@@ -325,3 +353,66 @@ def alloc_workspace(desc: ckv_layer_desc, seqs: Sequence[Seq], device) -> torch.
     if n == 0:
         raise CkvError(CKV_ERR_INVALID_ARG, "ckv_workspace_bytes")
     return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+# --------------------------------------------------------------------------
+# compression-error profile (decode attention, layer error, normalisation)
+# --------------------------------------------------------------------------
+def attn_desc(num_q_heads: int, num_kv_heads: int, head_dim: int,
+              dtype: torch.dtype = torch.bfloat16, scale: float = 0.0) -> ckv_attn_desc:
+    code = _DTYPE_CODE[dtype] if isinstance(dtype, torch.dtype) else int(dtype)
+    return ckv_attn_desc(num_q_heads, num_kv_heads, head_dim, code, scale, 0)
+
+
+def kv_cache(k: torch.Tensor, v: torch.Tensor) -> ckv_kv_cache:
+    """k, v [n_kv, n, d] with the same strides and d contiguous."""
+    if k.stride() != v.stride() or k.shape != v.shape or k.stride(2) != 1:
+        raise ValueError("k and v must be [n_kv, n, d] with equal strides, d contiguous")
+    return ckv_kv_cache(k.data_ptr(), v.data_ptr(), k.stride(0), k.stride(1), k.shape[1])
+
+
+def ckv_decode_workspace_bytes(desc: ckv_attn_desc, T: int, n: int) -> int:
+    return load().ckv_decode_workspace_bytes(ctypes.byref(desc), int(T), int(n))
+
+
+def ckv_decode_attention(desc: ckv_attn_desc, q: torch.Tensor, cache: ckv_kv_cache,
+                         out: torch.Tensor, workspace: torch.Tensor, stream=None) -> None:
+    """q [T, H, d] (d contiguous), out [T, H, d] fp32 contiguous."""
+    if out.dtype != torch.float32 or not out.is_contiguous():
+        raise ValueError("out must be contiguous fp32 [T, H, d]")
+    _check(load().ckv_decode_attention(ctypes.byref(desc), q.data_ptr(), q.stride(0), q.stride(1),
+                                       q.shape[0], ctypes.byref(cache), out.data_ptr(),
+                                       workspace.data_ptr(),
+                                       workspace.numel() * workspace.element_size(),
+                                       _stream(stream)), "ckv_decode_attention")
+
+
+def ckv_layer_error_workspace_bytes(desc: ckv_attn_desc, T: int, n_full: int, n_comp: int,
+                                    D: int) -> int:
+    return load().ckv_layer_error_workspace_bytes(ctypes.byref(desc), int(T), int(n_full),
+                                                  int(n_comp), int(D))
+
+
+def ckv_layer_error(desc: ckv_attn_desc, q: torch.Tensor, full: ckv_kv_cache, comp: ckv_kv_cache,
+                    w_o: torch.Tensor, eps: float, ratio: torch.Tensor, e: torch.Tensor,
+                    workspace: torch.Tensor, stream=None) -> None:
+    """q [T, H, d]; w_o [D, H*d] (rows contiguous); ratio [T] and e [1] fp32 on the device."""
+    if w_o.stride(1) != 1:
+        raise ValueError("w_o rows must be contiguous")
+    _check(load().ckv_layer_error(ctypes.byref(desc), q.data_ptr(), q.stride(0), q.stride(1),
+                                  q.shape[0], ctypes.byref(full), ctypes.byref(comp),
+                                  w_o.data_ptr(), w_o.stride(0), w_o.shape[0], float(eps),
+                                  ratio.data_ptr(), e.data_ptr(), workspace.data_ptr(),
+                                  workspace.numel() * workspace.element_size(), _stream(stream)),
+           "ckv_layer_error")
+
+
+def ckv_normalize_errors(e) -> np.ndarray:
+    """Eq. 10-12 on the host: e [n_sets, n_layers] -> e_tilde [n_layers] (float64)."""
+    a = np.ascontiguousarray(np.atleast_2d(np.asarray(e, dtype=np.float64)))
+    out = np.zeros(a.shape[1], dtype=np.float64)
+    _check(load().ckv_normalize_errors(a.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
+                                       a.shape[0], a.shape[1],
+                                       out.ctypes.data_as(ctypes.POINTER(ctypes.c_double))),
+           "ckv_normalize_errors")
+    return out

@@ -619,6 +619,188 @@ int ckv_allocate_budgets(const double* err_norm, int32_t n_layers, int64_t total
   return delta == 0 ? CKV_OK : CKV_ERR_BUDGET;
 }
 
+// ---- compression-error profile ---------------------------------------------
+namespace {
+
+constexpr int kDecodeTargetWgs = 512;  // decode workgroups over all KV heads
+constexpr int kDecodeSlotsPerChunk = 4;
+
+int check_attn(const ckv_attn_desc* d, int32_t T) {
+  if (!d || d->num_q_heads < 1 || d->num_kv_heads < 1 || d->num_q_heads % d->num_kv_heads)
+    return CKV_ERR_INVALID_ARG;
+  if (d->head_dim != 64 && d->head_dim != 128) return CKV_ERR_UNSUPPORTED;
+  if (d->dtype != CKV_BF16 && d->dtype != CKV_F16 && d->dtype != CKV_F32) return CKV_ERR_UNSUPPORTED;
+  if (!(d->scale > 0.f) && !(d->scale <= 0.f)) return CKV_ERR_INVALID_ARG;
+  if (isinf(d->scale)) return CKV_ERR_INVALID_ARG;
+  if (T < 1) return CKV_ERR_INVALID_ARG;
+  if ((int64_t)(d->num_q_heads / d->num_kv_heads) * T > 128) return CKV_ERR_UNSUPPORTED;
+  return CKV_OK;
+}
+
+int check_cache(const ckv_attn_desc* d, const ckv_kv_cache* c) {
+  const int64_t eb = elt_bytes(d->dtype);
+  if (!c || !c->k || !c->v || !aligned16(c->k) || !aligned16(c->v) || c->n < 1 ||
+      c->n >= ((int64_t)1 << 31))
+    return CKV_ERR_INVALID_ARG;
+  if (c->stride_tok < d->head_dim || c->stride_head < 0 || (c->stride_tok * eb) % 16 ||
+      (c->stride_head * eb) % 16)
+    return CKV_ERR_INVALID_ARG;
+  return CKV_OK;
+}
+
+int check_q(const ckv_attn_desc* d, const void* q, int64_t st, int64_t sh, int32_t T) {
+  const int64_t eb = elt_bytes(d->dtype);
+  if (!q || !aligned16(q) || st < 0 || sh < 0 || (st * eb) % 16 || (sh * eb) % 16)
+    return CKV_ERR_INVALID_ARG;
+  if (d->num_q_heads > 1 && sh < d->head_dim) return CKV_ERR_INVALID_ARG;
+  if (T > 1 && st < d->head_dim) return CKV_ERR_INVALID_ARG;
+  return CKV_OK;
+}
+
+// Chunks of the cache per KV head: about kDecodeTargetWgs workgroups in all,
+// each at least one 32-token block.
+int64_t decode_chunks(const ckv_attn_desc* d, int64_t n) {
+  int64_t c = ceil_div(kDecodeTargetWgs, d->num_kv_heads);
+  const int64_t blocks = ceil_div(n, 32);
+  return c < blocks ? c : blocks;
+}
+
+size_t decode_part_bytes(const ckv_attn_desc* d, int64_t n) {
+  return align_up((size_t)d->num_kv_heads * decode_chunks(d, n) * kDecodeSlotsPerChunk * 128 *
+                  (d->head_dim + 2) * sizeof(float));
+}
+
+void decode_args(const ckv_attn_desc* d, const void* q, int64_t st, int64_t sh, int32_t T,
+                 const ckv_kv_cache* c, float* out, void* ws, ckv::DecodeArgs& a) {
+  a.q = q;
+  a.q_st = st;
+  a.q_sh = sh;
+  a.k = c->k;
+  a.v = c->v;
+  a.kv_sh = c->stride_head;
+  a.kv_st = c->stride_tok;
+  a.n = c->n;
+  a.out = out;
+  a.part = static_cast<float*>(ws);
+  a.H = d->num_q_heads;
+  a.n_kv = d->num_kv_heads;
+  a.d = d->head_dim;
+  a.T = T;
+  a.n_chunks = (int32_t)decode_chunks(d, c->n);
+  a.chunk = (int32_t)(ceil_div(ceil_div(c->n, a.n_chunks), 32) * 32);
+  a.n_chunks = (int32_t)ceil_div(c->n, a.chunk);
+  a.n_slots = a.n_chunks * kDecodeSlotsPerChunk;
+  const float scale = d->scale > 0.f ? d->scale : 1.0f / sqrtf((float)d->head_dim);
+  a.alpha = (float)((double)scale * 1.4426950408889634);
+}
+
+}  // namespace
+
+size_t ckv_decode_workspace_bytes(const ckv_attn_desc* desc, int32_t T, int64_t n) {
+  if (check_attn(desc, T) != CKV_OK || n < 1 || n >= ((int64_t)1 << 31)) return 0;
+  return decode_part_bytes(desc, n);
+}
+
+int ckv_decode_attention(const ckv_attn_desc* desc, const void* q, int64_t q_stride_t,
+                         int64_t q_stride_h, int32_t T, const ckv_kv_cache* cache, float* out,
+                         void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_attn(desc, T);
+  if (rc != CKV_OK) return rc;
+  if ((rc = check_q(desc, q, q_stride_t, q_stride_h, T)) != CKV_OK) return rc;
+  if ((rc = check_cache(desc, cache)) != CKV_OK) return rc;
+  if (!out || ((uintptr_t)out & 3u)) return CKV_ERR_INVALID_ARG;
+  if (!workspace || !aligned16(workspace) ||
+      workspace_bytes < ckv_decode_workspace_bytes(desc, T, cache->n))
+    return CKV_ERR_WORKSPACE;
+  ckv::DecodeArgs a;
+  decode_args(desc, q, q_stride_t, q_stride_h, T, cache, out, workspace, a);
+  const hipError_t e = ckv::launch_decode(desc->dtype, a, (hipStream_t)stream);
+  return e == hipSuccess ? CKV_OK : hip_fail(e);
+}
+
+size_t ckv_layer_error_workspace_bytes(const ckv_attn_desc* desc, int32_t T, int64_t n_full,
+                                       int64_t n_comp, int32_t D) {
+  if (check_attn(desc, T) != CKV_OK || D < 1 || n_full < 1 || n_comp < 1 ||
+      n_full >= ((int64_t)1 << 31) || n_comp >= ((int64_t)1 << 31))
+    return 0;
+  const size_t outs = align_up((size_t)T * desc->num_q_heads * desc->head_dim * sizeof(float));
+  const size_t pa = decode_part_bytes(desc, n_full), pb = decode_part_bytes(desc, n_comp);
+  const size_t proj = align_up((size_t)(ceil_div(D, 32) + 1) * 2 * T * sizeof(float));
+  return 2 * outs + (pa > pb ? pa : pb) + proj;
+}
+
+int ckv_layer_error(const ckv_attn_desc* desc, const void* q, int64_t q_stride_t,
+                    int64_t q_stride_h, int32_t T, const ckv_kv_cache* full,
+                    const ckv_kv_cache* comp, const void* w_o, int64_t w_o_stride, int32_t D,
+                    float eps, float* ratio, float* e, void* workspace, size_t workspace_bytes,
+                    void* stream) {
+  int rc = check_attn(desc, T);
+  if (rc != CKV_OK) return rc;
+  if ((rc = check_q(desc, q, q_stride_t, q_stride_h, T)) != CKV_OK) return rc;
+  if ((rc = check_cache(desc, full)) != CKV_OK || (rc = check_cache(desc, comp)) != CKV_OK)
+    return rc;
+  const int64_t K = (int64_t)desc->num_q_heads * desc->head_dim;
+  const int64_t eb = elt_bytes(desc->dtype);
+  if (!w_o || !aligned16(w_o) || D < 1 || w_o_stride < K || (w_o_stride * eb) % 16)
+    return CKV_ERR_INVALID_ARG;
+  if (!(eps >= 0.f) || isinf(eps)) return CKV_ERR_INVALID_ARG;
+  if (!ratio || !e || ((uintptr_t)ratio & 3u) || ((uintptr_t)e & 3u)) return CKV_ERR_INVALID_ARG;
+  if (!workspace || !aligned16(workspace) ||
+      workspace_bytes < ckv_layer_error_workspace_bytes(desc, T, full->n, comp->n, D))
+    return CKV_ERR_WORKSPACE;
+  char* ws = static_cast<char*>(workspace);
+  const size_t outs = align_up((size_t)T * K * sizeof(float));
+  float* a_full = reinterpret_cast<float*>(ws);
+  float* a_comp = reinterpret_cast<float*>(ws + outs);
+  char* part = ws + 2 * outs;
+  const size_t pa = decode_part_bytes(desc, full->n), pb = decode_part_bytes(desc, comp->n);
+  float* proj = reinterpret_cast<float*>(part + (pa > pb ? pa : pb));
+  const hipStream_t st = (hipStream_t)stream;
+  ckv::DecodeArgs da;
+  hipError_t err;
+  decode_args(desc, q, q_stride_t, q_stride_h, T, full, a_full, part, da);
+  if ((err = ckv::launch_decode(desc->dtype, da, st)) != hipSuccess) return hip_fail(err);
+  decode_args(desc, q, q_stride_t, q_stride_h, T, comp, a_comp, part, da);
+  if ((err = ckv::launch_decode(desc->dtype, da, st)) != hipSuccess) return hip_fail(err);
+  ckv::ErrorArgs ea;
+  ea.a_full = a_full;
+  ea.a_comp = a_comp;
+  ea.w = w_o;
+  ea.w_stride = w_o_stride;
+  ea.T = T;
+  ea.D = D;
+  ea.K = K;
+  ea.eps = eps;
+  ea.part = proj;
+  ea.ratio = ratio;
+  ea.e = e;
+  if ((err = ckv::launch_error(desc->dtype, ea, st)) != hipSuccess) return hip_fail(err);
+  return CKV_OK;
+}
+
+int ckv_normalize_errors(const double* e, int32_t n_sets, int32_t n_layers, double* e_tilde) {
+  if (!e || !e_tilde || n_sets < 1 || n_layers < 1) return CKV_ERR_INVALID_ARG;
+  // every profiling set's errors as fractions of that set's total, the
+  // fractions averaged over the sets, and the averages as fractions of
+  // their own total
+  double* acc = e_tilde;
+  for (int32_t l = 0; l < n_layers; ++l) acc[l] = 0.0;
+  for (int32_t s = 0; s < n_sets; ++s) {
+    const double* row = e + (int64_t)s * n_layers;
+    double total = 0.0;
+    for (int32_t l = 0; l < n_layers; ++l) {
+      if (!isfinite(row[l]) || row[l] < 0.0) return CKV_ERR_INVALID_ARG;
+      total += row[l];
+    }
+    if (!(total > 0.0)) return CKV_ERR_INVALID_ARG;
+    for (int32_t l = 0; l < n_layers; ++l) acc[l] += (row[l] / total) / (double)n_sets;
+  }
+  double total = 0.0;
+  for (int32_t l = 0; l < n_layers; ++l) total += acc[l];
+  for (int32_t l = 0; l < n_layers; ++l) e_tilde[l] = acc[l] / total;
+  return CKV_OK;
+}
+
 const char* ckv_status_string(int status) {
   switch (status) {
     case CKV_OK: return "ok";

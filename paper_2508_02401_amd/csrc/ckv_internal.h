@@ -142,6 +142,37 @@ struct MultiArgs {
   int32_t n_layers;
 };
 
+// Decode attention of T query tokens over one KV cache (layer-error profile).
+struct DecodeArgs {
+  const void* q;           // [T][H][d]: token t, head h at t * q_st + h * q_sh
+  int64_t q_st, q_sh;
+  const void* k;           // [n_kv][n][d]
+  const void* v;
+  int64_t kv_sh, kv_st;
+  int64_t n;               // cached tokens
+  float* out;              // [T][H][d] fp32
+  float* part;             // [n_kv][n_slots][128][d + 2]: O rows, then (max, sum)
+  int32_t H, n_kv, d, T;
+  int32_t chunk;           // cached tokens per workgroup
+  int32_t n_chunks;
+  int32_t n_slots;         // partial slots per KV head: n_chunks * 4
+  float alpha;             // logit scale * log2(e)
+};
+
+// W_O projection and error ratios of one layer.
+struct ErrorArgs {
+  const float* a_full;     // [T][K] decode outputs with the full cache (K = H * d)
+  const float* a_comp;     // [T][K] with the compressed cache
+  const void* w;           // [D][K] W_O, row r at r * w_stride
+  int64_t w_stride;
+  int32_t T, D;
+  int64_t K;
+  float eps;
+  float* part;             // [ceil(D / 32) + 1][2T]: column sums of Y^2 per 32 rows, then in all
+  float* ratio;            // [T]
+  float* e;                // [1]
+};
+
 // Optional timing of one launch: start receives the kernel's start time and
 // stop its end time (hipExtLaunchKernel events, which add no marker packets to
 // the stream). Either may be null.
@@ -166,6 +197,10 @@ hipError_t launch_gather(const LayerArgs& a, int grid, hipStream_t st, const Tim
 // selection unit (layer, prompt, selection group), one workgroup each
 // (per_layer = prompts * selection groups)
 hipError_t launch_pool_units(const MultiArgs& m, hipStream_t st, const Timing& tm);
+// decode attention (partials, then their merge into a.out) and the error
+// ratios (projection partials, then the ratios and their sum)
+hipError_t launch_decode(int dtype, const DecodeArgs& a, hipStream_t st);
+hipError_t launch_error(int w_dtype, const ErrorArgs& a, hipStream_t st);
 hipError_t launch_select_units(const MultiArgs& m, hipStream_t st, const Timing& tm);
 
 }  // namespace ckv

@@ -385,3 +385,94 @@ def test_lse_binding_rejects_wrong_layout():
     s = ckv.Seq(None, None, None, 16, lse=torch.zeros(8, 4).t())
     with pytest.raises(ValueError):
         ckv._binding._seq_array([s])
+
+
+# ---- compression-error profile: host normalisation and validation ----------
+@pytest.mark.parametrize("seed", range(8))
+def test_normalize_errors_matches_oracle(seed):
+    rng = np.random.default_rng(seed)
+    e = rng.random((int(rng.integers(1, 5)), int(rng.integers(1, 40)))) + 1e-3
+    np.testing.assert_allclose(ckv.ckv_normalize_errors(e), oracle.normalize_errors(e),
+                               rtol=1e-13, atol=0)
+
+
+@pytest.mark.parametrize("bad", [np.zeros((2, 3)), np.array([[1.0, -1.0, 0.5]]),
+                                 np.array([[1.0, np.nan]])])
+def test_normalize_errors_rejects(bad):
+    with pytest.raises(ckv.CkvError) as err:
+        ckv.ckv_normalize_errors(bad)
+    assert err.value.status == ckv.CKV_ERR_INVALID_ARG
+
+
+def _adesc(**kw):
+    base = dict(num_q_heads=8, num_kv_heads=2, head_dim=64, dtype=ckv.CKV_BF16, scale=0.0)
+    base.update(kw)
+    d = ckv._binding.ckv_attn_desc()
+    for k, v in base.items():
+        setattr(d, k, v)
+    return d
+
+
+def _cache(**kw):
+    c = ckv._binding.ckv_kv_cache()
+    vals = dict(k=_BASE + 4096, v=_BASE + 8192, stride_head=100 * 64, stride_tok=64, n=100)
+    vals.update(kw)
+    for k, v in vals.items():
+        setattr(c, k, v)
+    return c
+
+
+def _decode(desc, cache, T=4, q=_BASE, qst=8 * 64, qsh=64, out=_BASE + 12288, ws=True):
+    lib = ckv.load()
+    return lib.ckv_decode_attention(ctypes.byref(desc), q, qst, qsh, T, ctypes.byref(cache), out,
+                                    _BASE + 32768 if ws else None, 1 << 40 if ws else 0, None)
+
+
+@pytest.mark.parametrize("bad,expect", [
+    (dict(head_dim=96), ckv.CKV_ERR_UNSUPPORTED),
+    (dict(dtype=9), ckv.CKV_ERR_UNSUPPORTED),
+    (dict(num_q_heads=7), ckv.CKV_ERR_INVALID_ARG),
+    (dict(scale=float("inf")), ckv.CKV_ERR_INVALID_ARG),
+])
+def test_decode_bad_descriptor(bad, expect):
+    assert _decode(_adesc(**bad), _cache()) == expect
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(T=0), ckv.CKV_ERR_INVALID_ARG),
+    (dict(T=33), ckv.CKV_ERR_UNSUPPORTED),       # 4 heads per group x 33 tokens > 128 rows
+    (dict(q=None), ckv.CKV_ERR_INVALID_ARG),
+    (dict(q=_BASE + 8), ckv.CKV_ERR_INVALID_ARG),
+    (dict(qsh=32), ckv.CKV_ERR_INVALID_ARG),
+    (dict(out=None), ckv.CKV_ERR_INVALID_ARG),
+    (dict(ws=False), ckv.CKV_ERR_WORKSPACE),
+])
+def test_decode_bad_arguments(kw, expect):
+    assert _decode(_adesc(), _cache(), **kw) == expect
+
+
+@pytest.mark.parametrize("kw", [dict(n=0), dict(k=None), dict(v=_BASE + 8200), dict(stride_tok=32),
+                                dict(stride_tok=65), dict(n=1 << 31)])
+def test_decode_bad_cache(kw):
+    assert _decode(_adesc(), _cache(**kw)) == ckv.CKV_ERR_INVALID_ARG
+
+
+def test_layer_error_validation():
+    lib = ckv.load()
+    d = _adesc()
+    full, comp = _cache(), _cache(n=20, stride_head=20 * 64)
+
+    def call(w_o=_BASE + 16384, w_stride=8 * 64, D=256, eps=1e-6, ratio=_BASE + 20480,
+             e=_BASE + 24576, ws=True):
+        return lib.ckv_layer_error(ctypes.byref(d), _BASE, 8 * 64, 64, 4, ctypes.byref(full),
+                                   ctypes.byref(comp), w_o, w_stride, D, eps, ratio, e,
+                                   _BASE + 32768 if ws else None, 1 << 40 if ws else 0, None)
+    assert call(w_o=None) == ckv.CKV_ERR_INVALID_ARG
+    assert call(w_stride=8 * 64 - 8) == ckv.CKV_ERR_INVALID_ARG
+    assert call(D=0) == ckv.CKV_ERR_INVALID_ARG
+    assert call(eps=-1.0) == ckv.CKV_ERR_INVALID_ARG
+    assert call(ratio=None) == ckv.CKV_ERR_INVALID_ARG
+    assert call(e=_BASE + 24578) == ckv.CKV_ERR_INVALID_ARG
+    assert call(ws=False) == ckv.CKV_ERR_WORKSPACE
+    assert ckv.ckv_layer_error_workspace_bytes(d, 4, 100, 20, 256) > 0
+    assert ckv.ckv_layer_error_workspace_bytes(d, 0, 100, 20, 256) == 0

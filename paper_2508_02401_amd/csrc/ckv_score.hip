@@ -220,27 +220,33 @@ __device__ __forceinline__ void stage_loop(uint4* const* slot, const char* kbase
 
 // Operand-reading and MFMA part shared by both passes: the wave's blocks of a
 // stage are sub, sub + WPQ, ... (NB of them; the caller guarantees that they
-// lie inside the stage); acc[i] receives the 32x32 logit tile of block i,
-// queries x keys when KEYS_AS_ROWS is false, keys x queries otherwise. All
-// operands are read first and the NB accumulation chains are interleaved, so
-// the MFMA pipe never waits on a single dependent chain. Blocks past the
-// prompt are computed too (their LDS rows are clamped copies) and the caller
-// ignores them.
-template <int DT, class S, int WPQ, bool KEYS_AS_ROWS>
-__device__ __forceinline__ void stage_tiles(const uint4* slot, const int* opoff, const uint4* q,
-                                            f32x16* acc) {
+// lie inside the stage) and its NQ query blocks' operands are q[0..NQ);
+// acc[j][i] receives the 32x32 logit tile of query block j and key block i,
+// queries x keys when KEYS_AS_ROWS is false, keys x queries otherwise. Every
+// key operand is read from LDS once and used for all NQ query blocks, and the
+// NQ*NB accumulation chains are interleaved, so the MFMA pipe never waits on
+// a single dependent chain. Blocks past the prompt are computed too (their
+// LDS rows are clamped copies) and the caller ignores them.
+template <int DT, class S, int WPQ, int NQ, bool KEYS_AS_ROWS>
+__device__ __forceinline__ void stage_tiles(const uint4* slot, const int* opoff,
+                                            const uint4 (*q)[S::NC], f32x16 (*acc)[(S::BLOCKS + WPQ - 1) / WPQ]) {
   constexpr int NB = (S::BLOCKS + WPQ - 1) / WPQ;
   constexpr int NC = S::NC;
   uint4 kr[NB][NC];
 #pragma unroll
   for (int i = 0; i < NB; ++i) S::operand(slot, i * WPQ, opoff, kr[i]);
 #pragma unroll
-  for (int i = 0; i < NB; ++i) acc[i] = f32x16{};
+  for (int j = 0; j < NQ; ++j)
+#pragma unroll
+    for (int i = 0; i < NB; ++i) acc[j][i] = f32x16{};
 #pragma unroll
   for (int c = 0; c < NC; ++c)
 #pragma unroll
-    for (int i = 0; i < NB; ++i)
-      acc[i] = KEYS_AS_ROWS ? mfma_chunk<DT>(kr[i][c], q[c], acc[i]) : mfma_chunk<DT>(q[c], kr[i][c], acc[i]);
+    for (int j = 0; j < NQ; ++j)
+#pragma unroll
+      for (int i = 0; i < NB; ++i)
+        acc[j][i] = KEYS_AS_ROWS ? mfma_chunk<DT>(kr[i][c], q[j][c], acc[j][i])
+                                 : mfma_chunk<DT>(q[j][c], kr[i][c], acc[j][i]);
 }
 
 // Stages of workgroup p of P over n_tok tokens: p, p+P, ... (none if p is
@@ -277,99 +283,119 @@ __device__ __forceinline__ void kpass_locate(const LayerArgs& a, const SeqArgs& 
 // ---------------------------------------------------------------------------
 // Pass 1: row statistics.
 // ---------------------------------------------------------------------------
-template <int DT, int D, int WPQ, class S, int NS>
+template <int DT, int D, int WPQ, int NQ, class S, int NS>
 __device__ __forceinline__ void rowstats_body(const LayerArgs& a, const SeqArgs& sq, int g, int p,
                                               int P, int sel0, int n_sel, int nqb,
-                                              uint4* const* slots, float2 (*red)[32]) {
+                                              uint4* const* slots, float2 (*red)[2][32]) {
   constexpr int NC = S::NC;
   constexpr int NB = (S::BLOCKS + WPQ - 1) / WPQ;
   const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
-  const int qb = wave / WPQ, sub = wave % WPQ;
-  const bool active = qb < nqb;
+  const int qg = wave / WPQ, sub = wave % WPQ;  // query group: blocks qg*NQ .. qg*NQ+NQ-1
   const int w8 = a.w8;
   const int64_t L = sq.L, Ls = L - a.w;
   const int64_t stride = (int64_t)P * S::ST;
   const float alpha = a.alpha;
   const char* kbase = static_cast<const char*>(sq.k) + (int64_t)g * sq.kv_sh * S::EB;
   const int ns = stages_of(L, S::ST, p, P);
-  // this lane's query row (column of the MFMA result) and its last visible key
-  const int64_t last = Ls + (qb * 32 + l32) % w8;  // >= L for padding rows
+  const bool active = qg * NQ < nqb;
 
-  uint4 q[NC];
-  if (active) load_queries<NC, S::EB>(a, sq, sel0, n_sel, qb, l32, h, q);
+  // this lane's query row in each of its blocks (column of the MFMA result)
+  // and that row's last visible key
+  uint4 q[NQ][NC];
+  int64_t last[NQ];
+#pragma unroll
+  for (int j = 0; j < NQ; ++j) {
+    const int qb = qg * NQ + j;
+    last[j] = Ls + (qb * 32 + l32) % w8;  // >= L for padding rows
+    if (qb < nqb) load_queries<NC, S::EB>(a, sq, sel0, n_sel, qb, l32, h, q[j]);
+    else
+#pragma unroll
+      for (int c = 0; c < NC; ++c) q[j][c] = make_uint4(0u, 0u, 0u, 0u);
+  }
   int opoff[NC];
   S::operand_offsets(l32, h, opoff);
 #pragma unroll
   for (int c = 0; c < NC; ++c) opoff[c] += sub * 32 * S::ROWB;
-  float m_run = -INFINITY, z_run = 0.f;
+  float m_run[NQ], z_run[NQ];
+#pragma unroll
+  for (int j = 0; j < NQ; ++j) {
+    m_run[j] = -INFINITY;
+    z_run[j] = 0.f;
+  }
 
   stage_loop<S, NS>(slots, kbase, sq.kv_st, (int64_t)p * S::ST, stride, ns, 0, L - 1, wave,
                     [] {}, [&](const uint4* slot, int k) {
     // waves past the stage's blocks (4 waves on a 2-block stage) sit out
     if (!active || sub >= S::BLOCKS) return;
     const int64_t ts = (int64_t)p * S::ST + k * stride + sub * 32;  // this wave's first block
-    f32x16 acc[NB];
-    stage_tiles<DT, S, WPQ, true>(slot, opoff, q, acc);
+    f32x16 acc[NQ][NB];
+    stage_tiles<DT, S, WPQ, NQ, true>(slot, opoff, q, acc);
 #pragma unroll
-    for (int i = 0; i < NB; ++i) {
-      // acc[i][v]: key t0 + acc_row(v, h) of this lane's query row
-      const int64_t t0 = ts + i * WPQ * 32;
-      if (t0 + 32 > Ls) {  // keys inside the window or past the prompt: causal
-                           // mask (a uniform branch; blocks past L mask all)
-        const int64_t rel = last - t0;
-        const int lim = rel < -1 ? -1 : (rel > 32 ? 32 : (int)rel);
+    for (int j = 0; j < NQ; ++j) {
+      if (qg * NQ + j >= nqb) continue;  // a query block past the group's rows (uniform)
 #pragma unroll
-        for (int v = 0; v < 16; ++v)
-          if (acc_row(v, h) > lim) acc[i][v] = -INFINITY;
+      for (int i = 0; i < NB; ++i) {
+        // acc[j][i][v]: key t0 + acc_row(v, h) of this lane's query row
+        const int64_t t0 = ts + i * WPQ * 32;
+        if (t0 + 32 > Ls) {  // keys inside the window or past the prompt: causal
+                             // mask (a uniform branch; blocks past L mask all)
+          const int64_t rel = last[j] - t0;
+          const int lim = rel < -1 ? -1 : (rel > 32 ? 32 : (int)rel);
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            if (acc_row(v, h) > lim) acc[j][i][v] = -INFINITY;
+        }
+        float mx = acc[j][i][0];
+#pragma unroll
+        for (int v = 1; v < 16; ++v) mx = fmaxf(mx, acc[j][i][v]);
+        const float m_new = fmaxf(m_run[j], mx);
+        const float ms = m_new == -INFINITY ? 0.f : m_new * alpha;
+        float z = z_run[j] * fast_exp2(m_run[j] * alpha - ms);
+#pragma unroll
+        for (int v = 0; v < 16; ++v) z += fast_exp2(fmaf(acc[j][i][v], alpha, -ms));
+        z_run[j] = z;
+        m_run[j] = m_new;
       }
-      float mx = acc[i][0];
-#pragma unroll
-      for (int v = 1; v < 16; ++v) mx = fmaxf(mx, acc[i][v]);
-      const float m_new = fmaxf(m_run, mx);
-      const float ms = m_new == -INFINITY ? 0.f : m_new * alpha;
-      float z = z_run * fast_exp2(m_run * alpha - ms);
-#pragma unroll
-      for (int v = 0; v < 16; ++v) z += fast_exp2(fmaf(acc[i][v], alpha, -ms));
-      z_run = z;
-      m_run = m_new;
     }
   });
 
   // merge the two lane halves (same query row, different keys), then the
-  // waves that share this query block
-  {
-    const float mo = __shfl_xor(m_run, 32);
-    const float zo = __shfl_xor(z_run, 32);
-    const float mn = fmaxf(m_run, mo);
+  // waves that share the query group
+#pragma unroll
+  for (int j = 0; j < NQ; ++j) {
+    const float mo = __shfl_xor(m_run[j], 32);
+    const float zo = __shfl_xor(z_run[j], 32);
+    const float mn = fmaxf(m_run[j], mo);
     const float msn = mn == -INFINITY ? 0.f : mn * alpha;
-    const float z = z_run * fast_exp2(m_run * alpha - msn) + zo * fast_exp2(mo * alpha - msn);
-    if (h == 0) red[wave][l32] = make_float2(mn, z);
+    const float z = z_run[j] * fast_exp2(m_run[j] * alpha - msn) + zo * fast_exp2(mo * alpha - msn);
+    if (h == 0) red[wave][j][l32] = make_float2(mn, z);
   }
   __syncthreads();
   if (tid < nqb * 32) {
     const int qq = tid >> 5, r = tid & 31;
+    const int qgq = qq / NQ, jq = qq - qgq * NQ;
     float m = -INFINITY;
 #pragma unroll
-    for (int sw = 0; sw < WPQ; ++sw) m = fmaxf(m, red[qq * WPQ + sw][r].x);
+    for (int sw = 0; sw < WPQ; ++sw) m = fmaxf(m, red[qgq * WPQ + sw][jq][r].x);
     const float ms = m == -INFINITY ? 0.f : m * alpha;
     float z = 0.f;
 #pragma unroll
     for (int sw = 0; sw < WPQ; ++sw)
-      z += red[qq * WPQ + sw][r].y * fast_exp2(red[qq * WPQ + sw][r].x * alpha - ms);
+      z += red[qgq * WPQ + sw][jq][r].y * fast_exp2(red[qgq * WPQ + sw][jq][r].x * alpha - ms);
     sq.partial[((int64_t)g * sq.n_split + p) * kMaxRows + tid] = make_float2(m, z);
   }
 }
 
 template <int DT, int D>
-__global__ __launch_bounds__(kKpThreads) void rowstats_kernel(const LayerArgs a) {
+__global__ __launch_bounds__(kKpThreads) __attribute__((amdgpu_waves_per_eu(2))) void rowstats_kernel(const LayerArgs a) {
   using S = Stager<DT, D, stage_bytes<DT, D>()>;
   constexpr int NS = 4;  // 4-slot ring
   __shared__ uint4 slot0[S::VEC];
   __shared__ uint4 slot1[S::VEC];
   __shared__ uint4 slot2[S::VEC];
   __shared__ uint4 slot3[S::VEC];
-  __shared__ float2 red[kKpWaves][32];
+  __shared__ float2 red[kKpWaves][2][32];
   uint4* const slots[NS] = {slot0, slot1, slot2, slot3};
 
   const int b = blockIdx.x;
@@ -390,9 +416,14 @@ __global__ __launch_bounds__(kKpThreads) void rowstats_kernel(const LayerArgs a)
   if (n_sel == 0) return;  // a group without chosen heads (shared scope) is not read
   const int wpq = waves_per_qblock(nqb);
   constexpr int W1 = kKpWaves, W2 = kKpWaves / 2, W4 = kKpWaves / 4;
-  if (wpq == W4) rowstats_body<DT, D, W4, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, red);
-  else if (wpq == W2) rowstats_body<DT, D, W2, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, red);
-  else rowstats_body<DT, D, W1, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, red);
+  // 3-4 query blocks on a stage of 2+ key blocks: each wave takes two query
+  // blocks and half the key blocks, so every key operand is read from LDS by
+  // two waves instead of four
+  if (S::BLOCKS >= 2 && nqb >= 3)
+    rowstats_body<DT, D, 2, 2, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, red);
+  else if (wpq == W4) rowstats_body<DT, D, W4, 1, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, red);
+  else if (wpq == W2) rowstats_body<DT, D, W2, 1, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, red);
+  else rowstats_body<DT, D, W1, 1, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, red);
 }
 
 // Online merge of (max logit, sum of exp2) pairs in exp2 units.
@@ -414,8 +445,11 @@ constexpr int kMergeLanes = kKpThreads / kMaxRows;  // threads per row in the ls
 // QM (query-block mode, when w8 is a multiple of 32): every 32-row query
 // block belongs to one head, so a lane sums its four 8-row groups in
 // registers and the block's column sums are one row of gsum; otherwise
-// gsum holds one row per 8-row group.
-template <int DT, int D, int WPQ, bool QM, class S, int NS>
+// gsum holds one row per 8-row group. DIRECT > 0 (QM, every head's DIRECT
+// query blocks inside one wave's NQ): the wave adds its head's block sums in
+// registers, in the order the fold would, and stores the window sums itself,
+// so gsum and the fold are not used.
+template <int DT, int D, int WPQ, int NQ, bool QM, int DIRECT, class S, int NS>
 __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq, int g, int p,
                                            int P, int sel0, int n_sel, int nqb,
                                            uint4* const* slots, float* gsum) {
@@ -424,19 +458,26 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
   constexpr int ST = S::ST;
   const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
-  const int qb = wave / WPQ, sub = wave % WPQ;
-  const bool active = qb < nqb;
+  const int qg = wave / WPQ, sub = wave % WPQ;  // query group: blocks qg*NQ .. qg*NQ+NQ-1
+  const bool active = qg * NQ < nqb;
   const int64_t Ls = sq.L - a.w;
   const int64_t stride = (int64_t)P * ST;
   const float alpha = a.alpha;
   const char* kbase = static_cast<const char*>(sq.k) + (int64_t)g * sq.kv_sh * S::EB;
   const int ns = stages_of(Ls, ST, p, P);
 
-  uint4 q[NC];
-  if (active) load_queries<NC, S::EB>(a, sq, sel0, n_sel, qb, l32, h, q);
-  // lse of this lane's 16 result rows qb*32 + 8*a4 + 4*h + e, in exp2 units:
-  // merged from pass 1's per-workgroup partials while the first stages load
-  float4 cv[4];
+  uint4 q[NQ][NC];
+#pragma unroll
+  for (int j = 0; j < NQ; ++j) {
+    if (qg * NQ + j < nqb) load_queries<NC, S::EB>(a, sq, sel0, n_sel, qg * NQ + j, l32, h, q[j]);
+    else
+#pragma unroll
+      for (int c = 0; c < NC; ++c) q[j][c] = make_uint4(0u, 0u, 0u, 0u);
+  }
+  // lse of this lane's 16 result rows qb*32 + 8*a4 + 4*h + e of each of its
+  // query blocks qb, in exp2 units: merged from pass 1's per-workgroup
+  // partials while the first stages load
+  float4 cv[NQ][4];
   auto merge_lse = [&] {
     // kMergeLanes threads per row, thread j merging partials j, j + kMergeLanes,
     // ...; their results meet in LDS in a fixed order (the gsum buffers are
@@ -479,10 +520,13 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
     __syncthreads();
     if (active) {
 #pragma unroll
-      for (int a4 = 0; a4 < 4; ++a4) {
-        const float* src = lse_l + qb * 32 + 8 * a4 + 4 * h;
-        cv[a4] = make_float4(src[0], src[1], src[2], src[3]);
-      }
+      for (int j = 0; j < NQ; ++j)
+#pragma unroll
+        for (int a4 = 0; a4 < 4; ++a4) {
+          // rows of a block past nqb are padding (+inf) and never used
+          const float* src = lse_l + (qg * NQ + j) * 32 + 8 * a4 + 4 * h;
+          cv[j][a4] = make_float4(src[0], src[1], src[2], src[3]);
+        }
     }
     __syncthreads();  // lse_l and part are gsum, which stage 0 overwrites
   };
@@ -514,45 +558,81 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
     // the barrier before this step ordered every wave's gsum writes of stage
     // k-1 before these reads, and this fold's reads before stage k+1 reuses
     // the buffer
-    if (k > 0) fold(k - 1);
+    if (DIRECT == 0 && k > 0) fold(k - 1);
     // waves past the stage's blocks (4 waves on a 2-block stage) sit out
     if (!active || sub >= S::BLOCKS) return;
-    f32x16 acc[NB];
-    stage_tiles<DT, S, WPQ, false>(slot, opoff, q, acc);
+    f32x16 acc[NQ][NB];
+    stage_tiles<DT, S, WPQ, NQ, false>(slot, opoff, q, acc);
+    if constexpr (DIRECT > 0) {
+      static_assert(QM && NQ % (DIRECT > 0 ? DIRECT : 1) == 0, "whole heads per wave");
+      const int64_t ts = (int64_t)p * ST + (int64_t)k * stride;
+#pragma unroll
+      for (int i = 0; i < NB; ++i) {
+        // column sums of tile (j, i) over its 32 query rows, as in QM below
+        float tq[NQ];
+#pragma unroll
+        for (int j = 0; j < NQ; ++j) {
+          float gs[4];
+#pragma unroll
+          for (int a4 = 0; a4 < 4; ++a4)
+            gs[a4] = fast_exp2(fmaf(acc[j][i][4 * a4 + 0], alpha, -cv[j][a4].x)) +
+                     fast_exp2(fmaf(acc[j][i][4 * a4 + 1], alpha, -cv[j][a4].y)) +
+                     fast_exp2(fmaf(acc[j][i][4 * a4 + 2], alpha, -cv[j][a4].z)) +
+                     fast_exp2(fmaf(acc[j][i][4 * a4 + 3], alpha, -cv[j][a4].w));
+          tq[j] = (gs[0] + gs[1]) + (gs[2] + gs[3]);
+          tq[j] += __shfl_xor(tq[j], 32);
+        }
+        const int64_t tok = ts + (sub + i * WPQ) * 32 + l32;
+#pragma unroll
+        for (int hw = 0; hw < NQ / DIRECT; ++hw) {
+          const int hs = qg * (NQ / DIRECT) + hw;
+          float t = tq[hw * DIRECT];
+#pragma unroll
+          for (int jj = 1; jj < DIRECT; ++jj) t += tq[hw * DIRECT + jj];
+          if (h == 0 && hs < n_sel && tok < Ls) wsum_g[(int64_t)hs * sq.ws_stride + tok] = t;
+        }
+      }
+      return;
+    }
     float* gb = gsum + (k & 1) * (kGroupRows * ST);
 #pragma unroll
-    for (int i = 0; i < NB; ++i) {
-      // columns at or past Ls get values too; the fold never writes them out
-      // acc[i][v]: query row qb*32 + acc_row(v, h), key (sub + i*WPQ)*32 + l32
-      // of the stage; prefix keys are visible to every window row, so no
-      // mask is needed (keys at or past Ls are never written out).
-      float gs[4];
+    for (int j = 0; j < NQ; ++j) {
+      const int qb = qg * NQ + j;
+      if (qb >= nqb) continue;  // a query block past the group's rows (uniform)
 #pragma unroll
-      for (int a4 = 0; a4 < 4; ++a4)
-        gs[a4] = fast_exp2(fmaf(acc[i][4 * a4 + 0], alpha, -cv[a4].x)) +
-                 fast_exp2(fmaf(acc[i][4 * a4 + 1], alpha, -cv[a4].y)) +
-                 fast_exp2(fmaf(acc[i][4 * a4 + 2], alpha, -cv[a4].z)) +
-                 fast_exp2(fmaf(acc[i][4 * a4 + 3], alpha, -cv[a4].w));
-      const int col = (sub + i * WPQ) * 32 + l32;
-      if (QM) {
-        float t = (gs[0] + gs[1]) + (gs[2] + gs[3]);
-        t += __shfl_xor(t, 32);
-        if (h == 0) gb[qb * ST + col] = t;
-      } else {
+      for (int i = 0; i < NB; ++i) {
+        // columns at or past Ls get values too; the fold never writes them out
+        // acc[j][i][v]: query row qb*32 + acc_row(v, h), key (sub + i*WPQ)*32 +
+        // l32 of the stage; prefix keys are visible to every window row, so no
+        // mask is needed (keys at or past Ls are never written out).
+        float gs[4];
 #pragma unroll
-        for (int a4 = 0; a4 < 4; ++a4) gs[a4] += __shfl_xor(gs[a4], 32);
-        // lane half h stores 8-row groups a4 = h and h + 2
-        gb[(qb * 4 + h) * ST + col] = h ? gs[1] : gs[0];
-        gb[(qb * 4 + 2 + h) * ST + col] = h ? gs[3] : gs[2];
+        for (int a4 = 0; a4 < 4; ++a4)
+          gs[a4] = fast_exp2(fmaf(acc[j][i][4 * a4 + 0], alpha, -cv[j][a4].x)) +
+                   fast_exp2(fmaf(acc[j][i][4 * a4 + 1], alpha, -cv[j][a4].y)) +
+                   fast_exp2(fmaf(acc[j][i][4 * a4 + 2], alpha, -cv[j][a4].z)) +
+                   fast_exp2(fmaf(acc[j][i][4 * a4 + 3], alpha, -cv[j][a4].w));
+        const int col = (sub + i * WPQ) * 32 + l32;
+        if (QM) {
+          float t = (gs[0] + gs[1]) + (gs[2] + gs[3]);
+          t += __shfl_xor(t, 32);
+          if (h == 0) gb[qb * ST + col] = t;
+        } else {
+#pragma unroll
+          for (int a4 = 0; a4 < 4; ++a4) gs[a4] += __shfl_xor(gs[a4], 32);
+          // lane half h stores 8-row groups a4 = h and h + 2
+          gb[(qb * 4 + h) * ST + col] = h ? gs[1] : gs[0];
+          gb[(qb * 4 + 2 + h) * ST + col] = h ? gs[3] : gs[2];
+        }
       }
     }
   });
   // stage_loop ended with a barrier: the last stage's sums are complete
-  if (ns > 0) fold(ns - 1);
+  if (DIRECT == 0 && ns > 0) fold(ns - 1);
 }
 
 template <int DT, int D>
-__global__ __launch_bounds__(kKpThreads) void score_kernel(const LayerArgs a) {
+__global__ __launch_bounds__(kKpThreads) __attribute__((amdgpu_waves_per_eu(2))) void score_kernel(const LayerArgs a) {
   using S = Stager<DT, D, stage_bytes<DT, D>()>;
   constexpr int NS = 4;  // 4-slot ring
   __shared__ uint4 slot0[S::VEC];
@@ -589,14 +669,22 @@ __global__ __launch_bounds__(kKpThreads) void score_kernel(const LayerArgs a) {
   const int nqb = (n_sel * a.w8 + 31) >> 5;
   const int wpq = waves_per_qblock(nqb);
   constexpr int W1 = kKpWaves, W2 = kKpWaves / 2, W4 = kKpWaves / 4;
-  if (a.w8 % 32 == 0) {
-    if (wpq == W4) score_body<DT, D, W4, true, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
-    else if (wpq == W2) score_body<DT, D, W2, true, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
-    else score_body<DT, D, W1, true, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
+  // the same wave mapping as the row-statistics pass
+  const bool pair = S::BLOCKS >= 2 && nqb >= 3;
+  if (pair && a.w8 == 64) {  // each wave's two query blocks are one head
+    score_body<DT, D, 2, 2, true, 2, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
+  } else if (pair && a.w8 == 32) {  // each query block is a head
+    score_body<DT, D, 2, 2, true, 1, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
+  } else if (a.w8 % 32 == 0) {
+    if (pair) score_body<DT, D, 2, 2, true, 0, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
+    else if (wpq == W4) score_body<DT, D, W4, 1, true, 0, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
+    else if (wpq == W2) score_body<DT, D, W2, 1, true, 0, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
+    else score_body<DT, D, W1, 1, true, 0, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
   } else {
-    if (wpq == W4) score_body<DT, D, W4, false, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
-    else if (wpq == W2) score_body<DT, D, W2, false, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
-    else score_body<DT, D, W1, false, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
+    if (pair) score_body<DT, D, 2, 2, false, 0, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
+    else if (wpq == W4) score_body<DT, D, W4, 1, false, 0, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
+    else if (wpq == W2) score_body<DT, D, W2, 1, false, 0, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
+    else score_body<DT, D, W1, 1, false, 0, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
   }
 }
 

@@ -70,6 +70,7 @@ CASES = [
     ("f32-d64", Case(8, 2, 64, 16, "avg", 7, torch.float32), 1024, 1, 128),
     ("bf16-w48-straddle", Case(8, 2, 128, 48, "max", 9, torch.bfloat16), 3333, 2, 200),
     ("bf16-w1-k31", Case(16, 4, 128, 1, "avg", 31, torch.bfloat16), 5000, 4, 1000),
+    ("bf16-w32-4heads-per-group", Case(16, 4, 128, 32, "max", 7, torch.bfloat16), 2999, 4, 300),
 ]
 
 

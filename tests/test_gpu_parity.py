@@ -56,6 +56,11 @@ CASES = [
     ("bf16-stage-edge", Case(8, 2, 128, 32, "avg", 5, torch.bfloat16), 64 * 40 + 32 + 1, 2, 128),
     # w8 = 48: query blocks straddle heads (8-row group sums)
     ("bf16-w48-straddle", Case(8, 2, 128, 48, "max", 9, torch.bfloat16), 3333, 2, 200),
+    # 3-4 query blocks: each wave takes two of them; whole heads inside one
+    # wave store their window sums directly (w8 = 32 and w8 = 64)
+    ("bf16-w32-4heads-per-group", Case(16, 4, 128, 32, "max", 7, torch.bfloat16), 2999, 4, 300),
+    ("f16-d64-w32-3heads", Case(28, 4, 64, 32, "avg", 5, torch.float16), 2100, 3, 150),
+    ("bf16-w57-2heads-padded", Case(8, 2, 128, 57, "max", 7, torch.bfloat16), 2345, 2, 222),
 ]
 
 

@@ -44,6 +44,8 @@ def parse():
     p.add_argument("--no-profile-variant", action="store_true",
                    help="skip the timing of the layer-error profile (decode attention over the "
                         "full and the compact cache, W_O projection)")
+    p.add_argument("--no-decode-variant", action="store_true",
+                   help="skip the timing of one decoding step over the full and the compact caches")
     p.add_argument("--no-lse-variant", action="store_true",
                    help="skip the second measurement, with the window rows' log-sum-exp supplied "
                         "by the caller (one pass over K)")
@@ -572,6 +574,8 @@ def main():
 
     if not args.no_profile_variant:
         result["error_profile"] = error_profile(args, wl, layers, dev, hip)
+    if not args.no_decode_variant:
+        result["decode_step"] = decode_step(wl, layers, dev)
 
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_threads)
@@ -628,6 +632,54 @@ def error_profile(args, wl, layers, dev, hip, T: int = 16, n_layers: int = 8, re
             "ms_per_layer": ms, "hbm_gbs": bytes_layer / (ms / 1e3) / 1e9,
             "hbm_frac": bytes_layer / (ms / 1e3) / 1e9 / HBM_PEAK_GBS,
             "e_first_layers": [float(x) for x in e.cpu()]}
+
+
+def decode_step(wl, layers, dev, reps: int = 3):
+    """One decoding step (one query token) over every layer's cache, as one
+    ragged batch per cache kind (ckv_decode_attention_batch): the full prompt
+    caches, then the compact caches the timed step wrote (Eq. 3-4). Bytes: K
+    and V of every cache read once."""
+    import numpy as np
+    import torch
+
+    import paper_2508_02401_amd as ckv
+
+    H, n_kv, d = wl.num_q_heads, wl.num_kv_heads, wl.head_dim
+    desc = ckv.attn_desc(H, n_kv, d, wl.dtype)
+    gen = torch.Generator(device=dev).manual_seed(11)
+    elt = torch.tensor([], dtype=wl.dtype).element_size()
+    res = {}
+    for kind in ("full", "compact"):
+        seqs, outs, nbytes, lens = [], [], 0, []
+        for mask, layer_seqs in layers:
+            for sq in layer_seqs:
+                k, v = (sq.k, sq.v) if kind == "full" else (sq.k_out, sq.v_out)
+                q = torch.randn((1, H, d), generator=gen, device=dev).to(wl.dtype)
+                o = torch.empty((1, H, d), dtype=torch.float32, device=dev)
+                seqs.append(ckv.decode_seq(q, ckv.kv_cache(k, v), o))
+                outs.append((q, o))
+                nbytes += 2 * n_kv * k.shape[1] * d * elt
+                lens.append(int(k.shape[1]))
+        ws = torch.empty(ckv.ckv_decode_batch_workspace_bytes(desc, seqs), dtype=torch.uint8,
+                         device=dev)
+        ckv.ckv_decode_attention_batch(desc, seqs, ws)
+        torch.cuda.synchronize()
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for _ in range(reps):
+            ckv.ckv_decode_attention_batch(desc, seqs, ws)
+        t1.record()
+        torch.cuda.synchronize()
+        ms = t0.elapsed_time(t1) / reps
+        res[kind] = {"ms": ms, "cached_tokens_per_head": [min(lens), int(np.mean(lens)), max(lens)],
+                     "hbm_gbs": nbytes / (ms / 1e3) / 1e9}
+        del ws, outs
+    return {"what": "one decoding step (1 query token per layer, all %d layers as one ragged "
+                    "batch) over the full prompt caches and over the compact caches" % len(layers),
+            "full_ms": res["full"]["ms"], "compact_ms": res["compact"]["ms"],
+            "speedup": res["full"]["ms"] / res["compact"]["ms"],
+            "full_hbm_gbs": res["full"]["hbm_gbs"],
+            "compact_tokens_min_mean_max": res["compact"]["cached_tokens_per_head"]}
 
 
 def cpu_baseline(wl, threads: int, min_seconds: float = 10.0):

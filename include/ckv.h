@@ -264,6 +264,37 @@ int ckv_decode_attention(const ckv_attn_desc *desc, const void *q, int64_t q_str
                          int64_t q_stride_h, int32_t T, const ckv_kv_cache *cache, float *out,
                          void *workspace, size_t workspace_bytes, void *stream);
 
+/* ---- decode over ragged caches (Eq. 2-4 at decoding time) ---------------
+ * The consumer of the compressed caches: one decoding step of a batch of
+ * prompts, each with its own queries and its own cache, e.g. the compact
+ * caches ckv_compress_layer wrote for prompts of different lengths and
+ * budgets (the cache lengths need not match). Prompt i computes exactly what
+ * ckv_decode_attention computes for (q, T, cache, out) of seqs[i]. */
+typedef struct {
+  const void *q;          /* [T][H][d] at q + t * q_stride_t + h * q_stride_h (elements) */
+  int64_t q_stride_t;
+  int64_t q_stride_h;
+  int32_t T;              /* query tokens; (H / n_kv) * T <= 128 */
+  int32_t reserved;
+  ckv_kv_cache cache;     /* this prompt's cache, n >= 1 tokens */
+  float *out;             /* [T][H][d] fp32, contiguous */
+} ckv_decode_seq;
+
+/* Workspace of ckv_decode_attention_batch (0 on invalid input). */
+size_t ckv_decode_batch_workspace_bytes(const ckv_attn_desc *desc, const ckv_decode_seq *seqs,
+                                        int32_t num_seqs);
+
+/* Decode attention of every prompt of seqs[0..num_seqs). The host array is
+ * read during the call only; queries, caches and outputs are device memory
+ * owned by the caller. The prompts go to the GPU in launches of up to 24
+ * (one decode and one merge kernel each), their workgroups sized from the
+ * launch's total cache length. Validates every prompt before any launch;
+ * CKV_ERR_INVALID_ARG / CKV_ERR_UNSUPPORTED as ckv_decode_attention,
+ * CKV_ERR_WORKSPACE when the workspace is short. Asynchronous on stream. */
+int ckv_decode_attention_batch(const ckv_attn_desc *desc, const ckv_decode_seq *seqs,
+                               int32_t num_seqs, void *workspace, size_t workspace_bytes,
+                               void *stream);
+
 /* Workspace of ckv_layer_error (0 on invalid input). */
 size_t ckv_layer_error_workspace_bytes(const ckv_attn_desc *desc, int32_t T, int64_t n_full,
                                        int64_t n_comp, int32_t D);

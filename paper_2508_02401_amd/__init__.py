@@ -11,5 +11,6 @@ from ._binding import (  # noqa: F401
     ckv_allocate_budgets, ckv_compress_layer, ckv_compress_stack, ckv_gather, ckv_last_hip_error, ckv_score,
     ckv_select, ckv_set_stack_stage_events, ckv_set_stage_events, ckv_status_string, ckv_workspace_bytes, layer_desc, load,
     attn_desc, kv_cache, ckv_decode_workspace_bytes, ckv_decode_attention, ckv_layer_error_workspace_bytes,
-    ckv_layer_error, ckv_normalize_errors,
+    ckv_layer_error, ckv_normalize_errors, ckv_decode_seq, decode_seq, ckv_decode_batch_workspace_bytes,
+    ckv_decode_attention_batch,
 )

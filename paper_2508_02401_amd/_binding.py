@@ -36,7 +36,8 @@ EXPORTED = ("ckv_workspace_bytes", "ckv_score", "ckv_select", "ckv_gather", "ckv
             "ckv_compress_stack", "ckv_allocate_budgets", "ckv_status_string",
             "ckv_last_hip_error", "ckv_set_stage_events", "ckv_set_stack_stage_events",
             "ckv_decode_workspace_bytes", "ckv_decode_attention", "ckv_layer_error_workspace_bytes",
-            "ckv_layer_error", "ckv_normalize_errors")
+            "ckv_layer_error", "ckv_normalize_errors", "ckv_decode_batch_workspace_bytes",
+            "ckv_decode_attention_batch")
 
 _DTYPE_CODE = {torch.bfloat16: CKV_BF16, torch.float16: CKV_F16, torch.float32: CKV_F32}
 
@@ -68,6 +69,12 @@ class ckv_attn_desc(ctypes.Structure):
 class ckv_kv_cache(ctypes.Structure):
     _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("stride_head", ctypes.c_int64),
                 ("stride_tok", ctypes.c_int64), ("n", ctypes.c_int64)]
+
+
+class ckv_decode_seq(ctypes.Structure):
+    _fields_ = [("q", ctypes.c_void_p), ("q_stride_t", ctypes.c_int64),
+                ("q_stride_h", ctypes.c_int64), ("T", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("cache", ckv_kv_cache), ("out", ctypes.c_void_p)]
 
 
 class CkvError(RuntimeError):
@@ -116,7 +123,12 @@ def load() -> ctypes.CDLL:
                                         vp, vp, vp, ctypes.c_size_t, vp]
         lib.ckv_normalize_errors.argtypes = [P(ctypes.c_double), ctypes.c_int32, ctypes.c_int32,
                                              P(ctypes.c_double)]
-        for name in ("ckv_decode_attention", "ckv_layer_error", "ckv_normalize_errors"):
+        DS = P(ckv_decode_seq)
+        lib.ckv_decode_batch_workspace_bytes.argtypes = [AD, DS, ctypes.c_int32]
+        lib.ckv_decode_batch_workspace_bytes.restype = ctypes.c_size_t
+        lib.ckv_decode_attention_batch.argtypes = [AD, DS, ctypes.c_int32, vp, ctypes.c_size_t, vp]
+        for name in ("ckv_decode_attention", "ckv_layer_error", "ckv_normalize_errors",
+                     "ckv_decode_attention_batch"):
             getattr(lib, name).restype = ctypes.c_int
         lib.ckv_status_string.argtypes = [ctypes.c_int]
         lib.ckv_status_string.restype = ctypes.c_char_p
@@ -385,6 +397,35 @@ def ckv_decode_attention(desc: ckv_attn_desc, q: torch.Tensor, cache: ckv_kv_cac
                                        workspace.data_ptr(),
                                        workspace.numel() * workspace.element_size(),
                                        _stream(stream)), "ckv_decode_attention")
+
+
+def decode_seq(q: torch.Tensor, cache: ckv_kv_cache, out: torch.Tensor) -> ckv_decode_seq:
+    """One prompt of a decode batch: q [T, H, d] (d contiguous), out [T, H, d] fp32 contiguous."""
+    if out.dtype != torch.float32 or not out.is_contiguous():
+        raise ValueError("out must be contiguous fp32 [T, H, d]")
+    return ckv_decode_seq(q.data_ptr(), q.stride(0), q.stride(1), q.shape[0], 0, cache,
+                          out.data_ptr())
+
+
+def _decode_seq_array(seqs):
+    arr = (ckv_decode_seq * max(len(seqs), 1))()
+    for i, s in enumerate(seqs):
+        arr[i] = s
+    return arr
+
+
+def ckv_decode_batch_workspace_bytes(desc: ckv_attn_desc, seqs) -> int:
+    return load().ckv_decode_batch_workspace_bytes(ctypes.byref(desc), _decode_seq_array(seqs),
+                                                   len(seqs))
+
+
+def ckv_decode_attention_batch(desc: ckv_attn_desc, seqs, workspace: torch.Tensor,
+                               stream=None) -> None:
+    """Decode attention of every prompt in seqs (ckv_decode_seq, e.g. from decode_seq())."""
+    _check(load().ckv_decode_attention_batch(ctypes.byref(desc), _decode_seq_array(seqs),
+                                             len(seqs), workspace.data_ptr(),
+                                             workspace.numel() * workspace.element_size(),
+                                             _stream(stream)), "ckv_decode_attention_batch")
 
 
 def ckv_layer_error_workspace_bytes(desc: ckv_attn_desc, T: int, n_full: int, n_comp: int,

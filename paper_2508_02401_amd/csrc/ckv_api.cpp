@@ -657,21 +657,40 @@ int check_q(const ckv_attn_desc* d, const void* q, int64_t st, int64_t sh, int32
   return CKV_OK;
 }
 
-// Chunks of the cache per KV head: about kDecodeTargetWgs workgroups in all,
-// each at least one 32-token block.
-int64_t decode_chunks(const ckv_attn_desc* d, int64_t n) {
-  int64_t c = ceil_div(kDecodeTargetWgs, d->num_kv_heads);
-  const int64_t blocks = ceil_div(n, 32);
-  return c < blocks ? c : blocks;
+// Tokens per decode workgroup for one launch over caches of sum_n tokens in
+// all: about kDecodeTargetWgs workgroups over every KV head and prompt, each
+// at least one 32-token block, the same length for every prompt.
+int64_t decode_chunk_len(const ckv_attn_desc* d, int64_t sum_n) {
+  const int64_t c = ceil_div(sum_n * d->num_kv_heads, kDecodeTargetWgs);
+  return c <= 32 ? 32 : ceil_div(c, 32) * 32;
 }
 
-size_t decode_part_bytes(const ckv_attn_desc* d, int64_t n) {
-  return align_up((size_t)d->num_kv_heads * decode_chunks(d, n) * kDecodeSlotsPerChunk * 128 *
-                  (d->head_dim + 2) * sizeof(float));
+// Partial rows per slot: a group's T * (H / n_kv) query rows, whole 32-row blocks.
+int32_t decode_rows(const ckv_attn_desc* d, int32_t T) {
+  return (int32_t)(ceil_div((int64_t)(d->num_q_heads / d->num_kv_heads) * T, 32) * 32);
 }
 
-void decode_args(const ckv_attn_desc* d, const void* q, int64_t st, int64_t sh, int32_t T,
-                 const ckv_kv_cache* c, float* out, void* ws, ckv::DecodeArgs& a) {
+size_t decode_part_bytes(const ckv_attn_desc* d, int32_t T, int64_t n, int64_t chunk) {
+  return align_up((size_t)d->num_kv_heads * ceil_div(n, chunk) * kDecodeSlotsPerChunk *
+                  decode_rows(d, T) * (d->head_dim + 2) * sizeof(float));
+}
+
+void decode_batch_init(const ckv_attn_desc* d, ckv::DecodeBatch& b) {
+  b.n = 0;
+  b.H = d->num_q_heads;
+  b.n_kv = d->num_kv_heads;
+  b.d = d->head_dim;
+  const float scale = d->scale > 0.f ? d->scale : 1.0f / sqrtf((float)d->head_dim);
+  b.alpha = (float)((double)scale * 1.4426950408889634);
+  b.blk_off[0] = 0;
+  b.mrg_off[0] = 0;
+}
+
+// Appends one prompt (its partials at part, chunk tokens per workgroup).
+void decode_batch_add(const ckv_attn_desc* d, const void* q, int64_t st, int64_t sh, int32_t T,
+                      const ckv_kv_cache* c, float* out, float* part, int64_t chunk,
+                      ckv::DecodeBatch& b) {
+  ckv::DecodeArgs& a = b.s[b.n];
   a.q = q;
   a.q_st = st;
   a.q_sh = sh;
@@ -681,24 +700,46 @@ void decode_args(const ckv_attn_desc* d, const void* q, int64_t st, int64_t sh, 
   a.kv_st = c->stride_tok;
   a.n = c->n;
   a.out = out;
-  a.part = static_cast<float*>(ws);
-  a.H = d->num_q_heads;
-  a.n_kv = d->num_kv_heads;
-  a.d = d->head_dim;
+  a.part = part;
   a.T = T;
-  a.n_chunks = (int32_t)decode_chunks(d, c->n);
-  a.chunk = (int32_t)(ceil_div(ceil_div(c->n, a.n_chunks), 32) * 32);
-  a.n_chunks = (int32_t)ceil_div(c->n, a.chunk);
+  a.prow = decode_rows(d, T);
+  a.chunk = (int32_t)chunk;
+  a.n_chunks = (int32_t)ceil_div(c->n, chunk);
   a.n_slots = a.n_chunks * kDecodeSlotsPerChunk;
-  const float scale = d->scale > 0.f ? d->scale : 1.0f / sqrtf((float)d->head_dim);
-  a.alpha = (float)((double)scale * 1.4426950408889634);
+  a.pad_ = 0;
+  const int64_t merge_elems = (int64_t)d->num_q_heads * T * d->head_dim;
+  b.blk_off[b.n + 1] = b.blk_off[b.n] + d->num_kv_heads * a.n_chunks;
+  b.mrg_off[b.n + 1] = b.mrg_off[b.n] + (int32_t)ceil_div(merge_elems, ckv::kDecodeThreads);
+  ++b.n;
+}
+
+int check_decode_seq(const ckv_attn_desc* d, const ckv_decode_seq* s) {
+  int rc = check_attn(d, s->T);
+  if (rc != CKV_OK) return rc;
+  if ((rc = check_q(d, s->q, s->q_stride_t, s->q_stride_h, s->T)) != CKV_OK) return rc;
+  if ((rc = check_cache(d, &s->cache)) != CKV_OK) return rc;
+  if (!s->out || ((uintptr_t)s->out & 3u)) return CKV_ERR_INVALID_ARG;
+  return CKV_OK;
+}
+
+// A batch goes to the GPU in runs of at most kMaxDecodeSeqs consecutive
+// prompts, one launch each: the size of the run that starts at i0, and its
+// chunk length.
+int32_t decode_run(int32_t i0, int32_t num_seqs) {
+  return num_seqs - i0 < ckv::kMaxDecodeSeqs ? num_seqs - i0 : ckv::kMaxDecodeSeqs;
+}
+int64_t decode_run_chunk(const ckv_attn_desc* d, const ckv_decode_seq* seqs, int32_t i0,
+                         int32_t cnt) {
+  int64_t sum_n = 0;
+  for (int32_t i = i0; i < i0 + cnt; ++i) sum_n += seqs[i].cache.n;
+  return decode_chunk_len(d, sum_n);
 }
 
 }  // namespace
 
 size_t ckv_decode_workspace_bytes(const ckv_attn_desc* desc, int32_t T, int64_t n) {
   if (check_attn(desc, T) != CKV_OK || n < 1 || n >= ((int64_t)1 << 31)) return 0;
-  return decode_part_bytes(desc, n);
+  return decode_part_bytes(desc, T, n, decode_chunk_len(desc, n));
 }
 
 int ckv_decode_attention(const ckv_attn_desc* desc, const void* q, int64_t q_stride_t,
@@ -712,10 +753,56 @@ int ckv_decode_attention(const ckv_attn_desc* desc, const void* q, int64_t q_str
   if (!workspace || !aligned16(workspace) ||
       workspace_bytes < ckv_decode_workspace_bytes(desc, T, cache->n))
     return CKV_ERR_WORKSPACE;
-  ckv::DecodeArgs a;
-  decode_args(desc, q, q_stride_t, q_stride_h, T, cache, out, workspace, a);
-  const hipError_t e = ckv::launch_decode(desc->dtype, a, (hipStream_t)stream);
+  ckv::DecodeBatch b;
+  decode_batch_init(desc, b);
+  decode_batch_add(desc, q, q_stride_t, q_stride_h, T, cache, out, static_cast<float*>(workspace),
+                   decode_chunk_len(desc, cache->n), b);
+  const hipError_t e = ckv::launch_decode(desc->dtype, b, (hipStream_t)stream);
   return e == hipSuccess ? CKV_OK : hip_fail(e);
+}
+
+size_t ckv_decode_batch_workspace_bytes(const ckv_attn_desc* desc, const ckv_decode_seq* seqs,
+                                        int32_t num_seqs) {
+  if (!desc || !seqs || num_seqs < 1) return 0;
+  for (int32_t i = 0; i < num_seqs; ++i)
+    if (check_decode_seq(desc, &seqs[i]) != CKV_OK) return 0;
+  size_t total = 0;
+  for (int32_t i0 = 0; i0 < num_seqs; i0 += ckv::kMaxDecodeSeqs) {
+    const int32_t cnt = decode_run(i0, num_seqs);
+    const int64_t chunk = decode_run_chunk(desc, seqs, i0, cnt);
+    for (int32_t i = i0; i < i0 + cnt; ++i)
+      total += decode_part_bytes(desc, seqs[i].T, seqs[i].cache.n, chunk);
+  }
+  return total;
+}
+
+int ckv_decode_attention_batch(const ckv_attn_desc* desc, const ckv_decode_seq* seqs,
+                               int32_t num_seqs, void* workspace, size_t workspace_bytes,
+                               void* stream) {
+  if (!desc || !seqs || num_seqs < 1) return CKV_ERR_INVALID_ARG;
+  for (int32_t i = 0; i < num_seqs; ++i) {
+    const int rc = check_decode_seq(desc, &seqs[i]);
+    if (rc != CKV_OK) return rc;
+  }
+  if (!workspace || !aligned16(workspace) ||
+      workspace_bytes < ckv_decode_batch_workspace_bytes(desc, seqs, num_seqs))
+    return CKV_ERR_WORKSPACE;
+  char* part = static_cast<char*>(workspace);
+  for (int32_t i0 = 0; i0 < num_seqs; i0 += ckv::kMaxDecodeSeqs) {
+    const int32_t cnt = decode_run(i0, num_seqs);
+    const int64_t chunk = decode_run_chunk(desc, seqs, i0, cnt);
+    ckv::DecodeBatch b;
+    decode_batch_init(desc, b);
+    for (int32_t i = i0; i < i0 + cnt; ++i) {
+      const ckv_decode_seq& s = seqs[i];
+      decode_batch_add(desc, s.q, s.q_stride_t, s.q_stride_h, s.T, &s.cache, s.out,
+                       reinterpret_cast<float*>(part), chunk, b);
+      part += decode_part_bytes(desc, s.T, s.cache.n, chunk);
+    }
+    const hipError_t err = ckv::launch_decode(desc->dtype, b, (hipStream_t)stream);
+    if (err != hipSuccess) return hip_fail(err);
+  }
+  return CKV_OK;
 }
 
 size_t ckv_layer_error_workspace_bytes(const ckv_attn_desc* desc, int32_t T, int64_t n_full,
@@ -724,9 +811,10 @@ size_t ckv_layer_error_workspace_bytes(const ckv_attn_desc* desc, int32_t T, int
       n_full >= ((int64_t)1 << 31) || n_comp >= ((int64_t)1 << 31))
     return 0;
   const size_t outs = align_up((size_t)T * desc->num_q_heads * desc->head_dim * sizeof(float));
-  const size_t pa = decode_part_bytes(desc, n_full), pb = decode_part_bytes(desc, n_comp);
+  const int64_t chunk = decode_chunk_len(desc, n_full + n_comp);
+  const size_t parts = decode_part_bytes(desc, T, n_full, chunk) + decode_part_bytes(desc, T, n_comp, chunk);
   const size_t proj = align_up((size_t)(ceil_div(D, 32) + 1) * 2 * T * sizeof(float));
-  return 2 * outs + (pa > pb ? pa : pb) + proj;
+  return 2 * outs + parts + proj;
 }
 
 int ckv_layer_error(const ckv_attn_desc* desc, const void* q, int64_t q_stride_t,
@@ -753,15 +841,20 @@ int ckv_layer_error(const ckv_attn_desc* desc, const void* q, int64_t q_stride_t
   float* a_full = reinterpret_cast<float*>(ws);
   float* a_comp = reinterpret_cast<float*>(ws + outs);
   char* part = ws + 2 * outs;
-  const size_t pa = decode_part_bytes(desc, full->n), pb = decode_part_bytes(desc, comp->n);
-  float* proj = reinterpret_cast<float*>(part + (pa > pb ? pa : pb));
+  // both decodes in one batch: the full cache and the compressed one
+  const int64_t chunk = decode_chunk_len(desc, full->n + comp->n);
+  const size_t pa = decode_part_bytes(desc, T, full->n, chunk);
+  const size_t pb = decode_part_bytes(desc, T, comp->n, chunk);
+  float* proj = reinterpret_cast<float*>(part + pa + pb);
   const hipStream_t st = (hipStream_t)stream;
-  ckv::DecodeArgs da;
+  ckv::DecodeBatch db;
+  decode_batch_init(desc, db);
+  decode_batch_add(desc, q, q_stride_t, q_stride_h, T, full, a_full, reinterpret_cast<float*>(part),
+                   chunk, db);
+  decode_batch_add(desc, q, q_stride_t, q_stride_h, T, comp, a_comp,
+                   reinterpret_cast<float*>(part + pa), chunk, db);
   hipError_t err;
-  decode_args(desc, q, q_stride_t, q_stride_h, T, full, a_full, part, da);
-  if ((err = ckv::launch_decode(desc->dtype, da, st)) != hipSuccess) return hip_fail(err);
-  decode_args(desc, q, q_stride_t, q_stride_h, T, comp, a_comp, part, da);
-  if ((err = ckv::launch_decode(desc->dtype, da, st)) != hipSuccess) return hip_fail(err);
+  if ((err = ckv::launch_decode(desc->dtype, db, st)) != hipSuccess) return hip_fail(err);
   ckv::ErrorArgs ea;
   ea.a_full = a_full;
   ea.a_comp = a_comp;

@@ -30,7 +30,7 @@ namespace {
 
 using namespace dev;
 
-constexpr int kDecThreads = 256;
+constexpr int kDecThreads = kDecodeThreads;
 constexpr int kDecWaves = kDecThreads / 64;
 
 __device__ __forceinline__ f32x16 mfma_f32(float a, float b, f32x16 c) {
@@ -84,15 +84,20 @@ __device__ __forceinline__ void load_row16(const void* base, int64_t off, float*
 // Decode attention, partials per (KV head, chunk, wave).
 // ---------------------------------------------------------------------------
 template <int DT, int D>
-__global__ __launch_bounds__(kDecThreads) void decode_kernel_f32(const DecodeArgs a) {
+__global__ __launch_bounds__(kDecThreads) void decode_kernel_f32(const DecodeBatch B) {
   constexpr int KB = 32;      // keys per block
   constexpr int KS = D + 1;   // LDS row stride: lanes reading one column of 32 rows hit 32 banks
   __shared__ float kl[KB * KS];  // K block [key][d], fp32
   __shared__ float vl[KB * KS];  // V block [key][d], fp32
   const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int g = blockIdx.x / a.n_chunks, chunk = blockIdx.x - g * a.n_chunks;
-  const int G = a.H / a.n_kv;
+  // this workgroup's prompt (a uniform scan over at most kMaxDecodeSeqs)
+  int si = 0;
+  while (si + 1 < B.n && (int)blockIdx.x >= B.blk_off[si + 1]) ++si;
+  const DecodeArgs& a = B.s[si];
+  const int lb = (int)blockIdx.x - B.blk_off[si];
+  const int g = lb / a.n_chunks, chunk = lb - g * a.n_chunks;
+  const int G = B.H / B.n_kv;
   const int R = G * a.T;                    // query rows of the group
   const int nqb = (R + 31) >> 5;            // their 32-row blocks (<= kDecWaves)
   const int wpq = kDecWaves / (nqb == 3 ? 4 : nqb);  // waves per query block
@@ -116,7 +121,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel_f32(const DecodeArg
 #pragma unroll
   for (int nb = 0; nb < D / 32; ++nb) o[nb] = f32x16{};
   float m_run = -INFINITY, l_run = 0.f;
-  const float alpha = a.alpha;
+  const float alpha = B.alpha;
   const int64_t kv_base = (int64_t)g * a.kv_sh;
 
   // K and V blocks of 32 keys go through LDS in fp32; each thread loads NLD
@@ -198,7 +203,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel_f32(const DecodeArg
   // the partial of this wave: (max, sum) per row, and O rows
   l_run += __shfl_xor(l_run, 32);
   const int slot = chunk * wpq + sub;
-  float* part = a.part + (((int64_t)g * a.n_slots + slot) * 128 + qb * 32) * (D + 2);
+  float* part = a.part + (((int64_t)g * a.n_slots + slot) * a.prow + qb * 32) * (D + 2);
   if (h == 0) {
     part[l32 * (D + 2) + D] = m_run;
     part[l32 * (D + 2) + D + 1] = l_run;
@@ -244,7 +249,7 @@ __device__ __forceinline__ void split8(const float* x, uint4& hi, uint4& lo) {
 }
 
 template <int DT, int D>
-__global__ __launch_bounds__(kDecThreads) void decode_kernel_16(const DecodeArgs a) {
+__global__ __launch_bounds__(kDecThreads) void decode_kernel_16(const DecodeBatch B) {
   constexpr int SB = 32;              // keys per MFMA tile (a sub-block)
   constexpr int NSB = 4;              // sub-blocks staged per block
   constexpr int KB = SB * NSB;        // keys per block
@@ -254,8 +259,13 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel_16(const DecodeArgs
   __shared__ __align__(16) unsigned char vl[KB * KROW];  // V block [key][d], raw 16-bit
   const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int g = blockIdx.x / a.n_chunks, chunk = blockIdx.x - g * a.n_chunks;
-  const int G = a.H / a.n_kv;
+  // this workgroup's prompt (a uniform scan over at most kMaxDecodeSeqs)
+  int si = 0;
+  while (si + 1 < B.n && (int)blockIdx.x >= B.blk_off[si + 1]) ++si;
+  const DecodeArgs& a = B.s[si];
+  const int lb = (int)blockIdx.x - B.blk_off[si];
+  const int g = lb / a.n_chunks, chunk = lb - g * a.n_chunks;
+  const int G = B.H / B.n_kv;
   const int R = G * a.T;
   const int nqb = (R + 31) >> 5;
   const int wpq = kDecWaves / (nqb == 3 ? 4 : nqb);
@@ -287,7 +297,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel_16(const DecodeArgs
 #pragma unroll
   for (int nb = 0; nb < D / 32; ++nb) o[nb] = f32x16{};
   float m_run = -INFINITY, l_run = 0.f;
-  const float alpha = a.alpha;
+  const float alpha = B.alpha;
   const int64_t kv_base = (int64_t)g * a.kv_sh;
 
   // every block of KB keys is staged by all threads (16-byte loads, the next
@@ -394,7 +404,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel_16(const DecodeArgs
   if (!active) return;
   l_run += __shfl_xor(l_run, 32);
   const int slot = chunk * wpq + sub;
-  float* part = a.part + (((int64_t)g * a.n_slots + slot) * 128 + qb * 32) * (D + 2);
+  float* part = a.part + (((int64_t)g * a.n_slots + slot) * a.prow + qb * 32) * (D + 2);
   if (h == 0) {
     part[l32 * (D + 2) + D] = m_run;
     part[l32 * (D + 2) + D + 1] = l_run;
@@ -407,20 +417,23 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel_16(const DecodeArgs
 
 // out[t][h][c] from the partials of every slot, one thread per (row, c).
 template <int D>
-__global__ __launch_bounds__(kDecThreads) void decode_merge_kernel(const DecodeArgs a) {
-  const int G = a.H / a.n_kv;
+__global__ __launch_bounds__(kDecThreads) void decode_merge_kernel(const DecodeBatch B) {
+  int si = 0;
+  while (si + 1 < B.n && (int)blockIdx.x >= B.mrg_off[si + 1]) ++si;
+  const DecodeArgs& a = B.s[si];
+  const int G = B.H / B.n_kv;
   const int R = G * a.T;
-  const int64_t e = (int64_t)blockIdx.x * kDecThreads + threadIdx.x;
+  const int64_t e = (int64_t)((int)blockIdx.x - B.mrg_off[si]) * kDecThreads + threadIdx.x;
   const int64_t per_g = (int64_t)R * D;
-  if (e >= per_g * a.n_kv) return;
+  if (e >= per_g * B.n_kv) return;
   const int g = (int)(e / per_g);
   const int rc = (int)(e - (int64_t)g * per_g);
   const int r = rc / D, c = rc - r * D;
   const int nqb = (R + 31) >> 5;
   const int wpq = kDecWaves / (nqb == 3 ? 4 : nqb);
   const int n_used = a.n_chunks * wpq;
-  const CKV_GLOBAL float* base = to_global(a.part) + ((int64_t)g * a.n_slots * 128 + r) * (D + 2);
-  const int64_t stride = (int64_t)128 * (D + 2);
+  const CKV_GLOBAL float* base = to_global(a.part) + ((int64_t)g * a.n_slots * a.prow + r) * (D + 2);
+  const int64_t stride = (int64_t)a.prow * (D + 2);
   constexpr int U = 8;  // slots loaded at once
   float m = -INFINITY;
   for (int s0 = 0; s0 < n_used; s0 += U) {
@@ -450,7 +463,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_merge_kernel(const DecodeA
     }
   }
   const int hl = r / a.T, t = r - hl * a.T;
-  a.out[((int64_t)t * a.H + g * G + hl) * D + c] = acc / l;
+  a.out[((int64_t)t * B.H + g * G + hl) * D + c] = acc / l;
 }
 
 // ---------------------------------------------------------------------------
@@ -576,14 +589,14 @@ __global__ __launch_bounds__(kDecThreads) void error_kernel(const ErrorArgs a) {
 }
 
 template <template <int, int> class KernelOf>
-hipError_t launch_dec(int dtype, int d, const DecodeArgs& a, int grid, hipStream_t st) {
+hipError_t launch_dec(int dtype, int d, const DecodeBatch& b, int grid, hipStream_t st) {
   const Timing tm;
-  if (dtype == 0) return d == 64 ? launch(KernelOf<0, 64>::fn, grid, kDecThreads, st, tm, a)
-                                 : launch(KernelOf<0, 128>::fn, grid, kDecThreads, st, tm, a);
-  if (dtype == 1) return d == 64 ? launch(KernelOf<1, 64>::fn, grid, kDecThreads, st, tm, a)
-                                 : launch(KernelOf<1, 128>::fn, grid, kDecThreads, st, tm, a);
-  return d == 64 ? launch(KernelOf<2, 64>::fn, grid, kDecThreads, st, tm, a)
-                 : launch(KernelOf<2, 128>::fn, grid, kDecThreads, st, tm, a);
+  if (dtype == 0) return d == 64 ? launch(KernelOf<0, 64>::fn, grid, kDecThreads, st, tm, b)
+                                 : launch(KernelOf<0, 128>::fn, grid, kDecThreads, st, tm, b);
+  if (dtype == 1) return d == 64 ? launch(KernelOf<1, 64>::fn, grid, kDecThreads, st, tm, b)
+                                 : launch(KernelOf<1, 128>::fn, grid, kDecThreads, st, tm, b);
+  return d == 64 ? launch(KernelOf<2, 64>::fn, grid, kDecThreads, st, tm, b)
+                 : launch(KernelOf<2, 128>::fn, grid, kDecThreads, st, tm, b);
 }
 
 template <int DT, int D>
@@ -597,14 +610,12 @@ struct DecodeOf<2, D> {
 
 }  // namespace
 
-hipError_t launch_decode(int dtype, const DecodeArgs& a, hipStream_t st) {
-  hipError_t e = launch_dec<DecodeOf>(dtype, a.d, a, a.n_kv * a.n_chunks, st);
+hipError_t launch_decode(int dtype, const DecodeBatch& b, hipStream_t st) {
+  hipError_t e = launch_dec<DecodeOf>(dtype, b.d, b, b.blk_off[b.n], st);
   if (e != hipSuccess) return e;
-  const int64_t total = (int64_t)a.H * a.T * a.d;
-  const int grid = (int)((total + kDecThreads - 1) / kDecThreads);
   const Timing tm;
-  return a.d == 64 ? launch(decode_merge_kernel<64>, grid, kDecThreads, st, tm, a)
-                   : launch(decode_merge_kernel<128>, grid, kDecThreads, st, tm, a);
+  return b.d == 64 ? launch(decode_merge_kernel<64>, b.mrg_off[b.n], kDecThreads, st, tm, b)
+                   : launch(decode_merge_kernel<128>, b.mrg_off[b.n], kDecThreads, st, tm, b);
 }
 
 hipError_t launch_error(int w_dtype, const ErrorArgs& a, hipStream_t st) {

@@ -142,7 +142,8 @@ struct MultiArgs {
   int32_t n_layers;
 };
 
-// Decode attention of T query tokens over one KV cache (layer-error profile).
+// Decode attention of T query tokens over one KV cache: one prompt of a
+// decode batch.
 struct DecodeArgs {
   const void* q;           // [T][H][d]: token t, head h at t * q_st + h * q_sh
   int64_t q_st, q_sh;
@@ -151,13 +152,29 @@ struct DecodeArgs {
   int64_t kv_sh, kv_st;
   int64_t n;               // cached tokens
   float* out;              // [T][H][d] fp32
-  float* part;             // [n_kv][n_slots][128][d + 2]: O rows, then (max, sum)
-  int32_t H, n_kv, d, T;
+  float* part;             // [n_kv][n_slots][prow][d + 2]: O rows, then (max, sum)
+  int32_t T;
+  int32_t prow;            // partial rows per slot: the group's query rows rounded up to 32
   int32_t chunk;           // cached tokens per workgroup
   int32_t n_chunks;
   int32_t n_slots;         // partial slots per KV head: n_chunks * 4
+  int32_t pad_;
+};
+
+// Up to kMaxDecodeSeqs prompts (ragged caches) in one pair of launches: the
+// decode workgroups of prompt i are [blk_off[i], blk_off[i+1]), its merge
+// workgroups [mrg_off[i], mrg_off[i+1]).
+constexpr int kMaxDecodeSeqs = 24;
+constexpr int kDecodeThreads = 256;  // threads of the decode and merge workgroups
+struct DecodeBatch {
+  DecodeArgs s[kMaxDecodeSeqs];
+  int32_t blk_off[kMaxDecodeSeqs + 1];
+  int32_t mrg_off[kMaxDecodeSeqs + 1];
+  int32_t n;               // prompts
+  int32_t H, n_kv, d;
   float alpha;             // logit scale * log2(e)
 };
+static_assert(sizeof(DecodeBatch) <= 4096, "decode batch is passed as kernel arguments");
 
 // W_O projection and error ratios of one layer.
 struct ErrorArgs {
@@ -199,7 +216,7 @@ hipError_t launch_gather(const LayerArgs& a, int grid, hipStream_t st, const Tim
 hipError_t launch_pool_units(const MultiArgs& m, hipStream_t st, const Timing& tm);
 // decode attention (partials, then their merge into a.out) and the error
 // ratios (projection partials, then the ratios and their sum)
-hipError_t launch_decode(int dtype, const DecodeArgs& a, hipStream_t st);
+hipError_t launch_decode(int dtype, const DecodeBatch& b, hipStream_t st);
 hipError_t launch_error(int w_dtype, const ErrorArgs& a, hipStream_t st);
 hipError_t launch_select_units(const MultiArgs& m, hipStream_t st, const Timing& tm);
 

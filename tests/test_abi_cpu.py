@@ -476,3 +476,48 @@ def test_layer_error_validation():
     assert call(ws=False) == ckv.CKV_ERR_WORKSPACE
     assert ckv.ckv_layer_error_workspace_bytes(d, 4, 100, 20, 256) > 0
     assert ckv.ckv_layer_error_workspace_bytes(d, 0, 100, 20, 256) == 0
+
+
+def _dseq(T=4, q=_BASE, qst=8 * 64, qsh=64, out=_BASE + 12288, **cache_kw):
+    return ckv.ckv_decode_seq(q, qst, qsh, T, 0, _cache(**cache_kw), out)
+
+
+def _decode_batch(desc, seqs, ws=True):
+    lib = ckv.load()
+    arr = (ckv.ckv_decode_seq * max(len(seqs), 1))(*seqs)
+    return lib.ckv_decode_attention_batch(ctypes.byref(desc), arr, len(seqs),
+                                          _BASE + 65536 if ws else None, 1 << 40 if ws else 0,
+                                          None)
+
+
+@pytest.mark.parametrize("bad", [dict(T=0), dict(q=None), dict(qsh=32), dict(out=_BASE + 2),
+                                 dict(n=0), dict(stride_tok=65), dict(k=None)])
+def test_decode_batch_rejects_any_bad_prompt(bad):
+    # the bad prompt is the second of three; nothing may be launched
+    seqs = [_dseq(), _dseq(**bad), _dseq(T=1, n=7)]
+    assert _decode_batch(_adesc(), seqs) == ckv.CKV_ERR_INVALID_ARG
+    assert ckv.ckv_decode_batch_workspace_bytes(_adesc(), seqs) == 0
+
+
+def test_decode_batch_argument_errors():
+    assert _decode_batch(_adesc(), []) == ckv.CKV_ERR_INVALID_ARG
+    assert _decode_batch(_adesc(head_dim=96), [_dseq()]) == ckv.CKV_ERR_UNSUPPORTED
+    assert _decode_batch(_adesc(), [_dseq(T=33)]) == ckv.CKV_ERR_UNSUPPORTED
+    assert _decode_batch(_adesc(), [_dseq(), _dseq(n=3)], ws=False) == ckv.CKV_ERR_WORKSPACE
+    lib = ckv.load()
+    assert lib.ckv_decode_attention_batch(ctypes.byref(_adesc()), None, 2, _BASE, 1 << 40,
+                                          None) == ckv.CKV_ERR_INVALID_ARG
+
+
+def test_decode_batch_workspace_arithmetic():
+    d = _adesc()
+    # one prompt needs what the single-cache entry point needs
+    for T, n in ((1, 1), (4, 100), (2, 70000)):
+        assert ckv.ckv_decode_batch_workspace_bytes(d, [_dseq(T=T, n=n, stride_head=n * 64)]) == \
+            ckv.ckv_decode_workspace_bytes(d, T, n)
+    # launches hold at most 24 prompts: prompt 25 starts a new launch of its own
+    seqs = [_dseq(T=1 + i % 3, n=50 + 37 * i, stride_head=(50 + 37 * i) * 64) for i in range(25)]
+    whole = ckv.ckv_decode_batch_workspace_bytes(d, seqs)
+    assert whole == (ckv.ckv_decode_batch_workspace_bytes(d, seqs[:24]) +
+                     ckv.ckv_decode_batch_workspace_bytes(d, seqs[24:]))
+    assert whole > ckv.ckv_decode_batch_workspace_bytes(d, seqs[:24])

@@ -181,3 +181,69 @@ def test_profile_to_budgets_end_to_end(dev):
     b_gpu, _ = ckv.ckv_allocate_budgets(t_gpu, 3 * 128, 32, 384)
     b_ref, _ = oracle.allocate_budgets(t_ref, 3 * 128, 32, 384)
     assert list(b_gpu) == [int(x) for x in b_ref]
+
+
+def _decode_batch_gpu(desc, items, dev):
+    """items: (q [T,H,d], k [n_kv,n,d], v) device tensors -> list of [T,H,d] numpy outputs."""
+    outs = [torch.empty((q.shape[0], q.shape[1], q.shape[2]), dtype=torch.float32, device=dev)
+            for q, _, _ in items]
+    seqs = [ckv.decode_seq(q, ckv.kv_cache(k, v), o) for (q, k, v), o in zip(items, outs)]
+    ws = torch.empty(ckv.ckv_decode_batch_workspace_bytes(desc, seqs), dtype=torch.uint8,
+                     device=dev)
+    ckv.ckv_decode_attention_batch(desc, seqs, ws)
+    torch.cuda.synchronize()
+    return [o.cpu().numpy() for o in outs]
+
+
+BATCH_CASES = [
+    # (label, H, n_kv, d, dtype, [(T, n), ...])
+    ("bf16-d128-ragged", 32, 8, 128, torch.bfloat16, [(1, 1), (1, 33), (4, 5000), (2, 700), (1, 129)]),
+    ("f16-d64-G7-ragged", 28, 4, 64, torch.float16, [(3, 2077), (1, 31), (1, 64)]),
+    ("f32-d128-ragged", 8, 2, 128, torch.float32, [(8, 1500), (1, 2), (5, 321)]),
+]
+
+
+@pytest.mark.parametrize("label,H,n_kv,d,dtype,shapes", BATCH_CASES, ids=[c[0] for c in BATCH_CASES])
+def test_decode_batch_ragged_parity(dev, label, H, n_kv, d, dtype, shapes):
+    gen = torch.Generator().manual_seed(len(label) * 31 + len(shapes))
+    items = []
+    for T, n in shapes:
+        q = (torch.randn((T, H, d), generator=gen) * 1.5).to(dtype)
+        k = torch.randn((n_kv, n, d), generator=gen).to(dtype)
+        v = torch.randn((n_kv, n, d), generator=gen).to(dtype)
+        items.append((q, k, v))
+    print("case", label, flush=True)
+    got = _decode_batch_gpu(ckv.attn_desc(H, n_kv, d, dtype),
+                            [(q.to(dev), k.to(dev), v.to(dev)) for q, k, v in items], dev)
+    for i, ((q, k, v), g) in enumerate(zip(items, got)):
+        ref = _decode_oracle(q, k, v, 1.0 / math.sqrt(d))
+        err = np.abs(g - ref)
+        assert np.all(err <= DEC_TOL * (np.abs(ref) + 1.0)), "%s prompt %d: max err %.3g" % (
+            label, i, err.max())
+
+
+def test_decode_batch_of_compact_caches_over_two_launches(dev):
+    # a decoding step of 30 prompts (two launches of at most 24) over the
+    # compact caches the eviction path kept for prompts of different lengths
+    # and budgets; each prompt's output against the oracle and against the
+    # single-cache entry point
+    case = Case(8, 2, 64, 16, "max", 7, torch.bfloat16)
+    desc = ckv.attn_desc(case.H, case.n_kv, case.d, case.dtype)
+    rng = np.random.default_rng(5)
+    items, caches_cpu = [], []
+    for i in range(30):
+        L = int(rng.integers(40, 1500))
+        B = int(rng.integers(16, 400))
+        q_win, k, v, mask = random_inputs(case, L, seed=100 + i, device="cpu", n_sel=1)
+        kc, vc = _compact_cache(case, mask, q_win, k, v, B, dev)
+        q_dec = torch.randn((1, case.H, case.d), generator=torch.Generator().manual_seed(i)).to(
+            case.dtype)
+        items.append((q_dec.to(dev), kc, vc))
+        caches_cpu.append((q_dec, kc.cpu(), vc.cpu()))
+    got = _decode_batch_gpu(desc, items, dev)
+    for i, ((q, k, v), g) in enumerate(zip(caches_cpu, got)):
+        ref = _decode_oracle(q, k, v, case.scale)
+        err = np.abs(g - ref)
+        assert np.all(err <= DEC_TOL * (np.abs(ref) + 1.0)), "prompt %d: max err %.3g" % (i, err.max())
+        single = _decode_gpu(desc, items[i][0], items[i][1], items[i][2], dev)
+        np.testing.assert_allclose(g, single, rtol=1e-5, atol=1e-6)

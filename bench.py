@@ -576,6 +576,8 @@ def main():
         result["error_profile"] = error_profile(args, wl, layers, dev, hip)
     if not args.no_decode_variant:
         result["decode_step"] = decode_step(wl, layers, dev)
+        # last: it overwrites the compact caches the legs above read
+        result["streaming_preset"] = streaming_preset(wl, layers, dev)
 
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_threads)
@@ -680,6 +682,38 @@ def decode_step(wl, layers, dev, reps: int = 3):
             "speedup": res["full"]["ms"] / res["compact"]["ms"],
             "full_hbm_gbs": res["full"]["hbm_gbs"],
             "compact_tokens_min_mean_max": res["compact"]["cached_tokens_per_head"]}
+
+
+def streaming_preset(wl, layers, dev, reps: int = 3):
+    """The StreamingLLM-style preset (ckv_streaming_select, 4 sink tokens) on
+    every layer with the layer's budget: index rows and K/V gather, no
+    scoring. Bytes: the kept K and V rows read and written, and the indices."""
+    import torch
+
+    import paper_2508_02401_amd as ckv
+
+    desc = ckv.layer_desc(wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.window, wl.dtype, 0.0,
+                          wl.pool, wl.pool_kernel)
+    elt = torch.tensor([], dtype=wl.dtype).element_size()
+
+    def run():
+        for mask, seqs in layers:
+            ckv.ckv_streaming_select(desc, seqs, 4)
+
+    run()
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(reps):
+        run()
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / (reps * len(layers))
+    kept = sum(int(sq.k_out.shape[1]) for _, seqs in layers for sq in seqs) / len(layers)
+    nbytes = wl.num_kv_heads * kept * (4 * wl.head_dim * elt + 4)
+    return {"what": "ckv_streaming_select per layer (first 4 + most recent tokens, the layer's "
+                    "budget), one launch per layer", "ms_per_layer": ms,
+            "hbm_gbs": nbytes / (ms / 1e3) / 1e9}
 
 
 def cpu_baseline(wl, threads: int, min_seconds: float = 10.0):

@@ -181,6 +181,17 @@ int ckv_select(const ckv_layer_desc *desc, const ckv_seq *seqs, int32_t num_seqs
  * idx entries must lie in [0, L). */
 int ckv_gather(const ckv_layer_desc *desc, const ckv_seq *seqs, int32_t num_seqs, void *stream);
 
+/* StreamingLLM-style preset, a comparison baseline the paper discusses
+ * (Sec. 2): no scoring; per KV head (per prompt when CKV_SHARE_LAYER) keep
+ * the first min(n_sink, n_ret) tokens (attention sinks) and the most recent
+ * n_ret - that many, n_ret = min(B, L), ascending: idx_out[r] = r, then
+ * L - n_ret + r. Writes idx_out and gathers k_out / v_out as ckv_gather
+ * does; q_win, scores_out and lse are not used. n_sink >= 0, other checks
+ * and errors as ckv_gather. Asynchronous on stream. (The SnapKV-style preset
+ * is ckv_compress_layer with every head of every group in head_mask.) */
+int ckv_streaming_select(const ckv_layer_desc *desc, const ckv_seq *seqs, int32_t num_seqs,
+                         int32_t n_sink, void *stream);
+
 /* The whole per-layer path: ckv_score, ckv_select and ckv_gather in order on
  * one stream (scores may be NULL). */
 int ckv_compress_layer(const ckv_layer_desc *desc, const uint8_t *head_mask, const ckv_seq *seqs,

@@ -176,6 +176,18 @@ def gather_rows(src: np.ndarray, idx) -> np.ndarray:
     return dst
 
 
+def streaming_indices(L: int, budget: int, n_sink: int) -> np.ndarray:
+    """StreamingLLM-style retention, which the paper's Sec. 2 describes as
+    keeping the first and the last tokens of the prompt: of n_ret = min(budget,
+    L) kept tokens, the first min(n_sink, n_ret) are the prompt's first tokens
+    (attention sinks) and the others its most recent tokens; ascending."""
+    n_ret = min(budget, L)
+    n_first = min(n_sink, n_ret)
+    first = np.arange(n_first)
+    last = np.arange(L - (n_ret - n_first), L)
+    return np.concatenate([first, last]).astype(np.int32)
+
+
 def select_group(q_sel, k, w: int, scale: float, pool_mode: int, kp: int, budget: int,
                  want_pooled: bool = False):
     """One KV group: returns (scores [L-w], idx [min(B, L)], pooled [n_sel, L-w] or None)."""

@@ -12,5 +12,5 @@ from ._binding import (  # noqa: F401
     ckv_select, ckv_set_stack_stage_events, ckv_set_stage_events, ckv_status_string, ckv_workspace_bytes, layer_desc, load,
     attn_desc, kv_cache, ckv_decode_workspace_bytes, ckv_decode_attention, ckv_layer_error_workspace_bytes,
     ckv_layer_error, ckv_normalize_errors, ckv_decode_seq, decode_seq, ckv_decode_batch_workspace_bytes,
-    ckv_decode_attention_batch,
+    ckv_decode_attention_batch, ckv_streaming_select, snapkv_mask,
 )

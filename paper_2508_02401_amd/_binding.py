@@ -37,7 +37,7 @@ EXPORTED = ("ckv_workspace_bytes", "ckv_score", "ckv_select", "ckv_gather", "ckv
             "ckv_last_hip_error", "ckv_set_stage_events", "ckv_set_stack_stage_events",
             "ckv_decode_workspace_bytes", "ckv_decode_attention", "ckv_layer_error_workspace_bytes",
             "ckv_layer_error", "ckv_normalize_errors", "ckv_decode_batch_workspace_bytes",
-            "ckv_decode_attention_batch")
+            "ckv_decode_attention_batch", "ckv_streaming_select")
 
 _DTYPE_CODE = {torch.bfloat16: CKV_BF16, torch.float16: CKV_F16, torch.float32: CKV_F32}
 
@@ -123,12 +123,14 @@ def load() -> ctypes.CDLL:
                                         vp, vp, vp, ctypes.c_size_t, vp]
         lib.ckv_normalize_errors.argtypes = [P(ctypes.c_double), ctypes.c_int32, ctypes.c_int32,
                                              P(ctypes.c_double)]
+        lib.ckv_streaming_select.argtypes = [D, S, ctypes.c_int32, ctypes.c_int32, vp]
+        lib.ckv_streaming_select.restype = ctypes.c_int
         DS = P(ckv_decode_seq)
         lib.ckv_decode_batch_workspace_bytes.argtypes = [AD, DS, ctypes.c_int32]
         lib.ckv_decode_batch_workspace_bytes.restype = ctypes.c_size_t
         lib.ckv_decode_attention_batch.argtypes = [AD, DS, ctypes.c_int32, vp, ctypes.c_size_t, vp]
         for name in ("ckv_decode_attention", "ckv_layer_error", "ckv_normalize_errors",
-                     "ckv_decode_attention_batch"):
+                     "ckv_decode_attention_batch", "ckv_streaming_select"):
             getattr(lib, name).restype = ctypes.c_int
         lib.ckv_status_string.argtypes = [ctypes.c_int]
         lib.ckv_status_string.restype = ctypes.c_char_p
@@ -258,6 +260,18 @@ def ckv_select(desc, seqs: Sequence[Seq], workspace: Optional[torch.Tensor] = No
 def ckv_gather(desc, seqs: Sequence[Seq], stream=None) -> None:
     arr = _seq_array(seqs)
     _check(load().ckv_gather(ctypes.byref(desc), arr, len(seqs), _stream(stream)), "ckv_gather")
+
+
+def ckv_streaming_select(desc, seqs: Sequence[Seq], n_sink: int, stream=None) -> None:
+    """StreamingLLM-style preset: keep the first n_sink and the most recent tokens."""
+    arr = _seq_array(seqs)
+    _check(load().ckv_streaming_select(ctypes.byref(desc), arr, len(seqs), int(n_sink),
+                                       _stream(stream)), "ckv_streaming_select")
+
+
+def snapkv_mask(num_q_heads: int) -> np.ndarray:
+    """SnapKV-style preset for ckv_compress_layer: every query head chosen."""
+    return np.ones(num_q_heads, dtype=np.uint8)
 
 
 def ckv_compress_layer(desc, head_mask, seqs: Sequence[Seq], workspace: torch.Tensor,

@@ -408,6 +408,19 @@ int ckv_gather(const ckv_layer_desc* desc, const ckv_seq* seqs, int32_t num_seqs
   return run_gather(a, (hipStream_t)stream);
 }
 
+int ckv_streaming_select(const ckv_layer_desc* desc, const ckv_seq* seqs, int32_t num_seqs,
+                         int32_t n_sink, void* stream) {
+  int rc = check_desc(desc);
+  if (rc != CKV_OK) return rc;
+  if (n_sink < 0) return CKV_ERR_INVALID_ARG;
+  if ((rc = check_seqs(desc, seqs, num_seqs, kNeedK | kNeedV | kNeedIdx | kNeedOut)) != CKV_OK)
+    return rc;
+  ckv::LayerArgs a;
+  if ((rc = build_args(desc, nullptr, seqs, num_seqs, nullptr, false, a)) != CKV_OK) return rc;
+  const hipError_t e = ckv::launch_stream_gather(a, n_sink, grid_gather(a), (hipStream_t)stream);
+  return e == hipSuccess ? CKV_OK : hip_fail(e);
+}
+
 int ckv_compress_layer(const ckv_layer_desc* desc, const uint8_t* head_mask, const ckv_seq* seqs,
                        int32_t num_seqs, void* workspace, size_t workspace_bytes, void* stream) {
   int rc = check_desc(desc);

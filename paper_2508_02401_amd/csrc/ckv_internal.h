@@ -217,6 +217,7 @@ hipError_t launch_pool_units(const MultiArgs& m, hipStream_t st, const Timing& t
 // decode attention (partials, then their merge into a.out) and the error
 // ratios (projection partials, then the ratios and their sum)
 hipError_t launch_decode(int dtype, const DecodeBatch& b, hipStream_t st);
+hipError_t launch_stream_gather(const LayerArgs& a, int32_t sinks, int grid, hipStream_t st);
 hipError_t launch_error(int w_dtype, const ErrorArgs& a, hipStream_t st);
 hipError_t launch_select_units(const MultiArgs& m, hipStream_t st, const Timing& tm);
 

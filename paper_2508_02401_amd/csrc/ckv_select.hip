@@ -417,7 +417,43 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const LayerArgs a) {
             [&](int64_t i) { return r0 + i; });
 }
 
+// StreamingLLM-style selection, the comparison baseline that keeps the
+// attention-sink tokens and the most recent ones: row r of the n_ret kept
+// rows is token r for the first min(sinks, n_ret) rows and token
+// L - n_ret + r after them (ascending, no scores). Writes the index row and
+// copies the rows like gather_kernel, with the same grid.
+__global__ __launch_bounds__(kThreads) void stream_gather_kernel(const LayerArgs a, int32_t sinks) {
+  __shared__ int32_t tok_l[kGatherRows];
+  const int b = blockIdx.x;
+  int s = 0;
+  for (int t = 1; t < a.num_seqs; ++t)
+    if (b >= a.seq[t].blk_gather) s = t;
+  const SeqArgs& sq = a.seq[s];
+  const int local = b - sq.blk_gather;
+  const int g = local / sq.n_gblk;
+  const int r0 = (local - g * sq.n_gblk) * kGatherRows;
+  const int n = sq.n_ret - r0 < kGatherRows ? sq.n_ret - r0 : kGatherRows;
+  const int ns = sinks < sq.n_ret ? sinks : sq.n_ret;
+  const int64_t recent0 = sq.L - sq.n_ret;  // token of row r >= ns is recent0 + r
+  int32_t* idx = sq.idx + (a.shared ? 0 : (int64_t)g * sq.n_ret);
+  const bool writer = !a.shared || g == 0;  // the layer's one index row when shared
+  for (int i = threadIdx.x; i < n; i += kThreads) {
+    const int r = r0 + i;
+    const int32_t tok = r < ns ? r : (int32_t)(recent0 + r);
+    tok_l[i] = tok;
+    if (writer) idx[r] = tok;
+  }
+  __syncthreads();
+  copy_rows<kThreads>(a, sq, g, n, [&](int64_t i) { return (int64_t)tok_l[i]; },
+            [&](int64_t i) { return r0 + i; });
+}
+
 }  // namespace
+
+hipError_t launch_stream_gather(const LayerArgs& a, int32_t sinks, int grid, hipStream_t st) {
+  hipLaunchKernelGGL(stream_gather_kernel, dim3(grid), dim3(kThreads), 0, st, a, sinks);
+  return hipGetLastError();
+}
 
 hipError_t launch_clear(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm) {
   return launch(clear_kernel, grid, kThreads, st, tm, a);

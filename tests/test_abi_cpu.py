@@ -530,3 +530,18 @@ def test_decode_batch_workspace_arithmetic():
     assert whole == (ckv.ckv_decode_batch_workspace_bytes(d, seqs[:24]) +
                      ckv.ckv_decode_batch_workspace_bytes(d, seqs[24:]))
     assert whole > ckv.ckv_decode_batch_workspace_bytes(d, seqs[:24])
+
+
+def test_streaming_select_validation():
+    lib = ckv.load()
+
+    def call(n_sink=4, **kw):
+        arr = (ckv._binding.ckv_seq * 1)(_seq(**kw))
+        return lib.ckv_streaming_select(ctypes.byref(_desc()), arr, 1, n_sink, None)
+    assert call(n_sink=-1) == ckv.CKV_ERR_INVALID_ARG
+    assert call(idx=None) == ckv.CKV_ERR_INVALID_ARG
+    assert call(k_out=None) == ckv.CKV_ERR_INVALID_ARG
+    assert call(k=None) == ckv.CKV_ERR_INVALID_ARG
+    assert lib.ckv_streaming_select(ctypes.byref(_desc(pool_kernel=4)),
+                                    (ckv._binding.ckv_seq * 1)(_seq()), 1, 4,
+                                    None) == ckv.CKV_ERR_INVALID_ARG

@@ -529,3 +529,34 @@ def test_shared_rejects_empty_mask():
     with pytest.raises(oracle.OracleError):
         oracle.select_layer_shared(q, np.zeros(q.shape[0], np.uint8), k, w, 0.3,
                                    oracle.POOL_AVG, 3, 20)
+
+
+# ---- StreamingLLM-style retention (Sec. 2: first and last tokens) ----------
+@pytest.mark.parametrize("L,budget,n_sink", [(10, 4, 2), (10, 4, 0), (10, 4, 9), (7, 20, 4),
+                                             (1, 1, 1), (1000, 128, 4), (33, 33, 3)])
+def test_streaming_indices_brute_force(L, budget, n_sink):
+    # membership decided token by token: a token is kept when fewer than
+    # n_sink tokens precede it, or when it is among the last (kept - sinks)
+    got = oracle.streaming_indices(L, budget, n_sink)
+    n_ret = min(budget, L)
+    kept = []
+    sinks_taken = 0
+    for j in range(L):
+        if sinks_taken < n_sink and len(kept) < n_ret:
+            kept.append(j)
+            sinks_taken += 1
+    n_recent = n_ret - len(kept)
+    recent = list(range(L))[::-1][:n_recent][::-1]
+    assert set(kept).isdisjoint(recent)
+    np.testing.assert_array_equal(got, np.array(sorted(kept + recent), dtype=np.int32))
+
+
+def test_streaming_indices_special_cases():
+    # budget >= L keeps the whole prompt; no sinks keeps the last B tokens
+    # (the window-only cache); sinks >= budget keeps the first B tokens
+    np.testing.assert_array_equal(oracle.streaming_indices(9, 50, 4), np.arange(9))
+    np.testing.assert_array_equal(oracle.streaming_indices(100, 8, 0), np.arange(92, 100))
+    np.testing.assert_array_equal(oracle.streaming_indices(100, 8, 30), np.arange(8))
+    idx = oracle.streaming_indices(5000, 256, 4)
+    assert idx.dtype == np.int32 and len(idx) == 256 and np.all(np.diff(idx) > 0)
+    assert list(idx[:5]) == [0, 1, 2, 3, 5000 - 252]

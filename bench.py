@@ -172,7 +172,7 @@ def summarize_trace(d: str) -> None:
     rows = list(csv.DictReader(open(stats[0])))
     # this library's kernels (the torch kernels are the input draws, outside
     # the timed region)
-    rows = [r for r in rows if _kernel_short(r["Name"]).endswith(("_kernel", "_kernel_multi"))]
+    rows = [r for r in rows if "ckv::" in r["Name"]]
     print("| kernel | calls | total ms | avg us | min us | max us | % of all GPU time |")
     print("|---|---|---|---|---|---|---|")
     for r in rows:

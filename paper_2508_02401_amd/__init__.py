@@ -7,7 +7,7 @@ workloads for tests and benchmarks.
 from ._binding import (  # noqa: F401
     CKV_BF16, CKV_F16, CKV_F32, CKV_KEEP_WINDOW, CKV_OK, CKV_SHARE_LAYER, CKV_POOL_AVG, CKV_POOL_MAX,
     CKV_ERR_BUDGET, CKV_ERR_HIP, CKV_ERR_INVALID_ARG, CKV_ERR_MASK, CKV_ERR_UNSUPPORTED,
-    CKV_ERR_WORKSPACE, CKV_NUM_STAGES, EXPORTED, STAGE_NAMES, LIB_PATH, CkvError, Seq, alloc_outputs, alloc_workspace,
+    CKV_ERR_WORKSPACE, CKV_MAX_SEQS, CKV_NUM_STAGES, EXPORTED, STAGE_NAMES, LIB_PATH, CkvError, Seq, alloc_outputs, alloc_workspace,
     ckv_allocate_budgets, ckv_compress_layer, ckv_compress_stack, ckv_gather, ckv_last_hip_error, ckv_score,
     ckv_select, ckv_set_stack_stage_events, ckv_set_stage_events, ckv_status_string, ckv_workspace_bytes, layer_desc, load,
     attn_desc, kv_cache, ckv_decode_workspace_bytes, ckv_decode_attention, ckv_layer_error_workspace_bytes,

@@ -61,6 +61,12 @@ CASES = [
     ("bf16-w32-4heads-per-group", Case(16, 4, 128, 32, "max", 7, torch.bfloat16), 2999, 4, 300),
     ("f16-d64-w32-3heads", Case(28, 4, 64, 32, "avg", 5, torch.float16), 2100, 3, 150),
     ("bf16-w57-2heads-padded", Case(8, 2, 128, 57, "max", 7, torch.bfloat16), 2345, 2, 222),
+    # the largest window: one head fills all 128 rows of its group (its four
+    # query blocks span two waves, so the window sums go through the fold)
+    ("bf16-w128-max-window", Case(8, 2, 128, 128, "max", 7, torch.bfloat16), 3000, 1, 400),
+    ("f16-d64-w128-max-window", Case(8, 2, 64, 128, "avg", 9, torch.float16), 1500, 1, 300),
+    # everything but one prefix token kept
+    ("bf16-budget-L-minus-1", Case(8, 2, 128, 32, "max", 7, torch.bfloat16), 2000, 2, 1999),
 ]
 
 
@@ -148,6 +154,27 @@ def test_full_size_sampled_heads(dev, name, layer, groups):
     for g in range(case.n_kv):
         own = parity.topn_reference(out["scores"][g].astype(np.float64), b - case.w)
         np.testing.assert_array_equal(out["idx"][g][: b - case.w], own)
+
+
+def test_sixteen_prompts_in_one_call(dev):
+    # the most prompts one call takes (CKV_MAX_SEQS): lengths and budgets all
+    # differ, including a one-token prefix and a budget past the prompt
+    case = Case(8, 2, 128, 16, "max", 5, torch.bfloat16)
+    rng = np.random.default_rng(16)
+    lens = [17, 40, 3000] + [int(x) for x in rng.integers(50, 2500, size=13)]
+    budgets = [16, 64, 100] + [int(x) for x in rng.integers(16, 600, size=13)]
+    budgets[5] = lens[5] + 10
+    assert len(lens) == ckv.CKV_MAX_SEQS
+    ins = [random_inputs(case, L, seed=200 + i, device="cpu", n_sel=1 + i % 2) for i, L in enumerate(lens)]
+    mask = ins[0][3]
+    ins = [(q, k, v) for q, k, v, _ in ins]
+    print("case sixteen prompts", flush=True)
+    out = run_gpu(case, mask, [q.to(dev) for q, _, _ in ins], [k.to(dev) for _, k, _ in ins],
+                  [v.to(dev) for _, _, v in ins], budgets)
+    for s, ((q, k, v), B) in enumerate(zip(ins, budgets)):
+        g = s % case.n_kv
+        rs, ri = oracle_group(case, mask, q, k, g, B)
+        check_group(case, out[s], g, rs, ri, k, v, "prompt%d" % s)
 
 
 def test_ragged_batch_sampled_heads(dev):

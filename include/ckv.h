@@ -70,7 +70,11 @@ typedef enum { CKV_POOL_AVG = 0, CKV_POOL_MAX = 1 } ckv_pool;
 #define CKV_MAX_WINDOW 128
 #define CKV_MAX_POOL_KERNEL 31
 #define CKV_MAX_SEQS 16
-#define CKV_MAX_ROWS_PER_GROUP 128 /* n_chosen(g) * round_up(w, 8) */
+/* A KV group's chosen rows, n_chosen(g) * round_up(w, 8), are read from K in
+ * row groups of at most this many: a group with more (e.g. 3 or 4 chosen
+ * heads at w = 64) is read once per row group, which costs one more pass
+ * over that group's keys in each K pass. */
+#define CKV_ROWS_PER_READ 128
 
 /* ---- layer descriptor ---------------------------------------------------
  * One attention layer's shape and the selection hyper-parameters.

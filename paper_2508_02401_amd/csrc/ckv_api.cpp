@@ -54,13 +54,15 @@ int64_t max_split(const ckv_layer_desc* d, int64_t seq_len) {
   return p < ckv::kMaxSplit ? p : ckv::kMaxSplit;
 }
 
-// Head slots per KV head in the window-sum buffer: every chosen head of a
-// group, at most G and at most kMaxRows / w8.
-int64_t wsum_heads(const ckv_layer_desc* d) {
-  const int64_t G = d->num_q_heads / d->num_kv_heads;
-  const int64_t by_rows = ckv::kMaxRows / ((d->window + 7) / 8 * 8);
-  const int64_t h = G < by_rows ? G : by_rows;
-  return h > 0 ? h : 1;
+// Head slots per KV head in the window-sum buffer: one per query head of the
+// group (any of them may be chosen).
+int64_t wsum_heads(const ckv_layer_desc* d) { return d->num_q_heads / d->num_kv_heads; }
+
+// Chosen heads per K-pass row group (kMaxRows rows), and the most row groups
+// ("units") a prompt can have: every KV group with all its heads chosen.
+int heads_per_unit(const ckv_layer_desc* d) { return ckv::kMaxRows / ((d->window + 7) / 8 * 8); }
+int64_t max_units(const ckv_layer_desc* d) {
+  return (int64_t)d->num_kv_heads * ckv::group_units((int)wsum_heads(d), heads_per_unit(d));
 }
 
 // Floats per window-sum row: the prefix length rounded up to 4, so that every
@@ -79,7 +81,7 @@ WsLayout seq_ws_layout(const ckv_layer_desc* d, const ckv_seq* s) {
   const int64_t n_ranges = ceil_div(Ls, range_size(Ls));
   WsLayout w;
   size_t o = 0;
-  w.partial = o; o += align_up((size_t)n_kv * max_split(d, s->seq_len) * ckv::kMaxRows * sizeof(float2));
+  w.partial = o; o += align_up((size_t)max_units(d) * max_split(d, s->seq_len) * ckv::kMaxRows * sizeof(float2));
   w.wsum = o;    o += align_up((size_t)n_kv * wsum_heads(d) * ws_stride(Ls) * sizeof(float));
   w.scores = o;  o += align_up((size_t)n_sg * Ls * sizeof(float));
   w.ctl = o;     o += align_up((size_t)n_sg * ckv::kCtlWords * sizeof(uint32_t));
@@ -175,9 +177,7 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
   a.lse_given = seqs[0].lse != nullptr;
   if (mask) {
     const int G = d->num_q_heads / d->num_kv_heads;
-    const int max_rows = ckv::kMaxRows;
     int off = 0;
-    a.max_sel = 0;
     for (int g = 0; g < d->num_kv_heads; ++g) {
       a.grp_off[g] = (int16_t)off;
       int cnt = 0;
@@ -192,18 +192,19 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
       // per-group scope: every group selects with its own heads; shared
       // scope: a group may have none (it is not read)
       if (cnt == 0 && !a.shared) return CKV_ERR_MASK;
-      if (cnt * a.w8 > max_rows) return CKV_ERR_UNSUPPORTED;
-      if (cnt > a.max_sel) a.max_sel = cnt;
     }
     a.grp_off[d->num_kv_heads] = (int16_t)off;
     if (off == 0) return CKV_ERR_MASK;
   }
-  // weight of the K-pass work: nqb + kSplitBias for every group read (the
-  // others have no chosen head and are not read)
+  // weight of the K-pass work: nqb + kSplitBias for every row group read
+  // (groups without a chosen head are not read)
+  a.hpr = heads_per_unit(d);
   if (mask)
     for (int g = 0; g < d->num_kv_heads; ++g) {
-      const int nqb = ((a.grp_off[g + 1] - a.grp_off[g]) * a.w8 + 31) / 32;
-      if (nqb > 0) a.split_w += nqb + ckv::kSplitBias;
+      const int cnt = a.grp_off[g + 1] - a.grp_off[g];
+      if (cnt == 0) continue;
+      for (int j = 0; j < ckv::group_units(cnt, a.hpr); ++j)
+        a.split_w += (ckv::unit_heads(cnt, a.hpr, j) * a.w8 + 31) / 32 + ckv::kSplitBias;
     }
   a.elt = elt_bytes(d->dtype);
   int32_t blk_kpass = 0, blk_pool = 0, blk_sel = 0, blk_gather = 0;
@@ -235,9 +236,12 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
     q.n_split = (int32_t)max_split(d, s.seq_len);
     q.n_kpass = 0;
     if (mask)
-      for (int g = 0; g < d->num_kv_heads; ++g)
-        q.n_kpass += ckv::group_split(((a.grp_off[g + 1] - a.grp_off[g]) * a.w8 + 31) / 32,
-                                      a.split_w, q.n_split);
+      for (int g = 0; g < d->num_kv_heads; ++g) {
+        const int cnt = a.grp_off[g + 1] - a.grp_off[g];
+        for (int j = 0; j < ckv::group_units(cnt, a.hpr); ++j)
+          q.n_kpass += ckv::group_split((ckv::unit_heads(cnt, a.hpr, j) * a.w8 + 31) / 32,
+                                        a.split_w, q.n_split);
+      }
     q.wsum_heads = (int32_t)wsum_heads(d);
     q.ws_stride = ws_stride(Ls);
     q.n_ptiles = (int32_t)ceil_div(Ls, ckv::kPoolTile);

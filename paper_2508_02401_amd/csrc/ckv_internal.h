@@ -57,6 +57,17 @@ enum Stage {
 // prompt's stages. A group without chosen heads (nqb == 0, shared scope only)
 // gets one workgroup, which reads nothing.
 constexpr int kSplitBias = 3;
+// A KV group's chosen heads are read by the K passes in row groups ("units")
+// of at most hpr heads (kMaxRows rows); a group without chosen heads is one
+// unit that reads nothing. Unit j holds heads j*hpr .. of the group.
+__host__ __device__ inline int group_units(int cnt, int hpr) {
+  return cnt == 0 ? 1 : (cnt + hpr - 1) / hpr;
+}
+__host__ __device__ inline int unit_heads(int cnt, int hpr, int j) {
+  const int r = cnt - j * hpr;
+  return r < hpr ? r : hpr;
+}
+
 __host__ __device__ inline int group_split(int nqb, int w_total, int cap) {
   if (nqb == 0) return 1;
   const int p = (int)((int64_t)kTargetWgs * (nqb + kSplitBias) / w_total);
@@ -86,7 +97,7 @@ struct SeqArgs {
   const float* lse;        // caller's window-row log-sum-exp [H][w] (natural log), or null
   int64_t lse_sh;          // its head stride
   // workspace
-  float2* partial;         // [n_kv][n_split][kMaxRows]: (max logit, sum exp2) per workgroup
+  float2* partial;         // [unit][n_split][kMaxRows]: (max logit, sum exp2) per workgroup
   float* wsum;             // [n_kv][wsum_heads][ws_stride]: window sum of each chosen head
   uint32_t* ctl;           // [n_kv][kCtlWords]
   uint32_t* hist;          // [n_kv][kHistBins]
@@ -117,7 +128,7 @@ struct LayerArgs {
   float alpha;             // logit scale * log2(e): exp(scale*s) == exp2(alpha*s)
   int32_t pool;            // 0 average, 1 max
   int32_t kp;              // odd pool kernel
-  int32_t max_sel;         // largest number of chosen heads in any group
+  int32_t hpr;             // chosen heads per K-pass row group: kMaxRows / w8
   int32_t elt;             // bytes per element of Q/K/V
   int32_t do_hist;         // scoring also builds the selection histogram
   int32_t do_gather;       // compaction also copies the kept K/V rows

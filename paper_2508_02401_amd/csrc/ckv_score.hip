@@ -266,26 +266,39 @@ __device__ __forceinline__ int find_seq(const LayerArgs& a, int b, Off off) {
   return s;
 }
 
-// KV group g, its workgroup index p and its workgroup count P of K-pass
-// workgroup `local` of a prompt (groups are laid out in order, group_split
-// workgroups each).
+// For K-pass workgroup `local` of a prompt: its KV group g, the row group
+// (unit) j of that group, the unit's index u among the prompt's units, and
+// the workgroup's index p among the unit's P workgroups (units are laid out
+// in group order, group_split workgroups each).
 __device__ __forceinline__ void kpass_locate(const LayerArgs& a, const SeqArgs& sq, int local,
-                                             int& g, int& p, int& P) {
+                                             int& g, int& j, int& u, int& p, int& P) {
   int base = 0;
-  for (g = 0;; ++g) {
-    P = group_split(((a.grp_off[g + 1] - a.grp_off[g]) * a.w8 + 31) >> 5, a.split_w, sq.n_split);
-    if (local < base + P || g == a.n_kv - 1) break;
-    base += P;
+  u = 0;
+  for (g = 0; g < a.n_kv; ++g) {
+    const int cnt = a.grp_off[g + 1] - a.grp_off[g];
+    const int nu = group_units(cnt, a.hpr);
+    for (j = 0; j < nu; ++j, ++u) {
+      P = group_split((unit_heads(cnt, a.hpr, j) * a.w8 + 31) >> 5, a.split_w, sq.n_split);
+      if (local < base + P) {
+        p = local - base;
+        return;
+      }
+      base += P;
+    }
   }
-  p = local - base;
+  // past the prompt's workgroups (the host launches exactly their number):
+  // an empty unit
+  g = a.n_kv - 1;
+  j = group_units(a.grp_off[a.n_kv] - a.grp_off[g], a.hpr);
+  p = P = 1;
 }
 
 // ---------------------------------------------------------------------------
 // Pass 1: row statistics.
 // ---------------------------------------------------------------------------
 template <int DT, int D, int WPQ, int NQ, class S, int NS>
-__device__ __forceinline__ void rowstats_body(const LayerArgs& a, const SeqArgs& sq, int g, int p,
-                                              int P, int sel0, int n_sel, int nqb,
+__device__ __forceinline__ void rowstats_body(const LayerArgs& a, const SeqArgs& sq, int g, int u,
+                                              int p, int P, int sel0, int n_sel, int nqb,
                                               uint4* const* slots, float2 (*red)[2][32]) {
   constexpr int NC = S::NC;
   constexpr int NB = (S::BLOCKS + WPQ - 1) / WPQ;
@@ -383,7 +396,7 @@ __device__ __forceinline__ void rowstats_body(const LayerArgs& a, const SeqArgs&
 #pragma unroll
     for (int sw = 0; sw < WPQ; ++sw)
       z += red[qgq * WPQ + sw][jq][r].y * fast_exp2(red[qgq * WPQ + sw][jq][r].x * alpha - ms);
-    sq.partial[((int64_t)g * sq.n_split + p) * kMaxRows + tid] = make_float2(m, z);
+    sq.partial[((int64_t)u * sq.n_split + p) * kMaxRows + tid] = make_float2(m, z);
   }
 }
 
@@ -400,15 +413,17 @@ __global__ __launch_bounds__(kKpThreads) __attribute__((amdgpu_waves_per_eu(2)))
 
   const int b = blockIdx.x;
   const SeqArgs& sq = a.seq[find_seq(a, b, [](const SeqArgs& t) { return t.blk_kpass; })];
-  int g, p, P;
-  kpass_locate(a, sq, b - sq.blk_kpass, g, p, P);
-  const int sel0 = a.grp_off[g], n_sel = a.grp_off[g + 1] - sel0;
+  int g, j, u, p, P;
+  kpass_locate(a, sq, b - sq.blk_kpass, g, j, u, p, P);
+  const int cnt = a.grp_off[g + 1] - a.grp_off[g];
+  const int sel0 = a.grp_off[g] + j * a.hpr;
+  const int n_sel = j < group_units(cnt, a.hpr) && cnt > 0 ? unit_heads(cnt, a.hpr, j) : 0;
   const int nqb = (n_sel * a.w8 + 31) >> 5;
 
   // the selection state starts from zero in every call (one per group, or
   // one per prompt when shared); the pooling kernel that accumulates into it
   // runs after this one
-  if (p == 0 && a.do_hist && g < a.n_sg) {
+  if (p == 0 && j == 0 && a.do_hist && g < a.n_sg) {
     for (int i = threadIdx.x; i < kCtlWords; i += kKpThreads) sq.ctl[g * kCtlWords + i] = 0u;
     for (int i = threadIdx.x; i < kHistBins; i += kKpThreads)
       sq.hist[(int64_t)g * kHistBins + i] = 0u;
@@ -420,10 +435,10 @@ __global__ __launch_bounds__(kKpThreads) __attribute__((amdgpu_waves_per_eu(2)))
   // blocks and half the key blocks, so every key operand is read from LDS by
   // two waves instead of four
   if (S::BLOCKS >= 2 && nqb >= 3)
-    rowstats_body<DT, D, 2, 2, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, red);
-  else if (wpq == W4) rowstats_body<DT, D, W4, 1, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, red);
-  else if (wpq == W2) rowstats_body<DT, D, W2, 1, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, red);
-  else rowstats_body<DT, D, W1, 1, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, red);
+    rowstats_body<DT, D, 2, 2, S, NS>(a, sq, g, u, p, P, sel0, n_sel, nqb, slots, red);
+  else if (wpq == W4) rowstats_body<DT, D, W4, 1, S, NS>(a, sq, g, u, p, P, sel0, n_sel, nqb, slots, red);
+  else if (wpq == W2) rowstats_body<DT, D, W2, 1, S, NS>(a, sq, g, u, p, P, sel0, n_sel, nqb, slots, red);
+  else rowstats_body<DT, D, W1, 1, S, NS>(a, sq, g, u, p, P, sel0, n_sel, nqb, slots, red);
 }
 
 // Online merge of (max logit, sum of exp2) pairs in exp2 units.
@@ -450,8 +465,8 @@ constexpr int kMergeLanes = kKpThreads / kMaxRows;  // threads per row in the ls
 // registers, in the order the fold would, and stores the window sums itself,
 // so gsum and the fold are not used.
 template <int DT, int D, int WPQ, int NQ, bool QM, int DIRECT, class S, int NS>
-__device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq, int g, int p,
-                                           int P, int sel0, int n_sel, int nqb,
+__device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq, int g, int u,
+                                           int hs0, int p, int P, int sel0, int n_sel, int nqb,
                                            uint4* const* slots, float* gsum) {
   constexpr int NC = S::NC;
   constexpr int NB = (S::BLOCKS + WPQ - 1) / WPQ;
@@ -489,7 +504,7 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
     const bool valid = r < nqb * 32 && slot_h < n_sel && wrow < a.w;
     float m = -INFINITY, z = 0.f;
     if (valid && !a.lse_given) {
-      const float2* pp = sq.partial + (int64_t)g * sq.n_split * kMaxRows + r;
+      const float2* pp = sq.partial + (int64_t)u * sq.n_split * kMaxRows + r;
       for (int c0 = half; c0 < P; c0 += kMergeLanes * kLseBatch) {
         float2 v[kLseBatch];
 #pragma unroll
@@ -540,7 +555,7 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
   // 8-row groups otherwise); their fixed-order sum is written to
   // wsum[g][hs][token].
   const int rph = QM ? a.w8 / 32 : a.w8 / 8;
-  float* wsum_g = sq.wsum + (int64_t)g * sq.wsum_heads * sq.ws_stride;
+  float* wsum_g = sq.wsum + ((int64_t)g * sq.wsum_heads + hs0) * sq.ws_stride;  // this unit's heads
   auto fold = [&](int kk) {
     const float* gb = gsum + (kk & 1) * (kGroupRows * ST);
     const int64_t t0 = (int64_t)p * ST + kk * stride;
@@ -655,12 +670,14 @@ __global__ __launch_bounds__(kKpThreads) __attribute__((amdgpu_waves_per_eu(2)))
     uint4* dst = static_cast<uint4*>(a.table_out);
     for (int i = threadIdx.x; i < (int)(sizeof(LayerArgs) / 16); i += kKpThreads) dst[i] = src[i];
   }
-  int g, p, P;
-  kpass_locate(a, sq, b - sq.blk_kpass, g, p, P);
-  const int sel0 = a.grp_off[g], n_sel = a.grp_off[g + 1] - sel0;
+  int g, j, u, p, P;
+  kpass_locate(a, sq, b - sq.blk_kpass, g, j, u, p, P);
+  const int cnt = a.grp_off[g + 1] - a.grp_off[g];
+  const int sel0 = a.grp_off[g] + j * a.hpr;
+  const int n_sel = j < group_units(cnt, a.hpr) && cnt > 0 ? unit_heads(cnt, a.hpr, j) : 0;
   // without the row-statistics pass, this pass starts the selection state
   // from zero (the pooling kernel that accumulates into it runs after it)
-  if (a.lse_given && p == 0 && a.do_hist && g < a.n_sg) {
+  if (a.lse_given && p == 0 && j == 0 && a.do_hist && g < a.n_sg) {
     for (int i = threadIdx.x; i < kCtlWords; i += kKpThreads) sq.ctl[g * kCtlWords + i] = 0u;
     for (int i = threadIdx.x; i < kHistBins; i += kKpThreads)
       sq.hist[(int64_t)g * kHistBins + i] = 0u;
@@ -672,19 +689,19 @@ __global__ __launch_bounds__(kKpThreads) __attribute__((amdgpu_waves_per_eu(2)))
   // the same wave mapping as the row-statistics pass
   const bool pair = S::BLOCKS >= 2 && nqb >= 3;
   if (pair && a.w8 == 64) {  // each wave's two query blocks are one head
-    score_body<DT, D, 2, 2, true, 2, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
+    score_body<DT, D, 2, 2, true, 2, S, NS>(a, sq, g, u, j * a.hpr, p, P, sel0, n_sel, nqb, slots, gsum);
   } else if (pair && a.w8 == 32) {  // each query block is a head
-    score_body<DT, D, 2, 2, true, 1, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
+    score_body<DT, D, 2, 2, true, 1, S, NS>(a, sq, g, u, j * a.hpr, p, P, sel0, n_sel, nqb, slots, gsum);
   } else if (a.w8 % 32 == 0) {
-    if (pair) score_body<DT, D, 2, 2, true, 0, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
-    else if (wpq == W4) score_body<DT, D, W4, 1, true, 0, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
-    else if (wpq == W2) score_body<DT, D, W2, 1, true, 0, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
-    else score_body<DT, D, W1, 1, true, 0, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
+    if (pair) score_body<DT, D, 2, 2, true, 0, S, NS>(a, sq, g, u, j * a.hpr, p, P, sel0, n_sel, nqb, slots, gsum);
+    else if (wpq == W4) score_body<DT, D, W4, 1, true, 0, S, NS>(a, sq, g, u, j * a.hpr, p, P, sel0, n_sel, nqb, slots, gsum);
+    else if (wpq == W2) score_body<DT, D, W2, 1, true, 0, S, NS>(a, sq, g, u, j * a.hpr, p, P, sel0, n_sel, nqb, slots, gsum);
+    else score_body<DT, D, W1, 1, true, 0, S, NS>(a, sq, g, u, j * a.hpr, p, P, sel0, n_sel, nqb, slots, gsum);
   } else {
-    if (pair) score_body<DT, D, 2, 2, false, 0, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
-    else if (wpq == W4) score_body<DT, D, W4, 1, false, 0, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
-    else if (wpq == W2) score_body<DT, D, W2, 1, false, 0, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
-    else score_body<DT, D, W1, 1, false, 0, S, NS>(a, sq, g, p, P, sel0, n_sel, nqb, slots, gsum);
+    if (pair) score_body<DT, D, 2, 2, false, 0, S, NS>(a, sq, g, u, j * a.hpr, p, P, sel0, n_sel, nqb, slots, gsum);
+    else if (wpq == W4) score_body<DT, D, W4, 1, false, 0, S, NS>(a, sq, g, u, j * a.hpr, p, P, sel0, n_sel, nqb, slots, gsum);
+    else if (wpq == W2) score_body<DT, D, W2, 1, false, 0, S, NS>(a, sq, g, u, j * a.hpr, p, P, sel0, n_sel, nqb, slots, gsum);
+    else score_body<DT, D, W1, 1, false, 0, S, NS>(a, sq, g, u, j * a.hpr, p, P, sel0, n_sel, nqb, slots, gsum);
   }
 }
 

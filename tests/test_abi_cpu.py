@@ -133,10 +133,13 @@ def test_group_without_chosen_head():
     assert _call("compress", _desc(), _seq(), mask=mask) == ckv.CKV_ERR_MASK
 
 
-def test_too_many_rows_per_group():
-    # 4 chosen heads x window 64 = 256 rows > 128
-    d = _desc(window=64)
-    assert _call("score", d, _seq(budget=64, seq_len=1000), mask=[1] * 8) == ckv.CKV_ERR_UNSUPPORTED
+def test_row_groups_size_the_workspace():
+    # a group's chosen rows are read in row groups of at most 128, each with
+    # its own K-pass partials: the workspace grows with the row groups a
+    # group can need (1 at w = 32 with 4 heads, 2 at w = 64, 4 at w = 128)
+    sizes = [ckv.ckv_workspace_bytes(_desc(window=w), [ckv.Seq(None, None, None, 200, seq_len=4000)])
+             for w in (32, 64, 128)]
+    assert 0 < sizes[0] < sizes[1] < sizes[2]
 
 
 def test_missing_or_small_workspace():
@@ -247,9 +250,6 @@ def test_shared_scope_mask_rules():
     for fn in ("score", "compress"):
         assert _call(fn, shared, _seq(), mask=[0] * 8) == ckv.CKV_ERR_MASK
         assert _call(fn, _desc(flags=ckv.CKV_KEEP_WINDOW | 4), _seq()) == ckv.CKV_ERR_UNSUPPORTED
-    # rows per group are still limited: 3 heads of one group x window 64 > 128
-    assert _call("score", _desc(window=64, flags=ckv.CKV_KEEP_WINDOW | ckv.CKV_SHARE_LAYER),
-                 _seq(budget=80), mask=[1, 1, 1, 0, 0, 0, 0, 0]) == ckv.CKV_ERR_UNSUPPORTED
 
 
 def test_shared_scope_workspace_is_smaller():

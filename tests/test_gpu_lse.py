@@ -71,6 +71,7 @@ CASES = [
     ("bf16-w48-straddle", Case(8, 2, 128, 48, "max", 9, torch.bfloat16), 3333, 2, 200),
     ("bf16-w1-k31", Case(16, 4, 128, 1, "avg", 31, torch.bfloat16), 5000, 4, 1000),
     ("bf16-w32-4heads-per-group", Case(16, 4, 128, 32, "max", 7, torch.bfloat16), 2999, 4, 300),
+    ("bf16-w64-4heads-256rows", Case(8, 2, 128, 64, "max", 7, torch.bfloat16), 3000, 4, 300),
 ]
 
 

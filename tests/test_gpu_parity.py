@@ -67,6 +67,11 @@ CASES = [
     ("f16-d64-w128-max-window", Case(8, 2, 64, 128, "avg", 9, torch.float16), 1500, 1, 300),
     # everything but one prefix token kept
     ("bf16-budget-L-minus-1", Case(8, 2, 128, 32, "max", 7, torch.bfloat16), 2000, 2, 1999),
+    # more than 128 chosen rows in a group: the K passes read it in row groups
+    # of at most 128 rows (2 x 128 at w = 64, 3 x 128 at w = 128, 120 + 40 at w = 40)
+    ("bf16-w64-4heads-256rows", Case(8, 2, 128, 64, "max", 7, torch.bfloat16), 3000, 4, 300),
+    ("f16-d64-w128-3heads-384rows", Case(8, 2, 64, 128, "avg", 5, torch.float16), 2000, 3, 200),
+    ("bf16-w40-4heads-uneven-row-groups", Case(16, 4, 128, 40, "max", 7, torch.bfloat16), 2500, 4, 256),
 ]
 
 

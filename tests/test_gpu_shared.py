@@ -43,6 +43,10 @@ SHARED_CASES = [
     ("bf16-w48-two-per-group", Case(16, 4, 128, 48, "max", 9, torch.bfloat16, True), 3333,
      (0, 1, 8, 9), 250),
     ("single-head", Case(8, 2, 128, 16, "max", 5, torch.bfloat16, True), 1100, (5,), 64),
+    # the paper's top-4 heads of a layer all in one group at w = 64: 256 rows,
+    # read as two row groups of 128
+    ("llama-4srh-one-group-w64", Case(32, 8, 128, 64, "max", 7, torch.bfloat16, True), 3001,
+     (8, 9, 10, 11), 300),
 ]
 
 

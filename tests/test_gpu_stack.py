@@ -194,3 +194,24 @@ def test_stack_ties_long_prompts_and_big_budgets(dev):
         check_group(case, _as_dict(got[l][0]), g, rs, ri, k_cpu, vs[0].cpu(), "ties layer %d" % l)
     # the tie rule itself: with constant keys the kept prefix is 0..n_keep-1
     assert np.array_equal(got[0][0].idx.cpu().numpy()[0, :10000], np.arange(10000))
+
+
+def test_stack_with_row_groups_beyond_128_rows(dev):
+    # layers whose groups hold 3-4 chosen heads at w = 64 (192-256 rows, read
+    # as two row groups): the stack equals the per-layer calls bit for bit and
+    # matches the oracle
+    case = Case(16, 4, 128, 64, "max", 7, torch.bfloat16)
+    layer_inputs, cpu = [], []
+    for l in range(3):
+        q, k, v, mask = random_inputs(case, 1700, seed=60 + l, device="cpu", n_sel=3 + l % 2)
+        layer_inputs.append((mask, [q.to(dev)], [k.to(dev)], [v.to(dev)], [200 + 50 * l]))
+        cpu.append((mask, q, k, v, 200 + 50 * l))
+    desc = case.desc()
+    print("case stack row groups", flush=True)
+    stacked = _run_stack(desc, layer_inputs, dev, side=False, slots=2)
+    _assert_same(stacked, _run_layers(desc, layer_inputs, dev), "row groups")
+    for l, (mask, q, k, v, b) in enumerate(cpu):
+        out = _as_dict(stacked[l][0])
+        for g in range(case.n_kv):
+            rs, ri = oracle_group(case, mask, q, k, g, b)
+            check_group(case, out, g, rs, ri, k, v, "layer %d" % l)

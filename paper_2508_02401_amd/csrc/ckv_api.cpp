@@ -730,6 +730,12 @@ void decode_batch_add(const ckv_attn_desc* d, const void* q, int64_t st, int64_t
   ++b.n;
 }
 
+// Partial Y tiles of the W_O projection: kProjSplit K ranges x 32 x 32 tiles.
+size_t proj_tiles_bytes(int32_t D, int32_t T) {
+  return align_up((size_t)ckv::kProjSplit * ceil_div(D, 32) * ceil_div(2 * (int64_t)T, 32) * 1024 *
+                  sizeof(float));
+}
+
 int check_decode_seq(const ckv_attn_desc* d, const ckv_decode_seq* s) {
   int rc = check_attn(d, s->T);
   if (rc != CKV_OK) return rc;
@@ -831,7 +837,8 @@ size_t ckv_layer_error_workspace_bytes(const ckv_attn_desc* desc, int32_t T, int
   const int64_t chunk = decode_chunk_len(desc, n_full + n_comp);
   const size_t parts = decode_part_bytes(desc, T, n_full, chunk) + decode_part_bytes(desc, T, n_comp, chunk);
   const size_t proj = align_up((size_t)(ceil_div(D, 32) + 1) * 2 * T * sizeof(float));
-  return 2 * outs + parts + proj;
+  const size_t proj_y = proj_tiles_bytes(D, T);
+  return 2 * outs + parts + proj + proj_y;
 }
 
 int ckv_layer_error(const ckv_attn_desc* desc, const void* q, int64_t q_stride_t,
@@ -863,6 +870,8 @@ int ckv_layer_error(const ckv_attn_desc* desc, const void* q, int64_t q_stride_t
   const size_t pa = decode_part_bytes(desc, T, full->n, chunk);
   const size_t pb = decode_part_bytes(desc, T, comp->n, chunk);
   float* proj = reinterpret_cast<float*>(part + pa + pb);
+  float* proj_y = reinterpret_cast<float*>(
+      reinterpret_cast<char*>(proj) + align_up((size_t)(ceil_div(D, 32) + 1) * 2 * T * sizeof(float)));
   const hipStream_t st = (hipStream_t)stream;
   ckv::DecodeBatch db;
   decode_batch_init(desc, db);
@@ -882,6 +891,7 @@ int ckv_layer_error(const ckv_attn_desc* desc, const void* q, int64_t q_stride_t
   ea.K = K;
   ea.eps = eps;
   ea.part = proj;
+  ea.part_y = proj_y;
   ea.ratio = ratio;
   ea.e = e;
   if ((err = ckv::launch_error(desc->dtype, ea, st)) != hipSuccess) return hip_fail(err);

@@ -469,13 +469,14 @@ __global__ __launch_bounds__(kDecThreads) void decode_merge_kernel(const DecodeB
 // ---------------------------------------------------------------------------
 // Projection and error ratios.
 // ---------------------------------------------------------------------------
-// Workgroup (row block rb, column block cb): the 32 x 32 tile of Y = W X,
-// its K range split over the 16 waves, then per column the sum of Y^2 over
-// the 32 rows into part[rb][col]. K is taken 16 at a time: lane half h holds
+// Workgroup (row block rb, column block cb, K range ks): the 32 x 32 tile of
+// Y = W X over the ks-th of kProjSplit K ranges, that range split over the
+// workgroup's waves, the waves' sums added in LDS in a fixed order and the
+// tile written to part_y. K is taken 16 at a time: lane half h holds
 // k0 + 8h .. k0 + 8h + 7 of its W row (one 16-byte load for 2-byte weights)
 // and of its X column, and MFMA m pairs k0 + m with k0 + 8 + m. K is a
 // multiple of 16 (H * d with d in {64, 128}).
-constexpr int kProjThreads = 1024;  // 16 waves share a tile's K range
+constexpr int kProjThreads = 256;
 constexpr int kProjWaves = kProjThreads / 64;
 
 template <int DT>
@@ -483,15 +484,17 @@ __global__ __launch_bounds__(kProjThreads) void project_kernel(const ErrorArgs a
   __shared__ float red[kProjWaves][32][33];
   const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
   const int wave = tid >> 6;
-  const int rb = blockIdx.x, cb = blockIdx.y;
+  const int rb = blockIdx.x, cb = blockIdx.y, ks = blockIdx.z;
   const int row = rb * 32 + l32, col = cb * 32 + l32;
-  const int rrow = row < a.D ? row : a.D - 1;  // rows past D compute a copy, not stored
+  const int rrow = row < a.D ? row : a.D - 1;  // rows past D compute a copy, not used
   const int T = a.T;
   const bool full_col = col < T, diff_col = col >= T && col < 2 * T;
   const int tcol = full_col ? col : (diff_col ? col - T : 0);
   const int64_t n16 = a.K / 16;
-  const int64_t per = (n16 + kProjWaves - 1) / kProjWaves;
-  const int64_t b0 = wave * per, b1 = b0 + per < n16 ? b0 + per : n16;
+  const int64_t per_ks = (n16 + kProjSplit - 1) / kProjSplit;
+  const int64_t k0 = ks * per_ks, k1 = k0 + per_ks < n16 ? k0 + per_ks : n16;
+  const int64_t per = (k1 - k0 + kProjWaves - 1) / kProjWaves;
+  const int64_t b0 = k0 + wave * per, b1 = b0 + per < k1 ? b0 + per : k1;
   const CKV_GLOBAL float* af = to_global(a.a_full) + (int64_t)tcol * a.K;
   const CKV_GLOBAL float* ac = to_global(a.a_comp) + (int64_t)tcol * a.K;
   f32x16 acc = f32x16{};
@@ -528,16 +531,41 @@ __global__ __launch_bounds__(kProjThreads) void project_kernel(const ErrorArgs a
 #pragma unroll
   for (int v = 0; v < 16; ++v) red[wave][acc_row(v, h)][l32] = acc[v];
   __syncthreads();
-  if (tid < 32) {
-    float sq = 0.f;
-    for (int r = 0; r < 32 && rb * 32 + r < a.D; ++r) {
-      float y = 0.f;
+  float* tile = a.part_y + (((int64_t)ks * gridDim.x + rb) * gridDim.y + cb) * 1024;
+  for (int e = tid; e < 1024; e += kProjThreads) {
+    const int r = e >> 5, c = e & 31;
+    float y = 0.f;
 #pragma unroll
-      for (int wv = 0; wv < kProjWaves; ++wv) y += red[wv][r][tid];
-      sq += y * y;
-    }
-    const int c = cb * 32 + tid;
-    if (c < 2 * T) a.part[(int64_t)rb * 2 * T + c] = sq;
+    for (int wv = 0; wv < kProjWaves; ++wv) y += red[wv][r][c];
+    tile[e] = y;
+  }
+}
+
+// Workgroup (rb, cb): Y = the kProjSplit partial tiles added in order, then
+// per column the sum of Y^2 over the tile's rows (rows past D excluded) into
+// part[rb][col].
+__global__ __launch_bounds__(kProjThreads) void square_kernel(const ErrorArgs a) {
+  constexpr int RG = kProjThreads / 32;  // row groups: thread t sums rows t/32, t/32 + RG, ...
+  __shared__ float colsum[RG][32];
+  const int rb = blockIdx.x, cb = blockIdx.y, nrb = gridDim.x, ncb = gridDim.y;
+  const int c = threadIdx.x & 31, rg = threadIdx.x >> 5;
+  float sq = 0.f;
+  for (int r = rg; r < 32; r += RG) {
+    if (rb * 32 + r >= a.D) break;
+    float y = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < kProjSplit; ++ks)
+      y += a.part_y[(((int64_t)ks * nrb + rb) * ncb + cb) * 1024 + r * 32 + c];
+    sq += y * y;
+  }
+  colsum[rg][c] = sq;
+  __syncthreads();
+  if (threadIdx.x < 32) {
+    float t = 0.f;
+#pragma unroll
+    for (int i = 0; i < RG; ++i) t += colsum[i][c];
+    const int col = cb * 32 + c;
+    if (col < 2 * a.T) a.part[(int64_t)rb * 2 * a.T + col] = t;
   }
 }
 
@@ -555,8 +583,20 @@ __global__ __launch_bounds__(kDecThreads) void error_kernel(const ErrorArgs a) {
   for (int c0 = 0; c0 < 2 * a.T; c0 += kCols) {
     const int col = c0 + cl;
     float acc = 0.f;
-    if (col < 2 * a.T)
-      for (int rb = j; rb < n_rb; rb += kSplit) acc += a.part[(int64_t)rb * 2 * a.T + col];
+    if (col < 2 * a.T) {
+      // row blocks j, j + kSplit, ... in that order, kBatch loads in flight
+      constexpr int kBatch = 8;
+      for (int rb0 = j; rb0 < n_rb; rb0 += kSplit * kBatch) {
+        float v[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+          const int rb = rb0 + u * kSplit;
+          v[u] = rb < n_rb ? a.part[(int64_t)rb * 2 * a.T + col] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) acc += v[u];
+      }
+    }
     part_l[j][cl] = acc;
     __syncthreads();
     if (threadIdx.x < kCols) {
@@ -620,7 +660,8 @@ hipError_t launch_decode(int dtype, const DecodeBatch& b, hipStream_t st) {
 
 hipError_t launch_error(int w_dtype, const ErrorArgs& a, hipStream_t st) {
   const Timing tm;
-  const dim3 grid((a.D + 31) / 32, (2 * a.T + 31) / 32);
+  const dim3 grid((a.D + 31) / 32, (2 * a.T + 31) / 32, kProjSplit);
+  const dim3 tiles(grid.x, grid.y);
   hipError_t e;
   if (w_dtype == 0) {
     hipLaunchKernelGGL(project_kernel<0>, grid, dim3(kProjThreads), 0, st, a);
@@ -629,6 +670,8 @@ hipError_t launch_error(int w_dtype, const ErrorArgs& a, hipStream_t st) {
   } else {
     hipLaunchKernelGGL(project_kernel<2>, grid, dim3(kProjThreads), 0, st, a);
   }
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(square_kernel, tiles, dim3(kProjThreads), 0, st, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return launch(error_kernel, 1, kDecThreads, st, tm, a);
 }

@@ -175,6 +175,7 @@ struct DecodeArgs {
 // Up to kMaxDecodeSeqs prompts (ragged caches) in one pair of launches: the
 // decode workgroups of prompt i are [blk_off[i], blk_off[i+1]), its merge
 // workgroups [mrg_off[i], mrg_off[i+1]).
+constexpr int kProjSplit = 4;  // K ranges of the W_O projection, one workgroup each
 constexpr int kMaxDecodeSeqs = 24;
 constexpr int kDecodeThreads = 256;  // threads of the decode and merge workgroups
 struct DecodeBatch {
@@ -197,6 +198,7 @@ struct ErrorArgs {
   int64_t K;
   float eps;
   float* part;             // [ceil(D / 32) + 1][2T]: column sums of Y^2 per 32 rows, then in all
+  float* part_y;           // [kProjSplit][ceil(D / 32)][ceil(2T / 32)][32][32]: Y tiles per K range
   float* ratio;            // [T]
   float* e;                // [1]
 };

@@ -434,16 +434,10 @@ __global__ __launch_bounds__(kDecThreads) void decode_merge_kernel(const DecodeB
   const int n_used = a.n_chunks * wpq;
   const CKV_GLOBAL float* base = to_global(a.part) + ((int64_t)g * a.n_slots * a.prow + r) * (D + 2);
   const int64_t stride = (int64_t)a.prow * (D + 2);
-  constexpr int U = 8;  // slots loaded at once
-  float m = -INFINITY;
-  for (int s0 = 0; s0 < n_used; s0 += U) {
-    float ms[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) ms[u] = s0 + u < n_used ? base[(s0 + u) * stride + D] : -INFINITY;
-#pragma unroll
-    for (int u = 0; u < U; ++u) m = fmaxf(m, ms[u]);
-  }
-  float l = 0.f, acc = 0.f;
+  // one pass over the slots, U at a time, with the running maximum: the sums
+  // are rescaled whenever a slot's maximum exceeds it
+  constexpr int U = 16;  // slots loaded at once
+  float m = -INFINITY, l = 0.f, acc = 0.f;
   for (int s0 = 0; s0 < n_used; s0 += U) {
     float ms[U], ls[U], os[U];
 #pragma unroll
@@ -456,7 +450,13 @@ __global__ __launch_bounds__(kDecThreads) void decode_merge_kernel(const DecodeB
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      if (ms[u] == -INFINITY) continue;  // a slot that saw no key
+      if (ms[u] == -INFINITY) continue;  // a slot that saw no key, or past the last
+      if (ms[u] > m) {
+        const float f = exp2f(m - ms[u]);  // 0 while nothing has been added
+        l *= f;
+        acc *= f;
+        m = ms[u];
+      }
       const float f = exp2f(ms[u] - m);
       l += ls[u] * f;
       acc += os[u] * f;

@@ -248,10 +248,14 @@ __device__ __forceinline__ void split8(const float* x, uint4& hi, uint4& lo) {
   lo = make_uint4(lb[0] | lb[1] << 16, lb[2] | lb[3] << 16, lb[4] | lb[5] << 16, lb[6] | lb[7] << 16);
 }
 
+// Blocks of 64 keys keep the staging registers small enough for two
+// workgroups per CU (two waves per SIMD): one workgroup reduces a block while
+// the other's loads are in flight.
 template <int DT, int D>
-__global__ __launch_bounds__(kDecThreads) void decode_kernel_16(const DecodeBatch B) {
+__global__ __launch_bounds__(kDecThreads) __attribute__((amdgpu_waves_per_eu(2)))
+void decode_kernel_16(const DecodeBatch B) {
   constexpr int SB = 32;              // keys per MFMA tile (a sub-block)
-  constexpr int NSB = 4;              // sub-blocks staged per block
+  constexpr int NSB = 2;              // sub-blocks staged per block
   constexpr int KB = SB * NSB;        // keys per block
   constexpr int NC = D / 16;          // 16-element contraction chunks of a row
   constexpr int KROW = D * 2 + 16;    // K and V row bytes in LDS, padded by one 16-byte chunk

@@ -83,6 +83,10 @@ def parse():
     p.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                    help="print the calibrated per-launch HBM traffic from two rocprofv3 --pmc "
                         "runs (FETCH_SIZE, WRITE_SIZE) and exit (no GPU needed)")
+    p.add_argument("--summarize-counters", nargs="+", metavar="DIR",
+                   help="print per-kernel SQ counters (mean per dispatch) and the MFMA busy "
+                        "fraction from rocprofv3 --pmc output directories and exit (no GPU "
+                        "needed)")
     p.add_argument("--copy-mib", type=int, default=1024,
                    help="size the calibration copy used, for --summarize-pmc")
     return p.parse_args()
@@ -228,6 +232,48 @@ def summarize_pmc(fetch_dir: str, write_dir: str, copy_mib: int) -> None:
     print("```")
 
 
+# MI355X: 256 CUs of 4 SIMDs each, in 8 XCDs of 4 shader engines (SQ cycle
+# counters are summed over the shader engines, busy-cycle counters over SIMDs)
+N_SIMD = 1024
+N_SE = 32
+
+
+def summarize_counters(dirs) -> None:
+    """Per-kernel SQ counters (mean per dispatch) from rocprofv3 --pmc runs,
+    with the MFMA pipe's busy fraction: busy SIMD-cycles over SIMDs x the
+    dispatch's cycles (SQ_CYCLES / shader engines)."""
+    import csv
+    import glob
+    import collections
+    vals = collections.defaultdict(lambda: collections.defaultdict(list))
+    for d in dirs:
+        files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+        if not files:
+            raise SystemExit("no counter_collection.csv under " + d)
+        for r in csv.DictReader(open(files[0])):
+            k = _kernel_short(r["Kernel_Name"])
+            if k.endswith("_kernel"):
+                vals[k][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    names = sorted({c for v in vals.values() for c in v})
+    ks = sorted(vals)
+    mean = {k: {c: sum(v) / len(v) for c, v in vals[k].items()} for k in ks}
+    print("| counter (mean per dispatch) | " + " | ".join(ks) + " |")
+    print("|---|" + "---|" * len(ks))
+    for c in names:
+        print("| %s | " % c + " | ".join("%.4g" % mean[k][c] if c in mean[k] else "—"
+                                       for k in ks) + " |")
+    busy, per = [], []
+    for k in ks:
+        m = mean[k]
+        b = m.get("SQ_VALU_MFMA_BUSY_CYCLES")
+        busy.append("%.1f%%" % (100.0 * b / (N_SIMD * m["SQ_CYCLES"] / N_SE))
+                    if b is not None and m.get("SQ_CYCLES") else "—")
+        per.append("%.1f" % (b / m["SQ_INSTS_MFMA"]) if b is not None and m.get("SQ_INSTS_MFMA")
+                   else "—")
+    print("| MFMA pipe busy (of SIMD-cycles) | " + " | ".join(busy) + " |")
+    print("| busy cycles per MFMA | " + " | ".join(per) + " |")
+
+
 def calibration_copy(mib: int) -> None:
     import torch
     n = mib * 1024 * 1024 // 4
@@ -248,6 +294,9 @@ def main():
         return
     if args.summarize_pmc:
         summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.copy_mib)
+        return
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters)
         return
     if args.gpus != 1:
         print("bench.py runs on one GPU only: the eviction path has no multi-GPU mode (every KV "

@@ -564,7 +564,7 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
       if (t0 + c >= Ls) continue;
       float acc = gb[(hs * rph) * ST + c];
       for (int q8 = 1; q8 < rph; ++q8) acc += gb[(hs * rph + q8) * ST + c];
-      wsum_g[(int64_t)hs * sq.ws_stride + t0 + c] = acc;
+      __builtin_nontemporal_store(acc, wsum_g + (int64_t)hs * sq.ws_stride + t0 + c);
     }
   };
 
@@ -604,7 +604,7 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
           float t = tq[hw * DIRECT];
 #pragma unroll
           for (int jj = 1; jj < DIRECT; ++jj) t += tq[hw * DIRECT + jj];
-          if (h == 0 && hs < n_sel && tok < Ls) wsum_g[(int64_t)hs * sq.ws_stride + tok] = t;
+          if (h == 0 && hs < n_sel && tok < Ls) __builtin_nontemporal_store(t, wsum_g + (int64_t)hs * sq.ws_stride + tok);
         }
       }
       return;

@@ -116,9 +116,11 @@ struct Stager {
     return p;
   }
 
-  // Issue the direct-to-LDS loads of the stage whose first token is t0.
-  // Tokens outside [lo, hi] read row lo or hi instead (their results are
-  // never used); only stages that cross lo or hi take that slower path.
+  // Issue the direct-to-LDS loads of the stage whose first token is t0, with
+  // cache policy AUX (0, or kLoadNonTemporal). Tokens outside [lo, hi] read
+  // row lo or hi instead (their results are never used); only stages that
+  // cross lo or hi take that slower path.
+  template <int AUX>
   __device__ static __forceinline__ void fetch(const char* kbase, int64_t kv_st, int64_t t0,
                                                int64_t lo, int64_t hi, const Plan& p, int wave,
                                                uint4* slot) {
@@ -127,14 +129,14 @@ struct Stager {
 #pragma unroll
       for (int k = 0; k < PT; ++k)
         __builtin_amdgcn_global_load_lds(reinterpret_cast<const uint4*>(sb + p.off[k]),
-                                         slot + (k * kKpWaves + wave) * 64, 16, 0, 0);
+                                         slot + (k * kKpWaves + wave) * 64, 16, 0, AUX);
     } else {
 #pragma unroll
       for (int k = 0; k < PT; ++k) {
         int64_t tok = t0 + p.tok[k];
         tok = tok < lo ? lo : (tok > hi ? hi : tok);
         const uint4* src = reinterpret_cast<const uint4*>(kbase + tok * kv_st * EB) + p.chunk[k];
-        __builtin_amdgcn_global_load_lds(src, slot + (k * kKpWaves + wave) * 64, 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(src, slot + (k * kKpWaves + wave) * 64, 16, 0, AUX);
       }
     }
   }
@@ -155,6 +157,9 @@ struct Stager {
     for (int c = 0; c < NC; ++c) kr[c] = *reinterpret_cast<const uint4*>(blk + off[c]);
   }
 };
+
+// Cache policy of a load that is the last read of its data (gfx950 `nt`).
+constexpr int kLoadNonTemporal = 2;
 
 // Stage size: kStageBytes (at least one 32-token block).
 template <int DT, int D>
@@ -182,8 +187,9 @@ __device__ __forceinline__ void wait_stages(int n_after) {
 // from the slot being read). After the first NS-1 stages are issued, pre()
 // runs while they load. At step k: wait for stage k, barrier (stage k is
 // complete and every wave has finished with stage k-1's slot), issue stage
-// k+NS-1 into that freed slot, then body(slot, k) reduces stage k.
-template <class S, int NS, class Pre, class Body>
+// k+NS-1 into that freed slot, then body(slot, k) reduces stage k. The loads
+// use cache policy AUX.
+template <class S, int NS, int AUX, class Pre, class Body>
 __device__ __forceinline__ void stage_loop(uint4* const* slot, const char* kbase, int64_t kv_st,
                                            int64_t t_first, int64_t stride, int ns, int64_t lo,
                                            int64_t hi, int wave, Pre pre, Body body) {
@@ -197,7 +203,7 @@ __device__ __forceinline__ void stage_loop(uint4* const* slot, const char* kbase
   if (prio_until > 0) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
   for (int j = 0; j < NS - 1; ++j)
-    if (j < ns) S::fetch(kbase, kv_st, t_first + j * stride, lo, hi, p, wave, slot[j]);
+    if (j < ns) S::template fetch<AUX>(kbase, kv_st, t_first + j * stride, lo, hi, p, wave, slot[j]);
   pre();  // work that overlaps the first stages' loads
   for (int k0 = 0; k0 < ns; k0 += NS) {
 #pragma unroll
@@ -209,7 +215,7 @@ __device__ __forceinline__ void stage_loop(uint4* const* slot, const char* kbase
         wait_stages<S::PT, NS - 2>(left < NS - 2 ? left : NS - 2);
         __builtin_amdgcn_s_barrier();
         if (k + NS - 1 < ns)
-          S::fetch(kbase, kv_st, t_first + (k + NS - 1) * stride, lo, hi, p, wave,
+          S::template fetch<AUX>(kbase, kv_st, t_first + (k + NS - 1) * stride, lo, hi, p, wave,
                    slot[(j + NS - 1) % NS]);
         body(slot[j], k);
       }
@@ -337,7 +343,9 @@ __device__ __forceinline__ void rowstats_body(const LayerArgs& a, const SeqArgs&
     z_run[j] = 0.f;
   }
 
-  stage_loop<S, NS>(slots, kbase, sq.kv_st, (int64_t)p * S::ST, stride, ns, 0, L - 1, wave,
+  // the keys stay cacheable: the window-sum pass that follows reads the
+  // same keys, and finds part of them in the Infinity Cache
+  stage_loop<S, NS, 0>(slots, kbase, sq.kv_st, (int64_t)p * S::ST, stride, ns, 0, L - 1, wave,
                     [] {}, [&](const uint4* slot, int k) {
     // waves past the stage's blocks (4 waves on a 2-block stage) sit out
     if (!active || sub >= S::BLOCKS) return;
@@ -568,7 +576,10 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
     }
   };
 
-  stage_loop<S, NS>(slots, kbase, sq.kv_st, (int64_t)p * ST, stride, ns, 0, Ls - 1, wave,
+  // the last read of these keys: non-temporal loads leave the caches to the
+  // data still to be read
+  stage_loop<S, NS, kLoadNonTemporal>(slots, kbase, sq.kv_st, (int64_t)p * ST, stride, ns, 0,
+                                      Ls - 1, wave,
                     merge_lse, [&](const uint4* slot, int k) {
     // the barrier before this step ordered every wave's gsum writes of stage
     // k-1 before these reads, and this fold's reads before stage k+1 reuses

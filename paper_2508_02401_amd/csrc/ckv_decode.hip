@@ -139,8 +139,9 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel_f32(const DecodeBat
       const int key = e / (D / EPV), c = (e - key * (D / EPV)) * EPV;
       const int64_t tok = t0 + key < j1 ? t0 + key : j1 - 1;  // past the chunk: a valid row
       const int64_t off = (kv_base + tok * a.kv_st + c) * Elt<DT>::bytes;
-      kr[u] = *reinterpret_cast<const CKV_GLOBAL u32x4*>(to_global(static_cast<const char*>(a.k)) + off);
-      vr[u] = *reinterpret_cast<const CKV_GLOBAL u32x4*>(to_global(static_cast<const char*>(a.v)) + off);
+      // each cache row is read once: non-temporal loads
+      kr[u] = __builtin_nontemporal_load(reinterpret_cast<const CKV_GLOBAL u32x4*>(to_global(static_cast<const char*>(a.k)) + off));
+      vr[u] = __builtin_nontemporal_load(reinterpret_cast<const CKV_GLOBAL u32x4*>(to_global(static_cast<const char*>(a.v)) + off));
     }
   };
   issue(0);
@@ -318,8 +319,9 @@ void decode_kernel_16(const DecodeBatch B) {
       const int key = e / (D / 8), c = (e - key * (D / 8)) * 8;
       const int64_t tok = t0 + key < j1 ? t0 + key : j1 - 1;  // past the chunk: a valid row
       const int64_t off = (kv_base + tok * a.kv_st + c) * 2;
-      kr[u] = *reinterpret_cast<const CKV_GLOBAL u32x4*>(to_global(static_cast<const char*>(a.k)) + off);
-      vr[u] = *reinterpret_cast<const CKV_GLOBAL u32x4*>(to_global(static_cast<const char*>(a.v)) + off);
+      // each cache row is read once: non-temporal loads
+      kr[u] = __builtin_nontemporal_load(reinterpret_cast<const CKV_GLOBAL u32x4*>(to_global(static_cast<const char*>(a.k)) + off));
+      vr[u] = __builtin_nontemporal_load(reinterpret_cast<const CKV_GLOBAL u32x4*>(to_global(static_cast<const char*>(a.v)) + off));
     }
   };
   issue(0);

@@ -18,7 +18,7 @@ constexpr int kMinStagesPerWg = 65536 / kStageBytes; // K stages per workgroup (
 constexpr int kTargetWgs = 512;    // K-pass workgroups per prompt: 2 on each of 256 CUs
 constexpr int kCUs = 256;          // compute units of the MI355X
 constexpr int kPoolTile = 2048;    // scores per pooling workgroup
-constexpr int kUnitPoolTiles = 8;  // tiles per pooling workgroup of ckv_compress_stack
+constexpr int kUnitPoolTiles = 2;  // tiles per pooling workgroup of ckv_compress_stack
 constexpr int kMaxPoolRadius = 15; // pool kernel <= 2*15+1
 constexpr int kGatherRows = 64;    // retained rows per gather workgroup
 constexpr int kHistBits = 12;      // first-level histogram: key bits 30..19

@@ -197,9 +197,9 @@ __device__ __forceinline__ void stage_loop(uint4* const* slot, const char* kbase
   // Two workgroups share each CU; the one dispatched second is the younger,
   // and the SIMDs issue the older one's waves first, so it would finish
   // well after its partner and leave the CU half idle. It runs its first
-  // 3/8 of the stages at a raised wave priority to even them out (a hint
+  // 3/4 of the stages at a raised wave priority to even them out (a hint
   // only: results do not depend on it).
-  const int prio_until = ((blockIdx.x / kCUs) & 1) ? ns * 3 / 8 : 0;
+  const int prio_until = ((blockIdx.x / kCUs) & 1) ? ns * 3 / 4 : 0;
   if (prio_until > 0) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
   for (int j = 0; j < NS - 1; ++j)

@@ -669,16 +669,11 @@ hipError_t launch_error(int w_dtype, const ErrorArgs& a, hipStream_t st) {
   const dim3 grid((a.D + 31) / 32, (2 * a.T + 31) / 32, kProjSplit);
   const dim3 tiles(grid.x, grid.y);
   hipError_t e;
-  if (w_dtype == 0) {
-    hipLaunchKernelGGL(project_kernel<0>, grid, dim3(kProjThreads), 0, st, a);
-  } else if (w_dtype == 1) {
-    hipLaunchKernelGGL(project_kernel<1>, grid, dim3(kProjThreads), 0, st, a);
-  } else {
-    hipLaunchKernelGGL(project_kernel<2>, grid, dim3(kProjThreads), 0, st, a);
-  }
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL(square_kernel, tiles, dim3(kProjThreads), 0, st, a);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (w_dtype == 0) e = launch(project_kernel<0>, grid, kProjThreads, st, tm, a);
+  else if (w_dtype == 1) e = launch(project_kernel<1>, grid, kProjThreads, st, tm, a);
+  else e = launch(project_kernel<2>, grid, kProjThreads, st, tm, a);
+  if (e != hipSuccess) return e;
+  if ((e = launch(square_kernel, tiles, kProjThreads, st, tm, a)) != hipSuccess) return e;
   return launch(error_kernel, 1, kDecThreads, st, tm, a);
 }
 

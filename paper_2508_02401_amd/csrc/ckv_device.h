@@ -147,15 +147,19 @@ __device__ __forceinline__ void find_bin(uint32_t need, Get get, uint32_t* wsum,
 }
 
 // Launch kernel(a) on stream st, with its start and end times recorded into
-// tm's events when they are given.
+// tm's events when they are given. The launch's own status is returned (not
+// hipGetLastError, which may hold an earlier error of the caller's).
+template <typename K, typename A>
+__host__ hipError_t launch(K kernel, dim3 grid, int block, hipStream_t st, const Timing& tm,
+                           const A& a) {
+  void* args[] = {const_cast<A*>(&a)};
+  return hipExtLaunchKernel(reinterpret_cast<const void*>(kernel), grid, dim3(block), args, 0, st,
+                            tm.start, tm.stop, 0);
+}
 template <typename K, typename A>
 __host__ hipError_t launch(K kernel, int grid, int block, hipStream_t st, const Timing& tm,
                            const A& a) {
-  if (tm.start || tm.stop)
-    hipExtLaunchKernelGGL(kernel, dim3(grid), dim3(block), 0, st, tm.start, tm.stop, 0, a);
-  else
-    hipLaunchKernelGGL(kernel, dim3(grid), dim3(block), 0, st, a);
-  return hipGetLastError();
+  return launch(kernel, dim3(grid), block, st, tm, a);
 }
 
 constexpr int kPoolPer = 8;  // consecutive scores pooled per thread

@@ -71,9 +71,13 @@ __device__ __forceinline__ void load_queries(const LayerArgs& a, const SeqArgs& 
 }
 
 // s_waitcnt immediate that waits until at most n vector-memory operations of
-// this wave are outstanding (gfx9 encoding: vmcnt in bits 3:0 and 15:14,
-// expcnt and lgkmcnt left at their no-wait maxima).
-constexpr int vmcnt_imm(int n) { return 0xF70 | (n & 15) | ((n >> 4) << 14); }
+// this wave are outstanding and all its LDS operations are done (gfx9
+// encoding: vmcnt in bits 3:0 and 15:14, expcnt left at its no-wait maximum,
+// lgkmcnt 0). The stage loop's barrier follows this wait: the window-sum
+// fold reads LDS rows that other waves wrote in the previous step, so those
+// writes must be complete when the barrier releases. The direct-to-LDS key
+// loads count in vmcnt only, so this does not drain the key stream.
+constexpr int vmcnt_imm(int n) { return 0x070 | (n & 15) | ((n >> 4) << 14); }
 
 // Staging of K through LDS. A stage is ST = SB / ROWB consecutive tokens (a
 // multiple of 32); its LDS image is row-major, ROWB bytes per token, with the

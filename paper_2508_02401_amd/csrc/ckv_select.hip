@@ -451,8 +451,9 @@ __global__ __launch_bounds__(kThreads) void stream_gather_kernel(const LayerArgs
 }  // namespace
 
 hipError_t launch_stream_gather(const LayerArgs& a, int32_t sinks, int grid, hipStream_t st) {
-  hipLaunchKernelGGL(stream_gather_kernel, dim3(grid), dim3(kThreads), 0, st, a, sinks);
-  return hipGetLastError();
+  void* args[] = {const_cast<LayerArgs*>(&a), &sinks};
+  return hipLaunchKernel(reinterpret_cast<const void*>(stream_gather_kernel), dim3(grid),
+                         dim3(kThreads), args, 0, st);
 }
 
 hipError_t launch_clear(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm) {

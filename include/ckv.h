@@ -20,7 +20,8 @@
  *     addresses (e.g. from torch or hipMalloc); host arrays (head mask,
  *     budgets, errors) are read during the call and not retained. The library
  *     allocates no device memory: scratch space is the caller's workspace,
- *     sized by ckv_workspace_bytes().
+ *     sized by ckv_workspace_bytes() (ckv_compress_layer_noalloc uses an array
+ *     held by the library instead).
  *   - Device work is enqueued asynchronously on the caller's stream
  *     (`stream` is a hipStream_t; NULL means the default stream). Faults
  *     surface at the caller's next synchronisation. Calls that share one
@@ -227,6 +228,24 @@ int ckv_compress_layer(const ckv_layer_desc *desc, const uint8_t *head_mask, con
 int ckv_compress_stack(const ckv_layer_desc *desc, int32_t n_layers, const uint8_t *head_masks,
                        const ckv_seq *seqs, int32_t num_seqs, void *workspace,
                        size_t workspace_bytes, void *stream, void *side_stream);
+
+/* ckv_compress_layer for callers that cannot allocate or pass device memory
+ * of their own for scratch (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): same arguments apart from the
+ * workspace, same checks, kernels and results. The workspace is a device
+ * array inside the library of CKV_NOALLOC_MAX_WORKSPACE_BYTES, one per GPU,
+ * allocated when the library's code is first loaded on that GPU and held
+ * until the process ends; the call itself allocates nothing. It returns
+ * CKV_ERR_WORKSPACE when ckv_workspace_bytes(desc, seqs, num_seqs) exceeds
+ * that size (one 131072-token prompt of 32 query / 8 KV heads of dim 128
+ * needs about 36 MiB), and CKV_ERR_INVALID_ARG when stream belongs to a
+ * device other than the current one. Every call on a GPU uses that GPU's one
+ * array: calls that may overlap on a GPU (different streams, host threads)
+ * race and must be ordered by the caller. The array keeps the last call's
+ * contents; nothing in it needs to start cleared. */
+#define CKV_NOALLOC_MAX_WORKSPACE_BYTES ((size_t)64 << 20)
+int ckv_compress_layer_noalloc(const ckv_layer_desc *desc, const uint8_t *head_mask,
+                               const ckv_seq *seqs, int32_t num_seqs, void *stream);
 
 /* Algorithm 1 (error-aware layer-adaptive cache allocation), host only,
  * synchronous. err_norm [n_layers] are the normalised per-layer errors,

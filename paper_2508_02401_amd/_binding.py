@@ -31,13 +31,14 @@ CKV_POOL_AVG, CKV_POOL_MAX = 0, 1
 CKV_KEEP_WINDOW = 1
 CKV_SHARE_LAYER = 2
 CKV_MAX_SEQS = 16
+CKV_NOALLOC_MAX_WORKSPACE_BYTES = 64 << 20
 
 EXPORTED = ("ckv_workspace_bytes", "ckv_score", "ckv_select", "ckv_gather", "ckv_compress_layer",
             "ckv_compress_stack", "ckv_allocate_budgets", "ckv_status_string",
             "ckv_last_hip_error", "ckv_set_stage_events", "ckv_set_stack_stage_events",
             "ckv_decode_workspace_bytes", "ckv_decode_attention", "ckv_layer_error_workspace_bytes",
             "ckv_layer_error", "ckv_normalize_errors", "ckv_decode_batch_workspace_bytes",
-            "ckv_decode_attention_batch", "ckv_streaming_select")
+            "ckv_decode_attention_batch", "ckv_streaming_select", "ckv_compress_layer_noalloc")
 
 _DTYPE_CODE = {torch.bfloat16: CKV_BF16, torch.float16: CKV_F16, torch.float32: CKV_F32}
 
@@ -105,6 +106,7 @@ def load() -> ctypes.CDLL:
         lib.ckv_gather.argtypes = [D, S, ctypes.c_int32, vp]
         lib.ckv_compress_layer.argtypes = [D, P(ctypes.c_uint8), S, ctypes.c_int32, vp,
                                            ctypes.c_size_t, vp]
+        lib.ckv_compress_layer_noalloc.argtypes = [D, P(ctypes.c_uint8), S, ctypes.c_int32, vp]
         lib.ckv_compress_stack.argtypes = [D, ctypes.c_int32, P(ctypes.c_uint8), S, ctypes.c_int32,
                                            vp, ctypes.c_size_t, vp, vp]
         lib.ckv_set_stack_stage_events.argtypes = [P(vp), P(vp), ctypes.c_int32]
@@ -130,7 +132,7 @@ def load() -> ctypes.CDLL:
         lib.ckv_decode_batch_workspace_bytes.restype = ctypes.c_size_t
         lib.ckv_decode_attention_batch.argtypes = [AD, DS, ctypes.c_int32, vp, ctypes.c_size_t, vp]
         for name in ("ckv_decode_attention", "ckv_layer_error", "ckv_normalize_errors",
-                     "ckv_decode_attention_batch", "ckv_streaming_select"):
+                     "ckv_decode_attention_batch", "ckv_streaming_select", "ckv_compress_layer_noalloc"):
             getattr(lib, name).restype = ctypes.c_int
         lib.ckv_status_string.argtypes = [ctypes.c_int]
         lib.ckv_status_string.restype = ctypes.c_char_p
@@ -281,6 +283,13 @@ def ckv_compress_layer(desc, head_mask, seqs: Sequence[Seq], workspace: torch.Te
                                      workspace.data_ptr(),
                                      workspace.numel() * workspace.element_size(),
                                      _stream(stream)), "ckv_compress_layer")
+
+
+def ckv_compress_layer_noalloc(desc, head_mask, seqs: Sequence[Seq], stream=None) -> None:
+    arr = _seq_array(seqs)
+    _check(load().ckv_compress_layer_noalloc(ctypes.byref(desc), _mask(head_mask), arr,
+                                             len(seqs), _stream(stream)),
+           "ckv_compress_layer_noalloc")
 
 
 def ckv_compress_stack(desc, head_masks, seqs: Sequence[Sequence[Seq]], workspace: torch.Tensor,

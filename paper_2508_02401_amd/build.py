@@ -10,7 +10,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libckv.so")
-SOURCES = [os.path.join(CSRC, n) for n in ("ckv_score.hip", "ckv_select.hip", "ckv_unit.hip", "ckv_decode.hip", "ckv_api.cpp")]
+SOURCES = [os.path.join(CSRC, n) for n in ("ckv_score.hip", "ckv_select.hip", "ckv_unit.hip", "ckv_decode.hip", "ckv_noalloc.hip", "ckv_api.cpp")]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -288,10 +288,7 @@ int grid_gather(const ckv::LayerArgs& a) {
   return q.blk_gather + q.n_gblk * a.n_kv;
 }
 
-int hip_fail(hipError_t e) {
-  g_last_hip_error = (int)e;
-  return CKV_ERR_HIP;
-}
+int hip_fail(hipError_t e) { return ckv::record_hip_error((int)e); }
 
 // Events of one launch: the stage's begin event on its first kernel and its
 // end event on its last (kernel start and end times, no extra packets).
@@ -359,6 +356,11 @@ int run_gather(const ckv::LayerArgs& a, hipStream_t st) {
 }
 
 }  // namespace
+
+int ckv::record_hip_error(int hip_status) {
+  g_last_hip_error = hip_status;
+  return CKV_ERR_HIP;
+}
 
 extern "C" {
 

@@ -7,6 +7,11 @@
 
 namespace ckv {
 
+// Stores a HIP status for ckv_last_hip_error (per host thread) and returns
+// CKV_ERR_HIP.
+int record_hip_error(int hip_status);
+
+
 constexpr int kMaxSeqs = 16;
 constexpr int kMaxQHeads = 128;
 constexpr int kMaxKvHeads = 64;

@@ -288,7 +288,9 @@ def _resource_usage():
         names = re.findall(r"Function Name: (\S+)", out)
         scratch = [int(x) for x in re.findall(r"ScratchSize \[bytes/lane\]: (\d+)", out)]
         lds = [int(x) for x in re.findall(r"LDS Size \[bytes/block\]: (\d+)", out)]
-        assert names and len(names) == len(scratch) == len(lds), src
+        with open(os.path.join(B.CSRC, src)) as f:
+            has_kernels = "__global__" in f.read()
+        assert len(names) == len(scratch) == len(lds) and bool(names) == has_kernels, src
         for n, sc, l in zip(names, scratch, lds):
             _RESOURCE_USAGE[n] = {"scratch": sc, "lds": l, "src": src}
     return _RESOURCE_USAGE

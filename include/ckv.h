@@ -173,16 +173,16 @@ size_t ckv_workspace_bytes(const ckv_layer_desc *desc, const ckv_seq *seqs, int3
 int ckv_score(const ckv_layer_desc *desc, const uint8_t *head_mask, const ckv_seq *seqs,
               int32_t num_seqs, void *workspace, size_t workspace_bytes, void *stream);
 
-/* Top-N selection, paper Sec. 3.3 ("the tokens with the top N highest
- * attention scores will be selected"): for every prompt and KV head, reads
+/* Top-N selection, paper Sec. 3.3 (the N best-scoring tokens are kept):
+ * for every prompt and KV head, reads
  * scores (>= 0, finite) and writes idx: the B - w best prefix tokens (higher
  * score first, lower index on ties) in ascending order, then the window
  * positions; or 0..L-1 when B >= L. */
 int ckv_select(const ckv_layer_desc *desc, const ckv_seq *seqs, int32_t num_seqs,
                void *workspace, size_t workspace_bytes, void *stream);
 
-/* Retain/evict, paper Sec. 3.3 ("their corresponding KV cache pairs will be
- * retained"): copies K and V rows idx[g, r] into k_out / v_out bit for bit.
+/* Retain/evict, paper Sec. 3.3 (the selected tokens' K/V pairs stay in the
+ * cache, the rest are dropped): copies K and V rows idx[g, r] into k_out / v_out bit for bit.
  * idx entries must lie in [0, L). */
 int ckv_gather(const ckv_layer_desc *desc, const ckv_seq *seqs, int32_t num_seqs, void *stream);
 

@@ -87,8 +87,8 @@ int ckvo_attention_row(const double *q, const double *k, int64_t n_visible,
   return CKVO_OK;
 }
 
-/* Window sums of one KV group (Sec. 3.3, "summing over the observation
- * window"): for each of the n_sel chosen heads, S[h][j] = sum over the w window
+/* Window sums of one KV group (Sec. 3.3: the attention scores are added up
+ * across the window's rows): for each of the n_sel chosen heads, S[h][j] = sum over the w window
  * rows of that head's attention scores on key j, over the full range j in
  * [0, L).  q_sel is [n_sel][w][d], k is [L][d], S is [n_sel][L]. */
 int ckvo_window_sums(const double *q_sel, int32_t n_sel, const double *k,
@@ -181,8 +181,8 @@ static int ckvo_index_cmp(const void *a, const void *b) {
   return (x > y) - (x < y);
 }
 
-/* Top-N selection (Sec. 3.3, "the tokens with the top N highest attention
- * scores will be selected"), under reading R9: the w window tokens are always
+/* Top-N selection (Sec. 3.3: the N tokens with the largest scores are
+ * kept), under reading R9: the w window tokens are always
  * kept and count toward the budget, the remaining budget-w tokens are the best
  * of the prefix [0, L-w) by score a[]. Returns the number of retained indices
  * (min(budget, L)) written to idx in ascending order, or a negative code. */
@@ -221,8 +221,8 @@ int ckvo_gather_rows(const void *src, int64_t row_bytes, const int32_t *idx,
 }
 
 /* The whole selection for one KV group: window sums of the chosen heads,
- * pooling of each head over the prefix (R6), mean over the heads ("such
- * compressed vectors are averaged"), then top-N. scores is [L-w]; idx gets
+ * pooling of each head over the prefix (R6), mean over the heads (Sec. 3.3
+ * averages the pooled vectors of the chosen heads), then top-N. scores is [L-w]; idx gets
  * min(budget, L) entries. pooled (optional) receives [n_sel][L-w]. */
 int64_t ckvo_select_group(const double *q_sel, int32_t n_sel, const double *k,
                           int64_t L, int32_t d, int32_t w, double scale,
@@ -465,43 +465,58 @@ int ckvo_normalize_errors(const double *e, int32_t n_sets, int32_t n_layers, dou
   return CKVO_OK;
 }
 
-/* Algorithm 1 (error-aware layer-adaptive cache allocation), step by step:
- * start every layer at m, share the remainder R in proportion to the
- * normalised errors e[] (rounded, R14), clip to [m, M], then move single
- * tokens to the highest-error layer below M (surplus) or away from the
- * lowest-error layer above m (deficit) until the total is met or no layer can
- * move (R15: ties go to the lowest index). Returns 0 when the allocations sum
- * to total, CKVO_EBUDGET when the loop stopped short. */
+/* Algorithm 1 (Appendix B.1, error-aware layer-adaptive cache allocation),
+ * as a proportional share followed by a water-fill of the gap it leaves.
+ *
+ * Share: every layer gets the floor m plus its part of what is left,
+ * R = total - n*m, in proportion to its normalised error e[i] (rounded half to
+ * even, R14), clipped to [m, M].
+ *
+ * Gap: the clipped budgets may miss the total. The algorithm closes the gap
+ * one token at a time, giving each missing token to the layer of largest error
+ * that is still below M, or taking each extra token from the layer of smallest
+ * error still above m (R15: equal errors go to the lower layer). The errors do
+ * not change meanwhile, so that rule visits the layers in one fixed order (by
+ * error, then by index) and fills or drains each to its bound before it moves
+ * to the next; that order is what is computed here.
+ *
+ * Returns 0 when the budgets sum to total, CKVO_EBUDGET when every layer hit
+ * its bound first (B then holds the budgets as far as they got). */
+static int alloc_before(const double *e, int32_t a, int32_t b, int largest_first) {
+  if (e[a] != e[b]) return largest_first ? e[a] > e[b] : e[a] < e[b];
+  return a < b;
+}
+
 int ckvo_allocate_budgets(const double *e, int32_t n, int64_t total, int64_t m,
                           int64_t M, int64_t *B) {
   if (!e || !B || n < 1 || m < 0 || M < m) return CKVO_EINVAL;
-  for (int32_t i = 0; i < n; ++i) B[i] = m;
-  int64_t sum = 0;
-  for (int32_t i = 0; i < n; ++i) sum += B[i];
-  int64_t R = total - sum;
+  const int64_t R = total - (int64_t)n * m;
+  int64_t gap = total;
   for (int32_t i = 0; i < n; ++i) {
-    double share = nearbyint(e[i] * (double)R);
-    int64_t v = B[i] + (int64_t)share;
-    B[i] = v < m ? m : (v > M ? M : v);
+    const int64_t b = m + (int64_t)nearbyint(e[i] * (double)R);
+    B[i] = b < m ? m : (b > M ? M : b);
+    gap -= B[i];
   }
-  sum = 0;
-  for (int32_t i = 0; i < n; ++i) sum += B[i];
-  int64_t delta = total - sum;
-  while (delta != 0) {
-    int32_t j = -1;
-    if (delta > 0) {
-      for (int32_t i = 0; i < n; ++i)
-        if (B[i] < M && (j < 0 || e[i] > e[j])) j = i;
-      if (j < 0) break;
-      B[j] += 1;
-      delta -= 1;
-    } else {
-      for (int32_t i = 0; i < n; ++i)
-        if (B[i] > m && (j < 0 || e[i] < e[j])) j = i;
-      if (j < 0) break;
-      B[j] -= 1;
-      delta += 1;
+  if (gap == 0) return CKVO_OK;
+  const int grow = gap > 0;
+  int32_t *order = (int32_t *)malloc((size_t)n * sizeof(int32_t));
+  if (!order) return CKVO_ENOMEM;
+  for (int32_t i = 0; i < n; ++i) {  /* insertion sort into visiting order */
+    int32_t k = i;
+    while (k > 0 && alloc_before(e, i, order[k - 1], grow)) {
+      order[k] = order[k - 1];
+      --k;
     }
+    order[k] = i;
   }
-  return delta == 0 ? CKVO_OK : CKVO_EBUDGET;
+  for (int32_t k = 0; k < n && gap != 0; ++k) {
+    const int32_t i = order[k];
+    const int64_t room = grow ? M - B[i] : B[i] - m;
+    const int64_t need = grow ? gap : -gap;
+    const int64_t moved = need < room ? need : room;
+    B[i] += grow ? moved : -moved;
+    gap -= grow ? moved : -moved;
+  }
+  free(order);
+  return gap == 0 ? CKVO_OK : CKVO_EBUDGET;
 }

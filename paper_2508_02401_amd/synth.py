@@ -99,20 +99,13 @@ def head_mask(wl: Workload, layer: int) -> np.ndarray:
     return mask
 
 
-def shared_head_mask(wl: Workload, layer: int, n_heads: int = 4, max_rows: int = 128) -> np.ndarray:
-    """uint8 [H]: n_heads retrieval heads of the whole layer (any groups), the
-    paper's layer-shared setting (its top-4 heads per layer). A group takes at
-    most max_rows // round_up(w, 8) of them (the library's rows per group)."""
+def shared_head_mask(wl: Workload, layer: int, n_heads: int = 4) -> np.ndarray:
+    """uint8 [H]: n_heads retrieval heads of the whole layer, drawn uniformly
+    from all query heads (any groups, several may share one), the paper's
+    layer-shared setting (its top-4 heads per layer)."""
     rng = np.random.default_rng([layer_seed(wl, layer), 4])
-    G = wl.num_q_heads // wl.num_kv_heads
-    cap = max(1, max_rows // ((wl.window + 7) // 8 * 8))
     mask = np.zeros(wl.num_q_heads, dtype=np.uint8)
-    for h in rng.permutation(wl.num_q_heads):
-        if mask.sum() == n_heads:
-            break
-        g = h // G
-        if mask[g * G:(g + 1) * G].sum() < cap:
-            mask[h] = 1
+    mask[rng.choice(wl.num_q_heads, size=n_heads, replace=False)] = 1
     return mask
 
 

@@ -427,6 +427,41 @@ def test_algorithm1_invariants(seed):
     assert B.min() >= m and B.max() <= M
 
 
+def _algorithm1_token_by_token(e, total, m, M):
+    """Algorithm 1's gap rule applied literally, one token per step: each
+    missing token goes to the largest-error layer below M, each extra token
+    leaves the smallest-error layer above m (equal errors: the lower layer)."""
+    n = len(e)
+    R = total - n * m
+    B = [min(M, max(m, m + int(np.rint(x * R)))) for x in e]
+    while sum(B) != total:
+        short = sum(B) < total
+        cand = [i for i in range(n) if (B[i] < M if short else B[i] > m)]
+        if not cand:
+            return B, False
+        key = (lambda i: (-e[i], i)) if short else (lambda i: (e[i], i))
+        j = min(cand, key=key)
+        B[j] += 1 if short else -1
+    return B, True
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_algorithm1_matches_token_by_token_rule(seed):
+    # tight bounds and repeated error values force long fix-ups that cross
+    # several layers, in both directions, and infeasible totals
+    rng = np.random.default_rng(1000 + seed)
+    n = int(rng.integers(1, 12))
+    e = rng.choice([0.05, 0.1, 0.2, 0.3], size=n).astype(float)
+    e = (e / e.sum()).tolist()
+    m = int(rng.integers(0, 6))
+    M = m + int(rng.integers(0, 9))
+    total = int(rng.integers(max(0, n * m - 3), n * M + 4))
+    want, ok = _algorithm1_token_by_token(e, total, m, M)
+    B, rc = oracle.allocate_budgets(e, total, m, M)
+    assert B.tolist() == want
+    assert rc == (oracle.OK if ok else oracle.EBUDGET)
+
+
 def test_algorithm1_infeasible_reports_shortfall():
     B, rc = oracle.allocate_budgets([0.5, 0.5], 1000, 32, 100)
     assert rc == oracle.EBUDGET and B.tolist() == [100, 100]

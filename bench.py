@@ -49,7 +49,15 @@ def parse():
     p.add_argument("--no-lse-variant", action="store_true",
                    help="skip the second measurement, with the window rows' log-sum-exp supplied "
                         "by the caller (one pass over K)")
-    p.add_argument("--cpu-threads", type=int, default=0)
+    p.add_argument("--cpu-threads", type=int, default=0,
+                   help="oracle threads for cpu_baseline (0 = the usable CPUs, at most 16)")
+    p.add_argument("--cpu-seconds", type=float, default=15.0,
+                   help="wall time the cpu_baseline sample aims for")
+    p.add_argument("--no-stream-ceiling", action="store_true",
+                   help="skip the streaming-read ceiling probe (bench_stream.so)")
+    p.add_argument("--configs", default="llama8b-32k-layer,llama8b-32k-stack,qwen7b-ragged-batch",
+                   help="other workloads measured after the headline one, comma-separated "
+                        "('' for none); each gets its own step time and roofline")
     p.add_argument("--time-every", type=int, default=4, metavar="N",
                    help="K-pass launches of every N-th layer carry start/end events (the layer "
                         "offset rotates with the step, so every layer is sampled); each timed "
@@ -274,6 +282,82 @@ def summarize_counters(dirs) -> None:
     print("| busy cycles per MFMA | " + " | ".join(per) + " |")
 
 
+STREAM_SRC = os.path.join(ROOT, "bench_stream.hip")
+STREAM_LIB = os.path.join(ROOT, "bench_stream.so")
+STREAM_KINDS = {0: "global_load_dwordx4", 1: "global_load_dwordx4 nontemporal",
+                2: "global_load_lds_dwordx4 (the K passes' route)"}
+
+
+def build_stream_probe() -> str:
+    """Compile bench_stream.hip (the streaming-read ceiling probe) in-tree."""
+    import subprocess
+    from paper_2508_02401_amd import build as B
+    tmp = STREAM_LIB + ".tmp%d" % os.getpid()
+    subprocess.run([B.HIPCC, "-x", "hip"] + B.COMMON + ["-shared", STREAM_SRC, "-o", tmp],
+                   check=True)
+    os.replace(tmp, STREAM_LIB)
+    return STREAM_LIB
+
+
+def stream_ceiling(dev, reps: int = 4, gib: int = 2, hot_mib: int = 128):
+    """Streaming-read rate of the GPU with each read route of bench_stream.so:
+    a cold sweep of a `gib` GiB buffer (8x the Infinity Cache, so nearly every
+    byte comes from HBM) at several grid sizes, and a hot re-read of `hot_mib`
+    MiB that the previous sweep left in the Infinity Cache. Times from events
+    around each launch on torch's current stream (the probe launches there)."""
+    import torch
+
+    if not os.path.exists(STREAM_LIB):
+        raise RuntimeError("bench_stream.so is not built; run __graft_entry__.build()")
+    lib = ctypes.CDLL(STREAM_LIB)
+    lib.bench_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
+                                      ctypes.c_int, ctypes.c_int, ctypes.c_void_p]
+    lib.bench_stream_read.restype = ctypes.c_int
+    n = gib << 30
+    buf = torch.full((n // 2,), 1.0, dtype=torch.bfloat16, device=dev)
+    sink = torch.zeros(256, dtype=torch.int32, device=dev)
+    st = torch.cuda.current_stream()
+
+    def launch(nbytes, grid, kind):
+        rc = lib.bench_stream_read(buf.data_ptr(), nbytes, sink.data_ptr(), grid, kind,
+                                   st.cuda_stream)
+        if rc != 0:
+            raise RuntimeError("bench_stream_read failed: hipError %d" % rc)
+
+    def timed(nbytes, grid, kind, warm):
+        ts = []
+        for _ in range(reps):
+            if warm:
+                launch(nbytes, grid, kind)  # leaves the bytes in the Infinity Cache
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(st)
+            launch(nbytes, grid, kind)
+            b.record(st)
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b))
+        ts.sort()
+        return ts[len(ts) // 2]  # median
+
+    out = {"cold_bytes": n, "hot_bytes": hot_mib << 20, "routes": {}}
+    best = 0.0
+    for kind, name in STREAM_KINDS.items():
+        cold = {}
+        for grid in (1024, 2048, 4096, 8192):
+            ms = timed(n, grid, kind, False)
+            cold[grid] = n / (ms / 1e3) / 1e9
+        g_best = max(cold, key=cold.get)
+        hot_ms = timed(hot_mib << 20, g_best, kind, True)
+        out["routes"][name] = {"cold_gbs_by_grid": cold, "cold_gbs": cold[g_best],
+                               "best_grid": g_best,
+                               "hot_gbs": (hot_mib << 20) / (hot_ms / 1e3) / 1e9}
+        best = max(best, cold[g_best])
+    out["ceiling_gbs"] = best
+    out["ceiling_frac_of_peak"] = best / HBM_PEAK_GBS
+    del buf
+    torch.cuda.empty_cache()
+    return out
+
+
 def calibration_copy(mib: int) -> None:
     import torch
     n = mib * 1024 * 1024 // 4
@@ -285,6 +369,297 @@ def calibration_copy(mib: int) -> None:
     print("bench: calibration copy of %d MiB done" % mib, file=sys.stderr, flush=True)
     del src, dst
     torch.cuda.empty_cache()
+
+
+def build_layers(args, wl, dev, n_layers, shared):
+    """Draw the workload's layers on the device, with Algorithm 1 budgets (or
+    the workload's fixed budget) and output buffers. Returns (desc, layers,
+    budgets[prompt][layer], element size); layers[l] = (mask, seqs)."""
+    import numpy as np
+    import torch
+
+    import paper_2508_02401_amd as ckv
+    from paper_2508_02401_amd import synth
+
+    desc = ckv.layer_desc(wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.window, wl.dtype, 0.0,
+                          wl.pool, wl.pool_kernel,
+                          ckv.CKV_KEEP_WINDOW | (ckv.CKV_SHARE_LAYER if shared else 0))
+    elt = torch.tensor([], dtype=wl.dtype).element_size()
+    errs = synth.layer_errors(wl)
+    budgets = []  # [prompt][layer]
+    for L in wl.seq_lens:
+        if wl.budget is not None:
+            budgets.append([wl.budget] * wl.n_layers)
+        else:
+            total, m, M = synth.budget_params(wl, L)
+            b, st = ckv.ckv_allocate_budgets(errs, total, m, M)
+            if st != ckv.CKV_OK:
+                raise RuntimeError("Algorithm 1 could not meet the total")
+            budgets.append([int(x) for x in b])
+    print("bench: drawing %d layers of %s" % (n_layers, wl.name), file=sys.stderr, flush=True)
+    layers = []
+    for l in range(n_layers):
+        inp = synth.layer_inputs(wl, l, dev)
+        seqs = [ckv.alloc_outputs(desc, ckv.Seq(inp.q_win[s], inp.k[s], inp.v[s], budgets[s][l]),
+                                  with_scores=False)
+                for s in range(len(wl.seq_lens))]
+        layers.append((synth.shared_head_mask(wl, l) if shared else inp.mask, seqs))
+    return desc, layers, budgets, elt
+
+
+def measure(args, wl, desc, layers, budgets, elt, dev, hip, schedule, shared=False,
+            copies=None, timed=("rowstats", "score")):
+    """Time args.steps steps of one schedule over the drawn layers and compute
+    the metric, the path's HBM rate and the dominant K pass's roofline.
+
+    schedule: "stack" (one ckv_compress_stack call per step, optionally with a
+    side stream), "layers" (ckv_compress_layer per layer over args.streams
+    streams), "pipeline" (ckv_score on one stream, ckv_select + ckv_gather on a
+    second, one layer apart) or "rotate" (one ckv_compress_layer per step on the
+    next of `copies`, distinct copies of a single layer's inputs, so every step
+    reads its K and V from HBM rather than from the 256 MB Infinity Cache).
+    Returns (result dict, stage means)."""
+    import numpy as np
+    import torch
+
+    import paper_2508_02401_amd as ckv
+
+    main = torch.cuda.current_stream()
+    n_layers = len(layers)
+    side = None
+    n_streams = 1
+    if schedule == "stack":
+        stack_slots = args.stack_slots if args.stack_slots > 0 else n_layers
+        if args.stack_side:
+            stack_slots = max(2, stack_slots)
+            side = torch.cuda.Stream()
+            n_streams = 2
+        ws_bytes = max(ckv.ckv_workspace_bytes(desc, seqs) for _, seqs in layers)
+        ws_stack = torch.empty(stack_slots * ws_bytes, dtype=torch.uint8, device=dev)
+        stack_masks = np.stack([m for m, _ in layers])
+        stack_seqs = [sq for _, sq in layers]
+        sched_text = ("ckv_compress_stack: the two K passes layer by layer, then pooling + "
+                      "selection + gather as four launches per batch of %d layers%s"
+                      % (stack_slots // (2 if args.stack_side else 1),
+                         ", on a side stream beside the next batch's K passes"
+                         if args.stack_side else ""))
+
+        def step(events=None):
+            if events is not None:
+                ns_ = ckv.CKV_NUM_STAGES
+                ckv.ckv_set_stack_stage_events(
+                    [[None] * ns_ if x is None else x[0] for x in events],
+                    [[None] * ns_ if x is None else x[1] for x in events])
+            ckv.ckv_compress_stack(desc, stack_masks, stack_seqs, ws_stack, main, side)
+            if events is not None:
+                ckv.ckv_set_stack_stage_events(None, None)
+    elif schedule == "pipeline":
+        n_streams = 2
+        side = torch.cuda.Stream()
+        ws_bytes = max(ckv.ckv_workspace_bytes(desc, seqs) for _, seqs in layers)
+        wss = [torch.empty(ws_bytes, dtype=torch.uint8, device=dev) for _ in range(2)]
+        score_bufs = [[torch.empty((wl.num_kv_heads, L - wl.window), dtype=torch.float32,
+                                   device=dev) for L in wl.seq_lens] for _ in range(2)]
+        for li, (mask, seqs) in enumerate(layers):
+            for si, sq in enumerate(seqs):
+                sq.scores = score_bufs[li % 2][si]
+        scored = [torch.cuda.Event(enable_timing=False) for _ in range(2)]
+        selected = [torch.cuda.Event(enable_timing=False) for _ in range(2)]
+        sched_text = ("pipeline: K passes + pooling on stream A, selection + gather on stream B, "
+                      "one layer apart")
+
+        def step(events=None):
+            side.wait_stream(main)
+            for li, (mask, seqs) in enumerate(layers):
+                slot = li % 2
+                if events is not None:
+                    ckv.ckv_set_stage_events(*(events[li] if events[li] is not None
+                                               else (None, None)))
+                if li >= 2:
+                    main.wait_event(selected[slot])  # layer li-2 is done with this slot
+                ckv.ckv_score(desc, mask, seqs, wss[slot], main)
+                scored[slot].record(main)
+                side.wait_event(scored[slot])
+                ckv.ckv_select(desc, seqs, wss[slot], side)
+                ckv.ckv_gather(desc, seqs, side)
+                selected[slot].record(side)
+            if events is not None:
+                ckv.ckv_set_stage_events(None, None)
+            main.wait_stream(side)
+    elif schedule == "rotate":
+        assert n_layers == 1 and copies
+        mask = layers[0][0]
+        ws = torch.empty(max(ckv.ckv_workspace_bytes(desc, c) for c in copies), dtype=torch.uint8,
+                         device=dev)
+        turn = [0]
+        sched_text = ("ckv_compress_layer, one layer per step, rotating over %d distinct copies "
+                      "of its inputs (%.2f GB) so that K and V come from HBM"
+                      % (len(copies), sum(int(sq.k.numel() + sq.v.numel()) * elt
+                                          for c in copies for sq in c) / 1e9))
+
+        def step(events=None):
+            c = copies[turn[0] % len(copies)]
+            turn[0] += 1
+            if events is not None and events[0] is not None:
+                ckv.ckv_set_stage_events(events[0][0], events[0][1])
+            ckv.ckv_compress_layer(desc, mask, c, ws, main)
+            if events is not None and events[0] is not None:
+                ckv.ckv_set_stage_events(None, None)
+    else:
+        n_streams = max(1, args.streams)
+        streams = [main] + [torch.cuda.Stream() for _ in range(n_streams - 1)]
+        ws_bytes = max(ckv.ckv_workspace_bytes(desc, seqs) for _, seqs in layers)
+        wss = [torch.empty(ws_bytes, dtype=torch.uint8, device=dev) for _ in range(n_streams)]
+        sched_text = "ckv_compress_layer per layer, round-robin over streams"
+
+        def step(events=None):
+            for st in streams[1:]:
+                st.wait_stream(main)
+            for li, (mask, seqs) in enumerate(layers):
+                si = li % n_streams
+                if events is not None:
+                    ckv.ckv_set_stage_events(*(events[li] if events[li] is not None
+                                               else (None, None)))
+                ckv.ckv_compress_layer(desc, mask, seqs, wss[si], streams[si])
+            if events is not None:
+                ckv.ckv_set_stage_events(None, None)
+            for st in streams[1:]:
+                main.wait_stream(st)
+    torch.cuda.synchronize()
+
+    # Warm up, then time args.steps steps. Only the stages in `timed` (the K
+    # passes) carry kernel start/end events, and only on every N-th layer of a
+    # step (the offset rotates with the step): each timed launch delays the
+    # dispatch of its neighbours by a few microseconds, so the other stages and
+    # layers are left untimed (their times are in the rocprofv3 kernel trace).
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ns = ckv.CKV_NUM_STAGES
+    idx = {n: ckv.STAGE_NAMES.index(n) for n in timed}
+    every = max(1, args.time_every)
+    ev = []  # ev[step][layer] = (begin, end) arrays, or None for an untimed layer
+    for k in range(args.steps):
+        per_layer = []
+        for li in range(n_layers):
+            if (li + k) % every != 0:
+                per_layer.append(None)
+                continue
+            b, e = [None] * ns, [None] * ns
+            for n in timed:
+                b[idx[n]], e[idx[n]] = hip.event(), hip.event()
+            per_layer.append((b, e))
+        ev.append(per_layer)
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record(main)
+    for k in range(args.steps):
+        step(ev[k])
+    t_end.record(main)
+    torch.cuda.synchronize()
+    wall_s = time.perf_counter() - wall0
+    ms_per_step = t_start.elapsed_time(t_end) / args.steps
+    stage_ms = {n: [] for n in timed}
+    sampled = []
+    for k in range(args.steps):
+        for li in range(n_layers):
+            if ev[k][li] is None:
+                continue
+            b, e = ev[k][li]
+            sampled.append(li)
+            for n in timed:
+                stage_ms[n].append(hip.elapsed_ms(b[idx[n]], e[idx[n]]))
+            for x in b + e:
+                if x is not None:
+                    hip.destroy(x)
+    stage_avg = {n: float(np.mean(v)) for n, v in stage_ms.items()}
+
+    tokens_per_layer = sum(wl.seq_lens)
+    value = tokens_per_layer * n_layers / (ms_per_step / 1e3)
+    n_kv, d, w = wl.num_kv_heads, wl.head_dim, wl.window
+    G = wl.num_q_heads // n_kv
+
+    def groups_read(mask):
+        # KV heads whose keys are streamed: those with a chosen query head
+        return len(set((np.nonzero(mask)[0] // G).tolist()))
+
+    # algorithmic bytes of the whole path per layer: K once, the chosen Q rows,
+    # the retained K/V rows read and written, the indices
+    n_sg = 1 if shared else n_kv  # index rows written per prompt
+    path_bytes = 0
+    for li, (mask, seqs) in enumerate(layers):
+        n_chosen = int(np.count_nonzero(mask))
+        for s, L in enumerate(wl.seq_lens):
+            n_ret = min(int(seqs[s].budget), L)
+            path_bytes += groups_read(mask) * L * d * elt + n_chosen * w * d * elt \
+                + 4 * n_kv * n_ret * d * elt + 4 * n_sg * n_ret
+    path_gbs = path_bytes / (ms_per_step / 1e3) / 1e9
+
+    # dominant kernel: the timed K pass with the longest mean launch
+    dom = max(timed, key=lambda n: stage_avg[n])
+    dom_bytes, flops = [], []
+    for li in sampled:
+        mask = layers[li][0]
+        n_chosen = int(np.count_nonzero(mask))
+        b = f = 0
+        for L in wl.seq_lens:
+            n_rd = groups_read(mask)
+            if dom == "rowstats":
+                # every key of the prompt and the chosen Q rows
+                b += n_rd * L * d * elt + n_chosen * w * d * elt
+            else:
+                # prefix keys, chosen Q rows, and the window sum of every
+                # chosen head written per prefix token
+                b += n_rd * (L - w) * d * elt + n_chosen * w * d * elt + n_chosen * (L - w) * 4
+            f += 2 * n_chosen * w * (L if dom == "rowstats" else (L - w)) * d
+        dom_bytes.append(b)
+        flops.append(f)
+    dom_gbs = float(np.mean(dom_bytes)) / (stage_avg[dom] / 1e3) / 1e9
+    dom_tflops = float(np.mean(flops)) / (stage_avg[dom] / 1e3) / 1e12
+    res = {
+        "ms_per_step": ms_per_step,
+        "value": value,
+        "config": {"workload": wl.name, "layers": n_layers, "q_heads": wl.num_q_heads,
+                   "kv_heads": n_kv, "head_dim": d, "seq_lens": list(wl.seq_lens),
+                   "window": w, "pool": "max" if wl.pool == 1 else "avg",
+                   "pool_kernel": wl.pool_kernel, "heads_per_group": list(wl.n_sel_choices),
+                   "budget_avg": float(np.mean([sq.budget for _, seqs in layers for sq in seqs])),
+                   "parallelism": "single GPU",
+                   "head_scope": "layer-shared, 4 heads per layer" if shared else "per KV group",
+                   "streams": n_streams, "schedule": sched_text},
+        "path_hbm_gbs": path_gbs,
+        "path_hbm_frac": path_gbs / HBM_PEAK_GBS,
+        "path_bytes_per_step": path_bytes,
+        "stage_ms_avg": stage_avg,
+        "roofline": {"kernel": dom + "_kernel", "bound": "hbm", "achieved": dom_gbs,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": dom_gbs / HBM_PEAK_GBS,
+                     "traffic": None, "avg_launch_ms": stage_avg[dom],
+                     "algorithmic_bytes_per_launch": float(np.mean(dom_bytes)),
+                     "timed_launches": len(sampled),
+                     "mfma_tflops": dom_tflops, "mfma_frac_bf16": dom_tflops / BF16_PEAK_TFLOPS},
+        "wall_s_timed": wall_s,
+    }
+    return res
+
+
+def rotate_copies(desc, layers, dev, min_bytes: int = 512 << 20, min_copies: int = 8):
+    """Distinct copies of a single layer's inputs (with their own outputs), at
+    least min_copies of them and at least min_bytes of K and V in total."""
+    import paper_2508_02401_amd as ckv
+
+    seqs = layers[0][1]
+    per = sum(int(sq.k.numel() + sq.v.numel()) * sq.k.element_size() for sq in seqs)
+    n = max(min_copies, -(-min_bytes // per))
+    copies = [seqs]
+    for _ in range(n - 1):
+        c = []
+        for sq in seqs:
+            x = ckv.Seq(sq.q_win.clone(), sq.k.clone(), sq.v.clone(), sq.budget)
+            c.append(ckv.alloc_outputs(desc, x, with_scores=False))
+        copies.append(c)
+    return copies
 
 
 def main():
@@ -317,234 +692,29 @@ def main():
     wl = synth.WORKLOADS[args.workload]
     n_layers = wl.n_layers if args.layers <= 0 else min(args.layers, wl.n_layers)
     shared = args.scope == "shared"
-    desc = ckv.layer_desc(wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.window, wl.dtype, 0.0,
-                          wl.pool, wl.pool_kernel,
-                          ckv.CKV_KEEP_WINDOW | (ckv.CKV_SHARE_LAYER if shared else 0))
-    elt = torch.tensor([], dtype=wl.dtype).element_size()
-
-    # budgets per layer and prompt (Algorithm 1 on the host, or the fixed budget)
-    errs = synth.layer_errors(wl)
-    budgets = []  # [prompt][layer]
-    for L in wl.seq_lens:
-        if wl.budget is not None:
-            budgets.append([wl.budget] * wl.n_layers)
-        else:
-            total, m, M = synth.budget_params(wl, L)
-            b, st = ckv.ckv_allocate_budgets(errs, total, m, M)
-            if st != ckv.CKV_OK:
-                raise RuntimeError("Algorithm 1 could not meet the total")
-            budgets.append([int(x) for x in b])
-
-    print("bench: drawing %d layers of %s" % (n_layers, wl.name), file=sys.stderr, flush=True)
-    layers = []
-    for l in range(n_layers):
-        inp = synth.layer_inputs(wl, l, dev)
-        seqs = [ckv.alloc_outputs(desc, ckv.Seq(inp.q_win[s], inp.k[s], inp.v[s], budgets[s][l]),
-                                  with_scores=False)
-                for s in range(len(wl.seq_lens))]
-        layers.append((synth.shared_head_mask(wl, l) if shared else inp.mask, seqs))
-    ws_bytes = max(ckv.ckv_workspace_bytes(desc, seqs) for _, seqs in layers)
-    main = torch.cuda.current_stream()
-    stack = args.schedule == "stack" and not args.pipeline
-    if stack:
-        # one call for the whole stack: the K passes layer by layer, the
-        # selection stages in launches covering a batch of layers
-        stack_slots = args.stack_slots if args.stack_slots > 0 else n_layers
-        if args.stack_side:
-            stack_slots = max(2, stack_slots)
-            side = torch.cuda.Stream()
-            streams = [main, side]
-        else:
-            side = None
-            streams = [main]
-        n_streams = len(streams)
-        ws_stack = torch.empty(stack_slots * ws_bytes, dtype=torch.uint8, device=dev)
-        stack_masks = np.stack([m for m, _ in layers])
-        stack_seqs = [sq for _, sq in layers]
-    elif args.pipeline:
-        # Two-stream pipeline: stream A runs the scoring stages (ckv_score: both
-        # K passes and the pooling) of every layer in order, stream B the
-        # selection and gather (ckv_select, ckv_gather) of layer l while A
-        # scores layer l+1. Two workspaces and score buffers alternate; events
-        # keep A from reusing a slot before B is done with it.
-        n_streams = 2
-        side = torch.cuda.Stream()
-        streams = [main, side]
-        wss = [torch.empty(ws_bytes, dtype=torch.uint8, device=dev) for _ in range(2)]
-        score_bufs = [[torch.empty((wl.num_kv_heads, L - wl.window), dtype=torch.float32, device=dev)
-                       for L in wl.seq_lens] for _ in range(2)]
-        for li, (mask, seqs) in enumerate(layers):
-            for si, sq in enumerate(seqs):
-                sq.scores = score_bufs[li % 2][si]
-        scored = [torch.cuda.Event(enable_timing=False) for _ in range(2)]
-        selected = [torch.cuda.Event(enable_timing=False) for _ in range(2)]
-    else:
-        n_streams = max(1, args.streams)
-        streams = [main] + [torch.cuda.Stream() for _ in range(n_streams - 1)]
-        wss = [torch.empty(ws_bytes, dtype=torch.uint8, device=dev) for _ in range(n_streams)]
-    torch.cuda.synchronize()
-
-    def step_pipeline(events=None):
-        side.wait_stream(main)
-        for li, (mask, seqs) in enumerate(layers):
-            slot = li % 2
-            if events is not None:
-                if events[li] is None:
-                    ckv.ckv_set_stage_events(None, None)
-                else:
-                    ckv.ckv_set_stage_events(events[li][0], events[li][1])
-            if li >= 2:
-                main.wait_event(selected[slot])  # layer li-2 is done with this slot
-            ckv.ckv_score(desc, mask, seqs, wss[slot], main)
-            scored[slot].record(main)
-            side.wait_event(scored[slot])
-            ckv.ckv_select(desc, seqs, wss[slot], side)
-            ckv.ckv_gather(desc, seqs, side)
-            selected[slot].record(side)
-        if events is not None:
-            ckv.ckv_set_stage_events(None, None)
-        main.wait_stream(side)
-
-    def step_layers(events=None):
-        # every layer is independent: layer l runs on stream l % n_streams
-        for st in streams[1:]:
-            st.wait_stream(main)
-        for li, (mask, seqs) in enumerate(layers):
-            si = li % n_streams
-            if events is not None:
-                if events[li] is None:
-                    ckv.ckv_set_stage_events(None, None)
-                else:
-                    ckv.ckv_set_stage_events(events[li][0], events[li][1])
-            ckv.ckv_compress_layer(desc, mask, seqs, wss[si], streams[si])
-        if events is not None:
-            ckv.ckv_set_stage_events(None, None)
-        for st in streams[1:]:
-            main.wait_stream(st)
-
-    def step_stack(events=None):
-        if events is not None:
-            ns_ = ckv.CKV_NUM_STAGES
-            ckv.ckv_set_stack_stage_events(
-                [[None] * ns_ if x is None else x[0] for x in events],
-                [[None] * ns_ if x is None else x[1] for x in events])
-        ckv.ckv_compress_stack(desc, stack_masks, stack_seqs, ws_stack, main, side)
-        if events is not None:
-            ckv.ckv_set_stack_stage_events(None, None)
-
-    step = step_stack if stack else (step_pipeline if args.pipeline else step_layers)
-
     hip = Hip()
-
-    def timed_run(timed):
-        """Warm up, then time args.steps steps. Only the stages in `timed` (K
-        passes) carry kernel start/end events, and only on every N-th layer of
-        a step (the offset rotates with the step): each timed launch delays
-        the dispatch of its neighbours by a few microseconds, so the other
-        stages and layers are left untimed (their times are in the rocprofv3
-        kernel trace). Returns (ms per step, mean launch ms per timed stage,
-        layer of every timed launch, wall seconds)."""
-        for _ in range(args.warmup):
-            step()
-        torch.cuda.synchronize()
-        ns = ckv.CKV_NUM_STAGES
-        idx = {n: ckv.STAGE_NAMES.index(n) for n in timed}
-        every = max(1, args.time_every)
-        ev = []  # ev[step][layer] = (begin, end) arrays, or None for an untimed layer
-        for k in range(args.steps):
-            per_layer = []
-            for li in range(n_layers):
-                if (li + k) % every != 0:
-                    per_layer.append(None)
-                    continue
-                b, e = [None] * ns, [None] * ns
-                for n in timed:
-                    b[idx[n]], e[idx[n]] = hip.event(), hip.event()
-                per_layer.append((b, e))
-            ev.append(per_layer)
-        t_start = torch.cuda.Event(enable_timing=True)
-        t_end = torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        wall0 = time.perf_counter()
-        t_start.record(main)
-        for k in range(args.steps):
-            step(ev[k])
-        t_end.record(main)
-        torch.cuda.synchronize()
-        wall_s = time.perf_counter() - wall0
-        ms = t_start.elapsed_time(t_end) / args.steps
-        stage_ms = {n: [] for n in timed}
-        sampled_layers = []
-        for k in range(args.steps):
-            for li in range(n_layers):
-                if ev[k][li] is None:
-                    continue
-                b, e = ev[k][li]
-                sampled_layers.append(li)
-                for n in timed:
-                    stage_ms[n].append(hip.elapsed_ms(b[idx[n]], e[idx[n]]))
-                for x in b + e:
-                    if x is not None:
-                        hip.destroy(x)
-        return ms, {n: float(np.mean(v)) for n, v in stage_ms.items()}, sampled_layers, wall_s
-
-    ms_per_step, stage_avg, sampled, wall = timed_run(("rowstats", "score"))
-
-    tokens_per_layer = sum(wl.seq_lens)
-    value = tokens_per_layer * n_layers / (ms_per_step / 1e3)
-
-    # algorithmic bytes of the whole path per layer (K once, chosen Q rows,
-    # retained K/V read + written, indices) and of the dominant kernel
+    desc, layers, budgets, elt = build_layers(args, wl, dev, n_layers, shared)
+    schedule = "pipeline" if args.pipeline else args.schedule
+    copies = None
+    if n_layers == 1 and schedule == "stack":
+        # a single layer fits in the Infinity Cache: rotate distinct copies
+        schedule = "rotate"
+        copies = rotate_copies(desc, layers, dev)
+    res = measure(args, wl, desc, layers, budgets, elt, dev, hip, schedule, shared, copies)
+    del copies
+    ms_per_step = res["ms_per_step"]
+    path_bytes = res["path_bytes_per_step"]
     n_kv, d, w = wl.num_kv_heads, wl.head_dim, wl.window
     G = wl.num_q_heads // n_kv
-
-    def groups_read(mask):
-        # KV heads whose keys are streamed: those with a chosen query head
-        return len(set((np.nonzero(mask)[0] // G).tolist()))
-
-    n_sg = 1 if shared else n_kv  # index rows written per prompt
-    path_bytes = 0
-    for li, (mask, seqs) in enumerate(layers):
-        n_chosen = int(np.count_nonzero(mask))
-        for s, L in enumerate(wl.seq_lens):
-            n_ret = min(budgets[s][li], L)
-            path_bytes += groups_read(mask) * L * d * elt + n_chosen * w * d * elt \
-                + 4 * n_kv * n_ret * d * elt + 4 * n_sg * n_ret
-    path_gbs = path_bytes / (ms_per_step / 1e3) / 1e9
-
-    # dominant kernel: the one with the largest share of the step
-    dom = max(("rowstats", "score"), key=lambda n: stage_avg[n])
-    dom_bytes = []
-    for li in sampled:
-        mask = layers[li][0]
-        n_chosen = int(np.count_nonzero(mask))
-        b = 0
-        for L in wl.seq_lens:
-            n_rd = groups_read(mask)
-            if dom == "rowstats":
-                # every key of the prompt and the chosen Q rows
-                b += n_rd * L * d * elt + n_chosen * w * d * elt
-            else:
-                # prefix keys, chosen Q rows, and the window sum of every
-                # chosen head written per prefix token
-                b += n_rd * (L - w) * d * elt + n_chosen * w * d * elt + n_chosen * (L - w) * 4
-        dom_bytes.append(b)
-    dom_gbs = float(np.mean(dom_bytes)) / (stage_avg[dom] / 1e3) / 1e9
-    # MFMA work of the dominant kernel (one logit pass over its keys)
-    flops = []
-    for li in sampled:
-        mask = layers[li][0]
-        n_chosen = int(np.count_nonzero(mask))
-        f = 0
-        for L in wl.seq_lens:
-            f += 2 * n_chosen * w * (L if dom == "rowstats" else (L - w)) * d
-        flops.append(f)
-    dom_tflops = float(np.mean(flops)) / (stage_avg[dom] / 1e3) / 1e12
-
-    traffic = committed_traffic(dom + "_kernel")  # counter-measured HBM bytes per launch
+    tokens_per_layer = sum(wl.seq_lens)
+    dom = res["roofline"]["kernel"]
+    traffic = committed_traffic(dom) if wl.name == "llama8b-128k-stack" else None
+    roof = dict(res["roofline"])
+    roof["traffic"] = traffic
+    roof["traffic_gbs"] = None if traffic is None else traffic / (roof["avg_launch_ms"] / 1e3) / 1e9
     result = {
         "metric": "prompt tokens compressed/sec per layer (L=32K/128K) + achieved HBM GB/s",
-        "value": value,
+        "value": res["value"],
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -556,33 +726,12 @@ def main():
         "dtype": {torch.bfloat16: "bf16", torch.float16: "f16", torch.float32: "f32"}[wl.dtype],
         "data": "synthetic (seeded N(0,1) Q/K/V with planted sink and span keys; no real "
                 "activations or datasets)",
-        "config": {"workload": wl.name, "layers": n_layers, "q_heads": wl.num_q_heads,
-                   "kv_heads": n_kv, "head_dim": d, "seq_lens": list(wl.seq_lens),
-                   "window": w, "pool": "max" if wl.pool == 1 else "avg",
-                   "pool_kernel": wl.pool_kernel, "heads_per_group": list(wl.n_sel_choices),
-                   "budget_avg": float(np.mean(budgets)), "parallelism": "single GPU",
-                   "head_scope": "layer-shared, 4 heads per layer" if shared else
-                                 "per KV group",
-                   "streams": n_streams,
-                   "schedule": ("ckv_compress_stack: the two K passes layer by layer, then "
-                                "pooling + selection + gather as four launches per batch of %d "
-                                "layers%s" % (stack_slots // (2 if args.stack_side else 1),
-                                              ", on a side stream beside the next batch's K passes"
-                                              if args.stack_side else "")) if stack else
-                               ("pipeline: K passes + pooling on stream A, selection + gather on "
-                                "stream B, one layer apart" if args.pipeline else
-                                "ckv_compress_layer per layer, round-robin over streams")},
-        "path_hbm_gbs": path_gbs,
-        "path_hbm_frac": path_gbs / HBM_PEAK_GBS,
-        "stage_ms_avg": stage_avg,
-        "roofline": {"kernel": dom + "_kernel", "bound": "hbm", "achieved": dom_gbs,
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": dom_gbs / HBM_PEAK_GBS,
-                     "traffic": traffic, "traffic_gbs": None if traffic is None else
-                     traffic / (stage_avg[dom] / 1e3) / 1e9, "avg_launch_ms": stage_avg[dom],
-                     "algorithmic_bytes_per_launch": float(np.mean(dom_bytes)),
-                     "timed_launches": len(sampled),
-                     "mfma_tflops": dom_tflops, "mfma_frac_bf16": dom_tflops / BF16_PEAK_TFLOPS},
-        "wall_s_timed": wall,
+        "config": res["config"],
+        "path_hbm_gbs": res["path_hbm_gbs"],
+        "path_hbm_frac": res["path_hbm_frac"],
+        "stage_ms_avg": res["stage_ms_avg"],
+        "roofline": roof,
+        "wall_s_timed": res["wall_s_timed"],
     }
 
     if not args.no_lse_variant:
@@ -609,17 +758,19 @@ def main():
                     del kt
                 sq.lse = lse
         torch.cuda.synchronize()
-        ms_lse, stage_lse, _, _ = timed_run(("score",))
+        r_lse = measure(args, wl, desc, layers, budgets, elt, dev, hip,
+                        "stack" if schedule == "rotate" else schedule, shared, timed=("score",))
         for mask, seqs in layers:
             for sq in seqs:
                 sq.lse = None
+        ms_lse = r_lse["ms_per_step"]
         result["caller_lse_variant"] = {
             "what": "same step with the window rows' log-sum-exp supplied by the caller's prefill "
                     "attention: no row-statistics pass, K read once",
             "ms_per_step": ms_lse, "value": tokens_per_layer * n_layers / (ms_lse / 1e3),
             "path_hbm_gbs": path_bytes / (ms_lse / 1e3) / 1e9,
             "path_hbm_frac": path_bytes / (ms_lse / 1e3) / 1e9 / HBM_PEAK_GBS,
-            "score_kernel_avg_us": stage_lse["score"] * 1e3}
+            "score_kernel_avg_us": r_lse["stage_ms_avg"]["score"] * 1e3}
 
     if not args.no_profile_variant:
         result["error_profile"] = error_profile(args, wl, layers, dev, hip)
@@ -629,7 +780,29 @@ def main():
         result["streaming_preset"] = streaming_preset(wl, layers, dev)
 
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_threads)
+        result["cpu_baseline"] = cpu_baseline(wl, layers, args.cpu_threads, args.cpu_seconds)
+    del layers
+    torch.cuda.empty_cache()
+
+    # the other workloads of the metric, each with its own step and roofline
+    others = {}
+    for name in [x for x in args.configs.split(",") if x and x != wl.name]:
+        owl = synth.WORKLOADS[name]
+        od, ol, ob, oe = build_layers(args, owl, dev, owl.n_layers, False)
+        if owl.n_layers == 1:
+            oc = rotate_copies(od, ol, dev)
+            r = measure(args, owl, od, ol, ob, oe, dev, hip, "rotate", False, oc)
+            del oc
+        else:
+            r = measure(args, owl, od, ol, ob, oe, dev, hip, "stack", False)
+        r.pop("path_bytes_per_step", None)
+        others[name] = r
+        del ol
+        torch.cuda.empty_cache()
+    if others:
+        result["other_configs"] = others
+    if not args.no_stream_ceiling:
+        result["stream_ceiling"] = stream_ceiling(dev)
     print(json.dumps(result), flush=True)
 
 
@@ -765,38 +938,76 @@ def streaming_preset(wl, layers, dev, reps: int = 3):
             "hbm_gbs": nbytes / (ms / 1e3) / 1e9}
 
 
-def cpu_baseline(wl, threads: int, min_seconds: float = 10.0):
-    """The fp64 oracle on a bounded sample of the workload: whole layers, in
-    order, until about min_seconds of oracle time have been spent (at most
-    every layer)."""
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(wl, layers, threads: int, min_seconds: float = 15.0):
+    """The fp64 oracle on a bounded sample of the timed workload: the same
+    inputs (converted to fp64 on the device and copied to the host, untimed)
+    and the same per-layer Algorithm 1 budgets. Independent (layer, prompt, KV
+    head) calls of the oracle's single-threaded group selection run
+    concurrently on `threads` host threads (ctypes releases the GIL), a batch
+    of whole layers at a time, until about min_seconds of wall time are spent.
+    The value is prompt tokens per second per layer, like the GPU's."""
+    import concurrent.futures as cf
+
     import numpy as np
+    import torch
 
     import oracle
-    from paper_2508_02401_amd import synth
 
-    n_threads = threads if threads > 0 else min(os.cpu_count() or 1, 16)
+    n_avail = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    # at most 16 threads: the CPU share of one GPU on a shared host
+    n_threads = threads if threads > 0 else max(1, min(n_avail or 1, 16))
     n_kv, G = wl.num_kv_heads, wl.num_q_heads // wl.num_kv_heads
-    scale = 1.0 / np.sqrt(wl.head_dim)
+    scale = 1.0 / float(np.sqrt(wl.head_dim))
     pool = oracle.POOL_MAX if wl.pool == 1 else oracle.POOL_AVG
-    b = wl.budget if wl.budget is not None else 2 * wl.window
-    spent, tokens, layers_done = 0.0, 0, 0
-    for layer in range(wl.n_layers):
-        inp = synth.layer_inputs(wl, layer, "cpu", with_v=False)
-        for s, L in enumerate(wl.seq_lens):
-            q = inp.q_win[s].double().numpy()
-            k = inp.k[s].double().numpy()
+    tasks_per_layer = n_kv * len(wl.seq_lens)
+    per_batch = max(1, -(-n_threads // tasks_per_layer))  # layers per batch: every thread busy
+
+    def run(q_sel, k, budget):
+        oracle.select_group(q_sel, k, wl.window, scale, pool, wl.pool_kernel, budget)
+
+    spent, layers_done, n_calls = 0.0, 0, 0
+    with cf.ThreadPoolExecutor(max_workers=n_threads) as ex:
+        li = 0
+        while li < len(layers) and spent < min_seconds:
+            batch = layers[li:li + per_batch]
+            jobs = []
+            for mask, seqs in batch:
+                for sq in seqs:
+                    for g in range(n_kv):
+                        heads = [g * G + t for t in range(G) if mask[g * G + t]]
+                        if not heads:
+                            continue
+                        q_sel = sq.q_win[heads].double().cpu().numpy()
+                        k = sq.k[g].double().cpu().numpy()
+                        jobs.append((q_sel, k, int(sq.budget)))
             t0 = time.perf_counter()
-            oracle.select_layer(q, inp.mask, k, wl.window, scale, pool, wl.pool_kernel, b,
-                                n_threads)
+            for f in [ex.submit(run, *j) for j in jobs]:
+                f.result()
             spent += time.perf_counter() - t0
-            tokens += L
-        layers_done += 1
-        if spent >= min_seconds:
-            break
-    return {"value": tokens / spent, "unit": "tokens/s", "cores": min(n_threads, n_kv),
-            "kind": "oracle",
-            "sample": "layers 0-%d of %s, every KV head and prompt (fp64 C oracle, OpenMP over "
-                      "KV heads); %.1f s of oracle time" % (layers_done - 1, wl.name, spent)}
+            n_calls += len(jobs)
+            layers_done += len(batch)
+            li += per_batch
+            del jobs
+    tokens = sum(wl.seq_lens) * layers_done
+    return {"value": tokens / spent, "unit": "tokens/s", "cores": n_threads,
+            "threads": n_threads, "host_cpus": os.cpu_count(), "cpus_available": n_avail,
+            "cpu_model": cpu_model(), "kind": "oracle",
+            "sample": "layers 0-%d of %s (the timed inputs and their Algorithm 1 budgets): %d "
+                      "single-threaded fp64 oracle calls, one per (layer, prompt, KV head), "
+                      "%d at a time; %.1f s of wall time" % (layers_done - 1, wl.name, n_calls,
+                                                             n_threads, spent)}
 
 
 if __name__ == "__main__":

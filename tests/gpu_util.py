@@ -27,15 +27,16 @@ class Case:
     kp: int
     dtype: torch.dtype
     shared: bool = False  # layer-shared selection (CKV_SHARE_LAYER)
+    explicit_scale: float = 0.0  # desc.scale; 0 selects the default 1/sqrt(d)
 
     def desc(self):
         flags = ckv.CKV_KEEP_WINDOW | (ckv.CKV_SHARE_LAYER if self.shared else 0)
-        return ckv.layer_desc(self.H, self.n_kv, self.d, self.w, self.dtype, 0.0, POOL[self.pool],
-                              self.kp, flags)
+        return ckv.layer_desc(self.H, self.n_kv, self.d, self.w, self.dtype, self.explicit_scale,
+                              POOL[self.pool], self.kp, flags)
 
     @property
     def scale(self) -> float:
-        return 1.0 / math.sqrt(self.d)
+        return self.explicit_scale if self.explicit_scale > 0 else 1.0 / math.sqrt(self.d)
 
 
 def run_gpu(case: Case, mask, q_list, k_list, v_list, budgets: Sequence[int],

@@ -82,6 +82,21 @@ def test_layer_parity(dev, label, case, L, n_sel, budget):
     _full_check(case, mask, q, k, v, budget, label, dev)
 
 
+@pytest.mark.parametrize("scale", [0.03, 0.2])
+def test_explicit_scale(dev, scale):
+    # desc.scale given explicitly (not the default 1/sqrt(d) = 0.088): a
+    # flatter (0.03) and a sharper (0.2) softmax, against the oracle at the
+    # same scale
+    case = Case(32, 8, 128, 32, "max", 7, torch.bfloat16, explicit_scale=scale)
+    q, k, v, mask = random_inputs(case, 3001, seed=int(scale * 1000), device="cpu", n_sel=2)
+    print("case explicit scale %g" % scale, flush=True)
+    out = _full_check(case, mask, q, k, v, 400, "scale %g" % scale, dev)
+    # the default scale gives different scores: the explicit one is really used
+    d_case = Case(32, 8, 128, 32, "max", 7, torch.bfloat16)
+    rs, _ = oracle_group(d_case, mask, q, k, 0, 400)
+    assert not np.allclose(out["scores"][0], rs, rtol=1e-2)
+
+
 @pytest.mark.parametrize("budget", [32, 33, 40, 1000])
 def test_window_edge_budgets(dev, budget):
     # L = w + 1: a one-token prefix; B = w keeps only the window, B >= L keeps all

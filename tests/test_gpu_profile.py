@@ -56,6 +56,8 @@ DECODE_CASES = [
     ("f32-d128-G4", 8, 2, 128, torch.float32, 8, 1500),
     ("f32-d64-128rows", 32, 1, 64, torch.float32, 4, 700),
     ("bf16-d64-96rows", 24, 2, 64, torch.bfloat16, 8, 3000),
+    # the full 131072-token caches of the long-context stack
+    ("bf16-d128-G4-131072", 32, 8, 128, torch.bfloat16, 2, 131072),
 ]
 
 
@@ -118,6 +120,8 @@ ERROR_CASES = [
     ("bf16-llama-shape", Case(32, 8, 128, 32, "max", 7, torch.bfloat16), 8192, 512, 4, 4096),
     ("f32-d128", Case(8, 2, 128, 32, "avg", 5, torch.float32), 2000, 200, 6, 1024),
     ("f16-d64-G7", Case(28, 4, 64, 32, "max", 7, torch.float16), 2500, 400, 3, 1792),
+    # a layer of the long-context stack: L = 131072, w = 64, 128 kept tokens
+    ("bf16-llama-131072", Case(32, 8, 128, 64, "max", 7, torch.bfloat16), 131072, 128, 4, 4096),
 ]
 
 
@@ -200,6 +204,10 @@ BATCH_CASES = [
     ("bf16-d128-ragged", 32, 8, 128, torch.bfloat16, [(1, 1), (1, 33), (4, 5000), (2, 700), (1, 129)]),
     ("f16-d64-G7-ragged", 28, 4, 64, torch.float16, [(3, 2077), (1, 31), (1, 64)]),
     ("f32-d128-ragged", 8, 2, 128, torch.float32, [(8, 1500), (1, 2), (5, 321)]),
+    # one decoding step as the long-context stack has it: a full 131072-token
+    # cache beside compact caches of a few hundred tokens
+    ("bf16-d128-131072-and-compact", 32, 8, 128, torch.bfloat16,
+     [(1, 131072), (1, 128), (1, 274), (1, 65)]),
 ]
 
 

@@ -55,6 +55,8 @@ def parse():
                    help="wall time the cpu_baseline sample aims for")
     p.add_argument("--no-stream-ceiling", action="store_true",
                    help="skip the streaming-read ceiling probe (bench_stream.so)")
+    p.add_argument("--stream-ceiling-only", action="store_true",
+                   help="run only the streaming-read ceiling probe and print its JSON")
     p.add_argument("--configs", default="llama8b-32k-layer,llama8b-32k-stack,qwen7b-ragged-batch",
                    help="other workloads measured after the headline one, comma-separated "
                         "('' for none); each gets its own step time and roofline")
@@ -172,6 +174,9 @@ def _kernel_short(name: str) -> str:
         return m.group(1)
     if "neg_kernel" in name:
         return "calibration_copy(neg)"
+    m = re.search(r"stream_read_kernel<(\d+)>", name)
+    if m:
+        return "stream_read_kernel<%s> (%s)" % (m.group(1), STREAM_KINDS[int(m.group(1))])
     return name[:60]
 
 
@@ -184,7 +189,7 @@ def summarize_trace(d: str) -> None:
     rows = list(csv.DictReader(open(stats[0])))
     # this library's kernels (the torch kernels are the input draws, outside
     # the timed region)
-    rows = [r for r in rows if "ckv::" in r["Name"]]
+    rows = [r for r in rows if "ckv::" in r["Name"] or "stream_read_kernel" in r["Name"]]
     print("| kernel | calls | total ms | avg us | min us | max us | % of all GPU time |")
     print("|---|---|---|---|---|---|---|")
     for r in rows:
@@ -687,6 +692,9 @@ def main():
 
     ckv.load()
     dev = torch.device("cuda:0")
+    if args.stream_ceiling_only:
+        print(json.dumps({"stream_ceiling": stream_ceiling(dev)}), flush=True)
+        return
     if args.calibrate_copy > 0:
         calibration_copy(args.calibrate_copy)
     wl = synth.WORKLOADS[args.workload]

@@ -2,9 +2,10 @@
 
 One step = the whole path (score, select, gather) over every layer of the
 workload, with all inputs already resident in HBM. By default one
-ckv_compress_stack call runs all layers: the two K passes of every layer on the
-main stream, the pooling, selection and gather of layer l on a side stream
-while layer l+1's K passes run. --schedule layers issues one
+ckv_compress_stack call runs all layers: the two K passes of every layer,
+consecutive layers alternating between the main stream and a side stream, then
+the pooling, selection and gather of all layers in two launches on the main
+stream. --schedule layers issues one
 ckv_compress_layer per layer instead; --pipeline runs ckv_score (both K passes
 and the pooling) of layer l+1 on one stream while ckv_select and ckv_gather of
 layer l run on another. Prints one JSON line.
@@ -66,14 +67,12 @@ def parse():
                         "launch delays its neighbours' dispatch by a few microseconds")
     p.add_argument("--stack-slots", type=int, default=0,
                    help="--schedule stack: layer slots of workspace (0 = one per layer); the "
-                        "selection stages run in launches covering that many layers (half as many "
-                        "with --stack-side)")
-    p.add_argument("--stack-side", type=int, default=0,
-                   help="--schedule stack: 1 runs a batch's selection stages on a side stream "
-                        "beside the next batch's K passes")
+                        "selection stages run in launches covering that many layers")
+    p.add_argument("--stack-side", type=int, default=1,
+                   help="--schedule stack: 1 (default) gives ckv_compress_stack a side stream, "
+                        "on which every other layer's K passes run; 0 runs them all on one stream")
     p.add_argument("--schedule", choices=("stack", "layers"), default="stack",
-                   help="stack: one ckv_compress_stack call over all layers, the selection of "
-                        "layer l on a side stream beside the K passes of layer l+1 (default); "
+                   help="stack: one ckv_compress_stack call over all layers (default); "
                         "layers: one ckv_compress_layer per layer (see --streams)")
     p.add_argument("--streams", type=int, default=1,
                    help="--schedule layers: layers are issued round-robin on this many streams "
@@ -436,18 +435,16 @@ def measure(args, wl, desc, layers, budgets, elt, dev, hip, schedule, shared=Fal
     if schedule == "stack":
         stack_slots = args.stack_slots if args.stack_slots > 0 else n_layers
         if args.stack_side:
-            stack_slots = max(2, stack_slots)
             side = torch.cuda.Stream()
             n_streams = 2
         ws_bytes = max(ckv.ckv_workspace_bytes(desc, seqs) for _, seqs in layers)
         ws_stack = torch.empty(stack_slots * ws_bytes, dtype=torch.uint8, device=dev)
         stack_masks = np.stack([m for m, _ in layers])
         stack_seqs = [sq for _, sq in layers]
-        sched_text = ("ckv_compress_stack: the two K passes layer by layer, then pooling + "
-                      "selection + gather as four launches per batch of %d layers%s"
-                      % (stack_slots // (2 if args.stack_side else 1),
-                         ", on a side stream beside the next batch's K passes"
-                         if args.stack_side else ""))
+        sched_text = ("ckv_compress_stack: the two K passes layer by layer%s, then pooling + "
+                      "selection + gather as two launches per batch of %d layers"
+                      % (", consecutive layers alternating between two streams"
+                         if args.stack_side else "", stack_slots))
 
         def step(events=None):
             if events is not None:

@@ -210,21 +210,21 @@ int ckv_compress_layer(const ckv_layer_desc *desc, const uint8_t *head_mask, con
  *       layer has the same prompt lengths.
  * Every layer's results are those of ckv_compress_layer on it. The workspace
  * is cut into slots of S = ckv_workspace_bytes(desc, seqs, num_seqs) bytes
- * (n = workspace_bytes / S of them, at least 1, or 2 with a side stream).
- * Layers go in batches of n (n / 2 with a side stream): the two K passes of
- * each layer of a batch run in order on stream, then the batch's selection
- * stages (pooling, top-N, compaction with the gather) run as four launches
- * that each cover the whole batch; a slot per layer of the batch keeps its
- * window sums and selection state meanwhile. With side_stream non-NULL and
- * different from stream, a batch's selection stages run on side_stream while
- * the next batch's K passes run on stream (the slots then form two halves
- * used in turn). The call forks side_stream from stream and joins it back, so
- * all its work is ordered after earlier work on stream and before later work
- * on stream, and side_stream is only ordered after its own earlier work
- * besides. On first use with a side stream the library creates 6 events for
- * the calling host thread and device and keeps them until the process ends.
- * If a launch fails mid-way (CKV_ERR_HIP) the layers before it are enqueued
- * and the fork may be left open: synchronise both streams before reuse. */
+ * (n = workspace_bytes / S of them, at least 1). Layers go in batches of n:
+ * the two K passes of each layer of a batch, then the batch's selection
+ * stages (pooling, top-N, compaction with the gather) as two launches that
+ * each cover the whole batch; a slot per layer of the batch keeps its window
+ * sums and selection state meanwhile. With side_stream non-NULL and different
+ * from stream, the K passes of consecutive layers of a batch alternate
+ * between stream and side_stream (one layer's launches start while the
+ * other's finish), and the batch's selection runs on stream after both. The
+ * call forks side_stream from stream and joins it back, so all its work is
+ * ordered after earlier work on stream and before later work on stream, and
+ * side_stream is only ordered after its own earlier work besides. On first
+ * use with a side stream the library creates 3 events for the calling host
+ * thread and device and keeps them until the process ends. If a launch fails
+ * mid-way (CKV_ERR_HIP) the layers before it are enqueued and the fork may be
+ * left open: synchronise both streams before reuse. */
 int ckv_compress_stack(const ckv_layer_desc *desc, int32_t n_layers, const uint8_t *head_masks,
                        const ckv_seq *seqs, int32_t num_seqs, void *workspace,
                        size_t workspace_bytes, void *stream, void *side_stream);

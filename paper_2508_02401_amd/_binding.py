@@ -295,8 +295,9 @@ def ckv_compress_layer_noalloc(desc, head_mask, seqs: Sequence[Seq], stream=None
 def ckv_compress_stack(desc, head_masks, seqs: Sequence[Sequence[Seq]], workspace: torch.Tensor,
                        stream=None, side_stream=None) -> None:
     """head_masks [n_layers][H]; seqs[l] is layer l's list of prompts (the same
-    lengths in every layer). With a side stream the workspace holds two layer
-    slots (2 * ckv_workspace_bytes of one layer)."""
+    lengths in every layer). The workspace holds at least one layer slot
+    (ckv_workspace_bytes of one layer); with a side stream, consecutive
+    layers' K passes alternate between the two streams."""
     n_layers = len(seqs)
     num_seqs = len(seqs[0]) if n_layers else 0
     if any(len(x) != num_seqs for x in seqs):

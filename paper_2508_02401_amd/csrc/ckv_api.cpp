@@ -21,7 +21,7 @@ thread_local void* const* g_stack_begin = nullptr;
 thread_local void* const* g_stack_end = nullptr;
 thread_local int32_t g_stack_layers = 0;
 constexpr int kMaxDevices = 16;
-enum SyncEvent { kEvFork = 0, kEvJoin = 1, kEvScored = 2, kEvSelected = 4, kNumSyncEvents = 6 };
+enum SyncEvent { kEvFork = 0, kEvScored = 1, kEvSelected = 2, kNumSyncEvents = 3 };
 thread_local hipEvent_t g_sync_ev[kMaxDevices][kNumSyncEvents] = {};
 
 constexpr size_t kAlign = 256;
@@ -479,16 +479,17 @@ int ckv_compress_stack(const ckv_layer_desc* desc, int32_t n_layers, const uint8
       return rc;
   }
   // Layers go in batches of `batch`, one workspace slot per layer of a batch:
-  // the K passes of the batch's layers on the stream, then its selection
-  // stages as four launches that each cover the whole batch. With a side
-  // stream the slots form two halves, and the selection of one batch runs
-  // there while the K passes of the next run on the stream.
+  // the K passes of the batch's layers, then its selection stages as two
+  // launches that each cover the whole batch. With a side stream the K passes
+  // of consecutive layers alternate between the two streams, so that one
+  // layer's launches ramp up while the other's drain; the batch's selection
+  // runs on the stream once both streams' K passes of the batch are done, and
+  // the side stream starts the next batch only after that selection (it
+  // reuses the slots).
   const size_t n_slots = workspace ? workspace_bytes / slot_bytes : 0;
-  if (!workspace || !aligned16(workspace) || n_slots < (two ? 2u : 1u)) return CKV_ERR_WORKSPACE;
-  int32_t batch = (int32_t)((two ? n_slots / 2 : n_slots) < (size_t)n_layers
-                                ? (two ? n_slots / 2 : n_slots)
-                                : (size_t)n_layers);
-  // fork/join and hand-off events of this thread on the current device
+  if (!workspace || !aligned16(workspace) || n_slots < 1) return CKV_ERR_WORKSPACE;
+  const int32_t batch = n_slots < (size_t)n_layers ? (int32_t)n_slots : n_layers;
+  // fork/join events of this thread on the current device
   hipEvent_t* ev = nullptr;
   if (two) {
     int dev = 0;
@@ -518,13 +519,14 @@ int ckv_compress_stack(const ckv_layer_desc* desc, int32_t n_layers, const uint8
       g_ev_end[i] = g_events_on ? (hipEvent_t)g_stack_end[l * ckv::kNumStages + i] : nullptr;
     }
   };
-  for (int32_t b0 = 0, j = 0; b0 < n_layers && rc == CKV_OK; b0 += batch, ++j) {
-    const int half = two ? (j & 1) : 0;
+  for (int32_t b0 = 0; b0 < n_layers && rc == CKV_OK; b0 += batch) {
     const int32_t nb = n_layers - b0 < batch ? n_layers - b0 : batch;
-    char* base = static_cast<char*>(workspace) + (size_t)half * batch * slot_bytes;
+    char* base = static_cast<char*>(workspace);
     hipError_t e;
-    // the selection of batch j-2 used these slots: wait until it is done
-    if (two && j >= 2 && (e = hipStreamWaitEvent(st, ev[kEvSelected + half], 0)) != hipSuccess) {
+    // the previous batch's selection (on the stream) used these slots
+    if (two && b0 > 0 &&
+        ((e = hipEventRecord(ev[kEvSelected], st)) != hipSuccess ||
+         (e = hipStreamWaitEvent(side, ev[kEvSelected], 0)) != hipSuccess)) {
       rc = hip_fail(e);
       break;
     }
@@ -539,17 +541,14 @@ int ckv_compress_stack(const ckv_layer_desc* desc, int32_t n_layers, const uint8
       a.do_gather = 1;
       a.table_out = ws;  // the argument block the selection launches read
       use_layer_events(l);
-      rc = run_kpasses(desc, a, st);
+      rc = run_kpasses(desc, a, two && (i & 1) ? side : st);
     }
     if (rc != CKV_OK) break;
-    hipStream_t sel = st;
-    if (two) {
-      if ((e = hipEventRecord(ev[kEvScored + half], st)) != hipSuccess ||
-          (e = hipStreamWaitEvent(side, ev[kEvScored + half], 0)) != hipSuccess) {
-        rc = hip_fail(e);
-        break;
-      }
-      sel = side;
+    if (two && nb > 1 &&
+        ((e = hipEventRecord(ev[kEvScored], side)) != hipSuccess ||
+         (e = hipStreamWaitEvent(st, ev[kEvScored], 0)) != hipSuccess)) {
+      rc = hip_fail(e);
+      break;
     }
     // the batch's selection stages in two launches: the pooling (with the
     // scores and histograms), then one workgroup per selection unit (layer,
@@ -563,7 +562,7 @@ int ckv_compress_stack(const ckv_layer_desc* desc, int32_t n_layers, const uint8
     m.per_layer = 0;
     for (int i = 0; i < a.num_seqs; ++i)
       m.per_layer += a.n_sg * (int32_t)ceil_div(a.seq[i].n_ptiles, ckv::kUnitPoolTiles);
-    if ((e = ckv::launch_pool_units(m, sel, timing(ckv::kStagePool, true, true))) != hipSuccess) {
+    if ((e = ckv::launch_pool_units(m, st, timing(ckv::kStagePool, true, true))) != hipSuccess) {
       rc = hip_fail(e);
       break;
     }
@@ -573,11 +572,7 @@ int ckv_compress_stack(const ckv_layer_desc* desc, int32_t n_layers, const uint8
       tm.start = g_ev_begin[ckv::kStageSelect];
       tm.stop = g_ev_end[ckv::kStageGather];
     }
-    if ((e = ckv::launch_select_units(m, sel, tm)) != hipSuccess) {
-      rc = hip_fail(e);
-      break;
-    }
-    if (two && (e = hipEventRecord(ev[kEvSelected + half], side)) != hipSuccess) {
+    if ((e = ckv::launch_select_units(m, st, tm)) != hipSuccess) {
       rc = hip_fail(e);
       break;
     }
@@ -587,13 +582,7 @@ int ckv_compress_stack(const ckv_layer_desc* desc, int32_t n_layers, const uint8
     g_ev_begin[i] = saved_b[i];
     g_ev_end[i] = saved_e[i];
   }
-  if (rc != CKV_OK) return rc;
-  if (two) {
-    hipError_t e;
-    if ((e = hipEventRecord(ev[kEvJoin], side)) != hipSuccess) return hip_fail(e);
-    if ((e = hipStreamWaitEvent(st, ev[kEvJoin], 0)) != hipSuccess) return hip_fail(e);
-  }
-  return CKV_OK;
+  return rc;
 }
 
 int ckv_allocate_budgets(const double* err_norm, int32_t n_layers, int64_t total, int32_t m,

@@ -334,24 +334,24 @@ def test_stack_rejects_bad_layers():
     assert _stack_call(_desc(pool_kernel=4), three, [ok_mask] * 3) == ckv.CKV_ERR_INVALID_ARG
 
 
-def test_stack_workspace_holds_two_slots_with_a_side_stream():
+def test_stack_workspace_needs_one_slot():
     lib = ckv.load()
     d = _desc()
     arr = (ckv._binding.ckv_seq * 1)(_seq())
     one = lib.ckv_workspace_bytes(ctypes.byref(d), arr, 1)
-    # a side stream needs two layer slots; the (fake) stream handle is never
-    # touched because the size check fails first
-    assert _stack_call(d, [[_seq()], [_seq()]], [[1] * 8] * 2, ws_bytes=2 * one - 1,
+    # one layer slot is the least the stack takes, with or without a side
+    # stream; the (fake) stream handle is never touched because the size check
+    # fails first
+    assert _stack_call(d, [[_seq()], [_seq()]], [[1] * 8] * 2, ws_bytes=one - 1,
                        side=0x1000) == ckv.CKV_ERR_WORKSPACE
     assert _stack_call(d, [[_seq()], [_seq()]], [[1] * 8] * 2, ws_bytes=0,
                        side=None) == ckv.CKV_ERR_WORKSPACE
 
 
 def test_selection_kernels_fit_beside_two_k_pass_workgroups():
-    # With a side stream, ckv_compress_stack pools a batch of layers while the
-    # next batch's K passes run, and a caller that runs layers on several
-    # streams can overlap one layer's selection kernels with another layer's
-    # K passes: each of those kernels must fit in the LDS that two K-pass
+    # A caller that runs layers on several streams can overlap one layer's
+    # selection kernels with another layer's K passes: each of those kernels
+    # must fit in the LDS that two K-pass
     # workgroups leave free on a CU (160 KB). The stack's one-workgroup-per-
     # group selection kernel is not among them (it holds a 131072-token
     # segment's bitmaps in LDS and waits for CUs to drain).

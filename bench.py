@@ -539,19 +539,32 @@ def measure(args, wl, desc, layers, budgets, elt, dev, hip, schedule, shared=Fal
     torch.cuda.synchronize()
     ns = ckv.CKV_NUM_STAGES
     idx = {n: ckv.STAGE_NAMES.index(n) for n in timed}
+    i_pool, i_sel, i_gat = (ckv.STAGE_NAMES.index(n) for n in ("pool", "select", "gather"))
+    # the stack's selection launches carry the events of the batch's first
+    # layer: with one batch, layer 0's pool begin and gather end bracket them
+    sel_timed = schedule == "stack" and args.stack_slots <= 0
     every = max(1, args.time_every)
     ev = []  # ev[step][layer] = (begin, end) arrays, or None for an untimed layer
+    kp_timed = []  # kp_timed[step][layer]: the K passes carry events
     for k in range(args.steps):
-        per_layer = []
+        per_layer, flags = [], []
         for li in range(n_layers):
-            if (li + k) % every != 0:
+            kp = (li + k) % every == 0
+            sel = sel_timed and li == 0
+            flags.append(kp)
+            if not kp and not sel:
                 per_layer.append(None)
                 continue
             b, e = [None] * ns, [None] * ns
-            for n in timed:
-                b[idx[n]], e[idx[n]] = hip.event(), hip.event()
+            if kp:
+                for n in timed:
+                    b[idx[n]], e[idx[n]] = hip.event(), hip.event()
+            if sel:
+                b[i_pool], e[i_pool] = hip.event(), hip.event()
+                b[i_sel], e[i_gat] = hip.event(), hip.event()
             per_layer.append((b, e))
         ev.append(per_layer)
+        kp_timed.append(flags)
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -560,19 +573,24 @@ def measure(args, wl, desc, layers, budgets, elt, dev, hip, schedule, shared=Fal
     for k in range(args.steps):
         step(ev[k])
     t_end.record(main)
+    host_s = time.perf_counter() - wall0  # enqueueing alone
     torch.cuda.synchronize()
     wall_s = time.perf_counter() - wall0
     ms_per_step = t_start.elapsed_time(t_end) / args.steps
     stage_ms = {n: [] for n in timed}
+    sel_ms = []
     sampled = []
     for k in range(args.steps):
         for li in range(n_layers):
             if ev[k][li] is None:
                 continue
             b, e = ev[k][li]
-            sampled.append(li)
-            for n in timed:
-                stage_ms[n].append(hip.elapsed_ms(b[idx[n]], e[idx[n]]))
+            if kp_timed[k][li]:
+                sampled.append(li)
+                for n in timed:
+                    stage_ms[n].append(hip.elapsed_ms(b[idx[n]], e[idx[n]]))
+            if b[i_pool] is not None:
+                sel_ms.append(hip.elapsed_ms(b[i_pool], e[i_gat]))
             for x in b + e:
                 if x is not None:
                     hip.destroy(x)
@@ -620,6 +638,30 @@ def measure(args, wl, desc, layers, budgets, elt, dev, hip, schedule, shared=Fal
         flops.append(f)
     dom_gbs = float(np.mean(dom_bytes)) / (stage_avg[dom] / 1e3) / 1e9
     dom_tflops = float(np.mean(flops)) / (stage_avg[dom] / 1e3) / 1e12
+    # The K-pass phase of the step as a whole: with a side stream two K-pass
+    # launches are in flight at once (one per stream), so a launch's own
+    # duration overstates its share of the step. Phase = step time minus the
+    # selection launches (timed on layer 0's events); bytes = the algorithmic
+    # bytes of every layer's timed passes.
+    kpass_phase = None
+    if sel_ms:
+        ph_bytes = 0
+        for mask, seqs in layers:
+            n_chosen = int(np.count_nonzero(mask))
+            for L in wl.seq_lens:
+                n_rd = groups_read(mask)
+                if "rowstats" in timed:
+                    ph_bytes += n_rd * L * d * elt + n_chosen * w * d * elt
+                ph_bytes += n_rd * (L - w) * d * elt + n_chosen * w * d * elt + n_chosen * (L - w) * 4
+        ph_ms = ms_per_step - float(np.mean(sel_ms))
+        kpass_phase = {"what": "the K passes of all %d layers (%s), %s: their algorithmic bytes "
+                               "over the step time minus the selection launches"
+                               % (n_layers, " + ".join(timed),
+                                  "two launches in flight, one per stream" if side is not None
+                                  else "one stream"),
+                       "ms": ph_ms, "selection_ms": float(np.mean(sel_ms)),
+                       "bytes": ph_bytes, "gbs": ph_bytes / (ph_ms / 1e3) / 1e9,
+                       "frac": ph_bytes / (ph_ms / 1e3) / 1e9 / HBM_PEAK_GBS}
     res = {
         "ms_per_step": ms_per_step,
         "value": value,
@@ -635,13 +677,16 @@ def measure(args, wl, desc, layers, budgets, elt, dev, hip, schedule, shared=Fal
         "path_hbm_frac": path_gbs / HBM_PEAK_GBS,
         "path_bytes_per_step": path_bytes,
         "stage_ms_avg": stage_avg,
+        "kpass_phase": kpass_phase,
         "roofline": {"kernel": dom + "_kernel", "bound": "hbm", "achieved": dom_gbs,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": dom_gbs / HBM_PEAK_GBS,
                      "traffic": None, "avg_launch_ms": stage_avg[dom],
                      "algorithmic_bytes_per_launch": float(np.mean(dom_bytes)),
                      "timed_launches": len(sampled),
+                     "launches_in_flight": 2 if side is not None else 1,
                      "mfma_tflops": dom_tflops, "mfma_frac_bf16": dom_tflops / BF16_PEAK_TFLOPS},
         "wall_s_timed": wall_s,
+        "host_enqueue_ms_per_step": host_s * 1e3 / args.steps,
     }
     return res
 
@@ -735,8 +780,10 @@ def main():
         "path_hbm_gbs": res["path_hbm_gbs"],
         "path_hbm_frac": res["path_hbm_frac"],
         "stage_ms_avg": res["stage_ms_avg"],
+        "kpass_phase": res["kpass_phase"],
         "roofline": roof,
         "wall_s_timed": res["wall_s_timed"],
+        "host_enqueue_ms_per_step": res["host_enqueue_ms_per_step"],
     }
 
     if not args.no_lse_variant:
@@ -775,7 +822,8 @@ def main():
             "ms_per_step": ms_lse, "value": tokens_per_layer * n_layers / (ms_lse / 1e3),
             "path_hbm_gbs": path_bytes / (ms_lse / 1e3) / 1e9,
             "path_hbm_frac": path_bytes / (ms_lse / 1e3) / 1e9 / HBM_PEAK_GBS,
-            "score_kernel_avg_us": r_lse["stage_ms_avg"]["score"] * 1e3}
+            "score_kernel_avg_us": r_lse["stage_ms_avg"]["score"] * 1e3,
+            "kpass_phase": r_lse["kpass_phase"]}
 
     if not args.no_profile_variant:
         result["error_profile"] = error_profile(args, wl, layers, dev, hip)

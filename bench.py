@@ -21,6 +21,7 @@ from __future__ import annotations
 
 import argparse
 import ctypes
+import gc
 import json
 import os
 import sys
@@ -110,8 +111,11 @@ class Hip:
         self.lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
                                                  ctypes.c_void_p]
         self.lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.free = []  # events handed back by destroy(), reused by event()
 
     def event(self):
+        if self.free:
+            return self.free.pop()
         e = ctypes.c_void_p()
         rc = self.lib.hipEventCreate(ctypes.byref(e))
         if rc != 0:
@@ -126,7 +130,9 @@ class Hip:
         return out.value
 
     def destroy(self, e):
-        self.lib.hipEventDestroy(e)
+        # kept for reuse: creating and destroying hundreds of events per
+        # measurement left later measurements' launches slow to submit
+        self.free.append(e)
 
 
 KERNEL_SOURCES = ("paper_2508_02401_amd/csrc/ckv_score.hip", "paper_2508_02401_amd/csrc/ckv_select.hip",
@@ -568,6 +574,10 @@ def measure(args, wl, desc, layers, budgets, elt, dev, hip, schedule, shared=Fal
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
+    # no garbage collection while steps are enqueued: a collection over the
+    # objects of earlier measurements stalls submission for milliseconds
+    gc.collect()
+    gc.disable()
     wall0 = time.perf_counter()
     t_start.record(main)
     for k in range(args.steps):
@@ -576,6 +586,7 @@ def measure(args, wl, desc, layers, budgets, elt, dev, hip, schedule, shared=Fal
     host_s = time.perf_counter() - wall0  # enqueueing alone
     torch.cuda.synchronize()
     wall_s = time.perf_counter() - wall0
+    gc.enable()
     ms_per_step = t_start.elapsed_time(t_end) / args.steps
     stage_ms = {n: [] for n in timed}
     sel_ms = []

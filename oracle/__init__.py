@@ -78,6 +78,14 @@ def _load():
                                           i32, d, i32, i32, i64, P(d), P(i32), i32]
         lib.ckvo_select_layer.restype = i64
         lib.ckvo_select_layer_shared.argtypes = lib.ckvo_select_layer.argtypes
+        lib.ckvo_select_tokens_all.argtypes = [P(d), i64, i64, P(i32)]
+        lib.ckvo_select_tokens_all.restype = i64
+        lib.ckvo_select_group_all.argtypes = [P(d), i32, P(d), i64, i32, i32, d, i32, i32, i64,
+                                              P(d), P(i32)]
+        lib.ckvo_select_group_all.restype = i64
+        lib.ckvo_select_layer_shared_all.argtypes = [P(d), P(ctypes.c_uint8), i32, i32, P(d), i64,
+                                                     i32, i32, d, i32, i32, i64, P(d), P(i32)]
+        lib.ckvo_select_layer_shared_all.restype = i64
         lib.ckvo_select_layer_shared.restype = i64
         lib.ckvo_decode_attention.argtypes = [P(d), P(d), P(d), i32, i32, i64, i32, d, P(d)]
         lib.ckvo_decode_attention.restype = ctypes.c_int
@@ -249,6 +257,53 @@ def select_layer_shared(q, mask, k, w: int, scale: float, pool_mode: int, kp: in
     if n < 0:
         raise OracleError(int(n), "select_layer_shared")
     return scores, idx
+
+
+def select_tokens_all(a, L: int, budget: int) -> np.ndarray:
+    """Keep-window flag off: the budget best tokens of [0, L) by score a[L]
+    (lower index first on ties), ascending; all L when budget >= L."""
+    a = _f64(a)
+    out = np.empty(min(budget, L) if budget >= 1 else 1, dtype=np.int32)
+    n = _load().ckvo_select_tokens_all(_ptr(a, ctypes.c_double), L, budget, _ptr(out, ctypes.c_int32))
+    if n < 0:
+        raise OracleError(int(n), "select_tokens_all")
+    return out[:n]
+
+
+def select_group_all(q_sel, k, w: int, scale: float, pool_mode: int, kp: int, budget: int):
+    """One KV group with the keep-window flag off: (scores [L], idx [min(B, L)])."""
+    q_sel, k = _f64(q_sel), _f64(k)
+    n_sel, w_, d = q_sel.shape
+    assert w_ == w
+    L = k.shape[0]
+    scores = np.empty(L, dtype=np.float64)
+    idx = np.empty(max(1, min(budget, L)), dtype=np.int32)
+    n = _load().ckvo_select_group_all(
+        _ptr(q_sel, ctypes.c_double), n_sel, _ptr(k, ctypes.c_double), L, d, w, scale,
+        pool_mode, kp, budget, _ptr(scores, ctypes.c_double), _ptr(idx, ctypes.c_int32))
+    if n < 0:
+        raise OracleError(int(n), "select_group_all")
+    return scores, idx[:n]
+
+
+def select_layer_shared_all(q, mask, k, w: int, scale: float, pool_mode: int, kp: int,
+                            budget: int):
+    """The layer-shared selection with the keep-window flag off. q [H, w, d],
+    mask [H], k [n_kv, L, d]: (scores [L], idx [min(B, L)])."""
+    q, k = _f64(q), _f64(k)
+    mask = np.ascontiguousarray(np.asarray(mask, dtype=np.uint8))
+    H, w_, d = q.shape
+    n_kv, L, d2 = k.shape
+    assert w_ == w and d2 == d and mask.shape == (H,)
+    scores = np.empty(L, dtype=np.float64)
+    idx = np.empty(max(1, min(budget, L)), dtype=np.int32)
+    n = _load().ckvo_select_layer_shared_all(
+        _ptr(q, ctypes.c_double), _ptr(mask, ctypes.c_uint8), H, n_kv, _ptr(k, ctypes.c_double),
+        L, d, w, scale, pool_mode, kp, budget, _ptr(scores, ctypes.c_double),
+        _ptr(idx, ctypes.c_int32))
+    if n < 0:
+        raise OracleError(int(n), "select_layer_shared_all")
+    return scores, idx[:n]
 
 
 def decode_attention(q, k, v, scale: float):

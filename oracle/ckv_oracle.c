@@ -34,7 +34,11 @@
  *      the whole layer pick one index set for every head; the mean runs over
  *      all chosen heads, each scored against its own group's keys).
  *   R9 the budget B counts the w window tokens, which are always kept; the
- *      other B-w come from the prefix; B >= L keeps every token.
+ *      other B-w come from the prefix; B >= L keeps every token. With the
+ *      keep-window flag off (the *_all functions) the window tokens are not
+ *      kept by rule: every column of [0, L) is scored (window columns by the
+ *      rows that see them, R2), pooled over [0, L) with R5's padding, and the
+ *      best B of all L tokens are kept (B >= 1).
  *   R10 equal scores: the lower token index wins.
  *   R11 retained indices are returned in ascending order.
  *   R13 query head h belongs to KV group h / (H / n_kv).
@@ -369,6 +373,108 @@ int64_t ckvo_select_layer_shared(const double *q, const uint8_t *mask, int32_t H
   free(pooled);
   if (status < 0) return status;
   return ckvo_select_tokens(scores, L, w, budget, idx);
+}
+
+/* Selection over the whole prompt, for the keep-window flag off (the
+ * alternative of reading R9): the window tokens are not kept by rule but
+ * compete with the prefix for the budget. Every column j in [0, L) is scored:
+ * a prefix column by all w window rows, a window column L-w+c only by the
+ * rows i >= c that see it (the causal window sums of ckvo_window_sums). */
+
+/* The budget tokens of [0, L) with the largest scores a[] (equal scores: the
+ * lower index first), written to idx in ascending order; all L when budget >=
+ * L. Returns the number written, or a negative code (budget < 1). */
+int64_t ckvo_select_tokens_all(const double *a, int64_t L, int64_t budget, int32_t *idx) {
+  if (!a || !idx || L < 1) return CKVO_EINVAL;
+  if (budget < 1) return CKVO_EBUDGET;
+  if (budget >= L) {
+    for (int64_t j = 0; j < L; ++j) idx[j] = (int32_t)j;
+    return L;
+  }
+  ckvo_ranked *r = (ckvo_ranked *)malloc(sizeof(ckvo_ranked) * (size_t)L);
+  if (!r) return CKVO_ENOMEM;
+  for (int64_t j = 0; j < L; ++j) {
+    r[j].score = a[j];
+    r[j].index = j;
+  }
+  qsort(r, (size_t)L, sizeof(ckvo_ranked), ckvo_rank_cmp);
+  for (int64_t t = 0; t < budget; ++t) idx[t] = (int32_t)r[t].index;
+  free(r);
+  qsort(idx, (size_t)budget, sizeof(int32_t), ckvo_index_cmp);
+  return budget;
+}
+
+/* One KV group over the whole prompt: window sums of the chosen heads over
+ * [0, L), each pooled over [0, L) (R5's padding at both ends), averaged over
+ * the heads (R6), then the budget best tokens of [0, L). scores is [L]; idx
+ * gets min(budget, L) entries. */
+int64_t ckvo_select_group_all(const double *q_sel, int32_t n_sel, const double *k, int64_t L,
+                              int32_t d, int32_t w, double scale, int32_t pool_mode, int32_t kp,
+                              int64_t budget, double *scores, int32_t *idx) {
+  if (!q_sel || !k || !scores || n_sel < 1 || w < 1 || L <= w) return CKVO_EINVAL;
+  if (kp < 1 || (kp % 2) == 0) return CKVO_EINVAL;
+  if (budget < 1) return CKVO_EBUDGET;
+  double *S = (double *)malloc(sizeof(double) * (size_t)(n_sel * L));
+  double *P = (double *)malloc(sizeof(double) * (size_t)L);
+  if (!S || !P) {
+    free(S);
+    free(P);
+    return CKVO_ENOMEM;
+  }
+  int rc = ckvo_window_sums(q_sel, n_sel, k, L, d, w, scale, S);
+  if (rc == CKVO_OK) {
+    for (int64_t j = 0; j < L; ++j) scores[j] = 0.0;
+    for (int32_t h = 0; h < n_sel; ++h) {
+      ckvo_pool(S + (int64_t)h * L, L, kp, pool_mode, P);
+      for (int64_t j = 0; j < L; ++j) scores[j] += P[j];
+    }
+    for (int64_t j = 0; j < L; ++j) scores[j] /= (double)n_sel;
+  }
+  free(S);
+  free(P);
+  if (rc != CKVO_OK) return rc;
+  if (!idx) return CKVO_OK;
+  return ckvo_select_tokens_all(scores, L, budget, idx);
+}
+
+/* The layer-shared selection (see ckvo_select_layer_shared) over the whole
+ * prompt: every chosen head's window sums over [0, L) against its own group's
+ * keys, pooled over [0, L), averaged over the chosen heads in head order, and
+ * the budget best tokens of [0, L). scores is [L]; idx gets min(budget, L)
+ * entries. */
+int64_t ckvo_select_layer_shared_all(const double *q, const uint8_t *mask, int32_t H,
+                                     int32_t n_kv, const double *k, int64_t L, int32_t d,
+                                     int32_t w, double scale, int32_t pool_mode, int32_t kp,
+                                     int64_t budget, double *scores, int32_t *idx) {
+  if (!q || !mask || !k || !scores || !idx || H < 1 || n_kv < 1 || H % n_kv)
+    return CKVO_EINVAL;
+  if (L <= w || w < 1 || d < 1 || kp < 1 || (kp % 2) == 0) return CKVO_EINVAL;
+  if (budget < 1) return CKVO_EBUDGET;
+  int32_t G = H / n_kv, n_chosen = 0;
+  for (int32_t h = 0; h < H; ++h) n_chosen += mask[h] != 0;
+  if (n_chosen == 0) return CKVO_EMASK;
+  double *S = (double *)malloc(sizeof(double) * (size_t)L);
+  double *P = (double *)malloc(sizeof(double) * (size_t)L);
+  if (!S || !P) {
+    free(S);
+    free(P);
+    return CKVO_ENOMEM;
+  }
+  for (int64_t j = 0; j < L; ++j) scores[j] = 0.0;
+  int rc = CKVO_OK;
+  for (int32_t h = 0; h < H && rc == CKVO_OK; ++h) {
+    if (!mask[h]) continue;
+    rc = ckvo_window_sums(q + (int64_t)h * w * d, 1, k + (int64_t)(h / G) * L * d, L, d, w,
+                          scale, S);
+    if (rc != CKVO_OK) break;
+    ckvo_pool(S, L, kp, pool_mode, P);
+    for (int64_t j = 0; j < L; ++j) scores[j] += P[j];
+  }
+  for (int64_t j = 0; j < L; ++j) scores[j] /= (double)n_chosen;
+  free(S);
+  free(P);
+  if (rc != CKVO_OK) return rc;
+  return ckvo_select_tokens_all(scores, L, budget, idx);
 }
 
 /* Decode attention (Eq. 2 for one query per head): head h attends to the

@@ -91,6 +91,79 @@ def test_hand_example_mean_then_pool_differs():
 
 
 # ---------------------------------------------------------------------------
+# Keep-window flag off: the whole prompt competes for the budget.
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("case", HAND["selection_no_window"]["cases"], ids=lambda c: c["why"][:40])
+def test_hand_example_selection_no_window(case):
+    mask = case["mask"]
+    scores, idx = oracle.select_group_all(HW_Q[mask], HW_K, HAND["window"], 1.0,
+                                          POOLS[case["pool"]], case["kp"], case["budget"])
+    assert idx.tolist() == case["idx"]
+    assert scores.shape == (6,)
+    for j in range(6):
+        expect = _frac(case["scores"][j])
+        assert _close(scores[j], expect), (j, scores[j], expect)
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_select_tokens_all_brute_force(seed):
+    # every subset of size B of a tiny prompt with many tied scores: exactly
+    # one of them has every kept token ranked above every dropped one (score
+    # descending, then lower index), and it is the oracle's
+    from itertools import combinations
+    rng = np.random.default_rng(300 + seed)
+    L = int(rng.integers(1, 9))
+    a = rng.integers(0, 4, size=L).astype(np.float64) / 4.0
+    for B in range(1, L + 2):
+        idx = oracle.select_tokens_all(a, L, B).tolist()
+        if B >= L:
+            assert idx == list(range(L))
+            continue
+        good = []
+        for T in combinations(range(L), B):
+            drop = [u for u in range(L) if u not in T]
+            if all(a[t] > a[u] or (a[t] == a[u] and t < u) for t in T for u in drop):
+                good.append(list(T))
+        assert len(good) == 1 and idx == good[0], (a.tolist(), B, idx, good)
+
+
+def test_select_tokens_all_rejects_empty_budget():
+    with pytest.raises(oracle.OracleError):
+        oracle.select_tokens_all(np.ones(5), 5, 0)
+
+
+@pytest.mark.parametrize("pool,kp", [("avg", 5), ("max", 7), ("max", 1)])
+def test_select_group_all_agrees_with_prefix_path_away_from_the_window(pool, kp):
+    # the prefix columns' scores are the same whether or not the window is
+    # kept, except within the pool radius of the prefix's end (where the
+    # whole-prompt pooling sees window columns instead of padding); with the
+    # window tokens excluded the whole-prompt top-B is a top-(B-w) of the prefix
+    rng = np.random.default_rng(kp)
+    L, w, d = 90, 6, 8
+    q = rng.standard_normal((2, w, d))
+    k = rng.standard_normal((L, d))
+    s_kw, _, _ = oracle.select_group(q, k, w, 0.3, POOLS[pool], kp, 20)
+    s_all, _ = oracle.select_group_all(q, k, w, 0.3, POOLS[pool], kp, 20)
+    r = kp // 2
+    np.testing.assert_allclose(s_all[:L - w - r], s_kw[:L - w - r], rtol=1e-14, atol=0)
+    assert not np.allclose(s_all[L - w - r:L - w], s_kw[L - w - r:], rtol=1e-6) or r == 0
+
+
+def test_select_layer_shared_all_matches_group_all_for_one_group():
+    # a layer of one KV group: the shared selection over its chosen heads is
+    # that group's own selection
+    rng = np.random.default_rng(12)
+    H, w, d, L = 4, 5, 8, 70
+    q = rng.standard_normal((H, w, d))
+    k = rng.standard_normal((1, L, d))
+    mask = np.array([1, 0, 1, 1], np.uint8)
+    s_sh, i_sh = oracle.select_layer_shared_all(q, mask, k, w, 0.4, oracle.POOL_MAX, 5, 17)
+    s_g, i_g = oracle.select_group_all(q[mask.astype(bool)], k[0], w, 0.4, oracle.POOL_MAX, 5, 17)
+    np.testing.assert_allclose(s_sh, s_g, rtol=1e-13)
+    assert i_sh.tolist() == i_g.tolist()
+
+
+# ---------------------------------------------------------------------------
 # Attention rows: library softmax, normalisation, scale, operand order.
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("seed", [0, 1, 2])

@@ -45,7 +45,7 @@ extern "C" {
 #define CKV_OK 0
 #define CKV_ERR_INVALID_ARG (-1) /* null pointer, bad size/stride/alignment, even pool kernel */
 #define CKV_ERR_UNSUPPORTED (-2) /* dtype, head_dim, window or head count outside the built set */
-#define CKV_ERR_BUDGET (-3)      /* budget below the window; Algorithm 1 could not meet the total */
+#define CKV_ERR_BUDGET (-3)      /* budget below the window (or below 1); Algorithm 1 could not meet the total */
 #define CKV_ERR_MASK (-4)        /* a KV group has no chosen query head (per-group scope), or no head at all */
 #define CKV_ERR_WORKSPACE (-5)   /* workspace missing or smaller than ckv_workspace_bytes() */
 #define CKV_ERR_HIP (-6)         /* a HIP runtime call failed; see ckv_last_hip_error() */
@@ -55,7 +55,14 @@ typedef enum { CKV_BF16 = 0, CKV_F16 = 1, CKV_F32 = 2 } ckv_dtype;
 typedef enum { CKV_POOL_AVG = 0, CKV_POOL_MAX = 1 } ckv_pool;
 
 /* flags */
-#define CKV_KEEP_WINDOW (1u << 0) /* required: the w window tokens are always kept and count in B */
+/* Window retention (the paper leaves it open; Sec. 3.3 follows SnapKV). With
+ * this flag the w window tokens are always kept and count in B: only the
+ * prefix [0, L-w) is scored and ranked, and the best B - w prefix tokens are
+ * kept beside the window (requires B >= w). Without it every token competes:
+ * all L columns are scored (window column L-w+c only by the window rows
+ * i >= c that see it), pooled over [0, L), and the best B of all L tokens are
+ * kept (requires B >= 1). Shapes that change with this flag are noted below. */
+#define CKV_KEEP_WINDOW (1u << 0)
 /* Head scope of the selection (paper Sec. 3.3). Without this flag every KV
  * group g ranks its tokens with its own chosen heads and keeps its own index
  * set. With it, the chosen heads of the whole layer (any groups; a group may
@@ -90,7 +97,8 @@ typedef enum { CKV_POOL_AVG = 0, CKV_POOL_MAX = 1 } ckv_pool;
  *                CKV_POOL_MAX (padding ignored); pool_kernel odd, 1..31
  *                (1 = no pooling). Stride 1; the neighbourhood of token j is
  *                [j - k/2, j + k/2] clipped to the ranked prefix [0, L - w).
- *   flags        must contain CKV_KEEP_WINDOW; may contain CKV_SHARE_LAYER.
+ *   flags        any of CKV_KEEP_WINDOW and CKV_SHARE_LAYER (other bits:
+ *                CKV_ERR_UNSUPPORTED).
  */
 typedef struct {
   int32_t num_q_heads;
@@ -114,17 +122,18 @@ typedef struct {
  *   k, v    [n_kv, L, d]: the prompt's key/value cache; token t of KV head g
  *           at k + g*kv_stride_head + t*kv_stride_tok (same strides for v).
  *   seq_len L > w, L < 2^31.
- *   budget  B, tokens kept per KV head including the w window tokens
- *           (B >= w). B >= L keeps every token. The top B - w of the prefix
- *           [0, L - w) are kept; ties go to the lower index.
- *   scores  [n_kv, L - w] fp32 ([L - w] under CKV_SHARE_LAYER): the averaged
- *           score of every prefix token. Written by ckv_score, read by
- *           ckv_select; may be NULL for ckv_compress_layer (the workspace holds
- *           it then).
+ *   budget  B, tokens kept per KV head. With CKV_KEEP_WINDOW it includes the
+ *           w window tokens (B >= w) and the top B - w of the prefix
+ *           [0, L - w) are kept; without it the top B of all L tokens are kept
+ *           (B >= 1). B >= L keeps every token. Ties go to the lower index.
+ *   scores  [n_kv, Lsc] fp32 ([Lsc] under CKV_SHARE_LAYER), Lsc = L - w with
+ *           CKV_KEEP_WINDOW and L without: the averaged score of every ranked
+ *           token. Written by ckv_score, read by ckv_select; may be NULL for
+ *           ckv_compress_layer (the workspace holds it then).
  *   idx     [n_kv, min(B, L)] int32 ([min(B, L)] under CKV_SHARE_LAYER):
  *           retained token positions per KV head (or for every head) in
- *           ascending order (the last w are L-w..L-1). Written by ckv_select,
- *           read by ckv_gather.
+ *           ascending order (with CKV_KEEP_WINDOW the last w are L-w..L-1).
+ *           Written by ckv_select, read by ckv_gather.
  *   k_out, v_out [n_kv, min(B, L), d] contiguous, dtype of the layer: the
  *           compact cache, row r of head g is K[g, idx[g, r], :] (idx[r] under
  *           CKV_SHARE_LAYER).
@@ -168,16 +177,18 @@ size_t ckv_workspace_bytes(const ckv_layer_desc *desc, const ckv_seq *seqs, int3
  * CKV_SHARE_LAYER, where at least one head of the layer must be chosen and
  * groups without one are not read. Writes
  * seqs[s].scores for every prompt s. Window row i (position L-w+i) attends to
- * keys 0..L-w+i; its softmax runs over all of them, and only the prefix
- * columns [0, L-w) are scored. */
+ * keys 0..L-w+i; its softmax runs over all of them. With CKV_KEEP_WINDOW only
+ * the prefix columns [0, L-w) are scored; without it all L columns are, a
+ * window column by the rows that see it. */
 int ckv_score(const ckv_layer_desc *desc, const uint8_t *head_mask, const ckv_seq *seqs,
               int32_t num_seqs, void *workspace, size_t workspace_bytes, void *stream);
 
 /* Top-N selection, paper Sec. 3.3 (the N best-scoring tokens are kept):
  * for every prompt and KV head, reads
- * scores (>= 0, finite) and writes idx: the B - w best prefix tokens (higher
- * score first, lower index on ties) in ascending order, then the window
- * positions; or 0..L-1 when B >= L. */
+ * scores (>= 0, finite) and writes idx: with CKV_KEEP_WINDOW the B - w best
+ * prefix tokens (higher score first, lower index on ties) in ascending order,
+ * then the window positions; without it the B best of all L tokens in
+ * ascending order; 0..L-1 when B >= L. */
 int ckv_select(const ckv_layer_desc *desc, const ckv_seq *seqs, int32_t num_seqs,
                void *workspace, size_t workspace_bytes, void *stream);
 

@@ -370,14 +370,16 @@ def ckv_set_stack_stage_events(begin, end) -> None:
 # --------------------------------------------------------------------------
 def alloc_outputs(desc: ckv_layer_desc, s: Seq, with_scores: bool = True) -> Seq:
     """Allocate scores/idx/k_out/v_out for one prompt on the device of s.k
-    (one score row and one index row under CKV_SHARE_LAYER)."""
+    (one score row and one index row under CKV_SHARE_LAYER; score rows of L - w
+    with CKV_KEEP_WINDOW, of L without)."""
     L = s.k.shape[1] if s.seq_len is None else s.seq_len
     n_kv, d = desc.num_kv_heads, desc.head_dim
     n_sg = 1 if desc.flags & CKV_SHARE_LAYER else n_kv
     n_ret = min(int(s.budget), L)
     dev = s.k.device
+    tail = desc.window if desc.flags & CKV_KEEP_WINDOW else 0  # tokens kept by rule, unscored
     if with_scores:
-        s.scores = torch.empty((n_sg, L - desc.window), dtype=torch.float32, device=dev)
+        s.scores = torch.empty((n_sg, L - tail), dtype=torch.float32, device=dev)
     s.idx = torch.empty((n_sg, n_ret), dtype=torch.int32, device=dev)
     s.k_out = torch.empty((n_kv, n_ret, d), dtype=s.k.dtype, device=dev)
     s.v_out = torch.empty((n_kv, n_ret, d), dtype=s.k.dtype, device=dev)

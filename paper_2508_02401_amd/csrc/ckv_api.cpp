@@ -38,6 +38,10 @@ int64_t range_size(int64_t Ls) {
   return per <= ckv::kRangeMin ? ckv::kRangeMin : ceil_div(per, ckv::kRangeMin) * ckv::kRangeMin;
 }
 
+// Tokens at the end of a prompt that are kept by rule and not ranked: the
+// window with CKV_KEEP_WINDOW, none without (then all L tokens are scored).
+int64_t kept_tail(const ckv_layer_desc* d) { return (d->flags & CKV_KEEP_WINDOW) ? d->window : 0; }
+
 // Selections per prompt: one per KV group, or one for the layer.
 int64_t sel_groups(const ckv_layer_desc* d) {
   return (d->flags & CKV_SHARE_LAYER) ? 1 : d->num_kv_heads;
@@ -65,7 +69,7 @@ int64_t max_units(const ckv_layer_desc* d) {
   return (int64_t)d->num_kv_heads * ckv::group_units((int)wsum_heads(d), heads_per_unit(d));
 }
 
-// Floats per window-sum row: the prefix length rounded up to 4, so that every
+// Floats per window-sum row: the scored length rounded up to 4, so that every
 // row starts 16-byte aligned.
 int64_t ws_stride(int64_t Ls) { return (Ls + 3) / 4 * 4; }
 
@@ -77,7 +81,7 @@ struct WsLayout {
 
 WsLayout seq_ws_layout(const ckv_layer_desc* d, const ckv_seq* s) {
   const int64_t n_kv = d->num_kv_heads, n_sg = sel_groups(d);
-  const int64_t Ls = s->seq_len - d->window;
+  const int64_t Ls = s->seq_len - kept_tail(d);  // scored length
   const int64_t n_ranges = ceil_div(Ls, range_size(Ls));
   WsLayout w;
   size_t o = 0;
@@ -114,8 +118,7 @@ int check_desc(const ckv_layer_desc* d) {
   if (d->pool != CKV_POOL_AVG && d->pool != CKV_POOL_MAX) return CKV_ERR_INVALID_ARG;
   if (d->pool_kernel < 1 || d->pool_kernel % 2 == 0) return CKV_ERR_INVALID_ARG;
   if (d->pool_kernel > CKV_MAX_POOL_KERNEL) return CKV_ERR_UNSUPPORTED;
-  if (!(d->flags & CKV_KEEP_WINDOW) || (d->flags & ~(CKV_KEEP_WINDOW | CKV_SHARE_LAYER)))
-    return CKV_ERR_UNSUPPORTED;
+  if (d->flags & ~(CKV_KEEP_WINDOW | CKV_SHARE_LAYER)) return CKV_ERR_UNSUPPORTED;
   if (!(d->scale > 0.f) && !(d->scale <= 0.f)) return CKV_ERR_INVALID_ARG;  // NaN
   if (isinf(d->scale)) return CKV_ERR_INVALID_ARG;
   return CKV_OK;
@@ -131,7 +134,7 @@ int check_seqs(const ckv_layer_desc* d, const ckv_seq* seqs, int32_t n, unsigned
   for (int32_t i = 0; i < n; ++i) {
     const ckv_seq& s = seqs[i];
     if (s.seq_len <= d->window || s.seq_len >= ((int64_t)1 << 31)) return CKV_ERR_INVALID_ARG;
-    if (s.budget < d->window) return CKV_ERR_BUDGET;
+    if (s.budget < (kept_tail(d) > 0 ? kept_tail(d) : 1)) return CKV_ERR_BUDGET;
     if ((need & kNeedQ) && (!s.q_win || !aligned16(s.q_win))) return CKV_ERR_INVALID_ARG;
     if (need & kNeedQ) {
       if (s.q_stride_head < 0 || s.q_stride_row < 0) return CKV_ERR_INVALID_ARG;
@@ -175,6 +178,7 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
   a.shared = (d->flags & CKV_SHARE_LAYER) ? 1 : 0;
   a.n_sg = (int32_t)sel_groups(d);
   a.lse_given = seqs[0].lse != nullptr;
+  a.tail = (int16_t)kept_tail(d);
   if (mask) {
     const int G = d->num_q_heads / d->num_kv_heads;
     int off = 0;
@@ -212,7 +216,7 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
   for (int32_t i = 0; i < n; ++i) {
     const ckv_seq& s = seqs[i];
     ckv::SeqArgs& q = a.seq[i];
-    const int64_t Ls = s.seq_len - d->window;
+    const int64_t Ls = s.seq_len - a.tail;  // scored length
     q.q = s.q_win;
     q.k = s.k;
     q.v = s.v;
@@ -222,7 +226,7 @@ int build_args(const ckv_layer_desc* d, const uint8_t* mask, const ckv_seq* seqs
     q.kv_st = s.kv_stride_tok;
     q.L = s.seq_len;
     q.n_ret = (int32_t)(s.budget < s.seq_len ? s.budget : s.seq_len);
-    q.n_keep = s.budget >= s.seq_len ? -1 : s.budget - d->window;
+    q.n_keep = s.budget >= s.seq_len ? -1 : s.budget - a.tail;
     q.scores = s.scores;
     q.idx = s.idx;
     q.k_out = s.k_out;

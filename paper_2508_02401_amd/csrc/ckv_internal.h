@@ -145,6 +145,8 @@ struct LayerArgs {
   int16_t grp_off[kMaxKvHeads + 1];  // chosen heads of group g: sel[grp_off[g] .. grp_off[g+1])
   uint8_t sel[kMaxQHeads];
   uint8_t sel_grp[kMaxQHeads];       // KV group of chosen head t (sel[t] / G)
+  int16_t tail;            // w when the window tokens are kept by rule (then only
+                           // [0, L - w) is scored and ranked), 0 when every token competes
   SeqArgs seq[kMaxSeqs];
 };
 

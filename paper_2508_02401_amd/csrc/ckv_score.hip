@@ -303,6 +303,20 @@ __device__ __forceinline__ void kpass_locate(const LayerArgs& a, const SeqArgs& 
   p = P = 1;
 }
 
+// Causal mask of a 32-key block of window-sum logits (pass 2's layout: lane
+// half h holds rows qb*32 + acc_row(v, h) of key tok): window row i of a
+// head (padded row index modulo w8) sees keys up to Lw + i, where Lw = L - w
+// is the window's first position. Only blocks that reach the window need it,
+// and only when the window columns are scored (the keep-window flag off).
+__device__ __forceinline__ void mask_window_block(f32x16& acc, int qb, int64_t tok, int64_t Lw,
+                                                  int w8, int h) {
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int iw = (qb * 32 + acc_row(v, h)) % w8;
+    if (tok > Lw + iw) acc[v] = -INFINITY;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Pass 1: row statistics.
 // ---------------------------------------------------------------------------
@@ -487,7 +501,10 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int qg = wave / WPQ, sub = wave % WPQ;  // query group: blocks qg*NQ .. qg*NQ+NQ-1
   const bool active = qg * NQ < nqb;
-  const int64_t Ls = sq.L - a.w;
+  // scored columns [0, Ls): the prefix when the window is kept by rule, the
+  // whole prompt otherwise (window columns then take the causal mask)
+  const int64_t Lw = sq.L - a.w, Ls = sq.L - a.tail;
+  const bool window_cols = a.tail == 0;
   const int64_t stride = (int64_t)P * ST;
   const float alpha = a.alpha;
   const char* kbase = static_cast<const char*>(sq.k) + (int64_t)g * sq.kv_sh * S::EB;
@@ -593,9 +610,18 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
     if (!active || sub >= S::BLOCKS) return;
     f32x16 acc[NQ][NB];
     stage_tiles<DT, S, WPQ, NQ, false>(slot, opoff, q, acc);
+    const int64_t ts = (int64_t)p * ST + (int64_t)k * stride;  // the stage's first key
+    if (window_cols && ts + ST > Lw) {  // a stage that reaches the window (uniform)
+#pragma unroll
+      for (int j = 0; j < NQ; ++j)
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+          const int64_t t0 = ts + (sub + i * WPQ) * 32;
+          if (t0 + 32 > Lw) mask_window_block(acc[j][i], qg * NQ + j, t0 + l32, Lw, a.w8, h);
+        }
+    }
     if constexpr (DIRECT > 0) {
       static_assert(QM && NQ % (DIRECT > 0 ? DIRECT : 1) == 0, "whole heads per wave");
-      const int64_t ts = (int64_t)p * ST + (int64_t)k * stride;
 #pragma unroll
       for (int i = 0; i < NB; ++i) {
         // column sums of tile (j, i) over its 32 query rows, as in QM below
@@ -633,8 +659,8 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
       for (int i = 0; i < NB; ++i) {
         // columns at or past Ls get values too; the fold never writes them out
         // acc[j][i][v]: query row qb*32 + acc_row(v, h), key (sub + i*WPQ)*32 +
-        // l32 of the stage; prefix keys are visible to every window row, so no
-        // mask is needed (keys at or past Ls are never written out).
+        // l32 of the stage; prefix keys are visible to every window row, and
+        // scored window keys were masked above.
         float gs[4];
 #pragma unroll
         for (int a4 = 0; a4 < 4; ++a4)
@@ -817,7 +843,7 @@ __device__ __forceinline__ void pool_body(const LayerArgs& a, int b) {
   const int local = b - sq.blk_pool;
   const int g = local / sq.n_ptiles;  // selection group (0 when shared)
   const int tile = local - g * sq.n_ptiles;
-  const int64_t Ls = sq.L - a.w;
+  const int64_t Ls = sq.L - a.tail;  // scored length
   // the heads averaged here: the group's chosen heads, or every chosen head
   // of the layer when the selection is shared
   const int t0 = a.shared ? 0 : a.grp_off[g];
@@ -867,7 +893,7 @@ __global__ __launch_bounds__(kThreads) void pool_units_kernel(const MultiArgs m)
   const int per_g = (sq.n_ptiles + kUnitPoolTiles - 1) / kUnitPoolTiles;
   const int g = local / per_g;
   const int chunk = local - g * per_g;
-  const int64_t Ls = sq.L - a.w;
+  const int64_t Ls = sq.L - a.tail;  // scored length
   const int t0 = a.shared ? 0 : a.grp_off[g];
   const int t1 = a.shared ? a.grp_off[a.n_kv] : a.grp_off[g + 1];
   for (int t = t0 + (int)threadIdx.x; t < t1; t += kThreads) {

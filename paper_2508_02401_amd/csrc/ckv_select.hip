@@ -61,7 +61,7 @@ __global__ __launch_bounds__(kThreads) void hist_kernel(const LayerArgs a) {
   const int g = local / sq.n_ranges, r = local - g * sq.n_ranges;
   if (sq.n_keep <= 0) return;
   const int tid = threadIdx.x;
-  const int64_t Ls = sq.L - a.w;
+  const int64_t Ls = sq.L - a.tail;  // scored length
   const float* sc = sq.scores + (int64_t)g * Ls;
   const int64_t j0 = (int64_t)r * sq.range;
   const int64_t j1 = j0 + sq.range < Ls ? j0 + sq.range : Ls;
@@ -175,7 +175,7 @@ __device__ __forceinline__ void filter_body(const LayerArgs& a, int b) {
   const int g = local / sq.n_ranges, r = local - g * sq.n_ranges;
   if (sq.n_keep <= 0) return;
   const int tid = threadIdx.x, lane = tid & 63;
-  const int64_t Ls = sq.L - a.w;
+  const int64_t Ls = sq.L - a.tail;  // scored length
   uint32_t* ctl = sq.ctl + g * kCtlWords;
   const uint32_t* ghist = sq.hist + (int64_t)g * kHistBins;
   const float* sc = sq.scores + (int64_t)g * Ls;
@@ -265,7 +265,7 @@ __device__ __forceinline__ void resolve_body(const LayerArgs& a, int b) {
   const int s = b / a.n_sg, g = b - s * a.n_sg;
   const SeqArgs& sq = a.seq[s];
   if (sq.n_keep <= 0) return;
-  resolve(sq, a.n_sg, g, sq.L - a.w, sq.ctl + g * kCtlWords, lds_a, lds_b, wsum, res);
+  resolve(sq, a.n_sg, g, sq.L - a.tail, sq.ctl + g * kCtlWords, lds_a, lds_b, wsum, res);
 }
 
 __global__ __launch_bounds__(kThreads) void resolve_kernel(const LayerArgs a) {
@@ -285,7 +285,7 @@ __device__ __forceinline__ void compact_body(const LayerArgs& a, int b) {
   const int local = b - sq.blk_sel;
   const int g = local / sq.n_ranges, r = local - g * sq.n_ranges;
   const int tid = threadIdx.x;
-  const int w = a.w;
+  const int w = a.tail;  // tokens kept by rule after the ranked ones
   const int64_t Ls = sq.L - w;
   int32_t* out = sq.idx + (int64_t)g * sq.n_ret;
   const int64_t j0 = (int64_t)r * sq.range;

@@ -120,7 +120,7 @@ __device__ __forceinline__ void unit_body(const LayerArgs& a, int u, UnitLds& sm
   const int tid = threadIdx.x, lane = tid & 63;
   const int s = u / a.n_sg, g = u - s * a.n_sg;
   const SeqArgs& sq = a.seq[s];
-  const int w = a.w;
+  const int w = a.tail;  // tokens kept by rule after the ranked ones
   const int64_t Ls = sq.L - w;
   // the KV heads whose rows this selection keeps
   const int gk0 = a.shared ? 0 : g, gk1 = a.shared ? a.n_kv : g + 1;

@@ -28,9 +28,16 @@ class Case:
     dtype: torch.dtype
     shared: bool = False  # layer-shared selection (CKV_SHARE_LAYER)
     explicit_scale: float = 0.0  # desc.scale; 0 selects the default 1/sqrt(d)
+    keep_window: bool = True     # CKV_KEEP_WINDOW: the window is kept by rule, not ranked
+
+    @property
+    def tail(self) -> int:
+        """Tokens at the end kept by rule (the window), 0 when all compete."""
+        return self.w if self.keep_window else 0
 
     def desc(self):
-        flags = ckv.CKV_KEEP_WINDOW | (ckv.CKV_SHARE_LAYER if self.shared else 0)
+        flags = (ckv.CKV_KEEP_WINDOW if self.keep_window else 0) | \
+            (ckv.CKV_SHARE_LAYER if self.shared else 0)
         return ckv.layer_desc(self.H, self.n_kv, self.d, self.w, self.dtype, self.explicit_scale,
                               POOL[self.pool], self.kp, flags)
 
@@ -67,13 +74,20 @@ def oracle_group(case: Case, mask, q: torch.Tensor, k: torch.Tensor, g: int, bud
     heads = chosen_heads(mask, case.H, case.n_kv, g)
     q_sel = q[heads].double().cpu().numpy()
     kg = k[g].double().cpu().numpy()
+    if not case.keep_window:
+        return oracle.select_group_all(q_sel, kg, case.w, case.scale, ORACLE_POOL[case.pool],
+                                       case.kp, int(budget))
     scores, idx, _ = oracle.select_group(q_sel, kg, case.w, case.scale, ORACLE_POOL[case.pool],
                                          case.kp, int(budget))
     return scores, idx
 
 
 def oracle_shared(case: Case, mask, q: torch.Tensor, k: torch.Tensor, budget: int):
-    """The layer-shared selection of the oracle: (scores [L-w], idx [min(B, L)])."""
+    """The layer-shared selection of the oracle: (scores [L-w] or [L], idx [min(B, L)])."""
+    if not case.keep_window:
+        return oracle.select_layer_shared_all(q.double().cpu().numpy(), mask,
+                                              k.double().cpu().numpy(), case.w, case.scale,
+                                              ORACLE_POOL[case.pool], case.kp, int(budget))
     return oracle.select_layer_shared(q.double().cpu().numpy(), mask, k.double().cpu().numpy(),
                                       case.w, case.scale, ORACLE_POOL[case.pool], case.kp,
                                       int(budget))
@@ -100,10 +114,10 @@ def check_group(case: Case, gpu: dict, g: int, ref_scores, ref_idx, k: torch.Ten
     else:
         rel = float("nan")
     gi = gpu["idx"][g]
-    ok, swaps, msg = parity.index_swaps(gi, ref_idx, ref_scores, L, case.w)
+    ok, swaps, msg = parity.index_swaps(gi, ref_idx, ref_scores, L, case.tail)
     assert ok, "%s group %d: %s" % (label, g, msg)
     # the GPU's selection is exactly the top-N of the GPU's own scores
-    n_keep = len(gi) - case.w
+    n_keep = len(gi) - case.tail
     if gs is not None and len(gi) < L:
         own = parity.topn_reference(np.asarray(gs, dtype=np.float64), n_keep)
         np.testing.assert_array_equal(gi[:n_keep], own, err_msg="%s group %d own top-N" % (label, g))

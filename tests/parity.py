@@ -29,7 +29,9 @@ def score_errors(gpu: np.ndarray, ref: np.ndarray):
 
 
 def index_swaps(gpu_idx: np.ndarray, ref_idx: np.ndarray, ref_scores: np.ndarray, L: int, w: int):
-    """Check one KV head's retained set. Returns (ok, swap count, message)."""
+    """Check one KV head's retained set; w is the number of tokens at the end
+    kept by rule (the window), 0 when every token is ranked. Returns (ok,
+    swap count, message)."""
     gpu_idx = np.asarray(gpu_idx, dtype=np.int64)
     ref_idx = np.asarray(ref_idx, dtype=np.int64)
     if gpu_idx.shape != ref_idx.shape:

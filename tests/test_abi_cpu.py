@@ -90,11 +90,30 @@ def _call(fn, desc, seq, mask=None, ws=True, n=1):
     (dict(num_q_heads=7), ckv.CKV_ERR_INVALID_ARG),
     (dict(window=0), ckv.CKV_ERR_INVALID_ARG),
     (dict(window=129), ckv.CKV_ERR_UNSUPPORTED),
-    (dict(flags=0), ckv.CKV_ERR_UNSUPPORTED),
+    (dict(flags=4), ckv.CKV_ERR_UNSUPPORTED),
+    (dict(flags=ckv.CKV_KEEP_WINDOW | ckv.CKV_SHARE_LAYER | 8), ckv.CKV_ERR_UNSUPPORTED),
     (dict(scale=float("nan")), ckv.CKV_ERR_INVALID_ARG),
 ])
 def test_bad_descriptor(fn, bad, expect):
     assert _call(fn, _desc(**bad), _seq()) == expect
+
+
+def test_keep_window_off_budget_rules_and_workspace():
+    # without CKV_KEEP_WINDOW every token competes: a budget below the window
+    # is fine, a budget of 0 is not; all L columns are scored, so the
+    # workspace grows by the window's columns
+    lib = ckv.load()
+    on, off = _desc(), _desc(flags=0)
+    arr = (ckv._binding.ckv_seq * 1)(_seq())
+    w_on = lib.ckv_workspace_bytes(ctypes.byref(on), arr, 1)
+    w_off = lib.ckv_workspace_bytes(ctypes.byref(off), arr, 1)
+    assert w_off > w_on > 0
+    assert _call("compress", on, _seq(budget=on.window - 1)) == ckv.CKV_ERR_BUDGET
+    assert _call("compress", off, _seq(budget=0)) == ckv.CKV_ERR_BUDGET
+    # validation passes (the launch then fails here, where there is no GPU)
+    assert _call("compress", off, _seq(budget=1)) not in (ckv.CKV_ERR_BUDGET,
+                                                           ckv.CKV_ERR_INVALID_ARG,
+                                                           ckv.CKV_ERR_UNSUPPORTED)
 
 
 @pytest.mark.parametrize("fn", ["score", "compress", "select", "gather"])

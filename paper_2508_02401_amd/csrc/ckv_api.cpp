@@ -566,7 +566,7 @@ int ckv_compress_stack(const ckv_layer_desc* desc, int32_t n_layers, const uint8
     m.per_layer = 0;
     for (int i = 0; i < a.num_seqs; ++i)
       m.per_layer += a.n_sg * (int32_t)ceil_div(a.seq[i].n_ptiles, ckv::kUnitPoolTiles);
-    if ((e = ckv::launch_pool_units(m, st, timing(ckv::kStagePool, true, true))) != hipSuccess) {
+    if ((e = ckv::launch_pool_units(m, desc->pool_kernel >> 1, st, timing(ckv::kStagePool, true, true))) != hipSuccess) {
       rc = hip_fail(e);
       break;
     }

@@ -23,7 +23,7 @@ constexpr int kMinStagesPerWg = 65536 / kStageBytes; // K stages per workgroup (
 constexpr int kTargetWgs = 512;    // K-pass workgroups per prompt: 2 on each of 256 CUs
 constexpr int kCUs = 256;          // compute units of the MI355X
 constexpr int kPoolTile = 2048;    // scores per pooling workgroup
-constexpr int kUnitPoolTiles = 2;  // tiles per pooling workgroup of ckv_compress_stack
+constexpr int kUnitPoolTiles = 4;  // tiles per pooling workgroup of ckv_compress_stack
 constexpr int kMaxPoolRadius = 15; // pool kernel <= 2*15+1
 constexpr int kGatherRows = 64;    // retained rows per gather workgroup
 constexpr int kHistBits = 12;      // first-level histogram: key bits 30..19
@@ -233,7 +233,7 @@ hipError_t launch_gather(const LayerArgs& a, int grid, hipStream_t st, const Tim
 // kUnitPoolTiles)), then the top-N through compaction and gather of every
 // selection unit (layer, prompt, selection group), one workgroup each
 // (per_layer = prompts * selection groups)
-hipError_t launch_pool_units(const MultiArgs& m, hipStream_t st, const Timing& tm);
+hipError_t launch_pool_units(const MultiArgs& m, int radius, hipStream_t st, const Timing& tm);
 // decode attention (partials, then their merge into a.out) and the error
 // ratios (projection partials, then the ratios and their sum)
 hipError_t launch_decode(int dtype, const DecodeBatch& b, hipStream_t st);

@@ -780,39 +780,95 @@ struct PoolJob {
 
 template <int R>
 __device__ __forceinline__ void pool_tile(const PoolJob& jb, uint32_t* hist_lds) {
-  constexpr int HW = (R + 3) / 4 * 4;  // halo loaded on each side
-  constexpr int NX = kPoolPer + 2 * HW;
-  const int tid = threadIdx.x;
+  constexpr int CH = (R + 3) / 4;  // 16-byte halo chunks on each side of an output chunk
+  constexpr int NX = 4 * (2 * CH + 1);
+  constexpr int NH = kPoolTile / (4 * kThreads);  // output chunks per thread and tile
+  const int tid = threadIdx.x, lane = tid & 63;
   const float pad = jb.is_max ? -INFINITY : 0.f;  // max ignores padding; avg counts it as 0
-  for (int tile = 0; tile < jb.n_tiles; ++tile) {
-    const int t_off = tile * kPoolTile + tid * kPoolPer;  // first score of this thread
-    const int64_t o0 = jb.j0 + t_off;
-    float total[kPoolPer];
-#pragma unroll
-    for (int u = 0; u < kPoolPer; ++u) total[u] = 0.f;
-    for (int hh = 0; hh < jb.n_heads; ++hh) {
-      float x[NX];
-      pool_inputs<HW>(jb.rows[hh], o0, jb.Ls, pad, x);
-#pragma unroll
-      for (int u = 0; u < kPoolPer; ++u) {
-        float v = x[HW + u];
-#pragma unroll
-        for (int dt = 1; dt <= R; ++dt) {
-          const float lo = x[HW + u - dt], hi = x[HW + u + dt];
-          v = jb.is_max ? fmaxf(v, fmaxf(lo, hi)) : v + (lo + hi);
-        }
-        total[u] += jb.is_max ? v : v * jb.inv_kp;
+  // Thread tid owns the 4-token chunks tid, tid + kThreads, ... of a tile, so
+  // that consecutive lanes load and store consecutive 16 bytes; the halo
+  // chunks come from the neighbouring lanes' loads (lanes at a wave's edge
+  // load theirs).
+  auto chunk_at = [&](const CKV_GLOBAL float* row, int64_t j) {  // tokens j..j+3, pad outside [0, Ls)
+    f32x4 c = {pad, pad, pad, pad};
+    if (j >= 0 && j < jb.Ls) {
+      c = *(const CKV_GLOBAL f32x4*)(row + j);  // inside the row's 4-float padding
+      if (j + 3 >= jb.Ls) {
+        if (j + 1 >= jb.Ls) c.y = pad;
+        if (j + 2 >= jb.Ls) c.z = pad;
+        c.w = pad;
       }
     }
-    const int n_mine = jb.n_out - t_off;  // scores of this thread inside the tile
+    return c;
+  };
+  for (int tile = 0; tile < jb.n_tiles; ++tile) {
 #pragma unroll
-    for (int u = 0; u < kPoolPer; ++u) {
-      if (u >= n_mine) break;
-      const float score = total[u] / (float)jb.n_heads;
-      jb.out[t_off + u] = score;
+    for (int hf = 0; hf < NH; ++hf) {
+      const int t_off = tile * kPoolTile + (hf * kThreads + tid) * 4;  // first token of the chunk
+      const int64_t j = jb.j0 + t_off;
+      float total[4] = {0.f, 0.f, 0.f, 0.f};
+      for (int hh = 0; hh < jb.n_heads; ++hh) {
+        const CKV_GLOBAL float* row = to_global(jb.rows[hh]);
+        const f32x4 c = chunk_at(row, j);
+        float x[NX];
+        x[4 * CH] = c.x;
+        x[4 * CH + 1] = c.y;
+        x[4 * CH + 2] = c.z;
+        x[4 * CH + 3] = c.w;
+#pragma unroll
+        for (int k = 1; k <= CH; ++k) {
+          f32x4 lo, hi;
+          lo.x = __shfl_up(c.x, k); lo.y = __shfl_up(c.y, k);
+          lo.z = __shfl_up(c.z, k); lo.w = __shfl_up(c.w, k);
+          hi.x = __shfl_down(c.x, k); hi.y = __shfl_down(c.y, k);
+          hi.z = __shfl_down(c.z, k); hi.w = __shfl_down(c.w, k);
+          if (lane < k) lo = chunk_at(row, j - 4 * k);
+          if (lane + k >= 64) hi = chunk_at(row, j + 4 * k);
+          const int l0 = 4 * (CH - k), h0 = 4 * (CH + k);
+          x[l0] = lo.x; x[l0 + 1] = lo.y; x[l0 + 2] = lo.z; x[l0 + 3] = lo.w;
+          x[h0] = hi.x; x[h0 + 1] = hi.y; x[h0 + 2] = hi.z; x[h0 + 3] = hi.w;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          float v = x[4 * CH + u];
+#pragma unroll
+          for (int dt = 1; dt <= R; ++dt) {
+            const float a = x[4 * CH + u - dt], b = x[4 * CH + u + dt];
+            v = jb.is_max ? fmaxf(v, fmaxf(a, b)) : v + (a + b);
+          }
+          total[u] += jb.is_max ? v : v * jb.inv_kp;
+        }
+      }
+      const int n_mine = jb.n_out - t_off;  // scores of this chunk inside the workgroup's range
+      if (n_mine <= 0) continue;
+      float sc[4];
+      uint32_t bin[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        sc[u] = total[u] / (float)jb.n_heads;
+        bin[u] = score_key(sc[u]) >> kHistShift;
+      }
+      CKV_GLOBAL float* o = jb.out + t_off;
+      if (n_mine >= 4 && ((uintptr_t)o & 15u) == 0) {
+        f32x4 w4 = {sc[0], sc[1], sc[2], sc[3]};
+        *(CKV_GLOBAL f32x4*)o = w4;
+      } else {
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (u < n_mine) o[u] = sc[u];
+      }
       if (jb.do_hist) {
-        const uint32_t bin = score_key(score) >> kHistShift;
-        atomicAdd(&hist_lds[bin >> 1], 1u << ((bin & 1u) * 16u));
+        // one LDS atomic per run of equal bins among the chunk's scores (max
+        // pooling makes plateaus), not one per score
+        uint32_t run = 0;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          if (u >= n_mine) break;
+          ++run;
+          if (u + 1 < 4 && u + 1 < n_mine && bin[u + 1] == bin[u]) continue;
+          atomicAdd(&hist_lds[bin[u] >> 1], run << ((bin[u] & 1u) * 16u));
+          run = 0;
+        }
       }
     }
   }
@@ -827,15 +883,6 @@ __device__ __forceinline__ void pool_tile(const PoolJob& jb, uint32_t* hist_lds)
 }
 
 template <int R>
-__device__ __forceinline__ void pool_dispatch(int r, const PoolJob& jb, uint32_t* hist) {
-  if constexpr (R >= kMaxPoolRadius) {
-    pool_tile<R>(jb, hist);
-  } else {
-    if (r == R) pool_tile<R>(jb, hist);
-    else pool_dispatch<R + 1>(r, jb, hist);
-  }
-}
-
 __device__ __forceinline__ void pool_body(const LayerArgs& a, int b) {
   __shared__ uint32_t hist_lds[kHistBins / 2];  // two 16-bit counts per word
   __shared__ const float* rows[kMaxQHeads];
@@ -868,15 +915,20 @@ __device__ __forceinline__ void pool_body(const LayerArgs& a, int b) {
   jb.inv_kp = 1.f / (float)a.kp;
   jb.out = to_global(sq.scores) + (int64_t)g * Ls + jb.j0;
   jb.ghist = sq.hist + (int64_t)g * kHistBins;
-  pool_dispatch<0>(a.kp >> 1, jb, hist_lds);  // radius 0..kMaxPoolRadius
+  pool_tile<R>(jb, hist_lds);
 }
 
-__global__ __launch_bounds__(kThreads) void pool_kernel(const LayerArgs a) { pool_body(a, blockIdx.x); }
+// One kernel per pool radius R = kp / 2 (the host picks it): each then keeps
+// only its own halo in registers, and the common small radii run at full
+// occupancy.
+template <int R>
+__global__ __launch_bounds__(kThreads) void pool_kernel(const LayerArgs a) { pool_body<R>(a, blockIdx.x); }
 
 // Pooling, head mean, scores and the first-level histogram of several layers
 // at once (ckv_compress_stack): layer l's argument block is read from device
 // memory, and each workgroup covers kUnitPoolTiles consecutive tiles of one
 // (prompt, selection group), merging its histogram once.
+template <int R>
 __global__ __launch_bounds__(kThreads) void pool_units_kernel(const MultiArgs m) {
   __shared__ uint32_t hist_lds[kHistBins / 2];  // two 16-bit counts per word
   __shared__ const float* rows[kMaxQHeads];
@@ -917,7 +969,7 @@ __global__ __launch_bounds__(kThreads) void pool_units_kernel(const MultiArgs m)
   jb.inv_kp = 1.f / (float)a.kp;
   jb.out = to_global(sq.scores) + (int64_t)g * Ls + jb.j0;
   jb.ghist = sq.hist + (int64_t)g * kHistBins;
-  pool_dispatch<0>(a.kp >> 1, jb, hist_lds);
+  pool_tile<R>(jb, hist_lds);
 }
 
 
@@ -950,12 +1002,29 @@ hipError_t launch_score(int dtype, const LayerArgs& a, int grid, hipStream_t st,
   return launch_typed<ScoreOf>(dtype, a, grid, st, tm);
 }
 
-hipError_t launch_pool(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm) {
-  return launch(pool_kernel, grid, kThreads, st, tm, a);
+// The pooling kernels of radius r, looked up at run time.
+template <int R>
+const void* pool_fn(int r, bool units) {
+  if constexpr (R >= kMaxPoolRadius) {
+    return units ? reinterpret_cast<const void*>(pool_units_kernel<R>)
+                 : reinterpret_cast<const void*>(pool_kernel<R>);
+  } else {
+    if (r != R) return pool_fn<R + 1>(r, units);
+    return units ? reinterpret_cast<const void*>(pool_units_kernel<R>)
+                 : reinterpret_cast<const void*>(pool_kernel<R>);
+  }
 }
 
-hipError_t launch_pool_units(const MultiArgs& m, hipStream_t st, const Timing& tm) {
-  return launch(pool_units_kernel, m.n_layers * m.per_layer, kThreads, st, tm, m);
+hipError_t launch_pool(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm) {
+  void* args[] = {const_cast<LayerArgs*>(&a)};
+  return hipExtLaunchKernel(pool_fn<0>(a.kp >> 1, false), dim3(grid), dim3(kThreads), args, 0, st,
+                            tm.start, tm.stop, 0);
+}
+
+hipError_t launch_pool_units(const MultiArgs& m, int radius, hipStream_t st, const Timing& tm) {
+  void* args[] = {const_cast<MultiArgs*>(&m)};
+  return hipExtLaunchKernel(pool_fn<0>(radius, true), dim3(m.n_layers * m.per_layer), dim3(kThreads),
+                            args, 0, st, tm.start, tm.stop, 0);
 }
 
 

@@ -725,11 +725,16 @@ void decode_batch_add(const ckv_attn_desc* d, const void* q, int64_t st, int64_t
   ++b.n;
 }
 
-// Partial Y tiles of the W_O projection: kProjSplit K ranges x 32 x 32 tiles.
-size_t proj_tiles_bytes(int32_t D, int32_t T) {
-  return align_up((size_t)ckv::kProjSplit * ceil_div(D, 32) * ceil_div(2 * (int64_t)T, 32) * 1024 *
-                  sizeof(float));
+// Partial Y tiles of the W_O projection: n_split K ranges x 32 x 32 tiles.
+size_t proj_tiles_bytes(int32_t D, int32_t T, int64_t K) {
+  return align_up((size_t)ckv::proj_splits(K) * ceil_div(D, 32) * ceil_div(2 * (int64_t)T, 32) *
+                  1024 * sizeof(float));
 }
+
+// Columns of the projection's right-hand side X = [A_full | A_comp - A_full],
+// padded to whole 32-column blocks, and the bytes of its two 16-bit parts.
+int32_t proj_cols(int32_t T) { return (int32_t)(ceil_div(2 * (int64_t)T, 32) * 32); }
+size_t proj_split_bytes(int32_t T, int64_t K) { return align_up((size_t)2 * proj_cols(T) * K * 2); }
 
 int check_decode_seq(const ckv_attn_desc* d, const ckv_decode_seq* s) {
   int rc = check_attn(d, s->T);
@@ -832,8 +837,10 @@ size_t ckv_layer_error_workspace_bytes(const ckv_attn_desc* desc, int32_t T, int
   const int64_t chunk = decode_chunk_len(desc, n_full + n_comp);
   const size_t parts = decode_part_bytes(desc, T, n_full, chunk) + decode_part_bytes(desc, T, n_comp, chunk);
   const size_t proj = align_up((size_t)(ceil_div(D, 32) + 1) * 2 * T * sizeof(float));
-  const size_t proj_y = proj_tiles_bytes(D, T);
-  return 2 * outs + parts + proj + proj_y;
+  const int64_t K = (int64_t)desc->num_q_heads * desc->head_dim;
+  const size_t proj_y = proj_tiles_bytes(D, T, K);
+  const size_t x_hl = proj_split_bytes(T, K);
+  return 2 * outs + parts + proj + proj_y + x_hl;
 }
 
 int ckv_layer_error(const ckv_attn_desc* desc, const void* q, int64_t q_stride_t,
@@ -887,6 +894,9 @@ int ckv_layer_error(const ckv_attn_desc* desc, const void* q, int64_t q_stride_t
   ea.eps = eps;
   ea.part = proj;
   ea.part_y = proj_y;
+  ea.x_hl = reinterpret_cast<uint16_t*>(reinterpret_cast<char*>(proj_y) + proj_tiles_bytes(D, T, K));
+  ea.n_split = ckv::proj_splits(K);
+  ea.n_cols = proj_cols(T);
   ea.ratio = ratio;
   ea.e = e;
   if ((err = ckv::launch_error(desc->dtype, ea, st)) != hipSuccess) return hip_fail(err);

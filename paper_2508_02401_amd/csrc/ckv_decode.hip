@@ -476,7 +476,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_merge_kernel(const DecodeB
 // Projection and error ratios.
 // ---------------------------------------------------------------------------
 // Workgroup (row block rb, column block cb, K range ks): the 32 x 32 tile of
-// Y = W X over the ks-th of kProjSplit K ranges, that range split over the
+// Y = W X over the ks-th of n_split K ranges, that range split over the
 // workgroup's waves, the waves' sums added in LDS in a fixed order and the
 // tile written to part_y. K is taken 16 at a time: lane half h holds
 // k0 + 8h .. k0 + 8h + 7 of its W row (one 16-byte load for 2-byte weights)
@@ -497,7 +497,7 @@ __global__ __launch_bounds__(kProjThreads) void project_kernel(const ErrorArgs a
   const bool full_col = col < T, diff_col = col >= T && col < 2 * T;
   const int tcol = full_col ? col : (diff_col ? col - T : 0);
   const int64_t n16 = a.K / 16;
-  const int64_t per_ks = (n16 + kProjSplit - 1) / kProjSplit;
+  const int64_t per_ks = (n16 + a.n_split - 1) / a.n_split;
   const int64_t k0 = ks * per_ks, k1 = k0 + per_ks < n16 ? k0 + per_ks : n16;
   const int64_t per = (k1 - k0 + kProjWaves - 1) / kProjWaves;
   const int64_t b0 = k0 + wave * per, b1 = b0 + per < k1 ? b0 + per : k1;
@@ -547,7 +547,137 @@ __global__ __launch_bounds__(kProjThreads) void project_kernel(const ErrorArgs a
   }
 }
 
-// Workgroup (rb, cb): Y = the kProjSplit partial tiles added in order, then
+// 16-bit W_O: the columns of X = [A_full | A_comp - A_full] (fp32) split into
+// two 16-bit parts in W_O's type, high = X rounded, low = X - high rounded,
+// so that the 16-bit MFMA of W_O with high and then low gives W_O X to about
+// 16 significant bits (W_O itself is exact in its type). x_hl is
+// [2][n_cols][K]; columns from 2T on are zero.
+template <int DT>
+__global__ __launch_bounds__(kProjThreads) void xsplit_kernel(const ErrorArgs a) {
+  const int64_t n = (int64_t)a.n_cols * a.K;
+  for (int64_t e = (int64_t)blockIdx.x * kProjThreads + threadIdx.x; e < n;
+       e += (int64_t)gridDim.x * kProjThreads) {
+    const int col = (int)(e / a.K);
+    const int64_t k = e - (int64_t)col * a.K;
+    float x = 0.f;
+    if (col < a.T) x = a.a_full[(int64_t)col * a.K + k];
+    else if (col < 2 * a.T)
+      x = a.a_comp[(int64_t)(col - a.T) * a.K + k] - a.a_full[(int64_t)(col - a.T) * a.K + k];
+    uint16_t hi, lo;
+    if constexpr (DT == 0) {  // bf16, round to nearest even (X is finite)
+      auto rne = [](float v) {
+        const uint32_t u = __float_as_uint(v);
+        return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+      };
+      hi = rne(x);
+      lo = rne(x - __uint_as_float((uint32_t)hi << 16));
+    } else {
+      const _Float16 h = (_Float16)x;
+      const _Float16 l = (_Float16)(x - (float)h);
+      hi = __builtin_bit_cast(uint16_t, h);
+      lo = __builtin_bit_cast(uint16_t, l);
+    }
+    a.x_hl[e] = hi;
+    a.x_hl[n + e] = lo;
+  }
+}
+
+// 16-bit W_O: workgroup (row blocks 4*bx .. 4*bx+3, column block cb, K range
+// ks); wave w computes the 32 x 32 tile of row block 4*bx + w over the K
+// range with the 32x32x16 MFMA (W_O rows against the high and then the low
+// part of X, one accumulator) and writes it to part_y.
+//
+// Every load of the workgroup is issued at the start, so that the whole
+// range is in flight at once: W_O in tiles of 32 rows x 128 k (8 KB, at most
+// kProjTiles per wave) into registers with contiguous loads (lane l of load i
+// takes 16-byte chunk l % 16 of tile row 4i + l / 16), and the X tiles the
+// four waves share (both parts, 32 columns) into LDS by all threads. A tile
+// of W_O then goes through the wave's LDS region. In LDS, chunk c of row (or
+// column) r sits at position c ^ (r % 16); lane half h of lane l32 reads
+// chunk 2j + h of row l32 for the j-th 16-k step of the tile, as its X column
+// does.
+constexpr int kProjTileK = 128;                                // k per tile
+constexpr int kProjTileLoads = 32 * kProjTileK * 2 / 16 / 64;  // 16-byte W_O loads per lane: 8
+constexpr int kProjTiles = kProjRangeK / kProjTileK;           // tiles per K range: 2
+constexpr int kProjXChunks = kProjTiles * 2 * 32 * (kProjTileK / 8);  // 16-byte X chunks: 2048
+constexpr int kProjXLoads = kProjXChunks / kProjThreads;              // per thread: 8
+
+template <int DT>
+__global__ __launch_bounds__(kProjThreads) void project16_kernel(const ErrorArgs a) {
+  __shared__ uint4 wl[kProjWaves][32 * (kProjTileK / 8)];  // a W_O tile per wave, 8 KB
+  __shared__ uint4 xl[kProjXChunks];                        // [tile][part][col][chunk], 32 KB
+  const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
+  const int wave = tid >> 6;
+  const int n_rb = (a.D + 31) / 32;
+  const int rb = blockIdx.x * kProjWaves + wave, cb = blockIdx.y, ks = blockIdx.z;
+  const int64_t n16 = a.K / 16;
+  const int64_t per_ks = (n16 + a.n_split - 1) / a.n_split;
+  const int64_t k0 = ks * per_ks, k1 = k0 + per_ks < n16 ? k0 + per_ks : n16;  // in 16-k steps
+  const int n_steps = k1 > k0 ? (int)(k1 - k0) : 0;  // <= kProjTiles * 8 (checked on the host)
+  const CKV_GLOBAL uint16_t* w0 = to_global(static_cast<const uint16_t*>(a.w));
+  const CKV_GLOBAL uint16_t* x0 = to_global(a.x_hl);
+  // this wave's W_O tiles (rows past D or k past the range: zeros)
+  u32x4 t[kProjTiles][kProjTileLoads];
+#pragma unroll
+  for (int tl = 0; tl < kProjTiles; ++tl)
+#pragma unroll
+    for (int i = 0; i < kProjTileLoads; ++i) {
+      const int r = 4 * i + lane / 16, c = lane % 16;
+      const int row = rb * 32 + r;
+      const bool ok = rb < n_rb && row < a.D && tl * 8 + c / 2 < n_steps;
+      const int64_t off =
+          ok ? (int64_t)row * a.w_stride + (k0 + tl * 8) * 16 + 8 * c : 0;
+      t[tl][i] = ok ? *reinterpret_cast<const CKV_GLOBAL u32x4*>(w0 + off) : u32x4{0u, 0u, 0u, 0u};
+    }
+  // the shared X tiles: chunk e = ((tile * 2 + part) * 32 + col) * 16 + c
+  u32x4 xv[kProjXLoads];
+#pragma unroll
+  for (int i = 0; i < kProjXLoads; ++i) {
+    const int e = i * kProjThreads + tid;
+    const int c = e % 16, col = (e / 16) % 32, part = (e / 512) % 2, tl = e / 1024;
+    const bool ok = tl * 8 + c / 2 < n_steps;
+    const int64_t off = ok ? ((int64_t)part * a.n_cols + cb * 32 + col) * a.K +
+                                 (k0 + tl * 8) * 16 + 8 * c
+                           : 0;
+    xv[i] = ok ? *reinterpret_cast<const CKV_GLOBAL u32x4*>(x0 + off) : u32x4{0u, 0u, 0u, 0u};
+  }
+#pragma unroll
+  for (int i = 0; i < kProjXLoads; ++i) {
+    const int e = i * kProjThreads + tid;
+    const int c = e % 16, rc = e / 16;  // rc = (tile * 2 + part) * 32 + col
+    xl[rc * 16 + (c ^ (rc & 15))] = make_uint4(xv[i].x, xv[i].y, xv[i].z, xv[i].w);
+  }
+  __syncthreads();
+  if (rb >= n_rb) return;  // after the barrier: these waves only helped load X
+  uint4* tile = wl[wave];
+  f32x16 acc = f32x16{};
+#pragma unroll
+  for (int tl = 0; tl < kProjTiles; ++tl) {
+    if (tl * 8 >= n_steps) break;
+#pragma unroll
+    for (int i = 0; i < kProjTileLoads; ++i) {
+      const int r = 4 * i + lane / 16, c = lane % 16;
+      tile[r * 16 + (c ^ (r & 15))] = make_uint4(t[tl][i].x, t[tl][i].y, t[tl][i].z, t[tl][i].w);
+    }
+    __builtin_amdgcn_wave_barrier();
+    const uint4* xh = xl + (tl * 2 + 0) * 32 * 16;
+    const uint4* xlo = xl + (tl * 2 + 1) * 32 * 16;
+#pragma unroll
+    for (int j = 0; j < kProjTileK / 16; ++j) {
+      const int pos = (2 * j + h) ^ (l32 & 15);
+      const uint4 wv = tile[l32 * 16 + pos];
+      acc = mfma_chunk<DT>(wv, xh[l32 * 16 + pos], acc);
+      acc = mfma_chunk<DT>(wv, xlo[l32 * 16 + pos], acc);
+    }
+    __builtin_amdgcn_wave_barrier();  // the next tile's stores come after these reads
+  }
+  // acc[v]: row rb*32 + acc_row(v, h), column cb*32 + l32
+  float* out = a.part_y + (((int64_t)ks * n_rb + rb) * gridDim.y + cb) * 1024;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) out[acc_row(v, h) * 32 + l32] = acc[v];
+}
+
+// Workgroup (rb, cb): Y = the n_split partial tiles added in order, then
 // per column the sum of Y^2 over the tile's rows (rows past D excluded) into
 // part[rb][col].
 __global__ __launch_bounds__(kProjThreads) void square_kernel(const ErrorArgs a) {
@@ -558,10 +688,17 @@ __global__ __launch_bounds__(kProjThreads) void square_kernel(const ErrorArgs a)
   float sq = 0.f;
   for (int r = rg; r < 32; r += RG) {
     if (rb * 32 + r >= a.D) break;
+    // the n_split partials in order, loaded 16 at a time
     float y = 0.f;
+    for (int ks0 = 0; ks0 < a.n_split; ks0 += 16) {
+      float v[16];
 #pragma unroll
-    for (int ks = 0; ks < kProjSplit; ++ks)
-      y += a.part_y[(((int64_t)ks * nrb + rb) * ncb + cb) * 1024 + r * 32 + c];
+      for (int u = 0; u < 16; ++u)
+        v[u] = ks0 + u < a.n_split ? a.part_y[(((int64_t)(ks0 + u) * nrb + rb) * ncb + cb) * 1024 + r * 32 + c]
+                                   : 0.f;
+#pragma unroll
+      for (int u = 0; u < 16; ++u) y += v[u];
+    }
     sq += y * y;
   }
   colsum[rg][c] = sq;
@@ -666,12 +803,23 @@ hipError_t launch_decode(int dtype, const DecodeBatch& b, hipStream_t st) {
 
 hipError_t launch_error(int w_dtype, const ErrorArgs& a, hipStream_t st) {
   const Timing tm;
-  const dim3 grid((a.D + 31) / 32, (2 * a.T + 31) / 32, kProjSplit);
+  const int n_rb = (a.D + 31) / 32;
+  const dim3 grid(n_rb, (2 * a.T + 31) / 32, a.n_split);
   const dim3 tiles(grid.x, grid.y);
   hipError_t e;
-  if (w_dtype == 0) e = launch(project_kernel<0>, grid, kProjThreads, st, tm, a);
-  else if (w_dtype == 1) e = launch(project_kernel<1>, grid, kProjThreads, st, tm, a);
-  else e = launch(project_kernel<2>, grid, kProjThreads, st, tm, a);
+  if (w_dtype == 2) {
+    e = launch(project_kernel<2>, grid, kProjThreads, st, tm, a);
+  } else {
+    // 16-bit W_O: split X once, then one wave per 32 x 32 tile and K range
+    const int64_t n = (int64_t)a.n_cols * a.K;
+    const int xg = (int)((n + kProjThreads - 1) / kProjThreads);  // one element per thread
+    e = w_dtype == 0 ? launch(xsplit_kernel<0>, xg, kProjThreads, st, tm, a)
+                     : launch(xsplit_kernel<1>, xg, kProjThreads, st, tm, a);
+    if (e != hipSuccess) return e;
+    const dim3 g16((n_rb + kProjWaves - 1) / kProjWaves, grid.y, a.n_split);
+    e = w_dtype == 0 ? launch(project16_kernel<0>, g16, kProjThreads, st, tm, a)
+                     : launch(project16_kernel<1>, g16, kProjThreads, st, tm, a);
+  }
   if (e != hipSuccess) return e;
   if ((e = launch(square_kernel, tiles, kProjThreads, st, tm, a)) != hipSuccess) return e;
   return launch(error_kernel, 1, kDecThreads, st, tm, a);

@@ -182,7 +182,13 @@ struct DecodeArgs {
 // Up to kMaxDecodeSeqs prompts (ragged caches) in one pair of launches: the
 // decode workgroups of prompt i are [blk_off[i], blk_off[i+1]), its merge
 // workgroups [mrg_off[i], mrg_off[i+1]).
-constexpr int kProjSplit = 4;  // K ranges of the W_O projection, one workgroup each
+constexpr int kProjSplit = 16;     // fewest K ranges of the W_O projection (partial tiles added in order)
+constexpr int kProjRangeK = 256;   // most k per K range of the 16-bit projection
+// K ranges of the W_O projection for K = H * d columns of W_O.
+inline int proj_splits(int64_t K) {
+  const int64_t n = (K + kProjRangeK - 1) / kProjRangeK;
+  return n > kProjSplit ? (int)n : kProjSplit;
+}
 constexpr int kMaxDecodeSeqs = 24;
 constexpr int kDecodeThreads = 256;  // threads of the decode and merge workgroups
 struct DecodeBatch {
@@ -205,7 +211,11 @@ struct ErrorArgs {
   int64_t K;
   float eps;
   float* part;             // [ceil(D / 32) + 1][2T]: column sums of Y^2 per 32 rows, then in all
-  float* part_y;           // [kProjSplit][ceil(D / 32)][ceil(2T / 32)][32][32]: Y tiles per K range
+  float* part_y;           // [n_split][ceil(D / 32)][ceil(2T / 32)][32][32]: Y tiles per K range
+  int32_t n_split;         // K ranges: proj_splits(K)
+  uint16_t* x_hl;          // 16-bit W_O: X = [A_full | A_comp - A_full] as [2][n_cols][K], the
+                           // high parts, then the low parts (X - high), in W_O's 16-bit type
+  int32_t n_cols;          // ceil(2T / 32) * 32
   float* ratio;            // [T]
   float* e;                // [1]
 };

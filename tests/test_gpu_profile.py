@@ -122,6 +122,10 @@ ERROR_CASES = [
     ("f16-d64-G7", Case(28, 4, 64, 32, "max", 7, torch.float16), 2500, 400, 3, 1792),
     # a layer of the long-context stack: L = 131072, w = 64, 128 kept tokens
     ("bf16-llama-131072", Case(32, 8, 128, 64, "max", 7, torch.bfloat16), 131072, 128, 4, 4096),
+    # K = H * d = 8192 columns of W_O: more than 16 K ranges of the projection,
+    # and more than 32 decoding steps (two 32-column blocks of X)
+    ("bf16-K8192-T20", Case(64, 16, 128, 32, "max", 7, torch.bfloat16), 2000, 200, 20, 1024),
+    ("f16-K8192", Case(64, 8, 128, 16, "avg", 5, torch.float16), 1500, 150, 3, 768),
 ]
 
 

@@ -549,13 +549,26 @@ def measure(args, wl, desc, layers, budgets, elt, dev, hip, schedule, shared=Fal
     # the stack's selection launches carry the events of the batch's first
     # layer: with one batch, layer 0's pool begin and gather end bracket them
     sel_timed = schedule == "stack" and args.stack_slots <= 0
-    every = max(1, args.time_every)
+    # The stack launches each K pass for up to CKV_STACK_LAYERS_PER_LAUNCH
+    # consecutive layers of a batch at once, with the first layer's events:
+    # chunk[l] lists the layers of the launch that starts at layer l.
+    chunk = {}
+    if schedule == "stack":
+        per = ckv.stack_layers_per_launch(wl.seq_lens)
+        batch = args.stack_slots if args.stack_slots > 0 else n_layers
+        for b0 in range(0, n_layers, batch):
+            for c in range(b0, min(b0 + batch, n_layers), per):
+                chunk[c] = list(range(c, min(c + per, b0 + batch, n_layers)))
+    else:
+        chunk = {l: [l] for l in range(n_layers)}
+    starts = sorted(chunk)
+    every = max(1, round(args.time_every / max(len(v) for v in chunk.values())))
     ev = []  # ev[step][layer] = (begin, end) arrays, or None for an untimed layer
     kp_timed = []  # kp_timed[step][layer]: the K passes carry events
     for k in range(args.steps):
         per_layer, flags = [], []
         for li in range(n_layers):
-            kp = (li + k) % every == 0
+            kp = li in chunk and (starts.index(li) + k) % every == 0
             sel = sel_timed and li == 0
             flags.append(kp)
             if not kp and not sel:
@@ -631,20 +644,21 @@ def measure(args, wl, desc, layers, budgets, elt, dev, hip, schedule, shared=Fal
     # dominant kernel: the timed K pass with the longest mean launch
     dom = max(timed, key=lambda n: stage_avg[n])
     dom_bytes, flops = [], []
-    for li in sampled:
-        mask = layers[li][0]
-        n_chosen = int(np.count_nonzero(mask))
+    for l0 in sampled:
         b = f = 0
-        for L in wl.seq_lens:
-            n_rd = groups_read(mask)
-            if dom == "rowstats":
-                # every key of the prompt and the chosen Q rows
-                b += n_rd * L * d * elt + n_chosen * w * d * elt
-            else:
-                # prefix keys, chosen Q rows, and the window sum of every
-                # chosen head written per prefix token
-                b += n_rd * (L - w) * d * elt + n_chosen * w * d * elt + n_chosen * (L - w) * 4
-            f += 2 * n_chosen * w * (L if dom == "rowstats" else (L - w)) * d
+        for li in chunk[l0]:  # the layers of the timed launch
+            mask = layers[li][0]
+            n_chosen = int(np.count_nonzero(mask))
+            for L in wl.seq_lens:
+                n_rd = groups_read(mask)
+                if dom == "rowstats":
+                    # every key of the prompt and the chosen Q rows
+                    b += n_rd * L * d * elt + n_chosen * w * d * elt
+                else:
+                    # prefix keys, chosen Q rows, and the window sum of every
+                    # chosen head written per prefix token
+                    b += n_rd * (L - w) * d * elt + n_chosen * w * d * elt + n_chosen * (L - w) * 4
+                f += 2 * n_chosen * w * (L if dom == "rowstats" else (L - w)) * d
         dom_bytes.append(b)
         flops.append(f)
     dom_gbs = float(np.mean(dom_bytes)) / (stage_avg[dom] / 1e3) / 1e9
@@ -694,6 +708,7 @@ def measure(args, wl, desc, layers, budgets, elt, dev, hip, schedule, shared=Fal
                      "traffic": None, "avg_launch_ms": stage_avg[dom],
                      "algorithmic_bytes_per_launch": float(np.mean(dom_bytes)),
                      "timed_launches": len(sampled),
+                     "layers_per_launch": max(len(v) for v in chunk.values()),
                      "launches_in_flight": 2 if side is not None else 1,
                      "mfma_tflops": dom_tflops, "mfma_frac_bf16": dom_tflops / BF16_PEAK_TFLOPS},
         "wall_s_timed": wall_s,

@@ -78,6 +78,15 @@ typedef enum { CKV_POOL_AVG = 0, CKV_POOL_MAX = 1 } ckv_pool;
 #define CKV_MAX_WINDOW 128
 #define CKV_MAX_POOL_KERNEL 31
 #define CKV_MAX_SEQS 16
+/* ckv_compress_stack launches each K pass for n consecutive layers of a
+ * batch at once, n = CKV_STACK_CHUNK_TOKENS / (sum of the prompt lengths of a
+ * layer), clamped to [1, CKV_STACK_LAYERS_PER_LAUNCH]: short prompts share a
+ * launch's ramp-up and drain, long ones keep one launch per layer (the second
+ * pass then finds part of the layer's keys still in the Infinity Cache).
+ * Per-layer stage events (ckv_set_stack_stage_events) are taken from the first
+ * layer of each launch. */
+#define CKV_STACK_LAYERS_PER_LAUNCH 3
+#define CKV_STACK_CHUNK_TOKENS 98304
 /* A KV group's chosen rows, n_chosen(g) * round_up(w, 8), are read from K in
  * row groups of at most this many: a group with more (e.g. 3 or 4 chosen
  * heads at w = 64) is read once per row group, which costs one more pass

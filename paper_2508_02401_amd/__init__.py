@@ -13,5 +13,6 @@ from ._binding import (  # noqa: F401
     attn_desc, kv_cache, ckv_decode_workspace_bytes, ckv_decode_attention, ckv_layer_error_workspace_bytes,
     ckv_layer_error, ckv_normalize_errors, ckv_decode_seq, decode_seq, ckv_decode_batch_workspace_bytes,
     ckv_decode_attention_batch, ckv_streaming_select, snapkv_mask,
-    CKV_NOALLOC_MAX_WORKSPACE_BYTES, ckv_compress_layer_noalloc,
+    CKV_NOALLOC_MAX_WORKSPACE_BYTES, ckv_compress_layer_noalloc, CKV_STACK_LAYERS_PER_LAUNCH,
+    CKV_STACK_CHUNK_TOKENS, stack_layers_per_launch,
 )

@@ -31,6 +31,15 @@ CKV_POOL_AVG, CKV_POOL_MAX = 0, 1
 CKV_KEEP_WINDOW = 1
 CKV_SHARE_LAYER = 2
 CKV_MAX_SEQS = 16
+CKV_STACK_LAYERS_PER_LAUNCH = 3
+CKV_STACK_CHUNK_TOKENS = 98304
+
+
+def stack_layers_per_launch(seq_lens) -> int:
+    """Layers per K-pass launch of ckv_compress_stack for prompts of these
+    lengths (the rule stated in include/ckv.h)."""
+    tokens = sum(int(x) for x in seq_lens)
+    return max(1, min(CKV_STACK_LAYERS_PER_LAUNCH, CKV_STACK_CHUNK_TOKENS // max(tokens, 1)))
 CKV_NOALLOC_MAX_WORKSPACE_BYTES = 64 << 20
 
 EXPORTED = ("ckv_workspace_bytes", "ckv_score", "ckv_select", "ckv_gather", "ckv_compress_layer",

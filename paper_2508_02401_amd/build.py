@@ -22,28 +22,35 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=" + ARCH,
           # MFMA results stay in VGPRs: the softmax reads them with VALU ops,
           # and accumulators in AGPRs would need a copy per element
           "-mllvm", "-amdgpu-mfma-vgpr-form",
+          # kernel argument blocks indexed at run time (the multi-layer K
+          # passes) are read in place; past InstCombine's default limit of
+          # uses it copies such a block to per-lane scratch instead
+          "-mllvm", "-instcombine-max-copied-from-constant-users=100000",
           "-I" + INCLUDE, "-I" + CSRC, "-Wall", "-Wno-unused-function"]
 
 
 def build(verbose: bool = False) -> str:
     """Compile every source and link libckv.so. Returns the library path."""
     objs = []
-    for src in SOURCES:
-        obj = os.path.join(CSRC, os.path.basename(src) + ".o")
-        lang = ["-x", "hip"]
-        cmd = [HIPCC] + lang + COMMON + ["-c", src, "-o", obj]
+    try:
+        for src in SOURCES:
+            obj = os.path.join(CSRC, os.path.basename(src) + ".o")
+            lang = ["-x", "hip"]
+            cmd = [HIPCC] + lang + COMMON + ["-c", src, "-o", obj]
+            if verbose:
+                print(" ".join(cmd), flush=True)
+            objs.append(obj)
+            subprocess.run(cmd, check=True)
+        tmp = LIB + ".tmp%d" % os.getpid()
+        cmd = [HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp] + objs
         if verbose:
             print(" ".join(cmd), flush=True)
         subprocess.run(cmd, check=True)
-        objs.append(obj)
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp] + objs
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
-    for o in objs:
-        os.remove(o)
+        os.replace(tmp, LIB)
+    finally:  # no stale objects, also when a compile fails
+        for o in objs:
+            if os.path.exists(o):
+                os.remove(o)
     return LIB
 
 

@@ -12,6 +12,9 @@
 namespace {
 
 thread_local int g_last_hip_error = 0;
+// ckv_compress_stack's kernel-argument staging for its multi-layer K-pass
+// launches (about 12 KB, so not on the stack)
+thread_local ckv::LayersArgs g_layers_args;
 thread_local hipEvent_t g_ev_begin[ckv::kNumStages] = {};
 thread_local hipEvent_t g_ev_end[ckv::kNumStages] = {};
 thread_local bool g_events_on = false;
@@ -534,18 +537,55 @@ int ckv_compress_stack(const ckv_layer_desc* desc, int32_t n_layers, const uint8
       rc = hip_fail(e);
       break;
     }
-    ckv::LayerArgs a;
-    for (int32_t i = 0; i < nb && rc == CKV_OK; ++i) {
-      const int32_t l = b0 + i;
-      char* ws = base + (size_t)i * slot_bytes;
-      if ((rc = build_args(desc, head_masks + (int64_t)l * desc->num_q_heads,
-                           seqs + (int64_t)l * num_seqs, num_seqs, ws, true, a)) != CKV_OK)
+    // The K passes in chunks of up to kLayersPerLaunch consecutive layers,
+    // one launch per pass and chunk (the argument blocks travel as kernel
+    // arguments): one ramp-up and drain per chunk rather than per layer.
+    // Chunks alternate between the streams; a chunk's layers all have caller
+    // row statistics or all have none. Stage events: the chunk's first layer.
+    ckv::LayersArgs& la = g_layers_args;
+    ckv::LayerArgs a;  // a layer of the batch (all have the same shape), for the selection below
+    int64_t tokens = 0;  // per layer
+    for (int32_t s = 0; s < num_seqs; ++s) tokens += seqs[s].seq_len;
+    const int per_launch = tokens >= CKV_STACK_CHUNK_TOKENS ? 1
+                           : (int)(CKV_STACK_CHUNK_TOKENS / tokens < ckv::kLayersPerLaunch
+                                       ? CKV_STACK_CHUNK_TOKENS / tokens
+                                       : ckv::kLayersPerLaunch);
+    for (int32_t i = 0, chunk = 0; i < nb && rc == CKV_OK; ++chunk) {
+      int n = 0, blk = 0;
+      for (; n < per_launch && i + n < nb; ++n) {
+        const int32_t l = b0 + i + n;
+        char* ws = base + (size_t)(i + n) * slot_bytes;
+        ckv::LayerArgs& al = la.lay[n];
+        if ((rc = build_args(desc, head_masks + (int64_t)l * desc->num_q_heads,
+                             seqs + (int64_t)l * num_seqs, num_seqs, ws, true, al)) != CKV_OK)
+          break;
+        if (n > 0 && al.lse_given != la.lay[0].lse_given) break;  // starts the next chunk
+        al.do_hist = 1;
+        al.do_gather = 1;
+        al.table_out = ws;  // the argument block the selection launches read
+        la.blk[n] = blk;
+        blk += grid_kpass(al);
+      }
+      if (rc != CKV_OK) break;
+      la.n = n;
+      la.blk[n] = blk;
+      use_layer_events(b0 + i);
+      const hipStream_t cs = two && (chunk & 1) ? side : st;
+      if (n == 1) {  // one layer: the per-layer kernels
+        if ((rc = run_kpasses(desc, la.lay[0], cs)) != CKV_OK) break;
+      } else if (!la.lay[0].lse_given &&
+          (e = ckv::launch_rowstats_layers(desc->dtype, la, blk, cs,
+                                           timing(ckv::kStageRowStats, true, true))) != hipSuccess) {
+        rc = hip_fail(e);
         break;
-      a.do_hist = 1;
-      a.do_gather = 1;
-      a.table_out = ws;  // the argument block the selection launches read
-      use_layer_events(l);
-      rc = run_kpasses(desc, a, two && (i & 1) ? side : st);
+      }
+      if (n > 1 && (e = ckv::launch_score_layers(desc->dtype, la, blk, cs,
+                                                 timing(ckv::kStageScore, true, true))) != hipSuccess) {
+        rc = hip_fail(e);
+        break;
+      }
+      if (i + n == nb) a = la.lay[n - 1];
+      i += n;
     }
     if (rc != CKV_OK) break;
     if (two && nb > 1 &&

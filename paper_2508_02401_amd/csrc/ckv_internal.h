@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "ckv.h"
+
 namespace ckv {
 
 // Stores a HIP status for ckv_last_hip_error (per host thread) and returns
@@ -150,6 +152,16 @@ struct LayerArgs {
   SeqArgs seq[kMaxSeqs];
 };
 
+// The K passes of several layers in one launch (ckv_compress_stack): the
+// argument blocks themselves travel as kernel arguments, layer l's
+// workgroups at blk[l] .. blk[l+1].
+constexpr int kLayersPerLaunch = CKV_STACK_LAYERS_PER_LAUNCH;
+struct LayersArgs {
+  LayerArgs lay[kLayersPerLaunch];
+  int32_t n;                        // layers in this launch
+  int32_t blk[kLayersPerLaunch + 1];
+};
+
 // Several layers' selection stages in one launch: layer l's argument block is
 // in device memory at table + l * stride (the scoring kernel of that layer put
 // it there), and every layer has per_layer workgroups.
@@ -231,6 +243,10 @@ struct Timing {
 // dtype codes match ckv_dtype. grid is the number of workgroups.
 hipError_t launch_rowstats(int dtype, const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
 hipError_t launch_score(int dtype, const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
+hipError_t launch_rowstats_layers(int dtype, const LayersArgs& m, int grid, hipStream_t st,
+                                  const Timing& tm);
+hipError_t launch_score_layers(int dtype, const LayersArgs& m, int grid, hipStream_t st,
+                               const Timing& tm);
 hipError_t launch_pool(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
 hipError_t launch_clear(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);
 hipError_t launch_hist(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm);

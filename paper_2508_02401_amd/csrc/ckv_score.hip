@@ -427,7 +427,7 @@ __device__ __forceinline__ void rowstats_body(const LayerArgs& a, const SeqArgs&
 }
 
 template <int DT, int D>
-__global__ __launch_bounds__(kKpThreads) __attribute__((amdgpu_waves_per_eu(2))) void rowstats_kernel(const LayerArgs a) {
+__device__ __forceinline__ void rowstats_block(const LayerArgs& a, const int b) {
   using S = Stager<DT, D, stage_bytes<DT, D>()>;
   constexpr int NS = 4;  // 4-slot ring
   __shared__ uint4 slot0[S::VEC];
@@ -437,7 +437,6 @@ __global__ __launch_bounds__(kKpThreads) __attribute__((amdgpu_waves_per_eu(2)))
   __shared__ float2 red[kKpWaves][2][32];
   uint4* const slots[NS] = {slot0, slot1, slot2, slot3};
 
-  const int b = blockIdx.x;
   const SeqArgs& sq = a.seq[find_seq(a, b, [](const SeqArgs& t) { return t.blk_kpass; })];
   int g, j, u, p, P;
   kpass_locate(a, sq, b - sq.blk_kpass, g, j, u, p, P);
@@ -465,6 +464,29 @@ __global__ __launch_bounds__(kKpThreads) __attribute__((amdgpu_waves_per_eu(2)))
   else if (wpq == W4) rowstats_body<DT, D, W4, 1, S, NS>(a, sq, g, u, p, P, sel0, n_sel, nqb, slots, red);
   else if (wpq == W2) rowstats_body<DT, D, W2, 1, S, NS>(a, sq, g, u, p, P, sel0, n_sel, nqb, slots, red);
   else rowstats_body<DT, D, W1, 1, S, NS>(a, sq, g, u, p, P, sel0, n_sel, nqb, slots, red);
+}
+
+template <int DT, int D>
+__global__ __launch_bounds__(kKpThreads) __attribute__((amdgpu_waves_per_eu(2))) void rowstats_kernel(const LayerArgs a) {
+  rowstats_block<DT, D>(a, blockIdx.x);
+}
+
+// The layer of workgroup b of a multi-layer K-pass launch.
+__device__ __forceinline__ int layer_of(const LayersArgs& m, int b) {
+  int l = 0;
+#pragma unroll
+  for (int i = 1; i < kLayersPerLaunch; ++i)
+    if (i < m.n && b >= m.blk[i]) l = i;
+  return l;
+}
+
+// The row-statistics passes of up to kLayersPerLaunch layers in one launch,
+// layer l's workgroups at blk[l] .. blk[l+1]: one ramp-up and drain for them
+// all.
+template <int DT, int D>
+__global__ __launch_bounds__(kKpThreads) __attribute__((amdgpu_waves_per_eu(2))) void rowstats_layers_kernel(const LayersArgs m) {
+  const int l = layer_of(m, blockIdx.x);
+  rowstats_block<DT, D>(m.lay[l], blockIdx.x - m.blk[l]);
 }
 
 // Online merge of (max logit, sum of exp2) pairs in exp2 units.
@@ -688,7 +710,7 @@ __device__ __forceinline__ void score_body(const LayerArgs& a, const SeqArgs& sq
 }
 
 template <int DT, int D>
-__global__ __launch_bounds__(kKpThreads) __attribute__((amdgpu_waves_per_eu(2))) void score_kernel(const LayerArgs a) {
+__device__ __forceinline__ void score_block(const LayerArgs& a, const int b) {
   using S = Stager<DT, D, stage_bytes<DT, D>()>;
   constexpr int NS = 4;  // 4-slot ring
   __shared__ uint4 slot0[S::VEC];
@@ -701,7 +723,6 @@ __global__ __launch_bounds__(kKpThreads) __attribute__((amdgpu_waves_per_eu(2)))
   static_assert(2 * kGroupRows * S::ST >= (2 * kMergeLanes + 1) * kMaxRows, "the lse merge fits in gsum");
   uint4* const slots[NS] = {slot0, slot1, slot2, slot3};
 
-  const int b = blockIdx.x;
   const SeqArgs& sq = a.seq[find_seq(a, b, [](const SeqArgs& t) { return t.blk_kpass; })];
   // the selection stages of a multi-layer launch read this layer's argument
   // block from device memory: workgroup 0 puts it there
@@ -744,6 +765,18 @@ __global__ __launch_bounds__(kKpThreads) __attribute__((amdgpu_waves_per_eu(2)))
     else if (wpq == W2) score_body<DT, D, W2, 1, false, 0, S, NS>(a, sq, g, u, j * a.hpr, p, P, sel0, n_sel, nqb, slots, gsum);
     else score_body<DT, D, W1, 1, false, 0, S, NS>(a, sq, g, u, j * a.hpr, p, P, sel0, n_sel, nqb, slots, gsum);
   }
+}
+
+template <int DT, int D>
+__global__ __launch_bounds__(kKpThreads) __attribute__((amdgpu_waves_per_eu(2))) void score_kernel(const LayerArgs a) {
+  score_block<DT, D>(a, blockIdx.x);
+}
+
+// The window-sum passes of up to kLayersPerLaunch layers in one launch.
+template <int DT, int D>
+__global__ __launch_bounds__(kKpThreads) __attribute__((amdgpu_waves_per_eu(2))) void score_layers_kernel(const LayersArgs m) {
+  const int l = layer_of(m, blockIdx.x);
+  score_block<DT, D>(m.lay[l], blockIdx.x - m.blk[l]);
 }
 
 // ---------------------------------------------------------------------------
@@ -991,6 +1024,25 @@ template <int DT, int D>
 struct ScoreOf {
   static constexpr auto fn = score_kernel<DT, D>;
 };
+template <int DT, int D>
+struct RowStatsLayersOf {
+  static constexpr auto fn = rowstats_layers_kernel<DT, D>;
+};
+template <int DT, int D>
+struct ScoreLayersOf {
+  static constexpr auto fn = score_layers_kernel<DT, D>;
+};
+
+template <template <int, int> class KernelOf>
+hipError_t launch_typed_layers(int dtype, const LayersArgs& m, int grid, hipStream_t st, const Timing& tm) {
+  const int d = m.lay[0].d;
+  if (dtype == 0) return d == 64 ? launch(KernelOf<0, 64>::fn, grid, kKpThreads, st, tm, m)
+                                 : launch(KernelOf<0, 128>::fn, grid, kKpThreads, st, tm, m);
+  if (dtype == 1) return d == 64 ? launch(KernelOf<1, 64>::fn, grid, kKpThreads, st, tm, m)
+                                 : launch(KernelOf<1, 128>::fn, grid, kKpThreads, st, tm, m);
+  return d == 64 ? launch(KernelOf<2, 64>::fn, grid, kKpThreads, st, tm, m)
+                 : launch(KernelOf<2, 128>::fn, grid, kKpThreads, st, tm, m);
+}
 
 }  // namespace
 
@@ -1000,6 +1052,16 @@ hipError_t launch_rowstats(int dtype, const LayerArgs& a, int grid, hipStream_t 
 
 hipError_t launch_score(int dtype, const LayerArgs& a, int grid, hipStream_t st, const Timing& tm) {
   return launch_typed<ScoreOf>(dtype, a, grid, st, tm);
+}
+
+hipError_t launch_rowstats_layers(int dtype, const LayersArgs& m, int grid, hipStream_t st,
+                                  const Timing& tm) {
+  return launch_typed_layers<RowStatsLayersOf>(dtype, m, grid, st, tm);
+}
+
+hipError_t launch_score_layers(int dtype, const LayersArgs& m, int grid, hipStream_t st,
+                               const Timing& tm) {
+  return launch_typed_layers<ScoreLayersOf>(dtype, m, grid, st, tm);
 }
 
 // The pooling kernels of radius r, looked up at run time.

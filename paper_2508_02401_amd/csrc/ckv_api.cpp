@@ -550,6 +550,8 @@ int ckv_compress_stack(const ckv_layer_desc* desc, int32_t n_layers, const uint8
                            : (int)(CKV_STACK_CHUNK_TOKENS / tokens < ckv::kLayersPerLaunch
                                        ? CKV_STACK_CHUNK_TOKENS / tokens
                                        : ckv::kLayersPerLaunch);
+    int gather_max = 0;   // the batch's largest per-layer gather grid
+    int64_t ret_max = 0;  // and its most rows kept by one selection unit
     for (int32_t i = 0, chunk = 0; i < nb && rc == CKV_OK; ++chunk) {
       int n = 0, blk = 0;
       for (; n < per_launch && i + n < nb; ++n) {
@@ -565,6 +567,9 @@ int ckv_compress_stack(const ckv_layer_desc* desc, int32_t n_layers, const uint8
         al.table_out = ws;  // the argument block the selection launches read
         la.blk[n] = blk;
         blk += grid_kpass(al);
+        if (grid_gather(al) > gather_max) gather_max = grid_gather(al);
+        for (int s = 0; s < al.num_seqs; ++s)
+          if (al.seq[s].n_ret > ret_max) ret_max = al.seq[s].n_ret;
       }
       if (rc != CKV_OK) break;
       la.n = n;
@@ -596,13 +601,17 @@ int ckv_compress_stack(const ckv_layer_desc* desc, int32_t n_layers, const uint8
     }
     // the batch's selection stages in two launches: the pooling (with the
     // scores and histograms), then one workgroup per selection unit (layer,
-    // prompt, selection group) from the threshold to the gathered rows;
-    // timed on the events of the batch's first layer
+    // prompt, selection group) from the threshold to the gathered rows; a
+    // third launch copies the rows when a unit keeps more than
+    // kUnitCopyRows of them, spread over all CUs rather than one per unit.
+    // Timed on the events of the batch's first layer.
     use_layer_events(b0);
     ckv::MultiArgs m;
     m.table = base;
     m.stride = (int64_t)slot_bytes;
     m.n_layers = nb;
+    m.unit_copy = ret_max <= ckv::kUnitCopyRows;
+    m.pad_ = 0;
     m.per_layer = 0;
     for (int i = 0; i < a.num_seqs; ++i)
       m.per_layer += a.n_sg * (int32_t)ceil_div(a.seq[i].n_ptiles, ckv::kUnitPoolTiles);
@@ -611,12 +620,21 @@ int ckv_compress_stack(const ckv_layer_desc* desc, int32_t n_layers, const uint8
       break;
     }
     m.per_layer = a.num_seqs * a.n_sg;
-    ckv::Timing tm;
+    ckv::Timing tm, tm_gather;
     if (g_events_on) {
       tm.start = g_ev_begin[ckv::kStageSelect];
       tm.stop = g_ev_end[ckv::kStageGather];
     }
+    if (!m.unit_copy) {  // the gather launch ends the stage
+      tm_gather.stop = tm.stop;
+      tm.stop = nullptr;
+    }
     if ((e = ckv::launch_select_units(m, st, tm)) != hipSuccess) {
+      rc = hip_fail(e);
+      break;
+    }
+    m.per_layer = gather_max;
+    if (!m.unit_copy && (e = ckv::launch_gather_layers(m, st, tm_gather)) != hipSuccess) {
       rc = hip_fail(e);
       break;
     }

@@ -28,6 +28,9 @@ constexpr int kPoolTile = 2048;    // scores per pooling workgroup
 constexpr int kUnitPoolTiles = 4;  // tiles per pooling workgroup of ckv_compress_stack
 constexpr int kMaxPoolRadius = 15; // pool kernel <= 2*15+1
 constexpr int kGatherRows = 64;    // retained rows per gather workgroup
+// A selection batch whose largest unit keeps more rows than this copies them
+// in a gather launch of its own: one workgroup per unit copies too slowly.
+constexpr int kUnitCopyRows = 2048;
 constexpr int kHistBits = 12;      // first-level histogram: key bits 30..19
 constexpr int kHistBins = 1 << kHistBits;
 constexpr int kHistShift = 31 - kHistBits;
@@ -170,6 +173,8 @@ struct MultiArgs {
   int64_t stride;
   int32_t per_layer;
   int32_t n_layers;
+  int32_t unit_copy;  // selection units copy their kept rows (else a gather launch follows)
+  int32_t pad_;
 };
 
 // Decode attention of T query tokens over one KV cache: one prompt of a
@@ -266,5 +271,7 @@ hipError_t launch_decode(int dtype, const DecodeBatch& b, hipStream_t st);
 hipError_t launch_stream_gather(const LayerArgs& a, int32_t sinks, int grid, hipStream_t st);
 hipError_t launch_error(int w_dtype, const ErrorArgs& a, hipStream_t st);
 hipError_t launch_select_units(const MultiArgs& m, hipStream_t st, const Timing& tm);
+// Gather of every layer of a batch: per_layer = the largest per-layer gather grid.
+hipError_t launch_gather_layers(const MultiArgs& m, hipStream_t st, const Timing& tm);
 
 }  // namespace ckv

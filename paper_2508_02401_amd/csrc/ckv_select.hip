@@ -395,12 +395,10 @@ __global__ __launch_bounds__(kThreads) void compact_kernel(const LayerArgs a) {
 }
 
 
-// Standalone retain/evict (ckv_gather): rows idx[g, r] of K and V for the
-// kGatherRows output rows of this workgroup. An out-of-range index leaves its
-// output row untouched.
-__global__ __launch_bounds__(kThreads) void gather_kernel(const LayerArgs a) {
-  __shared__ int32_t tok_l[kGatherRows];
-  const int b = blockIdx.x;
+// Retain/evict: rows idx[g, r] of K and V for the kGatherRows output rows of
+// gather workgroup b of the layer. An out-of-range index leaves its output
+// row untouched.
+__device__ __forceinline__ void gather_body(const LayerArgs& a, int b, int32_t* tok_l) {
   int s = 0;
   for (int t = 1; t < a.num_seqs; ++t)
     if (b >= a.seq[t].blk_gather) s = t;
@@ -415,6 +413,25 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const LayerArgs a) {
   __syncthreads();
   copy_rows<kThreads>(a, sq, g, n, [&](int64_t i) { return (int64_t)tok_l[i]; },
             [&](int64_t i) { return r0 + i; });
+}
+
+// Standalone retain/evict (ckv_gather).
+__global__ __launch_bounds__(kThreads) void gather_kernel(const LayerArgs a) {
+  __shared__ int32_t tok_l[kGatherRows];
+  gather_body(a, blockIdx.x, tok_l);
+}
+
+// The gather of a batch of layers after the selection units wrote their
+// indices: m.per_layer workgroups per layer, those past a layer's own grid
+// idle.
+__global__ __launch_bounds__(kThreads) void gather_layers_kernel(const MultiArgs m) {
+  __shared__ int32_t tok_l[kGatherRows];
+  const int l = blockIdx.x / m.per_layer;
+  const int b = blockIdx.x - l * m.per_layer;
+  const LayerArgs& a = layer_args(m, l);
+  const SeqArgs& last = a.seq[a.num_seqs - 1];
+  if (b >= last.blk_gather + last.n_gblk * a.n_kv) return;
+  gather_body(a, b, tok_l);
 }
 
 // StreamingLLM-style selection, the comparison baseline that keeps the
@@ -478,6 +495,10 @@ hipError_t launch_compact(const LayerArgs& a, int grid, hipStream_t st, const Ti
 
 hipError_t launch_gather(const LayerArgs& a, int grid, hipStream_t st, const Timing& tm) {
   return launch(gather_kernel, grid, kThreads, st, tm, a);
+}
+
+hipError_t launch_gather_layers(const MultiArgs& m, hipStream_t st, const Timing& tm) {
+  return launch(gather_layers_kernel, m.n_layers * m.per_layer, kThreads, st, tm, m);
 }
 
 

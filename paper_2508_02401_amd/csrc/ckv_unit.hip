@@ -16,7 +16,8 @@
 //   3. two LDS bitmaps per segment of 131072 tokens, one of the kept keys
 //      (above the threshold) and one of the keys equal to it; walking them in
 //      token order keeps the lowest-index equal keys, writes the indices in
-//      ascending order and copies their K/V rows.
+//      ascending order and copies their K/V rows (or leaves the copies to a
+//      gather launch when the batch keeps many rows per unit).
 // For a prompt of at most 131072 tokens whose threshold bin fits in LDS,
 // steps 2 and 3 read the scores once: the same pass marks the keys above the
 // bin and gathers the bin's keys.
@@ -116,7 +117,9 @@ __device__ __forceinline__ void scan_scores(const float* sc_p, int64_t j0, int64
   }
 }
 
-__device__ __forceinline__ void unit_body(const LayerArgs& a, int u, UnitLds& sm) {
+// copy: whether the unit copies its kept K/V rows (otherwise it writes only
+// the indices and a gather launch copies them).
+__device__ __forceinline__ void unit_body(const LayerArgs& a, int u, bool copy, UnitLds& sm) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int s = u / a.n_sg, g = u - s * a.n_sg;
   const SeqArgs& sq = a.seq[s];
@@ -129,12 +132,14 @@ __device__ __forceinline__ void unit_body(const LayerArgs& a, int u, UnitLds& sm
   CKV_GLOBAL int32_t* out = to_global(sq.idx) + (int64_t)g * sq.n_ret;
   if (n_keep < 0) {  // budget >= L: every token stays, in order
     for (int64_t j = tid; j < sq.L; j += kUT) out[j] = (int32_t)j;
-    for (int gk = gk0; gk < gk1; ++gk) copy_run<kUT>(a, sq, gk, 0, 0, sq.L);
+    if (copy)
+      for (int gk = gk0; gk < gk1; ++gk) copy_run<kUT>(a, sq, gk, 0, 0, sq.L);
     return;
   }
   // the window is always kept, after the prefix tokens
   for (int i = tid; i < w; i += kUT) out[n_keep + i] = (int32_t)(Ls + i);
-  for (int gk = gk0; gk < gk1; ++gk) copy_run<kUT>(a, sq, gk, n_keep, Ls, w);
+  if (copy)
+    for (int gk = gk0; gk < gk1; ++gk) copy_run<kUT>(a, sq, gk, n_keep, Ls, w);
   if (n_keep == 0) return;
 
   // 1. the first-level bin from the pooling kernel's histogram
@@ -265,7 +270,7 @@ __device__ __forceinline__ void unit_body(const LayerArgs& a, int u, UnitLds& sm
     // copies of the segment's kept rows, kUnitList rows per round
     const uint32_t n_seg = tot_kept < (uint32_t)n_keep - pos_carry ? tot_kept
                                                                     : (uint32_t)n_keep - pos_carry;
-    for (uint32_t r0 = 0; r0 < n_seg; r0 += kUnitList) {
+    for (uint32_t r0 = 0; copy && r0 < n_seg; r0 += kUnitList) {
       uint32_t li = first - pos_carry;
 #pragma unroll
       for (int i = 0; i < kPer; ++i) {
@@ -328,7 +333,7 @@ __device__ __forceinline__ void unit_body(const LayerArgs& a, int u, UnitLds& sm
 __global__ __launch_bounds__(kUT) void select_unit_kernel(const MultiArgs m) {
   __shared__ UnitLds sm;
   const int l = blockIdx.x / m.per_layer;
-  unit_body(layer_args(m, l), blockIdx.x - l * m.per_layer, sm);
+  unit_body(layer_args(m, l), blockIdx.x - l * m.per_layer, m.unit_copy != 0, sm);
 }
 
 }  // namespace

@@ -4,8 +4,8 @@ One step = the whole path (score, select, gather) over every layer of the
 workload, with all inputs already resident in HBM. By default one
 ckv_compress_stack call runs all layers: the two K passes of every layer,
 consecutive layers alternating between the main stream and a side stream, then
-the pooling, selection and gather of all layers in two launches on the main
-stream. --schedule layers issues one
+the pooling, selection and gather of all layers in two or three launches on
+the main stream. --schedule layers issues one
 ckv_compress_layer per layer instead; --pipeline runs ckv_score (both K passes
 and the pooling) of layer l+1 on one stream while ckv_select and ckv_gather of
 layer l run on another. Prints one JSON line.
@@ -448,7 +448,8 @@ def measure(args, wl, desc, layers, budgets, elt, dev, hip, schedule, shared=Fal
         stack_masks = np.stack([m for m, _ in layers])
         stack_seqs = [sq for _, sq in layers]
         sched_text = ("ckv_compress_stack: the two K passes layer by layer%s, then pooling + "
-                      "selection + gather as two launches per batch of %d layers"
+                      "selection + gather as two launches (three when a unit keeps over 2048 rows) "
+                      "per batch of %d layers"
                       % (", consecutive layers alternating between two streams"
                          if args.stack_side else "", stack_slots))
 

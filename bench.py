@@ -2,10 +2,10 @@
 
 One step = the whole path (score, select, gather) over every layer of the
 workload, with all inputs already resident in HBM. By default one
-ckv_compress_stack call runs all layers: the two K passes of every layer,
-consecutive layers alternating between the main stream and a side stream, then
-the pooling, selection and gather of all layers in two or three launches on
-the main stream. --schedule layers issues one
+ckv_compress_stack call runs all layers on one stream: the two K passes of
+every layer, then the pooling, selection and gather of all layers in two or
+three launches; a second leg ("side_stream_variant") times the same call with
+a side stream on which every other layer's K passes run. --schedule layers issues one
 ckv_compress_layer per layer instead; --pipeline runs ckv_score (both K passes
 and the pooling) of layer l+1 on one stream while ckv_select and ckv_gather of
 layer l run on another. Prints one JSON line.
@@ -55,6 +55,8 @@ def parse():
                    help="oracle threads for cpu_baseline (0 = the usable CPUs, at most 16)")
     p.add_argument("--cpu-seconds", type=float, default=15.0,
                    help="wall time the cpu_baseline sample aims for")
+    p.add_argument("--no-side-variant", action="store_true",
+                   help="skip the leg that times the stack with a side stream")
     p.add_argument("--no-stream-ceiling", action="store_true",
                    help="skip the streaming-read ceiling probe (bench_stream.so)")
     p.add_argument("--stream-ceiling-only", action="store_true",
@@ -62,16 +64,19 @@ def parse():
     p.add_argument("--configs", default="llama8b-32k-layer,llama8b-32k-stack,qwen7b-ragged-batch",
                    help="other workloads measured after the headline one, comma-separated "
                         "('' for none); each gets its own step time and roofline")
-    p.add_argument("--time-every", type=int, default=4, metavar="N",
+    p.add_argument("--time-every", type=int, default=8, metavar="N",
                    help="K-pass launches of every N-th layer carry start/end events (the layer "
                         "offset rotates with the step, so every layer is sampled); each timed "
                         "launch delays its neighbours' dispatch by a few microseconds")
     p.add_argument("--stack-slots", type=int, default=0,
                    help="--schedule stack: layer slots of workspace (0 = one per layer); the "
                         "selection stages run in launches covering that many layers")
-    p.add_argument("--stack-side", type=int, default=1,
-                   help="--schedule stack: 1 (default) gives ckv_compress_stack a side stream, "
-                        "on which every other layer's K passes run; 0 runs them all on one stream")
+    p.add_argument("--stack-side", type=int, default=0,
+                   help="--schedule stack: 1 gives ckv_compress_stack a side stream, on which "
+                        "every other layer's K passes run (two launches in flight, so each "
+                        "launch's own duration includes the other's share of HBM); 0 (default) "
+                        "runs them all on one stream, and a second leg times the side-stream "
+                        "schedule")
     p.add_argument("--schedule", choices=("stack", "layers"), default="stack",
                    help="stack: one ckv_compress_stack call over all layers (default); "
                         "layers: one ckv_compress_layer per layer (see --streams)")
@@ -179,6 +184,8 @@ def _kernel_short(name: str) -> str:
         return m.group(1)
     if "neg_kernel" in name:
         return "calibration_copy(neg)"
+    if "stream_copy_kernel" in name:
+        return "stream_copy_kernel"
     m = re.search(r"stream_read_kernel<(\d+)>", name)
     if m:
         return "stream_read_kernel<%s> (%s)" % (m.group(1), STREAM_KINDS[int(m.group(1))])
@@ -194,7 +201,7 @@ def summarize_trace(d: str) -> None:
     rows = list(csv.DictReader(open(stats[0])))
     # this library's kernels (the torch kernels are the input draws, outside
     # the timed region)
-    rows = [r for r in rows if "ckv::" in r["Name"] or "stream_read_kernel" in r["Name"]]
+    rows = [r for r in rows if "ckv::" in r["Name"] or "stream_" in r["Name"]]
     print("| kernel | calls | total ms | avg us | min us | max us | % of all GPU time |")
     print("|---|---|---|---|---|---|---|")
     for r in rows:
@@ -323,6 +330,9 @@ def stream_ceiling(dev, reps: int = 4, gib: int = 2, hot_mib: int = 128):
     lib.bench_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
                                       ctypes.c_int, ctypes.c_int, ctypes.c_void_p]
     lib.bench_stream_read.restype = ctypes.c_int
+    lib.bench_stream_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                      ctypes.c_int, ctypes.c_void_p]
+    lib.bench_stream_copy.restype = ctypes.c_int
     n = gib << 30
     buf = torch.full((n // 2,), 1.0, dtype=torch.bfloat16, device=dev)
     sink = torch.zeros(256, dtype=torch.int32, device=dev)
@@ -363,6 +373,27 @@ def stream_ceiling(dev, reps: int = 4, gib: int = 2, hot_mib: int = 128):
         best = max(best, cold[g_best])
     out["ceiling_gbs"] = best
     out["ceiling_frac_of_peak"] = best / HBM_PEAK_GBS
+    # an even read/write mix: the first half of the buffer copied to the second
+    half = n // 2
+    copy = {}
+    for grid in (1024, 2048, 4096, 8192):
+        ts = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(st)
+            rc = lib.bench_stream_copy(buf.data_ptr(), buf.data_ptr() + half, half, grid,
+                                       st.cuda_stream)
+            if rc != 0:
+                raise RuntimeError("bench_stream_copy failed: hipError %d" % rc)
+            b.record(st)
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b))
+        ts.sort()
+        copy[grid] = 2 * half / (ts[len(ts) // 2] / 1e3) / 1e9  # bytes read + written
+    g_best = max(copy, key=copy.get)
+    out["copy"] = {"what": "stream_copy_kernel: %d MiB copied, bytes read + written per second"
+                           % (half >> 20), "gbs_by_grid": copy, "gbs": copy[g_best],
+                   "frac_of_peak": copy[g_best] / HBM_PEAK_GBS}
     del buf
     torch.cuda.empty_cache()
     return out
@@ -448,7 +479,7 @@ def measure(args, wl, desc, layers, budgets, elt, dev, hip, schedule, shared=Fal
         stack_masks = np.stack([m for m, _ in layers])
         stack_seqs = [sq for _, sq in layers]
         sched_text = ("ckv_compress_stack: the two K passes layer by layer%s, then pooling + "
-                      "selection + gather as two launches (three when a unit keeps over 2048 rows) "
+                      "selection + gather as two launches (three when a unit keeps over 512 rows) "
                       "per batch of %d layers"
                       % (", consecutive layers alternating between two streams"
                          if args.stack_side else "", stack_slots))
@@ -718,6 +749,21 @@ def measure(args, wl, desc, layers, budgets, elt, dev, hip, schedule, shared=Fal
     return res
 
 
+def side_stream_leg(args, wl, desc, layers, budgets, elt, dev, hip, shared=False):
+    """The same stack step with a side stream for every other layer's K passes:
+    its step time and the K-pass phase's aggregate rate (per-launch durations
+    overlap there, so no per-launch roofline)."""
+    import copy
+
+    a2 = copy.copy(args)
+    a2.stack_side = 1
+    r = measure(a2, wl, desc, layers, budgets, elt, dev, hip, "stack", shared)
+    return {"what": "ckv_compress_stack with a side stream: consecutive layers' K passes "
+                    "alternate between two streams, two launches in flight",
+            "ms_per_step": r["ms_per_step"], "value": r["value"],
+            "path_hbm_frac": r["path_hbm_frac"], "kpass_phase": r["kpass_phase"]}
+
+
 def rotate_copies(desc, layers, dev, min_bytes: int = 512 << 20, min_copies: int = 8):
     """Distinct copies of a single layer's inputs (with their own outputs), at
     least min_copies of them and at least min_bytes of K and V in total."""
@@ -813,6 +859,10 @@ def main():
         "host_enqueue_ms_per_step": res["host_enqueue_ms_per_step"],
     }
 
+    if schedule == "stack" and not args.stack_side and not args.no_side_variant:
+        result["side_stream_variant"] = side_stream_leg(args, wl, desc, layers, budgets, elt, dev,
+                                                        hip, shared)
+
     if not args.no_lse_variant:
         # The same step with the window rows' log-sum-exp supplied by the
         # caller (a causal prefill attention kernel keeps it per query row):
@@ -875,6 +925,8 @@ def main():
             del oc
         else:
             r = measure(args, owl, od, ol, ob, oe, dev, hip, "stack", False)
+            if not args.stack_side and not args.no_side_variant:
+                r["side_stream_variant"] = side_stream_leg(args, owl, od, ol, ob, oe, dev, hip)
         r.pop("path_bytes_per_step", None)
         others[name] = r
         del ol

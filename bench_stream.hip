@@ -9,7 +9,8 @@
 //           take: every wave keeps three 4 KB stages of its own in flight in a
 //           private four-slot ring and waits for them with partial vmcnt waits.
 // Workgroups take 4 KB-per-wave chunks grid-stride, so consecutive waves read
-// consecutive chunks.
+// consecutive chunks. A copy kernel (bench_stream_copy) gives the rate of an
+// even read/write mix, the traffic of kernels that write as much as they read.
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 
@@ -83,7 +84,38 @@ __global__ __launch_bounds__(kThreads) void stream_read_kernel(const u32x4* __re
   if (s == kNever) sink[threadIdx.x] = s;
 }
 
+// dst[i] = src[i] for n16 16-byte units, grid-stride, four loads in flight
+// per lane before their stores.
+__global__ __launch_bounds__(kThreads) void stream_copy_kernel(const u32x4* __restrict__ x,
+                                                               u32x4* __restrict__ y, size_t n16) {
+  const size_t stride = (size_t)gridDim.x * kThreads;
+  size_t i = (size_t)blockIdx.x * kThreads + threadIdx.x;
+  for (; i + 3 * stride < n16; i += 4 * stride) {
+    const u32x4 a = x[i], b = x[i + stride], c = x[i + 2 * stride], d = x[i + 3 * stride];
+    y[i] = a;
+    y[i + stride] = b;
+    y[i + 2 * stride] = c;
+    y[i + 3 * stride] = d;
+  }
+  for (; i < n16; i += stride) y[i] = x[i];
+}
+
 }  // namespace
+
+// Copy `bytes` bytes from src to dst (distinct, 16-byte aligned, bytes a
+// multiple of 16) on `grid` workgroups of 256 threads. Returns a hipError_t
+// value (0 on success).
+extern "C" int bench_stream_copy(const void* src, void* dst, size_t bytes, int grid, void* stream) {
+  if (!src || !dst || bytes % 16 || ((size_t)src & 15) || ((size_t)dst & 15) || grid < 1 ||
+      grid > 65536)
+    return (int)hipErrorInvalidValue;
+  const u32x4* x = static_cast<const u32x4*>(src);
+  u32x4* y = static_cast<u32x4*>(dst);
+  size_t n16 = bytes / 16;
+  void* args[] = {(void*)&x, (void*)&y, (void*)&n16};
+  return (int)hipLaunchKernel(reinterpret_cast<const void*>(stream_copy_kernel), dim3(grid),
+                              dim3(kThreads), args, 0, static_cast<hipStream_t>(stream));
+}
 
 // Read `bytes` bytes at src once with read route `kind` on `grid` workgroups
 // of 256 threads. sink: 256 unsigned of device memory, written only when a

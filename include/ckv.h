@@ -234,7 +234,7 @@ int ckv_compress_layer(const ckv_layer_desc *desc, const uint8_t *head_mask, con
  * the two K passes of each layer of a batch, then the batch's selection
  * stages (pooling, top-N, compaction with the gather) as two launches that
  * each cover the whole batch (three when a selection unit keeps more than
- * 2048 rows: the gather then has a launch of its own); a slot per layer of the batch keeps its window
+ * 512 rows: the gather then has a launch of its own); a slot per layer of the batch keeps its window
  * sums and selection state meanwhile. With side_stream non-NULL and different
  * from stream, the K passes of consecutive layers of a batch alternate
  * between stream and side_stream (one layer's launches start while the

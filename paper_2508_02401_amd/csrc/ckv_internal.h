@@ -30,7 +30,7 @@ constexpr int kMaxPoolRadius = 15; // pool kernel <= 2*15+1
 constexpr int kGatherRows = 64;    // retained rows per gather workgroup
 // A selection batch whose largest unit keeps more rows than this copies them
 // in a gather launch of its own: one workgroup per unit copies too slowly.
-constexpr int kUnitCopyRows = 2048;
+constexpr int kUnitCopyRows = 512;
 constexpr int kHistBits = 12;      // first-level histogram: key bits 30..19
 constexpr int kHistBins = 1 << kHistBits;
 constexpr int kHistShift = 31 - kHistBits;

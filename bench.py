@@ -38,8 +38,9 @@ BF16_PEAK_TFLOPS = 2500.0
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=5)
-    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--steps", type=int, default=20)
+    # a few warm-up steps: the first ones after the layers are drawn run slower
+    p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--workload", default="llama8b-128k-stack")
     p.add_argument("--layers", type=int, default=0, help="limit the layer count (0 = all)")
     p.add_argument("--no-cpu-baseline", action="store_true")

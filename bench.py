@@ -65,10 +65,11 @@ def parse():
     p.add_argument("--configs", default="llama8b-32k-layer,llama8b-32k-stack,qwen7b-ragged-batch",
                    help="other workloads measured after the headline one, comma-separated "
                         "('' for none); each gets its own step time and roofline")
-    p.add_argument("--time-every", type=int, default=8, metavar="N",
+    p.add_argument("--time-every", type=int, default=32, metavar="N",
                    help="K-pass launches of every N-th layer carry start/end events (the layer "
                         "offset rotates with the step, so every layer is sampled); each timed "
-                        "launch delays its neighbours' dispatch by a few microseconds")
+                        "launch delays its neighbours' dispatch by 5-9 microseconds, so the "
+                        "default samples one layer per step of 32 layers")
     p.add_argument("--stack-slots", type=int, default=0,
                    help="--schedule stack: layer slots of workspace (0 = one per layer); the "
                         "selection stages run in launches covering that many layers")
@@ -595,14 +596,14 @@ def measure(args, wl, desc, layers, budgets, elt, dev, hip, schedule, shared=Fal
     else:
         chunk = {l: [l] for l in range(n_layers)}
     starts = sorted(chunk)
-    every = max(1, round(args.time_every / max(len(v) for v in chunk.values())))
+    every = max(1, min(len(starts), round(args.time_every / max(len(v) for v in chunk.values()))))
     ev = []  # ev[step][layer] = (begin, end) arrays, or None for an untimed layer
     kp_timed = []  # kp_timed[step][layer]: the K passes carry events
     for k in range(args.steps):
         per_layer, flags = [], []
         for li in range(n_layers):
             kp = li in chunk and (starts.index(li) + k) % every == 0
-            sel = sel_timed and li == 0
+            sel = sel_timed and li == 0 and k % 4 == 0  # selection events: every 4th step
             flags.append(kp)
             if not kp and not sel:
                 per_layer.append(None)

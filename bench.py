@@ -737,7 +737,9 @@ def measure(args, wl, desc, layers, budgets, elt, dev, hip, schedule, shared=Fal
         "path_bytes_per_step": path_bytes,
         "stage_ms_avg": stage_avg,
         "kpass_phase": kpass_phase,
-        "roofline": {"kernel": dom + "_kernel", "bound": "hbm", "achieved": dom_gbs,
+        "roofline": {"kernel": dom + ("_layers_kernel" if max(len(v) for v in chunk.values()) > 1
+                                      else "_kernel"),
+                     "bound": "hbm", "achieved": dom_gbs,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": dom_gbs / HBM_PEAK_GBS,
                      "traffic": None, "avg_launch_ms": stage_avg[dom],
                      "algorithmic_bytes_per_launch": float(np.mean(dom_bytes)),

@@ -215,3 +215,32 @@ def test_stack_with_row_groups_beyond_128_rows(dev):
         for g in range(case.n_kv):
             rs, ri = oracle_group(case, mask, q, k, g, b)
             check_group(case, out, g, rs, ri, k, v, "layer %d" % l)
+
+
+@pytest.mark.parametrize("pool,kp", [("max", 1), ("avg", 3), ("max", 9), ("avg", 15), ("max", 31)],
+                         ids=["max-k1", "avg-k3", "max-k9", "avg-k15", "max-k31"])
+def test_stack_pooling_radii_and_gather_split(dev, pool, kp):
+    # The stack's pooling kernel at halo widths 0-4 chunks (radius 0 to 15) over
+    # a ragged 8192-score span and tail, and both ways of copying the kept rows:
+    # budgets of 512 rows per unit copy in the selection launch, 513 in a gather
+    # launch of their own. One layer per batch (each way alone) and both layers in
+    # one batch (the split then covers both); bit-exact against per-layer calls,
+    # and every KV head of both layers against the oracle.
+    case = Case(8, 2, 64, 16, pool, kp, torch.bfloat16)
+    L = 8192 + 2 * 1024 + 16 + 5  # ragged: the scored span is not a multiple of 4
+    layer_inputs, cpu = [], []
+    for l, budget in enumerate((512, 513)):
+        q, k, v, mask = random_inputs(case, L, seed=700 + 10 * kp + l, device="cpu", n_sel=1 + l)
+        layer_inputs.append((mask, [q.to(dev)], [k.to(dev)], [v.to(dev)], [budget]))
+        cpu.append((mask, q, k, v, budget))
+    desc = case.desc()
+    print("stack pool %s k=%d" % (pool, kp), flush=True)
+    ref = _run_layers(desc, layer_inputs, dev)
+    for slots in (1, 2):
+        got = _run_stack(desc, layer_inputs, dev, False, slots=slots)
+        _assert_same(got, ref, "pool %s k=%d slots %d" % (pool, kp, slots))
+    for l, (mask, q, k, v, b) in enumerate(cpu):
+        out = _as_dict(got[l][0])
+        for g in range(case.n_kv):
+            rs, ri = oracle_group(case, mask, q, k, g, b)
+            check_group(case, out, g, rs, ri, k, v, "pool %s k=%d layer %d" % (pool, kp, l))

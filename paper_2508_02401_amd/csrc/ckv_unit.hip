@@ -37,7 +37,9 @@ constexpr int kSegWords = 4096;            // bitmap words of one output segment
 constexpr int kSegTokens = kSegWords * 32; // tokens of one output segment
 constexpr int kUnitList = 1024;            // kept rows listed per copy round
 constexpr int kScanBatch = 32;             // score loads in flight per thread
+constexpr int kBatchTokens = kUT * kScanBatch;  // tokens of one scan batch
 static_assert(kSegWords % kUT == 0, "bitmap words per thread");
+static_assert(kHistBins % kUT == 0 && kSegTokens % kBatchTokens == 0, "whole batches");
 
 struct UnitLds {
   uint32_t hist[kHistBins];
@@ -117,8 +119,6 @@ __device__ __forceinline__ void scan_scores(const float* sc_p, int64_t j0, int64
   }
 }
 
-// copy: whether the unit copies its kept K/V rows (otherwise it writes only
-// the indices and a gather launch copies them).
 __device__ __forceinline__ void unit_body(const LayerArgs& a, int u, bool copy, UnitLds& sm) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int s = u / a.n_sg, g = u - s * a.n_sg;
@@ -136,15 +136,19 @@ __device__ __forceinline__ void unit_body(const LayerArgs& a, int u, bool copy, 
       for (int gk = gk0; gk < gk1; ++gk) copy_run<kUT>(a, sq, gk, 0, 0, sq.L);
     return;
   }
+  // 1. the first-level bin from the pooling kernel's histogram, whose loads
+  // are in flight while the window rows are copied
+  const CKV_GLOBAL uint32_t* ghist = to_global(sq.hist) + (int64_t)g * kHistBins;
+  uint32_t hv[kHistBins / kUT];
+#pragma unroll
+  for (int k = 0; k < kHistBins / kUT; ++k) hv[k] = ghist[tid + k * kUT];
   // the window is always kept, after the prefix tokens
   for (int i = tid; i < w; i += kUT) out[n_keep + i] = (int32_t)(Ls + i);
   if (copy)
     for (int gk = gk0; gk < gk1; ++gk) copy_run<kUT>(a, sq, gk, n_keep, Ls, w);
   if (n_keep == 0) return;
-
-  // 1. the first-level bin from the pooling kernel's histogram
-  const CKV_GLOBAL uint32_t* ghist = to_global(sq.hist) + (int64_t)g * kHistBins;
-  for (int i = tid; i < kHistBins; i += kUT) sm.hist[i] = ghist[i];
+#pragma unroll
+  for (int k = 0; k < kHistBins / kUT; ++k) sm.hist[tid + k * kUT] = hv[k];
   __syncthreads();
   find_bin_unit(sm, kHistBins, (uint32_t)n_keep);
   // keys compare on (key >> shift) against prefix: those above are kept, and
@@ -172,11 +176,18 @@ __device__ __forceinline__ void unit_body(const LayerArgs& a, int u, bool copy, 
     // one pass: the keys above the bin into the bitmap (a wave's 64
     // consecutive tokens give two whole words, written by its lane 0), the
     // bin's keys into LDS
-    for (int i = tid; i < kSegWords; i += kUT) sm.emap[i] = 0u;
+    // the scan writes the bitmap words of whole batches up to Ls; the words
+    // past them are cleared here (scanning all 131072 tokens for a short
+    // prompt only wrote zeros there)
+    const int scanned = (int)((Ls + kBatchTokens - 1) / kBatchTokens) * (kBatchTokens / 32);
+    for (int i = tid; i < kSegWords; i += kUT) {
+      sm.emap[i] = 0u;
+      if (i >= scanned) sm.kmap[i] = 0u;
+    }
     if (tid == 0) sm.n_cand = 0u;
     __syncthreads();
     const uint32_t bin = prefix;
-    scan_scores(sc, 0, kSegTokens, Ls, [&](int64_t j, uint32_t key, bool in) {
+    scan_scores(sc, 0, Ls, Ls, [&](int64_t j, uint32_t key, bool in) {
       const uint32_t kb = key >> kHistShift;
       const uint64_t above = __ballot(in && kb > bin);
       if (lane == 0) {
@@ -313,7 +324,11 @@ __device__ __forceinline__ void unit_body(const LayerArgs& a, int u, bool copy, 
   }
   for (int64_t seg0 = 0; seg0 < Ls && pos_carry < (uint32_t)n_keep; seg0 += kSegTokens) {
     const int64_t seg1 = Ls - seg0 < kSegTokens ? Ls : seg0 + kSegTokens;
-    scan_scores(sc, seg0, seg0 + (int64_t)kSegTokens, seg1, [&](int64_t j, uint32_t key, bool in) {
+    // the scan writes the words of whole batches up to seg1, the rest are
+    // cleared (the previous segment's emit ended with a barrier)
+    const int scanned = (int)((seg1 - seg0 + kBatchTokens - 1) / kBatchTokens) * (kBatchTokens / 32);
+    for (int i = scanned + tid; i < kSegWords; i += kUT) sm.kmap[i] = sm.emap[i] = 0u;
+    scan_scores(sc, seg0, seg1, seg1, [&](int64_t j, uint32_t key, bool in) {
       const uint32_t p = key >> shift;
       const uint64_t above = __ballot(in && p > prefix);
       const uint64_t equal = __ballot(in && p == prefix);

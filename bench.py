@@ -863,11 +863,19 @@ def main():
         "host_enqueue_ms_per_step": res["host_enqueue_ms_per_step"],
     }
 
-    if schedule == "stack" and not args.stack_side and not args.no_side_variant:
-        result["side_stream_variant"] = side_stream_leg(args, wl, desc, layers, budgets, elt, dev,
-                                                        hip, shared)
+    def leg(key, fn, into=result):
+        # a leg that fails records its error; the headline line still prints
+        try:
+            into[key] = fn()
+        except Exception as exc:  # noqa: BLE001
+            print("bench: leg %s failed: %r" % (key, exc), file=sys.stderr, flush=True)
+            into[key] = {"error": repr(exc)}
 
-    if not args.no_lse_variant:
+    if schedule == "stack" and not args.stack_side and not args.no_side_variant:
+        leg("side_stream_variant",
+            lambda: side_stream_leg(args, wl, desc, layers, budgets, elt, dev, hip, shared))
+
+    def lse_leg():
         # The same step with the window rows' log-sum-exp supplied by the
         # caller (a causal prefill attention kernel keeps it per query row):
         # the row-statistics pass is skipped and K is read once. The values
@@ -891,13 +899,15 @@ def main():
                     del kt
                 sq.lse = lse
         torch.cuda.synchronize()
-        r_lse = measure(args, wl, desc, layers, budgets, elt, dev, hip,
-                        "stack" if schedule == "rotate" else schedule, shared, timed=("score",))
-        for mask, seqs in layers:
-            for sq in seqs:
-                sq.lse = None
+        try:
+            r_lse = measure(args, wl, desc, layers, budgets, elt, dev, hip,
+                            "stack" if schedule == "rotate" else schedule, shared, timed=("score",))
+        finally:
+            for mask, seqs in layers:
+                for sq in seqs:
+                    sq.lse = None
         ms_lse = r_lse["ms_per_step"]
-        result["caller_lse_variant"] = {
+        return {
             "what": "same step with the window rows' log-sum-exp supplied by the caller's prefill "
                     "attention: no row-statistics pass, K read once",
             "ms_per_step": ms_lse, "value": tokens_per_layer * n_layers / (ms_lse / 1e3),
@@ -906,21 +916,24 @@ def main():
             "score_kernel_avg_us": r_lse["stage_ms_avg"]["score"] * 1e3,
             "kpass_phase": r_lse["kpass_phase"]}
 
+    if not args.no_lse_variant:
+        leg("caller_lse_variant", lse_leg)
+
     if not args.no_profile_variant:
-        result["error_profile"] = error_profile(args, wl, layers, dev, hip)
+        leg("error_profile", lambda: error_profile(args, wl, layers, dev, hip))
     if not args.no_decode_variant:
-        result["decode_step"] = decode_step(wl, layers, dev)
+        leg("decode_step", lambda: decode_step(wl, layers, dev))
         # last: it overwrites the compact caches the legs above read
-        result["streaming_preset"] = streaming_preset(wl, layers, dev)
+        leg("streaming_preset", lambda: streaming_preset(wl, layers, dev))
 
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(wl, layers, args.cpu_threads, args.cpu_seconds)
+        leg("cpu_baseline", lambda: cpu_baseline(wl, layers, args.cpu_threads, args.cpu_seconds))
     del layers
     torch.cuda.empty_cache()
 
     # the other workloads of the metric, each with its own step and roofline
     others = {}
-    for name in [x for x in args.configs.split(",") if x and x != wl.name]:
+    def other_config(name):
         owl = synth.WORKLOADS[name]
         od, ol, ob, oe = build_layers(args, owl, dev, owl.n_layers, False)
         if owl.n_layers == 1:
@@ -932,13 +945,16 @@ def main():
             if not args.stack_side and not args.no_side_variant:
                 r["side_stream_variant"] = side_stream_leg(args, owl, od, ol, ob, oe, dev, hip)
         r.pop("path_bytes_per_step", None)
-        others[name] = r
         del ol
         torch.cuda.empty_cache()
+        return r
+
+    for name in [x for x in args.configs.split(",") if x and x != wl.name]:
+        leg(name, lambda: other_config(name), others)
     if others:
         result["other_configs"] = others
     if not args.no_stream_ceiling:
-        result["stream_ceiling"] = stream_ceiling(dev)
+        leg("stream_ceiling", lambda: stream_ceiling(dev))
     print(json.dumps(result), flush=True)
 
 
